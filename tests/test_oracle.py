@@ -1,0 +1,458 @@
+"""Pins for the CPU oracle (runs without a GPU).
+
+The oracle is checked against things other than itself: hand-derived golden
+cases, the brute-force definitions in tests/brute.py (a different route),
+closed forms, invariants and reductions to textbook/library routines. The
+mutation tests at the end plant plausible mistakes in a temporary copy of
+the oracle's C source and check that these pins catch every one of them.
+"""
+import ctypes
+import json
+import math
+import os
+import shutil
+import subprocess
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import scipy.special
+
+import brute
+import oracle
+from paper_2607_27952_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _orc_scores(wl, **kw):
+    return oracle.scores(wl.R, wl.G, wl.Hq, wl.Hkv, wl.Dh, wl.q, wl.k, wl.cu_seqlens, wl.vis_start,
+                         wl.cu_vis, oracle.BF16 if wl.qk_dtype == W.BF16 else oracle.F32,
+                         scale=wl.scale, **kw)
+
+
+def _fcode(dtype):
+    return oracle.BF16 if dtype == W.BF16 else oracle.F32
+
+
+def _make_wl(q, k, cu_seqlens, vis_start, cu_vis, Hq, Hkv, scale, dtype=W.F32, feats=None, Dv=1):
+    q = np.asarray(q, np.float32)
+    k = np.asarray(k, np.float32)
+    R = len(cu_seqlens) - 1
+    N = int(cu_vis[-1])
+    if feats is None:
+        feats = np.ones((N, Dv), np.float32)
+    return W.Workload(name="handmade", R=R, G=q.shape[0], Hq=Hq, Hkv=Hkv, Dh=q.shape[-1],
+                      qk_dtype=dtype, scale=scale, cu_seqlens=np.asarray(cu_seqlens, np.int32),
+                      vis_start=np.asarray(vis_start, np.int32), cu_vis=np.asarray(cu_vis, np.int32),
+                      q=W.to_bf16_bits(q) if dtype == W.BF16 else q,
+                      k=W.to_bf16_bits(k) if dtype == W.BF16 else k,
+                      Dv=feats.shape[1], f_dtype=W.F32, feats=feats,
+                      cu_keep=np.asarray([0] + [1] * R, np.int32).cumsum().astype(np.int32))
+
+
+# ---------------------------------------------------------------- scores (Eq. 6-8)
+
+def test_scores_golden_two_heads():
+    g = _load("scores_two_heads.json")
+    wl = _make_wl(g["q"], g["k"], g["cu_seqlens"], g["vis_start"], g["cu_vis"], g["Hq"], g["Hkv"], g["scale"])
+    w, rows = _orc_scores(wl, want_rows=True)
+    np.testing.assert_allclose(w, g["w"], rtol=g["rel_tol"])
+    np.testing.assert_allclose(rows, np.asarray(g["rows"]), rtol=g["rel_tol"])
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_scores_match_bruteforce(seed):
+    rng = np.random.default_rng(seed)
+    Hkv = int(rng.choice([1, 2, 3]))
+    g = int(rng.choice([1, 2, 3, 7]))
+    wl = W.tiny(seed, R=int(rng.integers(1, 4)), G=int(rng.integers(1, 4)), Hq=Hkv * g, Hkv=Hkv,
+                Dh=int(rng.choice([4, 8, 16])), n_range=(1, 24), t_range=(1, 12),
+                qk_dtype=[W.F32, W.BF16][seed % 2])
+    w, rows = _orc_scores(wl, want_rows=True)
+    wb, rows_b = brute.scores(wl, rng=np.random.default_rng(seed + 100), want_rows=True)
+    np.testing.assert_allclose(w, wb, rtol=1e-12, atol=0)
+    np.testing.assert_allclose(rows, rows_b, rtol=1e-11, atol=1e-300)
+
+
+def test_scores_rows_sum_to_one_and_w_normalised():
+    wl = W.tiny(5, R=3, G=2, Hq=6, Hkv=2, Dh=16, n_range=(5, 40), t_range=(2, 20))
+    w, rows = _orc_scores(wl, want_rows=True)
+    for r in range(wl.R):
+        a, b = wl.cu_seqlens[r], wl.cu_seqlens[r + 1]
+        np.testing.assert_allclose(rows[:, :, a:b].sum(axis=2), 1.0, atol=1e-12)
+        seg = w[wl.cu_vis[r]:wl.cu_vis[r + 1]]
+        assert abs(seg.sum() - 1.0) < 1e-12 and (seg >= 0).all()
+
+
+def test_scores_uniform_keys_closed_form():
+    """All keys equal: every row is uniform, so w_i = 1/N for any G, Hq."""
+    rng = np.random.default_rng(1)
+    N, T, G, Hq, Hkv, Dh = 37, 11, 3, 6, 3, 8
+    P = N + T
+    q = rng.standard_normal((G, 1, Hq, Dh))
+    k = np.broadcast_to(rng.standard_normal((1, 1, Hkv, Dh)), (G, P, Hkv, Dh)).copy()
+    wl = _make_wl(q, k, [0, P], [T // 4], [0, N], Hq, Hkv, 0.3)
+    np.testing.assert_allclose(_orc_scores(wl), 1.0 / N, rtol=1e-13)
+
+
+@pytest.mark.parametrize("delta", [0.5, 3.0, 9.0])
+def test_scores_planted_key_closed_form(delta):
+    """Zero keys except one visual key with scaled logit delta in every head:
+    w_planted = e^delta / (N - 1 + e^delta), whatever G and Hq."""
+    rng = np.random.default_rng(2)
+    N, T, G, Hkv, g, Dh, scale = 29, 7, 2, 2, 3, 8, 0.25
+    Hq = Hkv * g
+    P = N + T
+    v0, planted = 3, 11
+    q = np.zeros((G, 1, Hq, Dh))
+    k = np.zeros((G, P, Hkv, Dh))
+    for l in range(G):
+        for kv in range(Hkv):
+            u = rng.standard_normal(Dh)
+            q[l, 0, kv * g:(kv + 1) * g] = u           # heads of one group share a query
+            k[l, v0 + planted, kv] = (delta / scale) * u / np.dot(u, u)
+    wl = _make_wl(q.astype(np.float32), k, [0, P], [v0], [0, N], Hq, Hkv, scale)
+    # the fp32 rounding of q and k moves the planted logit by ~1e-7 relative
+    qq = W.as_f32(wl.q, W.F32).astype(np.float64)
+    kk = W.as_f32(wl.k, W.F32).astype(np.float64)
+    w = _orc_scores(wl)
+    # exact expectation from the rounded inputs, per head (closed form per row)
+    s = np.zeros(N)
+    for l in range(G):
+        for h in range(Hq):
+            d = scale * np.dot(qq[l, 0, h], kk[l, v0 + planted, h // g])
+            e = math.exp(d)
+            row_vis = np.full(N, 1.0 / (P - 1 + e))
+            row_vis[planted] = e / (P - 1 + e)
+            s += row_vis
+    np.testing.assert_allclose(w, s / s.sum(), rtol=1e-13)
+    assert abs(w[planted] - math.exp(delta) / (N - 1 + math.exp(delta))) < 1e-5
+
+
+def test_scores_single_head_is_softmax_over_visual_logits():
+    """G = Hq = 1: the text mass cancels in Eq. 8, leaving softmax over the visual logits."""
+    wl = W.tiny(9, R=2, G=1, Hq=1, Hkv=1, Dh=16, n_range=(10, 30), t_range=(3, 9), qk_dtype=W.F32)
+    w = _orc_scores(wl)
+    q = W.as_f32(wl.q, W.F32).astype(np.float64)
+    k = W.as_f32(wl.k, W.F32).astype(np.float64)
+    for r in range(wl.R):
+        a = int(wl.cu_seqlens[r]) + int(wl.vis_start[r])
+        logits = wl.scale * k[0, a:a + wl.n(r), 0] @ q[0, r, 0]
+        np.testing.assert_allclose(w[wl.cu_vis[r]:wl.cu_vis[r + 1]], scipy.special.softmax(logits), rtol=1e-13)
+
+
+def test_scores_two_token_row_is_logistic():
+    """P = 2: the last row is (expit(l0 - l1), expit(l1 - l0))."""
+    q = np.array([[[[0.3, -1.2, 0.7, 2.0]]]])
+    k = np.array([[[[1.0, 0.5, -0.25, 0.125]]], [[[-2.0, 1.0, 0.5, 0.75]]]]).reshape(1, 2, 1, 4)
+    wl = _make_wl(q, k, [0, 2], [0], [0, 1], 1, 1, 0.5)
+    w, rows = _orc_scores(wl, want_rows=True)
+    qf = W.as_f32(wl.q, W.F32).astype(np.float64)[0, 0, 0]
+    kf = W.as_f32(wl.k, W.F32).astype(np.float64)[0, :, 0]
+    l0, l1 = 0.5 * kf[0] @ qf, 0.5 * kf[1] @ qf
+    np.testing.assert_allclose(rows[0, 0], [scipy.special.expit(l0 - l1), scipy.special.expit(l1 - l0)], rtol=1e-13)
+    assert w[0] == 1.0
+
+
+@pytest.mark.parametrize("c", [-80.0, 80.0])
+def test_scores_logit_shift_invariance(c):
+    """Adding c to every logit of a row (k_j += c q / (sigma |q|^2)) leaves w unchanged."""
+    wl = W.tiny(4, R=2, G=2, Hq=3, Hkv=3, Dh=8, n_range=(6, 20), t_range=(2, 8), qk_dtype=W.F32)
+    w0 = _orc_scores(wl)
+    k = W.as_f32(wl.k, W.F32).astype(np.float64).copy()
+    q = W.as_f32(wl.q, W.F32).astype(np.float64)
+    for l in range(wl.G):
+        for r in range(wl.R):
+            a, b = wl.cu_seqlens[r], wl.cu_seqlens[r + 1]
+            for h in range(wl.Hq):
+                u = q[l, r, h]
+                k[l, a:b, h] += c * u / (wl.scale * np.dot(u, u))
+    wl2 = _make_wl(wl.q, k, wl.cu_seqlens, wl.vis_start, wl.cu_vis, wl.Hq, wl.Hkv, wl.scale)
+    w1 = _orc_scores(wl2)
+    assert np.all(np.isfinite(w1))
+    np.testing.assert_allclose(w1, w0, rtol=2e-5)   # the shifted keys are rounded to fp32
+
+
+def test_scores_permuting_visual_keys_permutes_w():
+    wl = W.tiny(6, R=1, G=2, Hq=4, Hkv=2, Dh=8, n_range=(12, 12), t_range=(5, 5), qk_dtype=W.F32)
+    w0 = _orc_scores(wl)
+    perm = np.random.default_rng(0).permutation(12)
+    k = wl.k.copy()
+    v0 = int(wl.vis_start[0])
+    k[:, v0:v0 + 12] = wl.k[:, v0 + perm]
+    wl2 = _make_wl(wl.q, k, wl.cu_seqlens, wl.vis_start, wl.cu_vis, wl.Hq, wl.Hkv, wl.scale)
+    np.testing.assert_allclose(_orc_scores(wl2), w0[perm], rtol=1e-14)
+
+
+# ---------------------------------------------------------------- selection (Eq. 9-12)
+
+def _sel(w, X, K, mode=oracle.KCENTER, dtype=W.F32):
+    X = np.asarray(X)
+    N = X.shape[0]
+    return oracle.select(1, X.shape[1], np.asarray(w, np.float32), X, [0, N], [0, K],
+                         _fcode(dtype), mode=mode)
+
+
+def test_select_golden_cases():
+    for case in _load("select_four_tokens.json")["cases"]:
+        X = np.asarray(case["feats"], np.float32)
+        kept, order, gains = _sel(case["w"], X, case["K"])
+        assert list(order) == case["order"], case["name"]
+        assert list(kept) == case["kept"], case["name"]
+        np.testing.assert_allclose(gains, case["gains"], rtol=max(case["gain_rel_tol"], 1e-12), atol=1e-12)
+        kept, order, _ = _sel(case["w"], X, case["K"], mode=oracle.TOPK)
+        assert list(kept) == case["topk_kept"] and list(order) == case["topk_order"], case["name"]
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_select_matches_bruteforce(seed):
+    rng = np.random.default_rng(seed)
+    N = int(rng.integers(2, 64))
+    Dv = int(rng.choice([3, 8, 32]))
+    X = rng.standard_normal((N, Dv)).astype(np.float32)
+    distinct = N
+    if seed % 3 == 0:                               # some exact duplicates
+        X[N // 2:] = X[:N - N // 2]
+        distinct = N // 2
+    w = rng.dirichlet(np.ones(N)).astype(np.float32)
+    # beyond the distinct rows every objective is a rounding-level zero, where the
+    # two routes may legitimately differ; that regime is pinned by exact cases instead
+    K = int(rng.integers(1, max(1, distinct) + 1))
+    kept, order, gains = _sel(w, X, K)
+    ob, gb = brute.select(w, X, K)
+    assert list(order) == list(ob)
+    np.testing.assert_allclose(gains, gb, rtol=1e-12, atol=1e-15)
+    assert list(kept) == sorted(ob)
+
+
+def test_select_bf16_features_match_bruteforce():
+    wl = W.tiny(21, R=3, n_range=(20, 60), Dv=48, comps=5)
+    w = np.random.default_rng(0).dirichlet(np.ones(wl.N_total)).astype(np.float32)
+    kept, order, _ = oracle.select(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, oracle.BF16)
+    X = W.as_f32(wl.feats, W.BF16)
+    for r in range(wl.R):
+        a, b = wl.cu_vis[r], wl.cu_vis[r + 1]
+        ob, _ = brute.select(w[a:b], X[a:b], wl.kk(r))
+        assert list(order[wl.cu_keep[r]:wl.cu_keep[r + 1]]) == list(ob)
+
+
+def test_select_orthogonal_features_is_topk():
+    """One-hot features: every coverage distance is 1, so the greedy is top-K by w."""
+    rng = np.random.default_rng(3)
+    N = 40
+    X = np.eye(N, dtype=np.float32) * rng.uniform(0.5, 3.0, size=(N, 1)).astype(np.float32)
+    w = rng.dirichlet(np.ones(N)).astype(np.float32)
+    w[7] = w[19]                                        # an exact tie
+    K = 17
+    _, order, _ = _sel(w, X, K)
+    expect = np.argsort(-w.astype(np.float64), kind="stable")[:K]
+    assert list(order) == list(expect)
+
+
+def test_select_uniform_weights_is_farthest_point():
+    rng = np.random.default_rng(4)
+    X = rng.standard_normal((50, 6)).astype(np.float32)
+    w = np.full(50, 1.0 / 50, np.float32)
+    _, order, _ = _sel(w, X, 12)
+    assert list(order) == list(brute.gonzalez(X.astype(np.float64), 12))
+
+
+def test_select_identical_features():
+    """delta is 0 after the first pick, so the rest are the lowest remaining indices."""
+    rng = np.random.default_rng(5)
+    X = np.tile(rng.standard_normal((1, 9)).astype(np.float32), (30, 1))
+    w = rng.dirichlet(np.ones(30)).astype(np.float32)
+    K = 8
+    kept, order, gains = _sel(w, X, K)
+    j1 = int(np.argmax(w))
+    rest = [i for i in range(30) if i != j1][:K - 1]
+    assert list(order) == [j1] + rest
+    assert np.all(gains[1:] == 0.0)
+
+
+def test_select_orthogonal_clusters_one_pick_each():
+    """Exact-duplicate clusters on orthogonal axes: one pick per cluster while any is uncovered."""
+    rng = np.random.default_rng(6)
+    C, per = 6, 5
+    X = np.repeat(np.eye(C, 8, dtype=np.float32), per, axis=0) * 2.0
+    w = rng.dirichlet(np.ones(C * per)).astype(np.float32)
+    _, order, _ = _sel(w, X, C)
+    assert sorted(set(int(i) // per for i in order)) == list(range(C))
+    # and within each cluster, the pick is that cluster's most relevant token
+    for i in order:
+        c = int(i) // per
+        assert w[i] == w[c * per:(c + 1) * per].max()
+
+
+def test_select_k_equals_one_and_n():
+    rng = np.random.default_rng(7)
+    X = rng.standard_normal((25, 4)).astype(np.float32)
+    w = rng.dirichlet(np.ones(25)).astype(np.float32)
+    kept, order, _ = _sel(w, X, 1)
+    assert list(order) == [int(np.argmax(w))]
+    kept, order, _ = _sel(w, X, 25)
+    assert list(kept) == list(range(25)) and sorted(order) == list(range(25))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_select_invariants(seed):
+    wl = W.tiny(30 + seed, R=3, n_range=(30, 120), Dv=40, comps=6)
+    w = np.random.default_rng(seed).dirichlet(np.ones(wl.N_total)).astype(np.float32)
+    kept, order, gains = oracle.select(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, oracle.BF16)
+    for r in range(wl.R):
+        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
+        kr, orr, gr = kept[a:b], order[a:b], gains[a:b]
+        assert len(set(orr)) == wl.kk(r)
+        assert np.all(np.diff(kr) > 0) and kr[0] >= 0 and kr[-1] < wl.n(r)
+        assert sorted(orr) == list(kr)
+        wr = w[wl.cu_vis[r]:wl.cu_vis[r + 1]]
+        assert orr[0] == int(np.argmax(wr))
+        assert np.all(np.diff(gr[1:]) <= 0)          # objective never grows after t = 1
+
+
+def test_select_power_of_two_scaling_invariant():
+    wl = W.tiny(40, R=2, n_range=(40, 80), Dv=24, comps=5, f_dtype=W.F32)
+    w = np.random.default_rng(1).dirichlet(np.ones(wl.N_total)).astype(np.float32)
+    _, o0, _ = oracle.select(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, oracle.F32)
+    scale = (2.0 ** np.random.default_rng(2).integers(-6, 7, size=(wl.N_total, 1))).astype(np.float32)
+    _, o1, _ = oracle.select(wl.R, wl.Dv, w, wl.feats * scale, wl.cu_vis, wl.cu_keep, oracle.F32)
+    assert list(o0) == list(o1)
+
+
+def test_topk_is_stable_sort():
+    rng = np.random.default_rng(8)
+    N = 300
+    w = rng.integers(0, 40, size=N).astype(np.float32) / 40   # many ties
+    X = rng.standard_normal((N, 3)).astype(np.float32)
+    kept, order, gains = _sel(w, X, 77, mode=oracle.TOPK)
+    expect = np.argsort(-w.astype(np.float64), kind="stable")[:77]
+    assert list(order) == list(expect)
+    assert list(kept) == sorted(expect)
+    np.testing.assert_array_equal(gains, w[expect])
+
+
+# ---------------------------------------------------------------- replay, gather, budget
+
+def test_replay_classifies_steps():
+    wl = W.tiny(50, R=2, n_range=(30, 60), Dv=16, comps=4, k_frac=0.5)
+    w = np.random.default_rng(3).dirichlet(np.ones(wl.N_total)).astype(np.float32)
+    _, order, _ = oracle.select(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, oracle.BF16)
+    st, mg = oracle.replay(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, order, oracle.BF16)
+    assert np.all(st == 0) and np.all(mg == 0)
+    bad = order.copy()
+    t = int(wl.cu_keep[0]) + 3
+    bad[t], bad[t + 1] = bad[t + 1], bad[t]            # swap two distinct-valued picks
+    st, mg = oracle.replay(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, bad, oracle.BF16)
+    assert st[t] == 2 and mg[t] > 1e-6
+    dup = order.copy()
+    dup[t] = dup[t - 1]
+    st, _ = oracle.replay(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, dup, oracle.BF16)
+    assert np.all(st[t:wl.cu_keep[1]] == 2)
+
+
+def test_replay_excuses_near_ties():
+    X = np.eye(4, dtype=np.float32)
+    w = np.array([0.5, 0.25, 0.25 * (1 - 2 ** -22), 0.0], np.float32)   # 2.4e-7 relative gap
+    st, mg = oracle.replay(1, 4, w, X, [0, 4], [0, 3], np.array([0, 2, 1], np.int32), oracle.F32)
+    assert list(st) == [0, 1, 0] and 0 < mg[1] < 1e-6
+
+
+def test_gather_is_byte_copy():
+    rng = np.random.default_rng(9)
+    feats = rng.integers(0, 2 ** 16, size=(50, 7), dtype=np.uint16)   # includes NaN patterns
+    cu_vis = np.array([0, 20, 50], np.int32)
+    cu_keep = np.array([0, 4, 9], np.int32)
+    kept = np.array([1, 5, 6, 19, 0, 3, 4, 28, 29], np.int32)
+    out = oracle.gather(2, feats, cu_vis, kept, cu_keep)
+    expect = np.concatenate([feats[0:20][kept[:4]], feats[20:50][kept[4:]]])
+    assert out.tobytes() == expect.tobytes()
+
+
+def test_budget_golden_and_exact():
+    for n, num, den, k in _load("budgets.json")["cases"]:
+        assert oracle.budget(n, num, den) == k
+    for n in range(1, 300):
+        for num, den in [(1, 8), (3, 8), (5, 8), (1, 3), (7, 9)]:
+            assert oracle.budget(n, num, den) == math.ceil(Fraction(n * num, den))
+
+
+# ---------------------------------------------------------------- planted mistakes
+
+MUTANTS = {
+    # dropped term: the last layer is never summed (Eq. 7)
+    "drop_layer": ("for (int l = 0; l < G; ++l) {", "for (int l = 0; l < G - 1 + (G == 1); ++l) {"),
+    # wrong index: query head h reads KV head h % Hkv instead of h / g
+    "kv_index": ("const int kv = h / g;", "const int kv = h % Hkv;"),
+    # softmax over the visual span only instead of the whole row (Eq. 6)
+    "visual_softmax": ("for (int64_t j = 0; j < P; ++j) Z += exp(logit[j] - m);",
+                       "for (int64_t j = v0; j < v0 + N; ++j) Z += exp(logit[j] - m);"),
+    # wrong sign in the coverage distance (Eq. 10)
+    "cover_sign": ("const double t = 1.0 - dot / sqrt(f->nn[i] * f->nn[j]);",
+                   "const double t = 1.0 + dot / sqrt(f->nn[i] * f->nn[j]);"),
+    # unnormalised features in Eq. 10
+    "no_normalise": ("const double t = 1.0 - dot / sqrt(f->nn[i] * f->nn[j]);",
+                     "const double t = 1.0 - dot;"),
+    # ties broken towards the highest index
+    "tie_high": ("if (best < 0 || o[i] > o[best]) best = i;", "if (best < 0 || o[i] >= o[best]) best = i;"),
+    # additive instead of multiplicative objective (Eq. 11)
+    "additive": ("o[i] = (double)w[row0 + i] * delta[i];\n      }\n      /* Eq. 11 */",
+                 "o[i] = (double)w[row0 + i] + delta[i];\n      }\n      /* Eq. 11 */"),
+    # coverage from the first pick only (delta not folded with later picks)
+    "no_min": ("if (c < delta[i]) delta[i] = c;\n        o[i] = (double)w[row0 + i] * delta[i];\n      }\n      /* Eq. 11 */",
+               "if (t == 1) delta[i] = c;\n        o[i] = (double)w[row0 + i] * delta[i];\n      }\n      /* Eq. 11 */"),
+    # zero-norm rows treated as covered (delta 0) instead of cosine 0 (delta 1)
+    "zero_norm": ("if (f->nn[i] <= 0.0 || f->nn[j] <= 0.0) return 1.0;",
+                  "if (f->nn[i] <= 0.0 || f->nn[j] <= 0.0) return 0.0;"),
+    # kept indices left in pick order instead of ascending (Eq. 12)
+    "unsorted_kept": ("if (sel[i]) kept[out0 + c++] = (int32_t)i;",
+                      "if (sel[i]) { kept[out0 + c] = order[out0 + c]; ++c; }"),
+}
+
+
+def _build_mutant(tmp_path, name):
+    src = open(os.path.join(os.path.dirname(oracle.__file__), "oracle.c")).read()
+    old, new = MUTANTS[name]
+    assert src.count(old) == 1, f"mutation site for {name} not found exactly once"
+    d = tmp_path / name
+    d.mkdir()
+    (d / "oracle.c").write_text(src.replace(old, new))
+    subprocess.run(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-o", str(d / "liboracle.so"),
+                    str(d / "oracle.c"), "-lm"], check=True)
+    (d / "__init__.py").write_text(open(oracle.__file__).read())
+    return d
+
+
+def _pins_pass():
+    """Run the cheap pins against the currently bound oracle library; True if all pass."""
+    checks = [test_scores_golden_two_heads, lambda: test_scores_match_bruteforce(1),
+              lambda: test_scores_match_bruteforce(2), lambda: test_scores_planted_key_closed_form(3.0),
+              test_select_golden_cases, lambda: test_select_matches_bruteforce(0),
+              lambda: test_select_matches_bruteforce(5), test_select_orthogonal_features_is_topk,
+              test_select_uniform_weights_is_farthest_point, lambda: test_select_invariants(0)]
+    for c in checks:
+        try:
+            c()
+        except AssertionError:
+            return False
+    return True
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(tmp_path, name):
+    d = _build_mutant(tmp_path, name)
+    saved = oracle._lib
+    try:
+        oracle._lib = None
+        path = oracle.LIB_PATH
+        oracle.LIB_PATH = str(d / "liboracle.so")
+        oracle.lib()
+        assert not _pins_pass(), f"planted mistake {name} went unnoticed"
+    finally:
+        oracle.LIB_PATH = path
+        oracle._lib = saved
