@@ -1,0 +1,193 @@
+/*
+ * last.h -- C ABI of the MI355X (gfx950) LAST token-selection library.
+ *
+ * LAST (arXiv 2607.27952) prunes visual tokens before edge-to-cloud
+ * transmission. This library implements the data-parallel hot path:
+ *
+ *   last_token_scores  Sec. 3.3, Eq. 6-8: the attention row of the last query
+ *                      token against every key of the guidance model's prefill
+ *                      (softmax over the whole visual + text context), its
+ *                      visual columns summed over guidance layers and heads,
+ *                      normalised over the visual tokens.
+ *   diverse_select     Sec. 3.4, Eq. 9-12: importance-weighted greedy k-center
+ *                      over unit-normalised encoder features under a budget
+ *                      K = ceil(rho N) (Eq. 2); or the Top-k ablation of
+ *                      Sec. 4.3, Table 5. Kept indices come out ascending.
+ *   gather_kept        Sec. 3.4, Eq. 12: the kept rows X_S, in original order,
+ *                      copied byte for byte for transmission.
+ *
+ * Conventions shared by every call
+ *   - Pointers without a suffix are device pointers; pointers suffixed _h are
+ *     host copies of the same small arrays, used for validation and launch
+ *     planning. Each _h array must hold exactly what its device twin holds.
+ *   - The caller owns every buffer, including the workspace (size it with the
+ *     matching *_workspace query). The library never allocates device memory,
+ *     never synchronises, and only enqueues work on `stream` (a hipStream_t;
+ *     NULL is the default stream).
+ *   - Every argument is validated on the host, from the _h copies, before any
+ *     HIP call. On error nothing is enqueued, outputs are left untouched, and
+ *     a non-zero last_status is returned. A failed kernel launch returns
+ *     LAST_ERR_DEVICE (possibly after earlier kernels of the same call have
+ *     been enqueued).
+ *   - Ragged batches of R requests are packed with CSR offsets (int32, length
+ *     R+1, starting at 0, non-decreasing). Indices into a request's visual
+ *     tokens are request-local int32 in [0, N_r).
+ *   - Results are deterministic: the same inputs give bitwise-identical
+ *     outputs on every run (fixed reduction orders, ties to the lowest index).
+ *   - Calls on different streams are independent if their workspaces and
+ *     outputs do not overlap.
+ */
+#ifndef LAST_H
+#define LAST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LAST_OK = 0,
+  LAST_ERR_INVALID = 1,     /* malformed arguments (shapes, CSR, budgets, NULLs) */
+  LAST_ERR_UNSUPPORTED = 2, /* valid but outside what the kernels implement */
+  LAST_ERR_WORKSPACE = 3,   /* workspace pointer NULL or smaller than required */
+  LAST_ERR_DEVICE = 4       /* a HIP call failed; see last_status_string */
+} last_status;
+
+typedef enum { LAST_F32 = 0, LAST_BF16 = 1 } last_dtype;
+
+typedef enum {
+  LAST_SEL_KCENTER = 0, /* Eq. 9-11: greedy argmax of w_i * delta_i */
+  LAST_SEL_TOPK = 1     /* Table 5 "LAST (Top-k)": the K largest w_i */
+} last_sel_mode;
+
+/*
+ * Batch description for last_token_scores.
+ *   R          number of requests (>= 1)
+ *   G          guidance layers whose rows are summed (Eq. 7 sums over layers;
+ *              any subset of a model's layers can be passed, G >= 1)
+ *   Hq, Hkv    query and key heads; Hq % Hkv == 0. Query head h reads KV head
+ *              h / (Hq / Hkv) (grouped-query attention). Eq. 7 sums over all
+ *              Hq query heads.
+ *   Dh         head dimension, 64 or 128 (others: LAST_ERR_UNSUPPORTED)
+ *   qk_dtype   storage type of q and k (LAST_F32 or LAST_BF16)
+ *   softmax_scale  sigma in softmax(sigma q.k); <= 0 selects 1/sqrt(Dh)
+ *   cu_seqlens [R+1] token offsets into k; P_r = cu_seqlens[r+1]-cu_seqlens[r]
+ *              is the prefill length of request r (>= 2). Its last token,
+ *              position P_r - 1, is the query token whose row is scored.
+ *   vis_start  [R] start of request r's visual span within its sequence
+ *   cu_vis     [R+1] offsets into scores (and into the features given to
+ *              diverse_select); N_r = cu_vis[r+1]-cu_vis[r] >= 1 visual tokens
+ *              occupy positions [vis_start[r], vis_start[r] + N_r), which must
+ *              end before the last token: vis_start[r] + N_r <= P_r - 1.
+ */
+typedef struct last_batch {
+  int32_t R, G, Hq, Hkv, Dh;
+  last_dtype qk_dtype;
+  float softmax_scale;
+  const int32_t *cu_seqlens, *cu_seqlens_h;
+  const int32_t *vis_start, *vis_start_h;
+  const int32_t *cu_vis, *cu_vis_h;
+} last_batch;
+
+/* Workspace bytes last_token_scores needs for this batch (0 if invalid). */
+size_t last_token_scores_workspace(const last_batch *b);
+
+/*
+ * Sec. 3.3, Eq. 6-8.
+ *   q          [G][R][Hq][Dh] the last query token of each request, per layer
+ *              (after rotary embedding, as the attention sees it)
+ *   k          [G][T_total][Hkv][Dh] keys of every prefill token (after rotary
+ *              embedding), T_total = cu_seqlens[R]
+ *   scores     [N_total] out: w~ per visual token; each request's entries are
+ *              >= 0 and sum to 1 (Eq. 8)
+ *   attn_rows  optional [G][Hq][T_total] out (NULL to skip): the full softmax
+ *              rows A^(l,h)[p*, :] of every request, for inspection
+ *   ws         device workspace of at least last_token_scores_workspace(b)
+ *              bytes, 256-byte aligned
+ */
+last_status last_token_scores(const last_batch *b, const void *q, const void *k,
+                              float *scores, float *attn_rows, void *ws,
+                              size_t ws_bytes, void *stream);
+
+/* Workspace bytes diverse_select needs (0 if the arguments are invalid). */
+size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,
+                                last_dtype fdtype, last_sel_mode mode);
+
+/*
+ * Sec. 3.4, Eq. 9-12 (mode LAST_SEL_KCENTER) or Sec. 4.3, Table 5
+ * (mode LAST_SEL_TOPK).
+ *   scores     [N_total] non-negative, finite fp32 relevance per visual token
+ *              (normally the output of last_token_scores; any source works;
+ *              negative or NaN entries are treated as 0)
+ *   feats      [N_total][Dv] encoder features X of the visual tokens,
+ *              row-major, fdtype (LAST_F32 or LAST_BF16); 1 <= Dv <= 65536
+ *   cu_vis     [R+1] as in last_batch; N_r <= 16384 per request
+ *   cu_keep    [R+1] budgets: K_r = cu_keep[r+1]-cu_keep[r], 1 <= K_r <= N_r
+ *              (use last_budget for K = ceil(rho N), Eq. 2)
+ *   kept       [K_total] out: the selected request-local indices, ascending
+ *              within each request (Eq. 12)
+ *   order      optional [K_total] out: the pick sequence j_1..j_K (k-center),
+ *              or the kept indices by decreasing score (Top-k)
+ *   gains      optional [K_total] out: w_j1 at t = 1 and w_jt * delta_jt at
+ *              t >= 2 (k-center), or the scores in pick order (Top-k)
+ * Ties in every argmax go to the lowest index. The coverage distance of
+ * Eq. 10 is 1 - cos clamped at 0; a zero-norm feature has cosine 0 with
+ * every token; bitwise-identical features are at distance exactly 0.
+ */
+last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype,
+                           last_sel_mode mode, const float *scores,
+                           const void *feats, const int32_t *cu_vis,
+                           const int32_t *cu_vis_h, const int32_t *cu_keep,
+                           const int32_t *cu_keep_h, int32_t *kept,
+                           int32_t *order, float *gains, void *ws,
+                           size_t ws_bytes, void *stream);
+
+/*
+ * Sec. 3.4, Eq. 12: out[t] = feats[cu_vis[r] + kept[t]] for every kept slot
+ * t of request r, copied byte for byte (row_bytes = Dv * elem_bytes).
+ *   kept       [K_total] request-local indices (e.g. from diverse_select);
+ *              an index outside [0, N_r) yields a zero-filled row
+ *   out        [K_total][Dv] out, same element type as feats
+ */
+last_status gather_kept(int32_t R, int32_t Dv, size_t elem_bytes,
+                        const void *feats, const int32_t *cu_vis,
+                        const int32_t *cu_vis_h, const int32_t *kept,
+                        const int32_t *cu_keep, const int32_t *cu_keep_h,
+                        void *out, void *stream);
+
+/* Sec. 3.2, Eq. 2: K = ceil(N * rho_num / rho_den), integer-exact, clamped
+ * to [1, N]; returns -1 for N < 1 or a ratio outside (0, 1]. */
+int32_t last_budget(int32_t N, int32_t rho_num, int32_t rho_den);
+
+/* Human-readable text for a status (static storage). For LAST_ERR_DEVICE it
+ * includes the most recent HIP error message seen by this thread. */
+const char *last_status_string(last_status s);
+
+/* Library version, as major * 10000 + minor * 100 + patch. */
+int32_t last_version(void);
+
+/*
+ * Optional per-kernel timing, for benchmarking. While enabled, every kernel
+ * the library launches is bracketed by a pair of HIP events on its stream
+ * (event creation happens on first use; no device memory is allocated).
+ * After the caller has synchronised the streams, last_profile_collect()
+ * folds the finished pairs into per-kernel totals, which
+ * last_profile_kernel() reports. Process-wide state, not thread-safe; off by
+ * default. Event pairs beyond the internal pool of 8192 are not recorded.
+ */
+last_status last_profile_enable(int32_t on);
+last_status last_profile_collect(void);
+void last_profile_reset(void);
+int32_t last_profile_count(void);
+/* i-th kernel's name, launch count and total milliseconds; returns 0 if
+ * there is no such entry. */
+int32_t last_profile_kernel(int32_t i, const char **name, int64_t *launches,
+                            double *total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAST_H */

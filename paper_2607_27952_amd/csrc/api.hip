@@ -1,0 +1,303 @@
+// C ABI of liblast: argument validation on the host, workspace sizing, and the
+// launch sequences of the three calls declared in include/last.h. Also the
+// status strings and the optional per-kernel event timing.
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "last_internal.h"
+
+namespace last {
+
+int score_max_pairs();
+
+// ------------------------------------------------------------ diagnostics
+static thread_local char g_err[256] = "";
+
+void note_hip_error(hipError_t e) {
+  snprintf(g_err, sizeof g_err, "%s (%d)", hipGetErrorString(e), (int)e);
+}
+
+namespace {
+struct Pending {
+  int kernel;
+  hipEvent_t start, stop;
+};
+struct Totals {
+  std::string name;
+  int64_t launches = 0;
+  double ms = 0.0;
+};
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> free_events;
+  std::vector<Pending> pending;
+  std::vector<Totals> totals;
+  int created = 0;
+  Pending open{-1, nullptr, nullptr};
+};
+Profiler &prof() {
+  static Profiler p;
+  return p;
+}
+constexpr int kMaxEventPairs = 8192;
+
+hipEvent_t take_event() {
+  Profiler &p = prof();
+  if (!p.free_events.empty()) {
+    hipEvent_t e = p.free_events.back();
+    p.free_events.pop_back();
+    return e;
+  }
+  if (p.created >= 2 * kMaxEventPairs) return nullptr;
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  ++p.created;
+  return e;
+}
+
+int kernel_id(const char *name) {
+  Profiler &p = prof();
+  for (size_t i = 0; i < p.totals.size(); ++i)
+    if (p.totals[i].name == name) return (int)i;
+  p.totals.push_back(Totals{name, 0, 0.0});
+  return (int)p.totals.size() - 1;
+}
+}  // namespace
+
+void launch_begin(const char *name, hipStream_t s) {
+  Profiler &p = prof();
+  p.open = Pending{-1, nullptr, nullptr};
+  if (!p.on) return;
+  hipEvent_t a = take_event(), b = take_event();
+  if (!a || !b) {
+    if (a) p.free_events.push_back(a);
+    if (b) p.free_events.push_back(b);
+    return;
+  }
+  if (hipEventRecord(a, s) != hipSuccess) {
+    p.free_events.push_back(a);
+    p.free_events.push_back(b);
+    return;
+  }
+  p.open = Pending{kernel_id(name), a, b};
+}
+
+hipError_t launch_end(hipStream_t s) {
+  hipError_t e = hipGetLastError();
+  Profiler &p = prof();
+  if (p.open.kernel >= 0) {
+    if (hipEventRecord(p.open.stop, s) == hipSuccess) {
+      p.pending.push_back(p.open);
+    } else {
+      p.free_events.push_back(p.open.start);
+      p.free_events.push_back(p.open.stop);
+    }
+    p.open = Pending{-1, nullptr, nullptr};
+  }
+  if (e != hipSuccess) note_hip_error(e);
+  return e;
+}
+
+// ------------------------------------------------------------ validation
+static bool csr_ok(const int32_t *cu, int32_t R, int32_t min_len) {
+  if (!cu || cu[0] != 0) return false;
+  for (int32_t r = 0; r < R; ++r)
+    if ((int64_t)cu[r + 1] - cu[r] < min_len) return false;
+  return true;
+}
+
+static last_status check_batch(const last_batch *b) {
+  if (!b) return LAST_ERR_INVALID;
+  if (b->R < 1 || b->G < 1 || b->Hq < 1 || b->Hkv < 1 || b->Dh < 1) return LAST_ERR_INVALID;
+  if (b->Hq % b->Hkv != 0) return LAST_ERR_INVALID;
+  if (b->qk_dtype != LAST_F32 && b->qk_dtype != LAST_BF16) return LAST_ERR_INVALID;
+  if (!isfinite(b->softmax_scale)) return LAST_ERR_INVALID;
+  if (!b->cu_seqlens || !b->vis_start || !b->cu_vis) return LAST_ERR_INVALID;
+  if (!csr_ok(b->cu_seqlens_h, b->R, 2) || !csr_ok(b->cu_vis_h, b->R, 1) || !b->vis_start_h)
+    return LAST_ERR_INVALID;
+  for (int32_t r = 0; r < b->R; ++r) {
+    const int64_t P = (int64_t)b->cu_seqlens_h[r + 1] - b->cu_seqlens_h[r];
+    const int64_t N = (int64_t)b->cu_vis_h[r + 1] - b->cu_vis_h[r];
+    const int64_t v = b->vis_start_h[r];
+    if (v < 0 || v + N > P - 1) return LAST_ERR_INVALID;
+  }
+  if (b->Dh != 64 && b->Dh != 128) return LAST_ERR_UNSUPPORTED;
+  if ((int64_t)b->G * b->Hq > score_max_pairs()) return LAST_ERR_UNSUPPORTED;
+  return LAST_OK;
+}
+
+static last_status check_select(int32_t R, const int32_t *cu_vis_h, int32_t Dv, last_dtype fdtype,
+                                last_sel_mode mode, const int32_t *cu_keep_h) {
+  if (R < 1 || Dv < 1 || Dv > 65536) return LAST_ERR_INVALID;
+  if (fdtype != LAST_F32 && fdtype != LAST_BF16) return LAST_ERR_INVALID;
+  if (mode != LAST_SEL_KCENTER && mode != LAST_SEL_TOPK) return LAST_ERR_INVALID;
+  if (!csr_ok(cu_vis_h, R, 1)) return LAST_ERR_INVALID;
+  if (cu_keep_h) {
+    if (!csr_ok(cu_keep_h, R, 1)) return LAST_ERR_INVALID;
+    for (int32_t r = 0; r < R; ++r)
+      if (cu_keep_h[r + 1] - cu_keep_h[r] > cu_vis_h[r + 1] - cu_vis_h[r]) return LAST_ERR_INVALID;
+  }
+  for (int32_t r = 0; r < R; ++r)
+    if (cu_vis_h[r + 1] - cu_vis_h[r] > kSelMaxN) return LAST_ERR_UNSUPPORTED;
+  if (mode == LAST_SEL_KCENTER && Dv % (fdtype == LAST_BF16 ? 8 : 4) != 0) return LAST_ERR_UNSUPPORTED;
+  return LAST_OK;
+}
+
+static bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+}  // namespace last
+
+using namespace last;
+
+extern "C" {
+
+size_t last_token_scores_workspace(const last_batch *b) {
+  if (check_batch(b) != LAST_OK) return 0;
+  const ScorePlan p = make_score_plan(b);
+  size_t bytes = 0;
+  carve_score_ws(nullptr, b, p, &bytes);
+  return bytes;
+}
+
+last_status last_token_scores(const last_batch *b, const void *q, const void *k, float *scores,
+                              float *attn_rows, void *ws, size_t ws_bytes, void *stream) {
+  last_status st = check_batch(b);
+  if (st != LAST_OK) return st;
+  if (!q || !k || !scores) return LAST_ERR_INVALID;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(scores, 4) || (attn_rows && !aligned(attn_rows, 4)))
+    return LAST_ERR_INVALID;
+  const ScorePlan p = make_score_plan(b);
+  size_t need = 0;
+  carve_score_ws(nullptr, b, p, &need);
+  if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
+  const ScoreWs w = carve_score_ws(ws, b, p, &need);
+  const float scale = b->softmax_scale > 0.f ? b->softmax_scale : 1.0f / sqrtf((float)b->Dh);
+  const hipError_t e = launch_scores(b, p, w, q, k, scores, attn_rows, scale, (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv, last_dtype fdtype,
+                                last_sel_mode mode) {
+  if (check_select(R, cu_vis_h, Dv, fdtype, mode, nullptr) != LAST_OK) return 0;
+  // The budgets do not change the workspace; size the scratch order/gains for K_r = N_r.
+  std::vector<int32_t> cu_keep(cu_vis_h, cu_vis_h + R + 1);
+  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_keep.data(), mode);
+  size_t bytes = 0;
+  carve_select_ws(nullptr, R, p, mode, &bytes);
+  // scratch for the pick order and gains when the caller does not want them
+  bytes += align_up((size_t)p.N_total * sizeof(int32_t), 256) + align_up((size_t)p.N_total * sizeof(float), 256);
+  return bytes;
+}
+
+last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode mode,
+                           const float *scores, const void *feats, const int32_t *cu_vis,
+                           const int32_t *cu_vis_h, const int32_t *cu_keep, const int32_t *cu_keep_h,
+                           int32_t *kept, int32_t *order, float *gains, void *ws, size_t ws_bytes,
+                           void *stream) {
+  if (!cu_keep_h) return LAST_ERR_INVALID;
+  last_status st = check_select(R, cu_vis_h, Dv, fdtype, mode, cu_keep_h);
+  if (st != LAST_OK) return st;
+  if (!scores || !feats || !cu_vis || !cu_keep || !kept) return LAST_ERR_INVALID;
+  if (!aligned(feats, 16)) return LAST_ERR_INVALID;
+  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_keep_h, mode);
+  size_t need = diverse_select_workspace(R, cu_vis_h, Dv, fdtype, mode);
+  if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
+  size_t used = 0;
+  const SelectWs w = carve_select_ws(ws, R, p, mode, &used);
+  char *tail = static_cast<char *>(ws) + used;
+  int32_t *order_ws = reinterpret_cast<int32_t *>(tail);
+  float *gains_ws = reinterpret_cast<float *>(tail + align_up((size_t)p.N_total * sizeof(int32_t), 256));
+  const hipError_t e = launch_select(R, Dv, fdtype, mode, p, w, scores, feats, cu_vis, cu_keep, kept,
+                                     order ? order : order_ws, gains ? gains : gains_ws,
+                                     (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+last_status gather_kept(int32_t R, int32_t Dv, size_t elem_bytes, const void *feats,
+                        const int32_t *cu_vis, const int32_t *cu_vis_h, const int32_t *kept,
+                        const int32_t *cu_keep, const int32_t *cu_keep_h, void *out, void *stream) {
+  if (R < 1 || Dv < 1 || Dv > 65536) return LAST_ERR_INVALID;
+  if (elem_bytes != 1 && elem_bytes != 2 && elem_bytes != 4 && elem_bytes != 8) return LAST_ERR_INVALID;
+  if (!csr_ok(cu_vis_h, R, 0) || !csr_ok(cu_keep_h, R, 0)) return LAST_ERR_INVALID;
+  if (!cu_vis || !cu_keep) return LAST_ERR_INVALID;
+  const int64_t K_total = cu_keep_h[R];
+  if (K_total > 0 && (!feats || !kept || !out)) return LAST_ERR_INVALID;
+  const hipError_t e = launch_gather(R, (int64_t)Dv * (int64_t)elem_bytes, K_total, cu_vis_h[R],
+                                     feats, cu_vis, kept, cu_keep, out, (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+int32_t last_budget(int32_t N, int32_t rho_num, int32_t rho_den) {
+  if (N < 1 || rho_num < 1 || rho_den < 1 || rho_num > rho_den) return -1;
+  int64_t k = ((int64_t)N * rho_num + rho_den - 1) / rho_den;
+  if (k < 1) k = 1;
+  if (k > N) k = N;
+  return (int32_t)k;
+}
+
+const char *last_status_string(last_status s) {
+  static thread_local char buf[320];
+  switch (s) {
+    case LAST_OK: return "ok";
+    case LAST_ERR_INVALID: return "invalid argument";
+    case LAST_ERR_UNSUPPORTED: return "unsupported configuration";
+    case LAST_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case LAST_ERR_DEVICE:
+      snprintf(buf, sizeof buf, "device error: %s", g_err[0] ? g_err : "unknown");
+      return buf;
+  }
+  return "unknown status";
+}
+
+int32_t last_version(void) { return 100; }
+
+last_status last_profile_enable(int32_t on) {
+  prof().on = on != 0;
+  return LAST_OK;
+}
+
+last_status last_profile_collect(void) {
+  Profiler &p = prof();
+  std::vector<Pending> keep;
+  for (const Pending &x : p.pending) {
+    float ms = 0.f;
+    const hipError_t e = hipEventElapsedTime(&ms, x.start, x.stop);
+    if (e == hipErrorNotReady) {
+      keep.push_back(x);
+      continue;
+    }
+    if (e == hipSuccess) {
+      p.totals[x.kernel].launches += 1;
+      p.totals[x.kernel].ms += ms;
+    }
+    p.free_events.push_back(x.start);
+    p.free_events.push_back(x.stop);
+  }
+  p.pending.swap(keep);
+  return p.pending.empty() ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+void last_profile_reset(void) {
+  Profiler &p = prof();
+  for (Totals &t : p.totals) {
+    t.launches = 0;
+    t.ms = 0.0;
+  }
+}
+
+int32_t last_profile_count(void) { return (int32_t)prof().totals.size(); }
+
+int32_t last_profile_kernel(int32_t i, const char **name, int64_t *launches, double *total_ms) {
+  Profiler &p = prof();
+  if (i < 0 || i >= (int32_t)p.totals.size()) return 0;
+  if (name) *name = p.totals[i].name.c_str();
+  if (launches) *launches = p.totals[i].launches;
+  if (total_ms) *total_ms = p.totals[i].ms;
+  return 1;
+}
+
+}  // extern "C"

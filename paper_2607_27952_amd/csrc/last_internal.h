@@ -1,0 +1,138 @@
+// Internal declarations of liblast: device helpers, launch bookkeeping and
+// the kernel launchers each source file provides to the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "last.h"
+
+namespace last {
+
+// ----------------------------------------------------------------- host side
+
+// Every launch goes through launch_begin / launch_end so that optional
+// per-kernel event timing can bracket it; launch_end also checks the launch.
+void launch_begin(const char *name, hipStream_t s);
+hipError_t launch_end(hipStream_t s);
+
+// Remember the last HIP error text for last_status_string (thread-local).
+void note_hip_error(hipError_t e);
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Workspace carving: consecutive 256-byte aligned segments.
+struct Carver {
+  char *base;
+  size_t off = 0;
+  explicit Carver(void *b) : base(static_cast<char *>(b)) {}
+  template <typename T>
+  T *take(size_t count) {
+    off = align_up(off, 256);
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+  size_t size() const { return align_up(off, 256); }
+};
+
+// ------------------------------------------------------------ score pass
+struct ScorePlan {
+  int32_t chunk_tokens;   // tokens per work chunk
+  int32_t head_groups;    // query-head groups per KV head (g split in <= 8)
+  int32_t g_max;          // heads per group template: 1, 2, 4 or 8
+  int64_t C_total;        // chunks over all requests
+  int64_t S_total;        // finalize slices over all requests
+  int32_t slice_tokens;   // visual tokens per finalize block
+  int64_t T_total, N_total;
+};
+
+struct ScoreWs {
+  int32_t *chunk_off, *chunk_req, *slice_off, *slice_req;
+  float4 *stats;  // [G][Hq][C_total] (chunk max, sum exp, visual sum exp, 0)
+  float *vlog;    // [G][Hq][N_total] scaled logits of visual columns
+};
+
+ScorePlan make_score_plan(const last_batch *b);
+ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t *bytes);
+hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
+                         const void *q, const void *k, float *scores, float *attn_rows,
+                         float scale, hipStream_t s);
+
+// ------------------------------------------------------------ selection
+constexpr int kGramTile = 128;       // Gram tile edge (rows of X per side)
+constexpr int kSelMaxN = 16384;      // largest request the register-resident greedy holds
+
+struct SelectPlan {
+  int64_t N_total, K_total;
+  int32_t N_max, K_max;
+  int64_t tiles_total;     // upper-triangular Gram tiles over all requests
+  int64_t d_elems;         // sum of N_r^2 (coverage matrices)
+  int32_t threads, ept;    // greedy / top-k block shape
+};
+
+struct SelectWs {
+  int32_t *tile_off, *tile_req;  // Gram tile prefix per request, tile -> request
+  int64_t *d_off;                // [R+1] element offsets of each request's N_r x N_r block
+  double *nn;                    // [N_total] squared feature norms
+  float *dmat;                   // coverage distances, sum N_r^2
+};
+
+SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,
+                            last_sel_mode mode);
+SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode mode,
+                         size_t *bytes);
+hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode mode,
+                         const SelectPlan &p, const SelectWs &w, const float *scores,
+                         const void *feats, const int32_t *cu_vis, const int32_t *cu_keep,
+                         int32_t *kept, int32_t *order, float *gains, hipStream_t s);
+
+// ------------------------------------------------------------ gather
+hipError_t launch_gather(int32_t R, int64_t row_bytes, int64_t K_total, int64_t N_total,
+                         const void *feats, const int32_t *cu_vis, const int32_t *kept,
+                         const int32_t *cu_keep, void *out, hipStream_t s);
+
+}  // namespace last
+
+// ----------------------------------------------------------------- device side
+namespace last_dev {
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// DPP lane permutations within rows of 16 lanes.
+__device__ __forceinline__ float dpp_xor1(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float dpp_xor2(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float dpp_half_mirror(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+}
+// Sum over each aligned group of 8 lanes; every lane of the group gets the total.
+__device__ __forceinline__ float sum8(float v) {
+  v += dpp_xor1(v);
+  v += dpp_xor2(v);
+  v += dpp_half_mirror(v);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+  return v;
+}
+__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
+  for (int m = 32; m >= 1; m >>= 1) {
+    unsigned long long o = __shfl_xor(v, m);
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+}  // namespace last_dev

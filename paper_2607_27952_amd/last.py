@@ -1,0 +1,303 @@
+"""ctypes binding over liblast.so (include/last.h). Argument marshalling only:
+every step of the path runs in the library's HIP kernels; PyTorch provides
+device memory and the current stream.
+
+The library must be built (``python -m paper_2607_27952_amd._build`` or
+``__graft_entry__.build()``); loading fails loudly if it is missing.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+import torch  # imported before the library so that both share torch's HIP runtime
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "liblast.so")
+
+LAST_OK, LAST_ERR_INVALID, LAST_ERR_UNSUPPORTED, LAST_ERR_WORKSPACE, LAST_ERR_DEVICE = range(5)
+LAST_F32, LAST_BF16 = 0, 1
+KCENTER, TOPK = 0, 1
+
+EXPORTS = ("last_token_scores_workspace", "last_token_scores", "diverse_select_workspace",
+           "diverse_select", "gather_kept", "last_budget", "last_status_string", "last_version",
+           "last_profile_enable", "last_profile_collect", "last_profile_reset",
+           "last_profile_count", "last_profile_kernel")
+
+
+class LastError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+
+
+class _Batch(ctypes.Structure):
+    _fields_ = [("R", ctypes.c_int32), ("G", ctypes.c_int32), ("Hq", ctypes.c_int32),
+                ("Hkv", ctypes.c_int32), ("Dh", ctypes.c_int32), ("qk_dtype", ctypes.c_int32),
+                ("softmax_scale", ctypes.c_float),
+                ("cu_seqlens", ctypes.c_void_p), ("cu_seqlens_h", ctypes.c_void_p),
+                ("vis_start", ctypes.c_void_p), ("vis_start_h", ctypes.c_void_p),
+                ("cu_vis", ctypes.c_void_p), ("cu_vis_h", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """Load liblast.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "or python -m paper_2607_27952_amd._build")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.last_token_scores_workspace.argtypes = [ctypes.POINTER(_Batch)]
+        L.last_token_scores_workspace.restype = SZ
+        L.last_token_scores.argtypes = [ctypes.POINTER(_Batch), P, P, P, P, P, SZ, P]
+        L.last_token_scores.restype = I32
+        L.diverse_select_workspace.argtypes = [I32, P, I32, I32, I32]
+        L.diverse_select_workspace.restype = SZ
+        L.diverse_select.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
+        L.diverse_select.restype = I32
+        L.gather_kept.argtypes = [I32, I32, SZ, P, P, P, P, P, P, P, P]
+        L.gather_kept.restype = I32
+        L.last_budget.argtypes = [I32, I32, I32]
+        L.last_budget.restype = I32
+        L.last_status_string.argtypes = [I32]
+        L.last_status_string.restype = ctypes.c_char_p
+        L.last_version.argtypes = []
+        L.last_version.restype = I32
+        L.last_profile_enable.argtypes = [I32]
+        L.last_profile_enable.restype = I32
+        L.last_profile_collect.argtypes = []
+        L.last_profile_collect.restype = I32
+        L.last_profile_reset.argtypes = []
+        L.last_profile_reset.restype = None
+        L.last_profile_count.argtypes = []
+        L.last_profile_count.restype = I32
+        L.last_profile_kernel.argtypes = [I32, ctypes.POINTER(ctypes.c_char_p),
+                                          ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)]
+        L.last_profile_kernel.restype = I32
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().last_status_string(int(status)).decode()
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return LAST_BF16
+    if t.dtype == torch.float32:
+        return LAST_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; expected bfloat16 or float32")
+
+
+def _i32_host(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _i32_dev(a: np.ndarray, device) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int32)).to(device)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator hands out 512-byte aligned blocks
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class Batch:
+    """A ragged batch of requests: host and device copies of the CSR arrays."""
+    R: int
+    G: int
+    Hq: int
+    Hkv: int
+    Dh: int
+    scale: float
+    cu_seqlens_h: np.ndarray
+    vis_start_h: np.ndarray
+    cu_vis_h: np.ndarray
+    cu_seqlens: torch.Tensor
+    vis_start: torch.Tensor
+    cu_vis: torch.Tensor
+
+    @staticmethod
+    def make(G, Hq, Hkv, Dh, cu_seqlens, vis_start, cu_vis, scale=0.0, device="cuda"):
+        cs, vs, cv = _i32_host(cu_seqlens), _i32_host(vis_start), _i32_host(cu_vis)
+        return Batch(R=len(cs) - 1, G=G, Hq=Hq, Hkv=Hkv, Dh=Dh, scale=float(scale),
+                     cu_seqlens_h=cs, vis_start_h=vs, cu_vis_h=cv, cu_seqlens=_i32_dev(cs, device),
+                     vis_start=_i32_dev(vs, device), cu_vis=_i32_dev(cv, device))
+
+    def struct(self, qk_dtype: int) -> _Batch:
+        return _Batch(self.R, self.G, self.Hq, self.Hkv, self.Dh, qk_dtype, self.scale,
+                      _ptr(self.cu_seqlens), _ptr(self.cu_seqlens_h), _ptr(self.vis_start),
+                      _ptr(self.vis_start_h), _ptr(self.cu_vis), _ptr(self.cu_vis_h))
+
+    @property
+    def T_total(self) -> int:
+        return int(self.cu_seqlens_h[-1])
+
+    @property
+    def N_total(self) -> int:
+        return int(self.cu_vis_h[-1])
+
+
+def token_scores_workspace(batch: Batch, qk_dtype=torch.bfloat16) -> int:
+    code = LAST_BF16 if qk_dtype == torch.bfloat16 else LAST_F32
+    b = batch.struct(code)
+    return int(lib().last_token_scores_workspace(ctypes.byref(b)))
+
+
+def token_scores(batch: Batch, q: torch.Tensor, k: torch.Tensor, scores=None, attn_rows=None,
+                 want_rows=False, ws=None, stream=None):
+    """last_token_scores (Eq. 6-8): returns scores [N_total] fp32 (and rows if asked)."""
+    code = _dtype_code(q)
+    if k.dtype != q.dtype:
+        raise TypeError("q and k must share a dtype")
+    b = batch.struct(code)
+    if scores is None:
+        scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
+    if want_rows and attn_rows is None:
+        attn_rows = torch.empty((batch.G, batch.Hq, batch.T_total), dtype=torch.float32, device=q.device)
+    need = int(lib().last_token_scores_workspace(ctypes.byref(b)))
+    if ws is None:
+        ws = _workspace(need, q.device)
+    st = lib().last_token_scores(ctypes.byref(b), _ptr(q), _ptr(k), _ptr(scores), _ptr(attn_rows),
+                                 _ptr(ws), ws.numel(), _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "last_token_scores")
+    return (scores, attn_rows) if want_rows else scores
+
+
+def select_workspace(cu_vis_h, Dv: int, f_dtype=torch.bfloat16, mode: int = KCENTER) -> int:
+    cv = _i32_host(cu_vis_h)
+    code = LAST_BF16 if f_dtype == torch.bfloat16 else LAST_F32
+    return int(lib().diverse_select_workspace(len(cv) - 1, _ptr(cv), Dv, code, mode))
+
+
+def diverse_select(scores: torch.Tensor, feats: torch.Tensor, cu_vis_h, cu_keep_h, cu_vis=None,
+                   cu_keep=None, mode: int = KCENTER, kept=None, order=None, gains=None,
+                   want_order=True, ws=None, stream=None):
+    """diverse_select (Eq. 9-12 or the Top-k ablation): returns (kept, order, gains)."""
+    dev = feats.device
+    cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
+    R = len(cv) - 1
+    Dv = feats.shape[-1]
+    code = _dtype_code(feats)
+    if cu_vis is None:
+        cu_vis = _i32_dev(cv, dev)
+    if cu_keep is None:
+        cu_keep = _i32_dev(ck, dev)
+    Kt = int(ck[-1])
+    if kept is None:
+        kept = torch.empty(Kt, dtype=torch.int32, device=dev)
+    if want_order and order is None:
+        order = torch.empty(Kt, dtype=torch.int32, device=dev)
+    if want_order and gains is None:
+        gains = torch.empty(Kt, dtype=torch.float32, device=dev)
+    if ws is None:
+        ws = _workspace(lib().diverse_select_workspace(R, _ptr(cv), Dv, code, mode), dev)
+    st = lib().diverse_select(R, Dv, code, mode, _ptr(scores), _ptr(feats), _ptr(cu_vis), _ptr(cv),
+                              _ptr(cu_keep), _ptr(ck), _ptr(kept), _ptr(order), _ptr(gains),
+                              _ptr(ws), ws.numel(), _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "diverse_select")
+    return kept, order, gains
+
+
+def gather_kept(feats: torch.Tensor, cu_vis_h, kept: torch.Tensor, cu_keep_h, cu_vis=None,
+                cu_keep=None, out=None, stream=None):
+    """gather_kept (Eq. 12): the kept rows of feats, byte for byte."""
+    dev = feats.device
+    cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
+    R = len(cv) - 1
+    Dv = feats.shape[-1]
+    if cu_vis is None:
+        cu_vis = _i32_dev(cv, dev)
+    if cu_keep is None:
+        cu_keep = _i32_dev(ck, dev)
+    if out is None:
+        out = torch.empty((int(ck[-1]), Dv), dtype=feats.dtype, device=dev)
+    st = lib().gather_kept(R, Dv, feats.element_size(), _ptr(feats), _ptr(cu_vis), _ptr(cv),
+                           _ptr(kept), _ptr(cu_keep), _ptr(ck), _ptr(out), _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "gather_kept")
+    return out
+
+
+def budget(n: int, num: int, den: int) -> int:
+    return int(lib().last_budget(int(n), int(num), int(den)))
+
+
+# ------------------------------------------------------------------ profiling
+def profile_enable(on: bool = True) -> None:
+    lib().last_profile_enable(1 if on else 0)
+
+
+def profile_reset() -> None:
+    lib().last_profile_reset()
+
+
+def profile_collect() -> dict:
+    """Fold finished kernel timings (call after synchronising). Returns
+    {kernel: (launches, total_ms)}."""
+    L = lib()
+    L.last_profile_collect()
+    out = {}
+    name = ctypes.c_char_p()
+    n = ctypes.c_int64()
+    ms = ctypes.c_double()
+    for i in range(L.last_profile_count()):
+        if L.last_profile_kernel(i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms)):
+            out[name.value.decode()] = (int(n.value), float(ms.value))
+    return out
+
+
+# ------------------------------------------------------------------ workloads
+def to_torch(x: np.ndarray, dtype: str, device) -> torch.Tensor:
+    """Upload a workload array (bf16 as uint16 bit patterns, or fp32)."""
+    if dtype == "bf16":
+        t = torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(device)
+
+
+@dataclass
+class DeviceWorkload:
+    batch: Batch
+    q: torch.Tensor
+    k: torch.Tensor
+    feats: torch.Tensor
+    cu_keep_h: np.ndarray
+    cu_keep: torch.Tensor
+    Dv: int
+
+    @staticmethod
+    def upload(wl, device="cuda") -> "DeviceWorkload":
+        batch = Batch.make(wl.G, wl.Hq, wl.Hkv, wl.Dh, wl.cu_seqlens, wl.vis_start, wl.cu_vis,
+                           scale=wl.scale, device=device)
+        return DeviceWorkload(batch=batch, q=to_torch(wl.q, wl.qk_dtype, device),
+                              k=to_torch(wl.k, wl.qk_dtype, device),
+                              feats=to_torch(wl.feats, wl.f_dtype, device),
+                              cu_keep_h=_i32_host(wl.cu_keep), cu_keep=_i32_dev(wl.cu_keep, device),
+                              Dv=wl.Dv)

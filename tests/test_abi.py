@@ -1,0 +1,189 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/last.h declares, and rejects malformed calls on the host before any
+HIP call (so these run on a machine with no GPU). Fake device pointers are
+host buffers filled with a sentinel; a rejected call must leave them as is.
+"""
+import ctypes
+import math
+import os
+import re
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from paper_2607_27952_amd import last
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "last.h")
+
+
+def _declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = set(re.findall(r"^\s*[A-Za-z_][\w\s\*]*?\b([a-z_][a-z0-9_]*)\s*\(", src, flags=re.M))
+    return sorted(n for n in names if not n.startswith("__"))
+
+
+def test_header_declares_the_path():
+    names = _declared_functions()
+    for n in ("last_token_scores", "diverse_select", "gather_kept", "last_budget",
+              "last_token_scores_workspace", "diverse_select_workspace", "last_status_string"):
+        assert n in names
+
+
+def test_library_exports_every_declared_function():
+    L = last.lib()
+    for n in _declared_functions():
+        assert hasattr(L, n), f"{n} declared in last.h but not exported"
+    assert set(last.EXPORTS) <= set(_declared_functions())
+    assert L.last_version() == 100
+
+
+def test_status_strings():
+    for s in range(5):
+        assert last.status_string(s)
+    assert last.status_string(0) == "ok"
+
+
+def test_budget_matches_eq2():
+    for n in range(1, 400):
+        for num, den in [(1, 8), (3, 8), (5, 8), (1, 9), (2, 3), (1, 1)]:
+            assert last.budget(n, num, den) == math.ceil(Fraction(n * num, den))
+    assert last.budget(0, 1, 8) == -1
+    assert last.budget(10, 0, 8) == -1
+    assert last.budget(10, 9, 8) == -1
+
+
+class Fake:
+    """Host buffers standing in for device pointers; never dereferenced by a rejected call."""
+
+    def __init__(self, n=4096):
+        self.buf = np.full(n, 0x5A5A5A5A, dtype=np.uint32)
+
+    @property
+    def p(self):
+        return self.buf.ctypes.data
+
+    def untouched(self):
+        return bool(np.all(self.buf == 0x5A5A5A5A))
+
+
+def _batch(R=2, G=1, Hq=4, Hkv=2, Dh=128, P=(20, 30), N=(10, 12), vis=(2, 3), dtype=last.LAST_BF16):
+    cs = np.zeros(R + 1, np.int32)
+    cs[1:] = np.cumsum(P)
+    cv = np.zeros(R + 1, np.int32)
+    cv[1:] = np.cumsum(N)
+    vs = np.asarray(vis, np.int32)
+    dev = Fake()
+    b = last._Batch(R, G, Hq, Hkv, Dh, dtype, 0.0, dev.p, cs.ctypes.data, dev.p, vs.ctypes.data,
+                    dev.p, cv.ctypes.data)
+    return b, (cs, cv, vs, dev)
+
+
+def _scores_call(b, ws_bytes=1 << 30):
+    q, k, out, ws = Fake(), Fake(), Fake(), Fake()
+    st = last.lib().last_token_scores(ctypes.byref(b), q.p, k.p, out.p, None, ws.p, ws_bytes, None)
+    assert out.untouched() and ws.untouched()
+    return st
+
+
+def test_scores_workspace_query():
+    b, keep = _batch()
+    assert last.lib().last_token_scores_workspace(ctypes.byref(b)) > 0
+    b.Hq = 3
+    assert last.lib().last_token_scores_workspace(ctypes.byref(b)) == 0
+
+
+@pytest.mark.parametrize("field,value,expect", [
+    ("R", 0, last.LAST_ERR_INVALID),
+    ("G", 0, last.LAST_ERR_INVALID),
+    ("Hq", 3, last.LAST_ERR_INVALID),          # Hq % Hkv != 0
+    ("Hkv", 0, last.LAST_ERR_INVALID),
+    ("Dh", 96, last.LAST_ERR_UNSUPPORTED),
+    ("qk_dtype", 7, last.LAST_ERR_INVALID),
+    ("softmax_scale", float("nan"), last.LAST_ERR_INVALID),
+    ("G", 2000, last.LAST_ERR_UNSUPPORTED),    # G * Hq over the finalize limit
+])
+def test_scores_rejects_bad_shapes(field, value, expect):
+    b, keep = _batch()
+    setattr(b, field, value)
+    assert _scores_call(b) == expect
+
+
+def test_scores_rejects_bad_csr():
+    b, keep = _batch(P=(20, 30), N=(10, 12), vis=(2, 3))
+    cs, cv, vs, dev = keep
+    cs[1] = 40                                    # decreasing offsets
+    assert _scores_call(b) == last.LAST_ERR_INVALID
+    b, keep = _batch(P=(20, 30), N=(10, 12), vis=(10, 3))   # span runs into the last token
+    assert _scores_call(b) == last.LAST_ERR_INVALID
+    b, keep = _batch(P=(20, 30), N=(10, 12), vis=(-1, 3))
+    assert _scores_call(b) == last.LAST_ERR_INVALID
+    b, keep = _batch(P=(1, 30), N=(0, 12), vis=(0, 3))        # P_r < 2 and N_r < 1
+    assert _scores_call(b) == last.LAST_ERR_INVALID
+    b, keep = _batch()
+    b.cu_vis_h = None
+    assert _scores_call(b) == last.LAST_ERR_INVALID
+
+
+def test_scores_rejects_null_and_small_workspace():
+    b, keep = _batch()
+    q, out, ws = Fake(), Fake(), Fake()
+    L = last.lib()
+    assert L.last_token_scores(ctypes.byref(b), None, q.p, out.p, None, ws.p, 1 << 30, None) == last.LAST_ERR_INVALID
+    need = L.last_token_scores_workspace(ctypes.byref(b))
+    assert L.last_token_scores(ctypes.byref(b), q.p, q.p, out.p, None, ws.p, need - 1, None) == last.LAST_ERR_WORKSPACE
+    assert L.last_token_scores(ctypes.byref(b), q.p, q.p, out.p, None, None, need, None) == last.LAST_ERR_WORKSPACE
+    assert L.last_token_scores(ctypes.byref(b), q.p + 2, q.p, out.p, None, ws.p, need, None) == last.LAST_ERR_INVALID
+    assert out.untouched() and ws.untouched()
+
+
+def _select_call(cv, ck, Dv=64, fdtype=last.LAST_BF16, mode=last.KCENTER, ws_bytes=1 << 40):
+    cv = np.asarray(cv, np.int32)
+    ck = None if ck is None else np.asarray(ck, np.int32)
+    dev, out, ws = Fake(), Fake(), Fake()
+    st = last.lib().diverse_select(len(cv) - 1, Dv, fdtype, mode, dev.p, dev.p, dev.p, cv.ctypes.data,
+                                   dev.p, None if ck is None else ck.ctypes.data, out.p, out.p, out.p,
+                                   ws.p, ws_bytes, None)
+    assert out.untouched() and ws.untouched()
+    return st
+
+
+def test_select_rejects_bad_budgets_and_shapes():
+    E = last.LAST_ERR_INVALID
+    assert _select_call([0, 10, 30], [0, 11, 15]) == E            # K_r > N_r
+    assert _select_call([0, 10, 30], [0, 0, 5]) == E              # K_r = 0
+    assert _select_call([0, 10, 30], None) == E                   # no host budgets
+    assert _select_call([0, 10, 10], [0, 5, 5]) == E              # N_r = 0
+    assert _select_call([1, 10, 30], [0, 5, 6]) == E              # offsets not from 0
+    assert _select_call([0, 10, 30], [0, 5, 6], Dv=0) == E
+    assert _select_call([0, 10, 30], [0, 5, 6], mode=5) == E
+    assert _select_call([0, 10, 30], [0, 5, 6], fdtype=3) == E
+    U = last.LAST_ERR_UNSUPPORTED
+    assert _select_call([0, 16385], [0, 5]) == U                  # request larger than the greedy holds
+    assert _select_call([0, 10, 30], [0, 5, 6], Dv=60) == U       # bf16 rows not 16-byte multiples
+    assert _select_call([0, 10, 30], [0, 5, 6], Dv=62, fdtype=last.LAST_F32) == U
+
+
+def test_select_workspace_and_small_workspace():
+    cv = np.array([0, 100, 350], np.int32)
+    need = last.lib().diverse_select_workspace(2, cv.ctypes.data, 64, last.LAST_BF16, last.KCENTER)
+    assert need >= (100 * 100 + 250 * 250) * 4
+    assert _select_call(cv, [0, 5, 6], ws_bytes=need - 1) == last.LAST_ERR_WORKSPACE
+    topk = last.lib().diverse_select_workspace(2, cv.ctypes.data, 64, last.LAST_BF16, last.TOPK)
+    assert 0 < topk < need
+    assert last.lib().diverse_select_workspace(2, cv.ctypes.data, 0, last.LAST_BF16, last.KCENTER) == 0
+
+
+def test_gather_rejects_bad_arguments():
+    cv = np.array([0, 10, 30], np.int32)
+    ck = np.array([0, 4, 6], np.int32)
+    dev, out = Fake(), Fake()
+    L = last.lib()
+    assert L.gather_kept(2, 64, 3, dev.p, dev.p, cv.ctypes.data, dev.p, dev.p, ck.ctypes.data, out.p, None) == last.LAST_ERR_INVALID
+    assert L.gather_kept(0, 64, 2, dev.p, dev.p, cv.ctypes.data, dev.p, dev.p, ck.ctypes.data, out.p, None) == last.LAST_ERR_INVALID
+    bad = np.array([0, 4, 2], np.int32)
+    assert L.gather_kept(2, 64, 2, dev.p, dev.p, cv.ctypes.data, dev.p, dev.p, bad.ctypes.data, out.p, None) == last.LAST_ERR_INVALID
+    assert L.gather_kept(2, 64, 2, None, dev.p, cv.ctypes.data, dev.p, dev.p, ck.ctypes.data, out.p, None) == last.LAST_ERR_INVALID
+    assert out.untouched()

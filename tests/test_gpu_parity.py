@@ -1,0 +1,353 @@
+"""HIP path vs the CPU oracle, on the same seeded inputs (needs an MI355X).
+
+Bars (the oracle is fp64; the library computes in fp32 with exact bf16 widening):
+  * scores   element-wise |gpu - oracle| <= 1e-5 * oracle (+ FLT_MIN floor);
+  * select   every GPU pick is replayed against the oracle (teacher forcing,
+             oracle.replay): it must be the oracle's own lowest-index argmax,
+             or within 1e-6 relative of the oracle's best objective (an
+             excused near-tie); zero failed steps. Kept sets are compared as
+             sets and must match exactly unless the replay excused a step;
+  * top-k    identical set and order (both sides rank the same fp32 values);
+  * gather   byte-identical rows.
+Small cases span several chunks/tiles with ragged tails; the five named
+workloads run at full size on the GPU and are checked on sampled requests.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2607_27952_amd import last
+from paper_2607_27952_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+FLT_MIN = np.finfo(np.float32).tiny
+SCORE_RTOL = 1e-5
+TIE_RTOL = 1e-6
+
+
+def _fd(dtype):
+    return oracle.BF16 if dtype == W.BF16 else oracle.F32
+
+
+def orc_scores(wl, want_rows=False):
+    return oracle.scores(wl.R, wl.G, wl.Hq, wl.Hkv, wl.Dh, wl.q, wl.k, wl.cu_seqlens, wl.vis_start,
+                         wl.cu_vis, _fd(wl.qk_dtype), scale=wl.scale, want_rows=want_rows)
+
+
+def gpu_scores(dw, want_rows=False):
+    out = last.token_scores(dw.batch, dw.q, dw.k, want_rows=want_rows)
+    torch.cuda.synchronize()
+    if want_rows:
+        return out[0].cpu().numpy(), out[1].cpu().numpy()
+    return out.cpu().numpy()
+
+
+def assert_scores(g, o, what=""):
+    g = np.asarray(g, np.float64)
+    err = np.abs(g - o)
+    bad = err > SCORE_RTOL * np.abs(o) + FLT_MIN
+    assert not bad.any(), (f"{what}: {bad.sum()} of {bad.size} scores off; worst rel "
+                           f"{np.max(err / np.maximum(np.abs(o), FLT_MIN)):.3g}")
+
+
+def gpu_select(dw_feats, scores_t, cu_vis, cu_keep, mode=last.KCENTER):
+    kept, order, gains = last.diverse_select(scores_t, dw_feats, cu_vis, cu_keep, mode=mode)
+    torch.cuda.synchronize()
+    return kept.cpu().numpy(), order.cpu().numpy(), gains.cpu().numpy()
+
+
+def check_selection(wl, w32, kept, order, tag=""):
+    """Replay the GPU pick sequence on the oracle; returns (exact, excused) step counts."""
+    R = wl.R
+    st, mg = oracle.replay(R, wl.Dv, w32, wl.feats, wl.cu_vis, wl.cu_keep, order, _fd(wl.f_dtype),
+                           rel_tol=TIE_RTOL)
+    failed = np.flatnonzero(st == 2)
+    assert failed.size == 0, f"{tag}: {failed.size} failed steps, first at {failed[:5]}, margins {mg[failed[:5]]}"
+    okept, _, _ = oracle.select(R, wl.Dv, w32, wl.feats, wl.cu_vis, wl.cu_keep, _fd(wl.f_dtype))
+    for r in range(R):
+        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
+        kr = kept[a:b]
+        assert np.all(np.diff(kr) > 0) and kr[0] >= 0 and kr[-1] < wl.n(r), f"{tag}: kept not ascending/in range"
+        assert sorted(order[a:b]) == list(kr), f"{tag}: kept is not the sorted pick set"
+        if np.all(st[a:b] == 0):
+            assert list(kr) == list(okept[a:b]), f"{tag}: request {r} set differs without any near-tie"
+    return int((st == 0).sum()), int((st == 1).sum())
+
+
+# ------------------------------------------------------------------ scores
+
+SCORE_CASES = [
+    # seed, R, G, Hq, Hkv, Dh, qk dtype, n_range, t_range
+    (0, 3, 1, 4, 4, 128, W.BF16, (1, 700), (1, 90)),
+    (1, 4, 2, 8, 2, 128, W.BF16, (200, 1500), (5, 300)),
+    (2, 2, 3, 14, 2, 64, W.BF16, (100, 900), (2, 40)),
+    (3, 5, 1, 16, 16, 64, W.F32, (1, 600), (1, 50)),
+    (4, 2, 2, 28, 4, 128, W.BF16, (1000, 3000), (20, 130)),
+    (5, 3, 1, 12, 2, 128, W.BF16, (256, 2000), (32, 256)),
+    (6, 2, 1, 32, 2, 128, W.F32, (50, 400), (3, 20)),         # g = 16: two head groups
+    (7, 6, 2, 6, 3, 64, W.F32, (1, 5), (1, 3)),               # tiny requests, P down to 2
+]
+
+
+@pytest.mark.parametrize("case", SCORE_CASES, ids=lambda c: f"s{c[0]}")
+def test_scores_parity_small(case):
+    seed, R, G, Hq, Hkv, Dh, dt, nr, tr = case
+    for sharp in (False, True):
+        wl = W.tiny(seed, R=R, G=G, Hq=Hq, Hkv=Hkv, Dh=Dh, n_range=nr, t_range=tr, qk_dtype=dt, sharp=sharp)
+        dw = last.DeviceWorkload.upload(wl)
+        assert_scores(gpu_scores(dw), orc_scores(wl), f"case {seed} sharp={sharp}")
+
+
+def test_scores_rows_debug_output():
+    wl = W.tiny(11, R=3, G=2, Hq=8, Hkv=2, Dh=128, n_range=(300, 900), t_range=(10, 80))
+    dw = last.DeviceWorkload.upload(wl)
+    s, rows = gpu_scores(dw, want_rows=True)
+    w, orows = orc_scores(wl, want_rows=True)
+    assert_scores(s, w, "scores")
+    for r in range(wl.R):
+        a, b = wl.cu_seqlens[r], wl.cu_seqlens[r + 1]
+        np.testing.assert_allclose(rows[:, :, a:b].astype(np.float64).sum(axis=2), 1.0, atol=1e-6)
+    assert_scores(rows.ravel(), orows.ravel(), "rows")
+
+
+@pytest.mark.parametrize("c", [-80.0, 80.0])
+def test_scores_large_logit_shift(c):
+    """Adding c to every logit of each row must not overflow or change w."""
+    wl = W.tiny(12, R=2, G=1, Hq=4, Hkv=4, Dh=64, n_range=(200, 600), t_range=(5, 40), qk_dtype=W.F32)
+    k = wl.k.astype(np.float64)
+    q = wl.q.astype(np.float64)
+    for r in range(wl.R):
+        a, b = wl.cu_seqlens[r], wl.cu_seqlens[r + 1]
+        for h in range(wl.Hq):
+            u = q[0, r, h]
+            k[0, a:b, h] += c * u / (wl.scale * np.dot(u, u))
+    wl.k = k.astype(np.float32)
+    g = gpu_scores(last.DeviceWorkload.upload(wl))
+    assert np.all(np.isfinite(g))
+    assert_scores(g, orc_scores(wl), f"shift {c}")
+
+
+def test_scores_deterministic():
+    wl = W.tiny(13, R=4, G=2, Hq=28, Hkv=4, Dh=128, n_range=(500, 2500), t_range=(10, 100))
+    dw = last.DeviceWorkload.upload(wl)
+    a = gpu_scores(dw)
+    b = gpu_scores(dw)
+    assert a.tobytes() == b.tobytes()
+
+
+# ------------------------------------------------------------------ selection
+
+SELECT_CASES = [
+    # seed, R, n_range, Dv, dtype, k_frac, comps
+    (20, 3, (1, 300), 64, W.BF16, None, 4),
+    (21, 2, (129, 700), 256, W.BF16, 0.25, 8),
+    (22, 4, (100, 400), 1024, W.BF16, 0.125, 16),
+    (23, 2, (300, 640), 136, W.BF16, 0.5, 5),      # Dv not a multiple of 64
+    (24, 3, (50, 500), 96, W.F32, 0.2, 6),
+    (25, 1, (1500, 2100), 512, W.BF16, 0.1, 24),
+]
+
+
+@pytest.mark.parametrize("case", SELECT_CASES, ids=lambda c: f"k{c[0]}")
+def test_select_parity_small(case):
+    seed, R, nr, Dv, dt, kf, comps = case
+    wl = W.tiny(seed, R=R, n_range=nr, Dv=Dv, f_dtype=dt, k_frac=kf, comps=comps)
+    rng = np.random.default_rng(seed)
+    w32 = np.concatenate([rng.dirichlet(np.ones(wl.n(r)) * 0.7) for r in range(R)]).astype(np.float32)
+    dw = last.DeviceWorkload.upload(wl)
+    kept, order, gains = gpu_select(dw.feats, torch.from_numpy(w32).cuda(), wl.cu_vis, wl.cu_keep)
+    check_selection(wl, w32, kept, order, f"case {seed}")
+    # gains: w at the first pick, then the objective at each pick, never increasing
+    for r in range(R):
+        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
+        assert gains[a] == w32[wl.cu_vis[r] + order[a]]
+        assert np.all(np.diff(gains[a + 1:b]) <= 0)
+
+
+def _select_handmade(X, w, K, dtype=W.F32):
+    X = np.asarray(X, np.float32)
+    N, Dv = X.shape
+    wl = W.Workload(name="hand", R=1, G=1, Hq=1, Hkv=1, Dh=64, qk_dtype=W.F32, scale=0.125,
+                    cu_seqlens=np.array([0, N + 1], np.int32), vis_start=np.array([0], np.int32),
+                    cu_vis=np.array([0, N], np.int32), q=None, k=None, Dv=Dv, f_dtype=dtype,
+                    feats=W.to_bf16_bits(X) if dtype == W.BF16 else X,
+                    cu_keep=np.array([0, K], np.int32))
+    feats = last.to_torch(wl.feats, dtype, "cuda")
+    w32 = np.asarray(w, np.float32)
+    kept, order, gains = gpu_select(feats, torch.from_numpy(w32).cuda(), wl.cu_vis, wl.cu_keep)
+    return wl, w32, kept, order, gains
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_select_edge_cases(dtype):
+    rng = np.random.default_rng(30)
+    Dv = 64
+    # K = 1 and K = N
+    X = rng.standard_normal((150, Dv))
+    w = rng.dirichlet(np.ones(150))
+    for K in (1, 150):
+        wl, w32, kept, order, _ = _select_handmade(X, w, K, dtype)
+        check_selection(wl, w32, kept, order, f"K={K}")
+    # N = 1
+    wl, w32, kept, order, gains = _select_handmade(X[:1], [1.0], 1, dtype)
+    assert list(kept) == [0] and list(order) == [0] and gains[0] == 1.0
+    # identical features: the rest are the lowest remaining indices, objective exactly 0
+    Xi = np.tile(X[:1], (200, 1))
+    wl, w32, kept, order, gains = _select_handmade(Xi, w[:150].tolist() + [0.001] * 50, 20, dtype)
+    j1 = int(np.argmax(w32))
+    assert list(order) == [j1] + [i for i in range(200) if i != j1][:19]
+    assert np.all(gains[1:] == 0.0)
+    # exact duplicates spread over several tiles, plus zero rows
+    Xd = rng.standard_normal((300, Dv))
+    Xd[150:] = Xd[:150]
+    Xd[[7, 77, 277]] = 0.0
+    wd = rng.dirichlet(np.ones(300))
+    wl, w32, kept, order, _ = _select_handmade(Xd, wd, 200, dtype)
+    check_selection(wl, w32, kept, order, "duplicates")
+    # one-hot rows: top-K by weight
+    Xo = np.eye(256, Dv * 4)[:, :Dv * 4]
+    wl, w32, kept, order, _ = _select_handmade(Xo, rng.dirichlet(np.ones(256)), 40, dtype)
+    assert list(order) == list(np.argsort(-w32.astype(np.float64), kind="stable")[:40])
+
+
+def test_select_deterministic():
+    wl = W.tiny(31, R=3, n_range=(400, 1200), Dv=512, k_frac=0.2, comps=12)
+    w32 = np.random.default_rng(1).dirichlet(np.ones(wl.N_total)).astype(np.float32)
+    dw = last.DeviceWorkload.upload(wl)
+    s = torch.from_numpy(w32).cuda()
+    a = gpu_select(dw.feats, s, wl.cu_vis, wl.cu_keep)
+    b = gpu_select(dw.feats, s, wl.cu_vis, wl.cu_keep)
+    for x, y in zip(a, b):
+        assert x.tobytes() == y.tobytes()
+
+
+@pytest.mark.parametrize("seed", [40, 41])
+def test_topk_parity(seed):
+    wl = W.tiny(seed, R=4, n_range=(1, 5000), Dv=64, k_frac=0.125)
+    rng = np.random.default_rng(seed)
+    w32 = (rng.integers(0, 50, size=wl.N_total) / 50.0).astype(np.float32)   # many ties
+    dw = last.DeviceWorkload.upload(wl)
+    kept, order, gains = gpu_select(dw.feats, torch.from_numpy(w32).cuda(), wl.cu_vis, wl.cu_keep,
+                                    mode=last.TOPK)
+    ok, oo, og = oracle.select(wl.R, wl.Dv, w32, wl.feats, wl.cu_vis, wl.cu_keep, oracle.BF16, mode=oracle.TOPK)
+    assert list(kept) == list(ok)
+    assert list(order) == list(oo)
+    np.testing.assert_array_equal(gains.astype(np.float64), og)
+
+
+# ------------------------------------------------------------------ gather
+
+@pytest.mark.parametrize("Dv,dtype", [(4096, np.uint16), (1536, np.uint16), (1024, np.float32), (77, np.uint16), (5, np.uint8)])
+def test_gather_bit_exact(Dv, dtype):
+    rng = np.random.default_rng(Dv)
+    cu_vis = np.array([0, 300, 301, 1000], np.int32)
+    cu_keep = np.array([0, 40, 41, 141], np.int32)
+    itemsize = np.dtype(dtype).itemsize
+    feats = rng.integers(0, 256, size=(1000, Dv * itemsize), dtype=np.uint8).view(dtype)   # NaN payloads too
+    kept = np.concatenate([np.sort(rng.choice(300, 40, replace=False)), [0],
+                           np.sort(rng.choice(699, 100, replace=False))]).astype(np.int32)
+    ft = torch.from_numpy(feats.view(np.int16) if dtype == np.uint16 else feats).cuda()
+    out = last.gather_kept(ft, cu_vis, torch.from_numpy(kept).cuda(), cu_keep)
+    torch.cuda.synchronize()
+    expect = oracle.gather(3, feats, cu_vis, kept, cu_keep)
+    assert out.cpu().numpy().tobytes() == expect.tobytes()
+
+
+def test_gather_out_of_range_index_gives_zero_row():
+    feats = torch.arange(40 * 16, dtype=torch.float32).reshape(40, 16).cuda()
+    out = last.gather_kept(feats, [0, 10, 40], torch.tensor([3, 10, 29, -1], dtype=torch.int32).cuda(), [0, 2, 4])
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    np.testing.assert_array_equal(o[0], feats[3].cpu().numpy())
+    assert np.all(o[1] == 0) and np.all(o[3] == 0)
+    np.testing.assert_array_equal(o[2], feats[39].cpu().numpy())
+
+
+# ------------------------------------------------------------------ full-size workloads
+
+CONFIG_SAMPLES = {
+    "c1_single_fp32": [0],
+    "c2_llava15": [0, 37],
+    "c3_llava_next": [5],
+    "c4_dynres": None,          # chosen from the drawn sizes: smallest, median and a large one
+    "c5_video": [3],
+}
+
+
+@pytest.fixture(scope="module")
+def workloads():
+    cache = {}
+
+    def get(name, budget=None):
+        key = (name, budget)
+        if key not in cache:
+            wl = W.make(name, budget=budget)
+            cache[key] = (wl, last.DeviceWorkload.upload(wl))
+        return cache[key]
+    return get
+
+
+def _samples(name, wl):
+    s = CONFIG_SAMPLES[name]
+    if s is not None:
+        return s
+    order = np.argsort(np.diff(wl.cu_vis))
+    return [int(order[0]), int(order[len(order) // 2]), int(order[-8])]
+
+
+@pytest.mark.parametrize("name", W.CONFIGS)
+def test_config_scores(name, workloads):
+    wl, dw = workloads(name)
+    g = gpu_scores(dw)
+    for r in range(wl.R):
+        seg = g[wl.cu_vis[r]:wl.cu_vis[r + 1]].astype(np.float64)
+        assert np.all(seg >= 0) and abs(seg.sum() - 1.0) < 1e-5
+    for r in _samples(name, wl):
+        sub = wl.subset([r])
+        assert_scores(g[wl.cu_vis[r]:wl.cu_vis[r + 1]], orc_scores(sub), f"{name} request {r}")
+
+
+@pytest.mark.parametrize("name", W.CONFIGS)
+def test_config_select(name, workloads):
+    wl, dw = workloads(name)
+    g = last.token_scores(dw.batch, dw.q, dw.k)
+    kept, order, gains = gpu_select(dw.feats, g, wl.cu_vis, dw.cu_keep_h)
+    gs = g.cpu().numpy()
+    for r in _samples(name, wl):
+        sub = wl.subset([r])
+        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
+        w_orc = orc_scores(sub).astype(np.float32)
+        # stage-isolated: the oracle's scores into the GPU selection
+        k2, o2, _ = gpu_select(last.to_torch(sub.feats, sub.f_dtype, "cuda"), torch.from_numpy(w_orc).cuda(),
+                               sub.cu_vis, sub.cu_keep)
+        check_selection(sub, w_orc, k2, o2, f"{name} request {r} (oracle scores)")
+        # end to end: the GPU's own scores and picks, replayed with the oracle's scores
+        ex, exc = check_selection(sub, w_orc, kept[a:b], order[a:b], f"{name} request {r} (end to end)")
+        assert ex + exc == b - a
+
+
+@pytest.mark.parametrize("budget", [128, 192])
+def test_c2_other_budgets(budget, workloads):
+    wl, dw = workloads("c2_llava15", budget)
+    g = last.token_scores(dw.batch, dw.q, dw.k)
+    kept, order, _ = gpu_select(dw.feats, g, wl.cu_vis, dw.cu_keep_h)
+    for r in (1, 63):
+        sub = wl.subset([r])
+        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
+        w_orc = orc_scores(sub).astype(np.float32)
+        check_selection(sub, w_orc, kept[a:b], order[a:b], f"c2 B={budget} request {r}")
+
+
+@pytest.mark.parametrize("name", W.CONFIGS)
+def test_config_gather(name, workloads):
+    wl, dw = workloads(name)
+    rng = np.random.default_rng(7)
+    kept = np.concatenate([np.sort(rng.choice(wl.n(r), wl.kk(r), replace=False)) for r in range(wl.R)]).astype(np.int32)
+    out = last.gather_kept(dw.feats, wl.cu_vis, torch.from_numpy(kept).cuda(), wl.cu_keep)
+    torch.cuda.synchronize()
+    expect = oracle.gather(wl.R, wl.feats, wl.cu_vis, kept, wl.cu_keep)
+    got = out.cpu()
+    got = got.view(torch.int16).numpy().view(np.uint16) if got.dtype == torch.bfloat16 else got.numpy()
+    assert got.tobytes() == expect.tobytes()
