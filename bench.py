@@ -1,0 +1,241 @@
+"""Benchmark of the LAST token-selection path on one MI355X.
+
+A step is one pass of the whole path over one batch that is already resident
+in HBM: last_token_scores -> diverse_select (k-center) -> gather_kept.
+
+Default workload: the LLaVA-1.5-shaped batch (64 requests of 576 visual +
+64 text tokens, 2 guidance layers of 32 heads, head_dim 128, bf16; budget
+B = 64 of 576; 576 x 4096 encoder features per request).
+
+Prints ONE JSON line on stdout. Per-kernel times come from HIP events that
+the library records on the launch stream around each kernel during the timed
+steps. The CPU oracle is timed on this host on a bounded sample of the same
+workload (cpu_baseline). Other lines go to stderr.
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="c2_llava15")
+    ap.add_argument("--budget", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target CPU time for the oracle sample")
+    return ap.parse_args()
+
+
+def describe(wl, budget):
+    n = np.diff(wl.cu_vis)
+    t = np.diff(wl.cu_seqlens) - n
+    ks = np.diff(wl.cu_keep)
+    return (f"{wl.name}: {wl.R} requests x ({int(n.mean()) if n.min() == n.max() else 'ragged'} visual + "
+            f"{int(t.mean()) if t.min() == t.max() else 'ragged'} text tokens), {wl.G} guidance layers, "
+            f"{wl.Hq}/{wl.Hkv} heads, head_dim {wl.Dh}, {wl.qk_dtype}; features {wl.Dv}-d {wl.f_dtype}; "
+            f"budget {int(ks[0]) if ks.min() == ks.max() else 'ceil(N/8)'}")
+
+
+def kernel_work(wl):
+    """Algorithmic bytes / flops per launch of each kernel, and its bound."""
+    elt = 2 if wl.qk_dtype == "bf16" else 4
+    felt = 2 if wl.f_dtype == "bf16" else 4
+    n = np.diff(wl.cu_vis).astype(np.float64)
+    k_bytes = wl.G * wl.T_total * wl.Hkv * wl.Dh * elt
+    q_bytes = wl.G * wl.R * wl.Hq * wl.Dh * elt
+    vlog = wl.G * wl.Hq * wl.N_total * 4
+    return {
+        # key rows + queries, each read once
+        "score_partial": ("hbm", k_bytes + q_bytes),
+        # visual logits in, scores out
+        "score_finalize": ("hbm", vlog + wl.N_total * 4),
+        # features read once
+        "sqnorm": ("hbm", wl.N_total * wl.Dv * felt),
+        # symmetric Gram of each request: N_r^2 * Dv multiply-adds counted as N_r^2 * Dv * 2 / 2
+        "gram": ("mfma", float(np.sum(n * n)) * wl.Dv),
+        # kept rows read and written
+        "gather": ("hbm", 2 * wl.K_total * wl.Dv * felt),
+    }
+
+
+def roofline_entry(name, bound, work, avg_ms):
+    if bound == "hbm":
+        ach = work / (avg_ms * 1e-3) / 1e9
+        return {"kernel": name, "bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4), "bytes_per_launch": int(work)}
+    ach = work / (avg_ms * 1e-3) / 1e12
+    return {"kernel": name, "bound": "mfma", "achieved": round(ach, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(ach / MFMA_BF16_PEAK_TFLOPS, 4), "flops_per_launch": int(work)}
+
+
+def traffic_for(kernel, workload):
+    """HBM bytes per launch measured by rocprofv3 counters, if a summary for this
+    kernel and workload exists and the kernel source is unchanged since."""
+    path = os.path.join(PROFILES, f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    src = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(src):
+        return None
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(wl, target_s):
+    import oracle
+    fd = oracle.BF16 if wl.f_dtype == "bf16" else oracle.F32
+    qd = oracle.BF16 if wl.qk_dtype == "bf16" else oracle.F32
+    threads = len(os.sched_getaffinity(0))
+
+    def run(sub):
+        t0 = time.perf_counter()
+        w = oracle.scores(sub.R, sub.G, sub.Hq, sub.Hkv, sub.Dh, sub.q, sub.k, sub.cu_seqlens,
+                          sub.vis_start, sub.cu_vis, qd, scale=sub.scale, nthreads=threads)
+        kept, _, _ = oracle.select(sub.R, sub.Dv, w.astype(np.float32), sub.feats, sub.cu_vis,
+                                   sub.cu_keep, fd, nthreads=threads)
+        oracle.gather(sub.R, sub.feats, sub.cu_vis, kept, sub.cu_keep)
+        return time.perf_counter() - t0
+
+    t_one = run(wl.subset([0]))
+    n = int(min(wl.R, max(1, math.ceil(target_s / max(t_one, 1e-6)))))
+    dt = run(wl if n == wl.R else wl.subset(list(range(n))))
+    return {"value": round(n / dt, 3), "unit": "requests/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {n} of {wl.R} requests, whole path (scores, k-center, gather) in fp64, "
+                      f"{dt:.1f} s on {threads} threads"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2607_27952_amd import last
+    from paper_2607_27952_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    wl = W.make(args.workload, budget=args.budget)
+    log(f"[bench] generated {wl.name} in {time.time() - t0:.1f}s")
+    dw = last.DeviceWorkload.upload(wl, device=dev)
+    b = dw.batch
+    stream = torch.cuda.current_stream()
+
+    # every buffer allocated once, outside the timed region
+    scores = torch.empty(wl.N_total, dtype=torch.float32, device=dev)
+    kept = torch.empty(wl.K_total, dtype=torch.int32, device=dev)
+    order = torch.empty(wl.K_total, dtype=torch.int32, device=dev)
+    gains = torch.empty(wl.K_total, dtype=torch.float32, device=dev)
+    out = torch.empty((wl.K_total, wl.Dv), dtype=dw.feats.dtype, device=dev)
+    ws_s = torch.empty(last.token_scores_workspace(b, dw.q.dtype), dtype=torch.uint8, device=dev)
+    ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8, device=dev)
+
+    def step():
+        last.token_scores(b, dw.q, dw.k, scores=scores, ws=ws_s)
+        last.diverse_select(scores, dw.feats, wl.cu_vis, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep,
+                            kept=kept, order=order, gains=gains, ws=ws_k)
+        last.gather_kept(dw.feats, wl.cu_vis, kept, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep, out=out)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    last.profile_reset()
+    last.profile_enable(True)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        step()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    t_end = time.perf_counter()
+    last.profile_enable(False)
+    prof = last.profile_collect()
+    elapsed = t_end - t_start
+    step_ms = np.array([a.elapsed_time(bb) for a, bb in ev])
+    ms_per_step = elapsed / args.steps * 1e3
+
+    work = kernel_work(wl)
+    kernels = {}
+    for name, (launches, total_ms) in prof.items():
+        kernels[name] = {"launches": launches, "avg_ms": round(total_ms / max(launches, 1), 5),
+                         "ms_per_step": round(total_ms / args.steps, 5)}
+    rooflines = []
+    for name, (bound, w) in work.items():
+        if name in kernels:
+            rooflines.append(roofline_entry(name, bound, w, kernels[name]["avg_ms"]))
+    dominant = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])[0]
+    main_roof = next((r for r in rooflines if r["kernel"] == dominant), None)
+    if main_roof is not None:
+        tr = traffic_for(dominant, args.workload)
+        main_roof = {k: main_roof[k] for k in ("bound", "achieved", "peak", "unit", "frac")} | {
+            "traffic": tr, "kernel": dominant}
+    score_ms = sum(kernels[k]["ms_per_step"] for k in kernels if k.startswith("score"))
+    select_ms = sum(kernels[k]["ms_per_step"] for k in kernels
+                    if k in ("select_plan", "sqnorm", "gram", "greedy", "topk"))
+    gather_ms = kernels.get("gather", {}).get("ms_per_step", 0.0)
+
+    res = {
+        "metric": "requests/sec and visual tokens scored/sec per GPU; p50 select latency",
+        "value": round(wl.R * args.steps / elapsed, 2),
+        "unit": "requests/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": describe(wl, args.budget), "requests": wl.R, "visual_tokens": wl.N_total,
+                   "kept_tokens": wl.K_total, "arithmetic": "bf16 inputs, fp32 FMA score pass, bf16 MFMA "
+                   "Gram with fp32 partial sums folded into fp64, fp32 objective"},
+        "visual_tokens_scored_per_s": round(wl.N_total / (score_ms * 1e-3), 1) if score_ms > 0 else None,
+        "p50_select_latency_ms": round(float(np.median(step_ms)), 4),
+        "p90_select_latency_ms": round(float(np.percentile(step_ms, 90)), 4),
+        "stage_ms_per_step": {"scores": round(score_ms, 4), "select": round(select_ms, 4),
+                              "gather": round(gather_ms, 4)},
+        "kernels": kernels,
+        "roofline": main_roof,
+        "rooflines": rooflines,
+        "cpu_baseline": None,
+        "device": torch.cuda.get_device_name(0),
+    }
+    if not args.no_cpu_baseline:
+        t0 = time.time()
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        log(f"[bench] cpu baseline took {time.time() - t0:.1f}s")
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()
