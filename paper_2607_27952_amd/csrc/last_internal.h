@@ -39,6 +39,7 @@ struct Carver {
 
 // ------------------------------------------------------------ score pass
 struct ScorePlan {
+  bool stream;            // contiguous all-heads kernel (Hkv divides 32, Hq/Hkv <= 8)
   int32_t chunk_tokens;   // tokens per work chunk
   int32_t head_groups;    // query-head groups per KV head (g split in <= 8)
   int32_t g_max;          // heads per group template: 1, 2, 4 or 8
@@ -51,7 +52,9 @@ struct ScorePlan {
 struct ScoreWs {
   int32_t *chunk_off, *chunk_req, *slice_off, *slice_req;
   float4 *stats;  // [G][Hq][C_total] (chunk max, sum exp, visual sum exp, 0)
-  float *vlog;    // [G][Hq][N_total] scaled logits of visual columns
+  float *vlog;    // [N_total][G * Hq] scaled logits of visual columns, token-major
+  float2 *rowstat;  // [R][G * Hq] merged (max, 1 / sum exp) of every row
+  float *mass;      // [R] total visual mass sum_{l,h} V / Z
 };
 
 ScorePlan make_score_plan(const last_batch *b);
@@ -67,16 +70,18 @@ constexpr int kSelMaxN = 16384;      // largest request the register-resident gr
 struct SelectPlan {
   int64_t N_total, K_total;
   int32_t N_max, K_max;
-  int64_t tiles_total;     // upper-triangular Gram tiles over all requests
+  int64_t tiles_diag;      // diagonal Gram tiles over all requests
+  int64_t tiles_off;       // Gram tiles strictly above the diagonal
   int64_t d_elems;         // sum of N_r^2 (coverage matrices)
   int32_t threads, ept;    // greedy / top-k block shape
 };
 
 struct SelectWs {
-  int32_t *tile_off, *tile_req;  // Gram tile prefix per request, tile -> request
-  int64_t *d_off;                // [R+1] element offsets of each request's N_r x N_r block
-  double *nn;                    // [N_total] squared feature norms
-  float *dmat;                   // coverage distances, sum N_r^2
+  int32_t *dtile_off, *dtile_req;  // diagonal tile prefix per request, tile -> request
+  int32_t *otile_off, *otile_req;  // off-diagonal tile prefix per request, tile -> request
+  int64_t *d_off;                  // [R+1] element offsets of each request's N_r x N_r block
+  double *nn, *inv;                // [N_total] squared feature norms and 1 / norm
+  float *dmat;                     // coverage distances, sum N_r^2
 };
 
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,

@@ -7,22 +7,29 @@
 //
 //   k_score_plan      one block: per-request chunk/slice prefix sums and the
 //                     chunk -> request / slice -> request maps.
-//   k_score_partial   one block per (layer, chunk of tokens, KV head, query-head
-//                     group). Streams the chunk's key rows once (each row is
-//                     Dh * elt bytes; 8 lanes cover one row with 16-byte loads,
-//                     so a wave reads 8 rows per instruction), forms the logits
-//                     of every query head sharing that KV head with exact
-//                     bf16 -> fp32 widening and fp32 FMAs, reduces each row over
-//                     its 8 lanes with DPP, and keeps the chunk's logits in LDS.
-//                     It then writes, per head, the chunk's max m, sum of
-//                     exp(l - m) over all tokens Z and over the visual tokens V,
-//                     and the raw logits of the visual columns.
-//   k_score_finalize  one block per slice of a request's visual tokens. Merges
-//                     the chunk statistics of every (layer, head) row into the
-//                     row's max M and normaliser Z, forms
-//                     s_i = sum_{l,h} exp(l_i - M) / Z   (Eq. 6-7)
-//                     and divides by the visual mass sum_{l,h} V / Z, which is
-//                     sum_i s_i (Eq. 8), so no second pass over s is needed.
+//   k_score_stream    one block per (layer, chunk of tokens). The chunk's key
+//                     rows for all KV heads are one contiguous byte range,
+//                     streamed once: 8 lanes cover one row with 16-byte loads
+//                     (a wave reads 8 rows = 2 KB per instruction pair for
+//                     Dh = 128 bf16). Each lane keeps one KV head for the whole
+//                     block, so the query slices of that head's Hq/Hkv query
+//                     heads stay in registers; bf16 dots use v_dot2_f32_bf16,
+//                     fp32 dots use FMAs. A row's dot is reduced over its 8
+//                     lanes with DPP and lane j of the row stores query head
+//                     j's logit into the chunk's token-major LDS tile. Then
+//                     all threads form, per head, the chunk's max m and the
+//                     sums of exp(l - m) over every token (Z) and over the
+//                     visual tokens (V), and copy the visual logits out.
+//   k_score_partial   fallback for KV-head counts that do not divide 32: one
+//                     block per (layer, chunk, KV head, query-head group), the
+//                     chunk's logits staged in LDS.
+//   k_score_merge     one block per request: merges the chunk statistics of
+//                     every (layer, head) row into the row's max M and
+//                     normaliser Z, and sums the visual mass S = sum V / Z,
+//                     which equals sum_i s_i (Eq. 8).
+//   k_score_finalize  one block per slice of a request's visual tokens:
+//                     s_i = sum_{l,h} exp(l_i - M) / Z   (Eq. 6-7), over S,
+//                     so no second pass over s is needed.
 //
 // Every reduction has a fixed order, so results are bitwise reproducible.
 #include <algorithm>
@@ -34,13 +41,22 @@ using namespace last_dev;
 
 namespace {
 
+#ifndef LAST_SCORE_UNROLL
+#define LAST_SCORE_UNROLL 4
+#endif
+#ifndef LAST_SCORE_WG_KB
+#define LAST_SCORE_WG_KB 192
+#endif
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kUnroll = 4;          // row groups (8 rows each) in flight per wave
-constexpr int kMaxChunk = 4096;     // tokens per chunk, upper bound
+constexpr int kUnroll = LAST_SCORE_UNROLL;  // row groups (8 rows each) in flight per wave
+constexpr int64_t kWgBytes = (int64_t)LAST_SCORE_WG_KB * 1024;  // key bytes per stream block
+constexpr int kMaxChunk = 4096;             // tokens per chunk (fallback kernel), upper bound
 constexpr int kLdsLogitFloats = 8192;
-constexpr int kSliceTokens = 256;   // visual tokens per finalize block
-constexpr int kMaxPairs = 4096;     // G * Hq handled by the finalize block
+constexpr int kSliceTokens = 256;           // visual tokens per finalize block
+constexpr int kMaxPairs = 4096;             // G * Hq handled by the finalize block
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 template <typename T, int DH>
 struct RowShape {
@@ -59,6 +75,11 @@ __device__ __forceinline__ void widen(const uint4 v, float *f, uint16_t) {
 __device__ __forceinline__ void widen(const uint4 v, float *f, float) {
   f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
   f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+}
+
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b),
+                                         c, false);
 }
 
 // Exclusive scan of one int per thread over the block; returns the prefix and
@@ -119,14 +140,218 @@ __global__ __launch_bounds__(kThreads) void k_score_plan(
   }
 }
 
+// Per-lane query slices: bf16 kept packed for v_dot2_f32_bf16, fp32 as is.
+template <typename T, int DH, int GQ>
+struct QSlice;
+#ifndef LAST_SCORE_DOT2
+#define LAST_SCORE_DOT2 1
+#endif
+#if LAST_SCORE_DOT2
+template <int DH, int GQ>
+struct QSlice<uint16_t, DH, GQ> {
+  using RS = RowShape<uint16_t, DH>;
+  uint32_t w[GQ][RS::kElems / 2];
+  __device__ void load(const uint16_t *q0, int DHs, int sub) {
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh)
+#pragma unroll
+      for (int p = 0; p < RS::kNP; ++p) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(q0 + (int64_t)hh * DHs + (sub + 8 * p) * RS::kEP);
+        w[hh][p * 4 + 0] = v.x;
+        w[hh][p * 4 + 1] = v.y;
+        w[hh][p * 4 + 2] = v.z;
+        w[hh][p * 4 + 3] = v.w;
+      }
+  }
+  __device__ void dots(const uint4 (&kv)[RS::kNP], float (&acc)[GQ]) const {
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) {
+      float a = 0.f;
+#pragma unroll
+      for (int p = 0; p < RS::kNP; ++p) {
+        a = dot2_bf16(kv[p].x, w[hh][p * 4 + 0], a);
+        a = dot2_bf16(kv[p].y, w[hh][p * 4 + 1], a);
+        a = dot2_bf16(kv[p].z, w[hh][p * 4 + 2], a);
+        a = dot2_bf16(kv[p].w, w[hh][p * 4 + 3], a);
+      }
+      acc[hh] = a;
+    }
+  }
+};
+#else
+// bf16 widened exactly to fp32 once per key element, then one FMA per head.
+template <int DH, int GQ>
+struct QSlice<uint16_t, DH, GQ> {
+  using RS = RowShape<uint16_t, DH>;
+  float f[GQ][RS::kElems];
+  __device__ void load(const uint16_t *q0, int DHs, int sub) {
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh)
+#pragma unroll
+      for (int p = 0; p < RS::kNP; ++p) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(q0 + (int64_t)hh * DHs + (sub + 8 * p) * RS::kEP);
+        widen(v, &f[hh][p * RS::kEP], uint16_t());
+      }
+  }
+  __device__ void dots(const uint4 (&kv)[RS::kNP], float (&acc)[GQ]) const {
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) acc[hh] = 0.f;
+#pragma unroll
+    for (int p = 0; p < RS::kNP; ++p) {
+      float kf[RS::kEP];
+      widen(kv[p], kf, uint16_t());
+#pragma unroll
+      for (int e = 0; e < RS::kEP; ++e)
+#pragma unroll
+        for (int hh = 0; hh < GQ; ++hh) acc[hh] = fmaf(kf[e], f[hh][p * RS::kEP + e], acc[hh]);
+    }
+  }
+};
+#endif
+template <int DH, int GQ>
+struct QSlice<float, DH, GQ> {
+  using RS = RowShape<float, DH>;
+  float f[GQ][RS::kElems];
+  __device__ void load(const float *q0, int DHs, int sub) {
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh)
+#pragma unroll
+      for (int p = 0; p < RS::kNP; ++p) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(q0 + (int64_t)hh * DHs + (sub + 8 * p) * RS::kEP);
+        widen(v, &f[hh][p * RS::kEP], float());
+      }
+  }
+  __device__ void dots(const uint4 (&kv)[RS::kNP], float (&acc)[GQ]) const {
+#pragma unroll
+    for (int hh = 0; hh < GQ; ++hh) acc[hh] = 0.f;
+#pragma unroll
+    for (int p = 0; p < RS::kNP; ++p) {
+      float kf[RS::kEP];
+      widen(kv[p], kf, float());
+#pragma unroll
+      for (int e = 0; e < RS::kEP; ++e)
+#pragma unroll
+        for (int hh = 0; hh < GQ; ++hh) acc[hh] = fmaf(kf[e], f[hh][p * RS::kEP + e], acc[hh]);
+    }
+  }
+};
+
+// Requires (8 * kWaves) % Hkv == 0, so that every lane keeps one KV head.
+// LDS holds the chunk's logits token-major, [CH][Hq].
+template <typename T, int DH, int GQ>
+__global__ __launch_bounds__(kThreads) void k_score_stream(
+    const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
+    const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
+    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req, int R, int Hq,
+    int Hkv, int CH, int64_t C_total, int64_t T_total, int GL, float scale,
+    float *__restrict__ vlog, float4 *__restrict__ stats, float *__restrict__ rows) {
+  using RS = RowShape<T, DH>;
+  extern __shared__ float s_log[];          // [CH][Hq]
+  __shared__ float4 s_part[kThreads];
+
+  const int64_t c = blockIdx.x % C_total;
+  const int l = (int)(blockIdx.x / C_total);
+  const int r = chunk_req[c];
+  const int c_local = (int)(c - chunk_off[r]);
+  const int64_t tok0 = cu_seqlens[r];
+  const int P = cu_seqlens[r + 1] - (int)tok0;
+  const int t_begin = c_local * CH;
+  const int nt = min(P - t_begin, CH);
+  if (nt <= 0) return;
+  const int nrows = nt * Hkv;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rr = lane >> 3, sub = lane & 7;
+  const int kvh = (8 * wave + rr) % Hkv;
+
+  QSlice<T, DH, GQ> qs;
+  qs.load(q + (((int64_t)l * R + r) * Hq + kvh * GQ) * DH, DH, sub);
+
+  const T *kchunk = k + ((int64_t)l * T_total + tok0 + t_begin) * Hkv * DH;
+  const int ngroups = (nrows + 7) >> 3;
+  for (int j = 0; wave + kWaves * j < ngroups; j += kUnroll) {
+    uint4 buf[kUnroll][RS::kNP];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int row = min((wave + kWaves * (j + u)) * 8 + rr, nrows - 1);
+      const T *kp = kchunk + (int64_t)row * DH;
+#pragma unroll
+      for (int p = 0; p < RS::kNP; ++p)
+        buf[u][p] = *reinterpret_cast<const uint4 *>(kp + (sub + 8 * p) * RS::kEP);
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      float acc[GQ];
+      qs.dots(buf[u], acc);
+      float mine = 0.f;
+#pragma unroll
+      for (int hh = 0; hh < GQ; ++hh) {
+        const float s = sum8(acc[hh]);
+        if (sub == hh) mine = s;
+      }
+      const int row = (wave + kWaves * (j + u)) * 8 + rr;
+      if (row < nrows && sub < GQ) s_log[row * GQ + sub] = mine * scale;   // = [t][kvh*GQ+sub]
+    }
+  }
+  __syncthreads();
+
+  // Chunk statistics per head: max over every token, then the sums of
+  // exp(l - max) over every token and over the visual ones. tph threads per
+  // head take every tph-th token; their partials merge in a fixed order.
+  const int v_lo = vis_start[r] - t_begin;
+  const int v_hi = v_lo + (cu_vis[r + 1] - cu_vis[r]);
+  const int tph = max(1, kThreads / Hq);
+  for (int h0 = 0; h0 < Hq; h0 += kThreads / tph) {
+    const int h = h0 + (int)threadIdx.x / tph, sl = (int)threadIdx.x % tph;
+    const bool act = (int)threadIdx.x / tph < kThreads / tph && h < Hq;
+    float m = -INFINITY, z = 0.f, v = 0.f;
+    if (act) {
+      for (int t = sl; t < nt; t += tph) m = fmaxf(m, s_log[t * Hq + h]);
+      for (int t = sl; t < nt; t += tph) {
+        const float e = expf(s_log[t * Hq + h] - m);
+        z += e;
+        if (t >= v_lo && t < v_hi) v += e;
+      }
+    }
+    s_part[threadIdx.x] = make_float4(m, z, v, 0.f);
+    __syncthreads();
+    if (act && sl == 0) {
+      float M = -INFINITY;
+      for (int x = 0; x < tph; ++x) M = fmaxf(M, s_part[threadIdx.x + x].x);
+      float Z = 0.f, V = 0.f;
+      for (int x = 0; x < tph; ++x) {
+        const float4 e = s_part[threadIdx.x + x];
+        const float f = e.x == -INFINITY ? 0.f : expf(e.x - M);
+        Z = fmaf(e.y, f, Z);
+        V = fmaf(e.z, f, V);
+      }
+      stats[((int64_t)l * Hq + h) * C_total + c] = make_float4(M, Z, V, 0.f);
+    }
+    __syncthreads();
+  }
+
+  // Visual logits, token-major, coalesced; and every logit if rows are asked.
+  const int GH = GL * Hq;
+  const int vb = max(0, v_lo), ve = min(nt, v_hi);
+  const int64_t vtok0 = (int64_t)cu_vis[r] - vis_start[r] + t_begin;
+  for (int e = vb * Hq + (int)threadIdx.x; e < ve * Hq; e += kThreads) {
+    const int t = e / Hq, h = e - t * Hq;
+    vlog[(vtok0 + t) * GH + (int64_t)l * Hq + h] = s_log[e];
+  }
+  if (rows)
+    for (int e = threadIdx.x; e < nt * Hq; e += kThreads) {
+      const int t = e / Hq, h = e - t * Hq;
+      rows[((int64_t)l * Hq + h) * T_total + tok0 + t_begin + t] = s_log[e];
+    }
+}
+
 template <typename T, int DH, int GM>
 __global__ __launch_bounds__(kThreads) void k_score_partial(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req, int R, int Hq,
-    int Hkv, int g, int HG, int CH, int64_t C_total, int64_t T_total, int64_t N_total,
-    float scale, float *__restrict__ vlog, float4 *__restrict__ stats,
-    float *__restrict__ rows) {
+    int Hkv, int g, int HG, int CH, int64_t C_total, int64_t T_total, int GL, float scale,
+    float *__restrict__ vlog, float4 *__restrict__ stats, float *__restrict__ rows) {
   using RS = RowShape<T, DH>;
   extern __shared__ float s_logit[];   // [GM][CH]
   __shared__ float s_red[kWaves][GM];
@@ -151,7 +376,6 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rr = lane >> 3, sub = lane & 7;
 
-  // This lane's slice of every query vector, widened to fp32 once.
   float qf[GM][RS::kElems];
 #pragma unroll
   for (int hh = 0; hh < GM; ++hh) {
@@ -204,8 +428,6 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
   }
   __syncthreads();
 
-  // Chunk statistics per head: max over every token, then sums of exp(l - m)
-  // over every token and over the visual ones.
   const int v_r = vis_start[r];
   const int N_r = cu_vis[r + 1] - cu_vis[r];
   const int vb = max(0, v_r - t_begin), ve = min(nt, v_r + N_r - t_begin);
@@ -236,10 +458,8 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
         z += e;
         if (t >= vb && t < ve) v += e;
       }
-    z = wave_sum(z);
-    v = wave_sum(v);
-    zs[hh] = z;
-    vs[hh] = v;
+    zs[hh] = wave_sum(z);
+    vs[hh] = wave_sum(v);
   }
 #pragma unroll
   for (int hh = 0; hh < GM; ++hh)
@@ -270,11 +490,11 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
     stats[((int64_t)l * Hq + h0 + hh) * C_total + c] = make_float4(mm, zz, x, 0.f);
   }
 
-  // Raw scaled logits of the visual columns (and of every column if asked).
-  const int64_t vdst0 = (int64_t)cu_vis[r] + t_begin - v_r;
+  const int GH = GL * Hq;
+  const int64_t vtok0 = (int64_t)cu_vis[r] + t_begin - v_r;
   for (int hh = 0; hh < gh; ++hh) {
-    float *dst = vlog + ((int64_t)l * Hq + h0 + hh) * N_total + vdst0;
-    for (int t = vb + threadIdx.x; t < ve; t += kThreads) dst[t] = s_logit[hh * CH + t];
+    for (int t = vb + threadIdx.x; t < ve; t += kThreads)
+      vlog[(vtok0 + t) * GH + (int64_t)l * Hq + h0 + hh] = s_logit[hh * CH + t];
     if (rows) {
       float *rd = rows + ((int64_t)l * Hq + h0 + hh) * T_total + tok0 + t_begin;
       for (int t = threadIdx.x; t < nt; t += kThreads) rd[t] = s_logit[hh * CH + t];
@@ -282,17 +502,15 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_score_finalize(
-    const float *__restrict__ vlog, const float4 *__restrict__ stats,
-    const int32_t *__restrict__ cu_vis, const int32_t *__restrict__ chunk_off,
-    const int32_t *__restrict__ slice_off, const int32_t *__restrict__ slice_req, int GH,
-    int64_t C_total, int64_t N_total, int SL, float *__restrict__ scores) {
-  __shared__ float sM[kMaxPairs], sInvZ[kMaxPairs], sMass[kMaxPairs];
+// Per request: merge the chunk statistics of every (layer, head) row into its
+// max M and 1/Z, and the total visual mass S = sum_{l,h} V / Z (= sum_i s_i).
+__global__ __launch_bounds__(kThreads) void k_score_merge(
+    const float4 *__restrict__ stats, const int32_t *__restrict__ chunk_off, int GH,
+    int64_t C_total, float2 *__restrict__ rowstat, float *__restrict__ mass) {
   __shared__ float s_red[kWaves];
-  const int b = blockIdx.x;
-  const int r = slice_req[b];
-  const int sl = b - slice_off[r];
+  const int r = blockIdx.x;
   const int c0 = chunk_off[r], c1 = chunk_off[r + 1];
+  float part = 0.f;
   for (int p = threadIdx.x; p < GH; p += kThreads) {
     const float4 *st = stats + (int64_t)p * C_total;
     float M = -INFINITY;
@@ -304,26 +522,49 @@ __global__ __launch_bounds__(kThreads) void k_score_finalize(
       Z = fmaf(s.y, e, Z);
       V = fmaf(s.z, e, V);
     }
-    sM[p] = M;
-    sInvZ[p] = 1.0f / Z;
-    sMass[p] = V / Z;
+    rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
+    part += V / Z;
   }
-  __syncthreads();
-  float part = 0.f;
-  for (int p = threadIdx.x; p < GH; p += kThreads) part += sMass[p];
   part = wave_sum(part);
   if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = part;
   __syncthreads();
-  float S = 0.f;
-  for (int w = 0; w < kWaves; ++w) S += s_red[w];
-  const float invS = 1.0f / S;
+  if (threadIdx.x == 0) {
+    float S = 0.f;
+    for (int w = 0; w < kWaves; ++w) S += s_red[w];
+    mass[r] = S;
+  }
+}
 
+// s_i = sum_{l,h} exp(l_i - M) / Z (Eq. 6-7), divided by S (Eq. 8).
+__global__ __launch_bounds__(kThreads) void k_score_finalize(
+    const float *__restrict__ vlog, const float2 *__restrict__ rowstat,
+    const float *__restrict__ mass, const int32_t *__restrict__ cu_vis,
+    const int32_t *__restrict__ slice_off, const int32_t *__restrict__ slice_req, int GH, int SL,
+    float *__restrict__ scores) {
+  __shared__ float2 sMZ[kMaxPairs];
+  const int b = blockIdx.x;
+  const int r = slice_req[b];
+  const int sl = b - slice_off[r];
+  for (int p = threadIdx.x; p < GH; p += kThreads) sMZ[p] = rowstat[(int64_t)r * GH + p];
+  __syncthreads();
+  const float invS = 1.0f / mass[r];
   const int64_t n0 = cu_vis[r];
   const int N_r = cu_vis[r + 1] - (int)n0;
   const int end = min(N_r, (sl + 1) * SL);
   for (int i = sl * SL + threadIdx.x; i < end; i += kThreads) {
+    const float *lg = vlog + (n0 + i) * GH;
     float acc = 0.f;
-    for (int p = 0; p < GH; ++p) acc = fmaf(expf(vlog[(int64_t)p * N_total + n0 + i] - sM[p]), sInvZ[p], acc);
+    if ((GH & 3) == 0) {
+      for (int p = 0; p < GH; p += 4) {
+        const float4 x = *reinterpret_cast<const float4 *>(lg + p);
+        acc = fmaf(expf(x.x - sMZ[p].x), sMZ[p].y, acc);
+        acc = fmaf(expf(x.y - sMZ[p + 1].x), sMZ[p + 1].y, acc);
+        acc = fmaf(expf(x.z - sMZ[p + 2].x), sMZ[p + 2].y, acc);
+        acc = fmaf(expf(x.w - sMZ[p + 3].x), sMZ[p + 3].y, acc);
+      }
+    } else {
+      for (int p = 0; p < GH; ++p) acc = fmaf(expf(lg[p] - sMZ[p].x), sMZ[p].y, acc);
+    }
     scores[n0 + i] = acc * invS;
   }
 }
@@ -347,6 +588,33 @@ __global__ __launch_bounds__(kThreads) void k_rows_finalize(
 }
 
 template <typename T, int DH>
+hipError_t launch_stream_dh(const last_batch *b, const last::ScorePlan &p, const last::ScoreWs &w,
+                            const void *q, const void *k, float *attn_rows, float scale,
+                            hipStream_t s) {
+  const int g = b->Hq / b->Hkv;
+  const int64_t blocks = (int64_t)b->G * p.C_total;
+  const size_t lds = (size_t)p.chunk_tokens * b->Hq * sizeof(float);
+  last::launch_begin("score_partial", s);
+#define LAST_LAUNCH_GQ(GQV)                                                                        \
+  hipLaunchKernelGGL((k_score_stream<T, DH, GQV>), dim3((unsigned)blocks), dim3(kThreads), lds, s, \
+                     (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,          \
+                     w.chunk_off, w.chunk_req, b->R, b->Hq, b->Hkv, p.chunk_tokens, p.C_total,   \
+                     p.T_total, b->G, scale, w.vlog, w.stats, attn_rows)
+  switch (g) {
+    case 1: LAST_LAUNCH_GQ(1); break;
+    case 2: LAST_LAUNCH_GQ(2); break;
+    case 3: LAST_LAUNCH_GQ(3); break;
+    case 4: LAST_LAUNCH_GQ(4); break;
+    case 5: LAST_LAUNCH_GQ(5); break;
+    case 6: LAST_LAUNCH_GQ(6); break;
+    case 7: LAST_LAUNCH_GQ(7); break;
+    default: LAST_LAUNCH_GQ(8); break;
+  }
+#undef LAST_LAUNCH_GQ
+  return last::launch_end(s);
+}
+
+template <typename T, int DH>
 hipError_t launch_partial_dh(const last_batch *b, const last::ScorePlan &p,
                              const last::ScoreWs &w, const void *q, const void *k,
                              float *attn_rows, float scale, hipStream_t s) {
@@ -358,7 +626,7 @@ hipError_t launch_partial_dh(const last_batch *b, const last::ScorePlan &p,
   hipLaunchKernelGGL((k_score_partial<T, DH, GMV>), dim3((unsigned)blocks), dim3(kThreads), lds, \
                      s, (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,      \
                      w.chunk_off, w.chunk_req, b->R, b->Hq, b->Hkv, g, p.head_groups,           \
-                     p.chunk_tokens, p.C_total, p.T_total, p.N_total, scale, w.vlog, w.stats,    \
+                     p.chunk_tokens, p.C_total, p.T_total, b->G, scale, w.vlog, w.stats,         \
                      attn_rows)
   switch (p.g_max) {
     case 1: LAST_LAUNCH_GM(1); break;
@@ -377,17 +645,30 @@ namespace last {
 ScorePlan make_score_plan(const last_batch *b) {
   ScorePlan p{};
   const int g = b->Hq / b->Hkv;
-  p.g_max = g <= 1 ? 1 : g <= 2 ? 2 : g <= 4 ? 4 : 8;
-  p.head_groups = (g + p.g_max - 1) / p.g_max;
   p.T_total = b->cu_seqlens_h[b->R];
   p.N_total = b->cu_vis_h[b->R];
-  // Aim for ~2048 blocks (8 per CU) while keeping each chunk's logits in LDS.
-  const int64_t rows = (int64_t)b->G * b->Hkv * p.head_groups * p.T_total;
-  int64_t ch = (rows + 2047) / 2048;
-  ch = (ch + 63) / 64 * 64;
-  const int64_t ch_cap = std::min<int64_t>(kMaxChunk, kLdsLogitFloats / p.g_max);
-  p.chunk_tokens = (int32_t)std::max<int64_t>(256, std::min<int64_t>(ch, ch_cap));
   p.slice_tokens = kSliceTokens;
+  const int64_t elt = b->qk_dtype == LAST_BF16 ? 2 : 4;
+  // The streaming kernel keeps one KV head per lane; that needs Hkv | 32 and at
+  // most 8 query heads per KV head.
+  p.stream = (8 * kWaves) % b->Hkv == 0 && g <= 8;
+  if (p.stream) {
+    p.g_max = g;
+    p.head_groups = 1;
+    const int64_t tok_bytes = (int64_t)b->Hkv * b->Dh * elt;
+    int64_t ch = (kWgBytes + tok_bytes - 1) / tok_bytes;
+    ch = std::min<int64_t>(ch, kLdsLogitFloats / b->Hq);   // the chunk's logits live in LDS
+    p.chunk_tokens = (int32_t)std::max<int64_t>(1, ch);
+  } else {
+    p.g_max = g <= 1 ? 1 : g <= 2 ? 2 : g <= 4 ? 4 : 8;
+    p.head_groups = (g + p.g_max - 1) / p.g_max;
+    // ~2048 blocks while each chunk's logits fit in LDS
+    const int64_t rows = (int64_t)b->G * b->Hkv * p.head_groups * p.T_total;
+    int64_t ch = (rows + 2047) / 2048;
+    ch = (ch + 63) / 64 * 64;
+    const int64_t ch_cap = std::min<int64_t>(kMaxChunk, kLdsLogitFloats / p.g_max);
+    p.chunk_tokens = (int32_t)std::max<int64_t>(256, std::min<int64_t>(ch, ch_cap));
+  }
   p.C_total = 0;
   p.S_total = 0;
   for (int r = 0; r < b->R; ++r) {
@@ -408,6 +689,8 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
   w.slice_req = cv.take<int32_t>(p.S_total);
   w.stats = cv.take<float4>((size_t)b->G * b->Hq * p.C_total);
   w.vlog = cv.take<float>((size_t)b->G * b->Hq * p.N_total);
+  w.rowstat = cv.take<float2>((size_t)b->R * b->G * b->Hq);
+  w.mass = cv.take<float>(b->R);
   *bytes = cv.size();
   return w;
 }
@@ -424,18 +707,29 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
   hipError_t e = launch_end(s);
   if (e != hipSuccess) return e;
 
-  if (b->qk_dtype == LAST_BF16)
-    e = b->Dh == 64 ? launch_partial_dh<uint16_t, 64>(b, p, w, q, k, attn_rows, scale, s)
-                    : launch_partial_dh<uint16_t, 128>(b, p, w, q, k, attn_rows, scale, s);
+  const bool bf = b->qk_dtype == LAST_BF16;
+  if (p.stream)
+    e = bf ? (b->Dh == 64 ? launch_stream_dh<uint16_t, 64>(b, p, w, q, k, attn_rows, scale, s)
+                          : launch_stream_dh<uint16_t, 128>(b, p, w, q, k, attn_rows, scale, s))
+           : (b->Dh == 64 ? launch_stream_dh<float, 64>(b, p, w, q, k, attn_rows, scale, s)
+                          : launch_stream_dh<float, 128>(b, p, w, q, k, attn_rows, scale, s));
   else
-    e = b->Dh == 64 ? launch_partial_dh<float, 64>(b, p, w, q, k, attn_rows, scale, s)
-                    : launch_partial_dh<float, 128>(b, p, w, q, k, attn_rows, scale, s);
+    e = bf ? (b->Dh == 64 ? launch_partial_dh<uint16_t, 64>(b, p, w, q, k, attn_rows, scale, s)
+                          : launch_partial_dh<uint16_t, 128>(b, p, w, q, k, attn_rows, scale, s))
+           : (b->Dh == 64 ? launch_partial_dh<float, 64>(b, p, w, q, k, attn_rows, scale, s)
+                          : launch_partial_dh<float, 128>(b, p, w, q, k, attn_rows, scale, s));
+  if (e != hipSuccess) return e;
+
+  launch_begin("score_merge", s);
+  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)b->R), dim3(kThreads), 0, s, w.stats, w.chunk_off,
+                     b->G * b->Hq, p.C_total, w.rowstat, w.mass);
+  e = launch_end(s);
   if (e != hipSuccess) return e;
 
   launch_begin("score_finalize", s);
   hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog,
-                     w.stats, b->cu_vis, w.chunk_off, w.slice_off, w.slice_req, b->G * b->Hq,
-                     p.C_total, p.N_total, p.slice_tokens, scores);
+                     w.rowstat, w.mass, b->cu_vis, w.slice_off, w.slice_req, b->G * b->Hq,
+                     p.slice_tokens, scores);
   e = launch_end(s);
   if (e != hipSuccess || !attn_rows) return e;
 

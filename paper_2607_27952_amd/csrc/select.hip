@@ -7,18 +7,19 @@
 // passes over X), the distances are formed once as a matrix on the matrix
 // cores and each step reads one row of it:
 //
-//   k_select_plan   per-request Gram tile prefix, tile -> request map and the
-//                   element offset of each request's N_r x N_r block.
-//   k_sqnorm_bf16   |x_i|^2 with the very arithmetic the Gram uses for its
-//                   diagonal (32x32x16 bf16 MFMA, fp32 partial sums over
-//                   64-element chunks folded into fp64), so that a row and
-//                   its bitwise duplicate get coverage distance exactly 0.
-//   k_gram_bf16     upper-triangular 128x128 tiles of X_r X_r^T on MFMA
+//   k_select_plan   per-request prefixes of the diagonal and off-diagonal
+//                   Gram tiles, tile -> request maps, and the element offset
+//                   of each request's N_r x N_r block.
+//   k_gram_bf16     128x128 tiles of X_r X_r^T on MFMA
 //                   (v_mfma_f32_32x32x16_bf16; bf16 products are exact, the
 //                   fp32 accumulator is folded into fp64 every 64 elements),
 //                   then delta_ij = max(0, 1 - dot_ij / (|x_i| |x_j|)) in fp64,
-//                   stored as fp32 in both (i, j) and (j, i).
-//   k_sqnorm_f32 / k_gram_f32   the same for fp32 features, in fp64 VALU FMAs.
+//                   stored as fp32. A first launch over the diagonal tiles also
+//                   yields |x_i|^2 from the same arithmetic (so a row and its
+//                   bitwise duplicate get distance exactly 0); a second launch
+//                   covers the tiles above the diagonal and mirrors them.
+//   k_sqnorm_f32 / k_gram_f32   the same for fp32 features, in fp64 VALU FMAs
+//                   (norms in a separate pass with the dots' loop order).
 //   k_greedy        one block per request; w and delta live in registers.
 //                   Step t loads row j_{t-1} of the distance block, folds it
 //                   into delta with min, and takes the block-wide argmax of
@@ -44,11 +45,9 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kTile = last::kGramTile;   // 128
 constexpr int kKS = 64;                  // elements per k stage = one fp64 fold chunk
-constexpr int kLdsPitch = kKS + 8;       // bf16 per LDS row (pad against bank conflicts)
-constexpr int kGramThreads = 256;
 
 // ------------------------------------------------------------------ plan
-__device__ int block_excl_scan_i64(int64_t v, int64_t *sh, int64_t *total, int64_t *out) {
+__device__ void block_excl_scan_i64(int64_t v, int64_t *sh, int64_t *total, int64_t *out) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int64_t x = v;
   for (int o = 1; o < 64; o <<= 1) {
@@ -65,242 +64,535 @@ __device__ int block_excl_scan_i64(int64_t v, int64_t *sh, int64_t *total, int64
   __syncthreads();
   *total = tot;
   *out = before + x - v;
-  return 0;
 }
 
+// Per request: nb = ceil(N / 128) row blocks give nb diagonal Gram tiles and
+// nb (nb - 1) / 2 tiles above the diagonal; the N x N block starts at d_off.
 __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__ cu_vis, int R,
-                                                     int64_t tiles_cap,
-                                                     int32_t *__restrict__ tile_off,
-                                                     int32_t *__restrict__ tile_req,
+                                                     int64_t diag_cap, int64_t off_cap,
+                                                     int32_t *__restrict__ dtile_off,
+                                                     int32_t *__restrict__ dtile_req,
+                                                     int32_t *__restrict__ otile_off,
+                                                     int32_t *__restrict__ otile_req,
                                                      int64_t *__restrict__ d_off) {
   __shared__ int64_t sh[4];
-  int64_t carry_t = 0, carry_d = 0;
+  int64_t carry_d = 0, carry_o = 0, carry_m = 0;
   for (int base = 0; base < R; base += 256) {
     const int r = base + (int)threadIdx.x;
-    int64_t nt = 0, nd = 0;
+    int64_t nd = 0, no = 0, nm = 0;
     if (r < R) {
       const int64_t N = cu_vis[r + 1] - cu_vis[r];
-      const int64_t tb = (N + kTile - 1) / kTile;
-      nt = tb * (tb + 1) / 2;
-      nd = N * N;
+      nd = (N + kTile - 1) / kTile;
+      no = nd * (nd - 1) / 2;
+      nm = N * N;
     }
-    int64_t tt, td, pt, pd;
-    block_excl_scan_i64(nt, sh, &tt, &pt);
+    int64_t td, to, tm, pd, po, pm;
     block_excl_scan_i64(nd, sh, &td, &pd);
-    pt += carry_t;
+    block_excl_scan_i64(no, sh, &to, &po);
+    block_excl_scan_i64(nm, sh, &tm, &pm);
     pd += carry_d;
+    po += carry_o;
+    pm += carry_m;
     if (r < R) {
-      tile_off[r] = (int32_t)pt;
-      d_off[r] = pd;
-      for (int64_t c = 0; c < nt; ++c)
-        if (pt + c < tiles_cap) tile_req[pt + c] = r;
+      dtile_off[r] = (int32_t)pd;
+      otile_off[r] = (int32_t)po;
+      d_off[r] = pm;
+      for (int64_t c = 0; c < nd; ++c)
+        if (pd + c < diag_cap) dtile_req[pd + c] = r;
+      for (int64_t c = 0; c < no; ++c)
+        if (po + c < off_cap) otile_req[po + c] = r;
     }
-    carry_t += tt;
     carry_d += td;
+    carry_o += to;
+    carry_m += tm;
   }
   if (threadIdx.x == 0) {
-    tile_off[R] = (int32_t)carry_t;
-    d_off[R] = carry_d;
+    dtile_off[R] = (int32_t)carry_d;
+    otile_off[R] = (int32_t)carry_o;
+    d_off[R] = carry_m;
   }
 }
 
-// ------------------------------------------------- shared MFMA arithmetic
-// One fold chunk: four 16-deep MFMA steps accumulated in fp32 from zero.
-// a[s], b[s] hold this lane's operands for step s (row l%32, elements
-// chunk*64 + s*16 + (l/32)*8 .. +8). Both the Gram tiles and the norm pass
-// go through this function, so equal operands give bitwise-equal sums.
-__device__ __forceinline__ f32x16 mfma_chunk(const bf16x8 (&a)[4], const bf16x8 (&b)[4]) {
-  f32x16 acc = {};
-#pragma unroll
-  for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[s], b[s], acc, 0, 0, 0);
-  return acc;
-}
-
-__device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t *p) {
-  const uint4 v = *reinterpret_cast<const uint4 *>(p);
-  return __builtin_bit_cast(bf16x8, v);
-}
-
-// |x_i|^2 for bf16 features: one wave per 32 consecutive rows (rows past
-// N_total use zeros; every row's norm only involves itself).
-__global__ __launch_bounds__(256) void k_sqnorm_bf16(const uint16_t *__restrict__ X, int64_t N_total,
-                                                     int Dv, double *__restrict__ nn) {
-  const int lane = threadIdx.x & 63;
-  const int64_t row0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 32;
-  if (row0 >= N_total) return;
-  const int64_t row = row0 + (lane & 31);
-  const bool valid = row < N_total;
-  const uint16_t *xp = X + (valid ? row : 0) * Dv + (lane >> 5) * 8;
-  f32x16 zero = {};
-  double acc64[16];
-#pragma unroll
-  for (int v = 0; v < 16; ++v) acc64[v] = 0.0;
-  const int nchunks = (Dv + kKS - 1) / kKS;
-  for (int ch = 0; ch < nchunks; ++ch) {
-    bf16x8 a[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const int kk = ch * kKS + s * 16 + (lane >> 5) * 8;
-      if (valid && kk < Dv)
-        a[s] = load_bf16x8(xp + ch * kKS + s * 16);
-      else
-        a[s] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
-    }
-    const f32x16 acc = mfma_chunk(a, a);
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc64[v] += (double)acc[v];
+// Map a request-local index of the tiles strictly above the diagonal to (I, J).
+__device__ __forceinline__ void tile_ij_upper(int t, int nb, int &I, int &J) {
+  int i = 0, rem = t;
+  while (rem >= nb - 1 - i) {
+    rem -= nb - 1 - i;
+    ++i;
   }
-  (void)zero;
-  // lane l holds column c = l%32, rows (l/32)*4 + (v%4) + 8*(v/4); the diagonal
-  // element of column c sits in the half hi = (c%8)/4 at v = 4*(c/8) + (c%8) - 4*hi.
-  const int c = lane & 31, hi = lane >> 5;
-  if (((c & 7) >> 2) == hi) {
-    const int vsel = 4 * (c >> 3) + (c & 7) - 4 * hi;
-    double d = 0.0;
-#pragma unroll
-    for (int v = 0; v < 16; ++v)
-      if (v == vsel) d = acc64[v];
-    if (row0 + c < N_total) nn[row0 + c] = d;
-  }
+  I = i;
+  J = i + 1 + rem;
 }
 
-__device__ __forceinline__ float coverage(double dot, double nni, double nnj) {
+__device__ __forceinline__ float coverage(double dot, double nni, double nnj, double invi, double invj) {
   // Eq. 10 term: 1 - cos, clamped at 0. Zero-norm rows have cosine 0.
   // Bitwise-identical rows give dot == nni == nnj exactly, hence distance 0.
   if (nni <= 0.0 || nnj <= 0.0) return 1.0f;
   if (dot == nni && nni == nnj) return 0.0f;
-  const double t = 1.0 - dot / sqrt(nni * nnj);
+  const double t = 1.0 - dot * invi * invj;
   return t > 0.0 ? (float)t : 0.0f;
 }
 
-// Map a request-local upper-triangular tile index to (I, J), I <= J.
-__device__ __forceinline__ void tile_ij(int t, int nb, int &I, int &J) {
-  int i = 0, rem = t;
-  while (rem >= nb - i) {
-    rem -= nb - i;
-    ++i;
-  }
-  I = i;
-  J = i + rem;
-}
+// ------------------------------------------------- Gram on the matrix cores
+// Dot products accumulate in fp32 over stages of 64 columns (four 16-deep
+// v_mfma_f32_32x32x16_bf16 steps starting from zero); each stage's partial
+// sums are then added into fp64 totals. Diagonal tiles (which also yield the
+// squared norms) and off-diagonal tiles run this same schedule, so equal
+// operand rows give bitwise-equal sums.
+//
+// Block tile 128 x 128 (rows of X_r against rows of X_r), WM x WN waves, each
+// wave TM x TN MFMA tiles of 32 x 32. A stage of each operand is 128 rows x
+// 64 bf16 in LDS, the 16-byte piece p of row r at slot r*8 + (p ^ ((r>>1)&7))
+// so that the fragment reads of 16 consecutive rows hit distinct banks. Two
+// stages alternate; the next stage is fetched into registers while the
+// current one feeds the matrix cores.
+#ifndef LAST_GRAM_LAYOUT
+#define LAST_GRAM_LAYOUT 1
+#endif
+#if LAST_GRAM_LAYOUT == 0
+constexpr int kWM = 2, kWN = 2, kTM = 2, kTN = 2;
+#elif LAST_GRAM_LAYOUT == 1
+constexpr int kWM = 4, kWN = 2, kTM = 1, kTN = 2;
+#else
+constexpr int kWM = 4, kWN = 4, kTM = 1, kTN = 1;
+#endif
+constexpr int kGramWaves = kWM * kWN;
+constexpr int kGramThreads = 64 * kGramWaves;
+constexpr int kPieces = kTile * 8;                     // 16-byte pieces per operand stage
+constexpr int kLoadsPerThread = kPieces / kGramThreads;
+static_assert(kWM * kTM == 4 && kWN * kTN == 4, "128 x 128 block tile");
 
-__global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
+__device__ __forceinline__ int lds_slot(int row, int piece) { return row * 8 + (piece ^ ((row >> 1) & 7)); }
+
+template <bool DIAG>
+__global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
     const uint16_t *__restrict__ X, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
-    const int64_t *__restrict__ d_off, const double *__restrict__ nn, int Dv, int64_t tiles_total,
-    int64_t d_cap, float *__restrict__ dmat) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[kTile * kLdsPitch];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[kTile * kLdsPitch];
+    const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv, int Dv,
+    int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
+  __shared__ uint4 sA[2][kPieces];
+  __shared__ uint4 sB[DIAG ? 1 : 2][DIAG ? 1 : kPieces];
+  __shared__ double s_nn[2][kTile], s_inv[2][kTile];   // [0]: rows of A, [1]: rows of B
 
-  // XCD-aware order: consecutive logical tiles (same request, shared row
-  // blocks) go to the same XCD, which receives every 8th block.
-  const int64_t nb_grid = gridDim.x;
-  const int64_t per_xcd = nb_grid / 8;
-  const int64_t t_glob = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  if (t_glob >= tiles_total) return;
-  const int r = tile_req[t_glob];
+  int64_t t = blockIdx.x;
+  if (!DIAG) {
+    // XCD-aware order: consecutive tiles (same request, shared row blocks)
+    // go to the same XCD, which receives every 8th block.
+    const int64_t per_xcd = gridDim.x / 8;
+    t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  }
+  if (t >= tiles) return;
+  const int r = tile_req[t];
   const int64_t n0 = cu_vis[r];
   const int N = cu_vis[r + 1] - (int)n0;
   const int nb = (N + kTile - 1) / kTile;
   int I, J;
-  tile_ij((int)(t_glob - tile_off[r]), nb, I, J);
+  if (DIAG) {
+    I = J = (int)(t - tile_off[r]);
+  } else {
+    tile_ij_upper((int)(t - tile_off[r]), nb, I, J);
+  }
   const int rowA0 = I * kTile, rowB0 = J * kTile;
+  const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
   const uint16_t *XA = X + (n0 + rowA0) * Dv;
   const uint16_t *XB = X + (n0 + rowB0) * Dv;
-  const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wy = wave >> 1, wx = wave & 1;
+  const int wm = wave / kWN, wn = wave % kWN;
 
-  double acc64[2][2][16];
+  double acc64[kTM][kTN][16];
+  f32x16 acc[kTM][kTN];
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int tm = 0; tm < kTM; ++tm)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+    for (int tn = 0; tn < kTN; ++tn) {
+      acc[tm][tn] = f32x16{};
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc64[mi][ni][v] = 0.0;
+      for (int v = 0; v < 16; ++v) acc64[tm][tn][v] = 0.0;
+    }
 
-  // global -> LDS staging: thread covers rows tid/8 + 32*j, 16-byte piece tid%8
-  const int lrow = tid >> 3, lpiece = tid & 7;
-  const int nchunks = (Dv + kKS - 1) / kKS;
-  uint4 ra[4], rb[4];
+  uint4 ra[kLoadsPerThread], rb[DIAG ? 1 : kLoadsPerThread];
   auto gload = [&](int ch) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = lrow + 32 * j;
-      const int kk = ch * kKS + lpiece * 8;
-      ra[j] = (row < nA && kk < Dv) ? *reinterpret_cast<const uint4 *>(XA + (int64_t)row * Dv + kk)
-                                    : make_uint4(0, 0, 0, 0);
-      rb[j] = (row < nB && kk < Dv) ? *reinterpret_cast<const uint4 *>(XB + (int64_t)row * Dv + kk)
-                                    : make_uint4(0, 0, 0, 0);
+    for (int j = 0; j < kLoadsPerThread; ++j) {
+      const int e = tid + kGramThreads * j, row = e >> 3, k = ch * kKS + (e & 7) * 8;
+      ra[j] = (row < nA && k < Dv) ? *reinterpret_cast<const uint4 *>(XA + (int64_t)row * Dv + k)
+                                   : make_uint4(0, 0, 0, 0);
+      if (!DIAG)
+        rb[DIAG ? 0 : j] = (row < nB && k < Dv) ? *reinterpret_cast<const uint4 *>(XB + (int64_t)row * Dv + k)
+                                                : make_uint4(0, 0, 0, 0);
     }
   };
-  gload(0);
-  for (int ch = 0; ch < nchunks; ++ch) {
-    __syncthreads();
+  auto sstore = [&](int buf) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = lrow + 32 * j;
-      *reinterpret_cast<uint4 *>(&sA[row * kLdsPitch + lpiece * 8]) = ra[j];
-      *reinterpret_cast<uint4 *>(&sB[row * kLdsPitch + lpiece * 8]) = rb[j];
+    for (int j = 0; j < kLoadsPerThread; ++j) {
+      const int e = tid + kGramThreads * j, slot = lds_slot(e >> 3, e & 7);
+      sA[buf][slot] = ra[j];
+      if (!DIAG) sB[DIAG ? 0 : buf][slot] = rb[DIAG ? 0 : j];
     }
+  };
+
+  const int nch = (Dv + kKS - 1) / kKS;
+  gload(0);
+  sstore(0);
+  __syncthreads();
+  for (int ch = 0; ch < nch; ++ch) {
+    const int buf = ch & 1;
+    if (ch + 1 < nch) gload(ch + 1);
+    const uint4 *pa = sA[buf];
+    const uint4 *pb = DIAG ? sA[buf] : sB[DIAG ? 0 : buf];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int piece = s * 2 + (lane >> 5);
+      bf16x8 a[kTM], b[kTN];
+#pragma unroll
+      for (int tm = 0; tm < kTM; ++tm)
+        a[tm] = __builtin_bit_cast(bf16x8, pa[lds_slot((wm * kTM + tm) * 32 + (lane & 31), piece)]);
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn)
+        b[tn] = __builtin_bit_cast(bf16x8, pb[lds_slot((wn * kTN + tn) * 32 + (lane & 31), piece)]);
+#pragma unroll
+      for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < kTN; ++tn)
+          acc[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[tm], b[tn], acc[tm][tn], 0, 0, 0);
+    }
+#pragma unroll
+    for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc64[tm][tn][v] += (double)acc[tm][tn][v];
+        acc[tm][tn] = f32x16{};
+      }
+    if (ch + 1 < nch) sstore((ch + 1) & 1);
     __syncthreads();
-    if (ch + 1 < nchunks) gload(ch + 1);
-    bf16x8 a[2][4], b[2][4];
-#pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int row = wy * 64 + mi * 32 + (lane & 31);
-        a[mi][s] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const uint4 *>(&sA[row * kLdsPitch + s * 16 + (lane >> 5) * 8]));
-      }
-#pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int row = wx * 64 + ni * 32 + (lane & 31);
-        b[ni][s] = __builtin_bit_cast(
-            bf16x8, *reinterpret_cast<const uint4 *>(&sB[row * kLdsPitch + s * 16 + (lane >> 5) * 8]));
-      }
-#pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const f32x16 acc = mfma_chunk(a[mi], b[ni]);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) acc64[mi][ni][v] += (double)acc[v];
-      }
   }
 
-  // Epilogue: coverage distances, written to (i, j) and mirrored to (j, i).
+  // Squared norms (diagonal tiles) or the norms of both row blocks, into LDS.
+  // In a 32 x 32 MFMA tile, lane l holds column l%32 and rows
+  // (l/32)*4 + (v%4) + 8*(v/4); column c's diagonal element is in half
+  // hi = (c%8)/4 at v = 4*(c/8) + (c%8) - 4*hi.
+  if (DIAG) {
+#pragma unroll
+    for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn) {
+        if (wm * kTM + tm != wn * kTN + tn) continue;
+        const int c = lane & 31, hi = lane >> 5;
+        if (((c & 7) >> 2) != hi) continue;
+        const int vsel = 4 * (c >> 3) + (c & 7) - 4 * hi;
+        double d = 0.0;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (v == vsel) d = acc64[tm][tn][v];
+        s_nn[0][(wm * kTM + tm) * 32 + c] = d;
+      }
+    __syncthreads();
+    for (int i = tid; i < kTile; i += kGramThreads) {
+      const double v = s_nn[0][i];
+      const double iv = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
+      s_inv[0][i] = iv;
+      s_nn[1][i] = v;
+      s_inv[1][i] = iv;
+      if (i < nA) {
+        nn[n0 + rowA0 + i] = v;
+        inv[n0 + rowA0 + i] = iv;
+      }
+    }
+  } else {
+    for (int i = tid; i < 2 * kTile; i += kGramThreads) {
+      const int side = i / kTile, x = i % kTile;
+      const int row = (side ? rowB0 : rowA0) + x;
+      const bool ok = x < (side ? nB : nA);
+      s_nn[side][x] = ok ? nn[n0 + row] : 0.0;
+      s_inv[side][x] = ok ? inv[n0 + row] : 0.0;
+    }
+  }
+  __syncthreads();
+
+  // Coverage distances, written to (i, j) and, off the diagonal, to (j, i).
   float *D = dmat + d_off[r];
-  const double *nnr = nn + n0;
   const int64_t dlim = d_cap - d_off[r];
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int tm = 0; tm < kTM; ++tm)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      const int j = rowB0 + wx * 64 + ni * 32 + (lane & 31);
-      const double nnj = j < N ? nnr[j] : 0.0;
+    for (int tn = 0; tn < kTN; ++tn) {
+      const int jl = (wn * kTN + tn) * 32 + (lane & 31), j = rowB0 + jl;
+      const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
 #pragma unroll
       for (int vq = 0; vq < 4; ++vq) {
-        const int ibase = rowA0 + wy * 64 + mi * 32 + (lane >> 5) * 4 + 8 * vq;
+        const int il0 = (wm * kTM + tm) * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
         float dv[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const int i = ibase + u;
-          dv[u] = (i < N && j < N) ? coverage(acc64[mi][ni][4 * vq + u], nnr[i], nnj) : 0.f;
+          const int i = i0 + u;
+          dv[u] = (i < N && j < N) ? coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u], nnj,
+                                              s_inv[0][il0 + u], invj)
+                                   : 0.f;
           if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
         }
-        if (I != J && j < N) {
-          const int64_t o = (int64_t)j * N + ibase;
-          if (ibase + 3 < N && ((d_off[r] + o) & 3) == 0 && o + 3 < dlim) {
+        if (!DIAG && j < N) {
+          const int64_t o = (int64_t)j * N + i0;
+          if (i0 + 3 < N && ((d_off[r] + o) & 3) == 0 && o + 3 < dlim) {
             *reinterpret_cast<float4 *>(D + o) = make_float4(dv[0], dv[1], dv[2], dv[3]);
           } else {
 #pragma unroll
             for (int u = 0; u < 4; ++u)
-              if (ibase + u < N && o + u < dlim) D[o + u] = dv[u];
+              if (i0 + u < N && o + u < dlim) D[o + u] = dv[u];
+          }
+        }
+      }
+    }
+}
+
+// The same tiles with the operands streamed straight into LDS by
+// global_load_lds_dwordx4 (lane i's 16 bytes land at M0 + 16 i), through a
+// ring of kRing stages of 64 columns: the loads for stage ch + kRing - 1 are
+// in flight while stage ch feeds the matrix cores. The loads are issued from
+// inline assembly so that the compiler does not serialise every LDS read
+// behind them; this kernel waits for them itself (s_waitcnt vmcnt) before the
+// block barrier that publishes a stage. Each stage is one fold chunk; two
+// accumulator sets alternate so that folding chunk c - 1 into fp64 can overlap
+// the matrix-core work of chunk c. Needs Dv % 128 == 0 (an even stage count).
+#ifndef LAST_GRAM_RING
+#define LAST_GRAM_RING 4
+#endif
+constexpr int kRing = LAST_GRAM_RING;
+static_assert((kRing & (kRing - 1)) == 0, "power-of-two ring");
+constexpr int kDmaCols = kKS;                               // columns per ring stage (64)
+constexpr int kDmaPieces = kTile * kDmaCols * 2 / 16;       // 16-byte pieces per operand stage (1024)
+constexpr int kDmaInstr = kDmaPieces / 64;                  // wave instructions per operand stage (16)
+
+__device__ __forceinline__ uint32_t lds_u32(const void *p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void *)p);
+}
+
+// lds: wave-uniform LDS byte address (goes to M0); base: wave-uniform global
+// address; voff: this lane's byte offset from base.
+__device__ __forceinline__ void dma16(uint32_t lds, const void *base, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory");
+}
+__device__ __forceinline__ const void *uniform_ptr(const void *p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+template <bool DIAG>
+__global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
+    const uint16_t *__restrict__ X, const int32_t *__restrict__ cu_vis,
+    const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
+    const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv, int Dv,
+    int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
+  constexpr int kOps = DIAG ? 1 : 2;
+  constexpr int kInstr = kOps * kDmaInstr;                  // per stage, all operands
+  static_assert(kInstr % kGramWaves == 0, "even DMA split");
+  constexpr int kPerWave = kInstr / kGramWaves;
+  constexpr int kSteady = (kRing - 2) * kPerWave;           // loads allowed in flight at a stage boundary
+  static_assert(kSteady <= 15, "vmcnt immediate");
+  __shared__ uint4 sbuf[kRing][kOps][kDmaPieces];
+  __shared__ double s_nn[2][kTile], s_inv[2][kTile];
+
+  int64_t t = blockIdx.x;
+  if (!DIAG) {
+    // XCD-aware order: consecutive tiles (same request, shared row blocks)
+    // go to the same XCD, which receives every 8th block.
+    const int64_t per_xcd = gridDim.x / 8;
+    t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+  }
+  if (t >= tiles) return;
+  const int r = tile_req[t];
+  const int64_t n0 = cu_vis[r];
+  const int N = cu_vis[r + 1] - (int)n0;
+  const int nb = (N + kTile - 1) / kTile;
+  int I, J;
+  if (DIAG) {
+    I = J = (int)(t - tile_off[r]);
+  } else {
+    tile_ij_upper((int)(t - tile_off[r]), nb, I, J);
+  }
+  const int rowA0 = I * kTile, rowB0 = J * kTile;
+  const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / kWN, wn = wave % kWN;
+
+  // This wave's DMA instructions: q = wave + kGramWaves * x, operand q / 16,
+  // LDS slots (q % 16) * 64 + lane of the stage. The operand's row-block base
+  // and the LDS address are wave-uniform (scalar); each lane's byte offset
+  // within the row block is fixed for the whole loop.
+  const void *gbase[kPerWave];
+  uint32_t voff[kPerWave], dst[kPerWave];
+#pragma unroll
+  for (int x = 0; x < kPerWave; ++x) {
+    const int q = wave + kGramWaves * x, op = q / kDmaInstr, qi = q % kDmaInstr;
+    const int slot = qi * 64 + lane, row = slot >> 3, piece = (slot & 7) ^ (row & 7);
+    const int rr = min(row, (op ? nB : nA) - 1);
+    gbase[x] = uniform_ptr(X + (n0 + (op ? rowB0 : rowA0)) * (int64_t)Dv);
+    voff[x] = (uint32_t)((rr * (int64_t)Dv + piece * 8) * 2);
+    dst[x] = __builtin_amdgcn_readfirstlane(lds_u32(&sbuf[0][op][qi * 64]));
+  }
+  constexpr uint32_t kStageBytes = kOps * kDmaPieces * 16;
+  const int nst = Dv / kDmaCols;
+  auto issue = [&](int st) {
+    const uint32_t off = (uint32_t)(st & (kRing - 1)) * kStageBytes;
+#pragma unroll
+    for (int x = 0; x < kPerWave; ++x)
+      dma16(dst[x] + off, (const char *)gbase[x] + (int64_t)st * kDmaCols * 2, voff[x]);
+  };
+
+  // fragment slots: row (block row) * 8 + (piece ^ (row & 7))
+  int aslot[kTM][4], bslot[kTN][4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int piece = s * 2 + (lane >> 5);
+#pragma unroll
+    for (int tm = 0; tm < kTM; ++tm) {
+      const int row = (wm * kTM + tm) * 32 + (lane & 31);
+      aslot[tm][s] = row * 8 + (piece ^ (row & 7));
+    }
+#pragma unroll
+    for (int tn = 0; tn < kTN; ++tn) {
+      const int row = (wn * kTN + tn) * 32 + (lane & 31);
+      bslot[tn][s] = row * 8 + (piece ^ (row & 7));
+    }
+  }
+
+  double acc64[kTM][kTN][16];
+#pragma unroll
+  for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < kTN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc64[tm][tn][v] = 0.0;
+  f32x16 accP[kTM][kTN], accQ[kTM][kTN];
+
+  auto fold = [&](const f32x16 (&a)[kTM][kTN]) {
+#pragma unroll
+    for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc64[tm][tn][v] += (double)a[tm][tn][v];
+  };
+  // One stage: wait for it, publish it, refill the ring, run its four
+  // 16-deep MFMA steps into `cur` (from zero), and fold the previous chunk.
+  auto stage = [&](int ch, f32x16 (&cur)[kTM][kTN], const f32x16 (&prev)[kTM][kTN]) {
+    if (ch + kRing - 2 < nst)
+      vm_wait<kSteady>();
+    else
+      vm_wait<0>();
+    __syncthreads();
+    if (ch + kRing - 1 < nst) issue(ch + kRing - 1);
+    const uint4 *pa = sbuf[ch & (kRing - 1)][0];
+    const uint4 *pb = sbuf[ch & (kRing - 1)][kOps - 1];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      bf16x8 a[kTM], b[kTN];
+#pragma unroll
+      for (int tm = 0; tm < kTM; ++tm) a[tm] = __builtin_bit_cast(bf16x8, pa[aslot[tm][s]]);
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn) b[tn] = __builtin_bit_cast(bf16x8, pb[bslot[tn][s]]);
+#pragma unroll
+      for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < kTN; ++tn)
+          cur[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[tm], b[tn], s == 0 ? f32x16{} : cur[tm][tn],
+                                                                0, 0, 0);
+    }
+    fold(prev);
+  };
+
+  // nst is even here (Dv % 128 == 0); the first fold adds zeros, exactly.
+#pragma unroll
+  for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < kTN; ++tn) accQ[tm][tn] = f32x16{};
+  for (int st = 0; st < kRing - 1 && st < nst; ++st) issue(st);
+  for (int ch = 0; ch < nst; ch += 2) {
+    stage(ch, accP, accQ);
+    stage(ch + 1, accQ, accP);
+  }
+  fold(accQ);
+  __syncthreads();
+
+  // Squared norms (diagonal tiles) or the norms of both row blocks, into LDS.
+  // In a 32 x 32 MFMA tile, lane l holds column l%32 and rows
+  // (l/32)*4 + (v%4) + 8*(v/4); column c's diagonal element is in half
+  // hi = (c%8)/4 at v = 4*(c/8) + (c%8) - 4*hi.
+  if (DIAG) {
+#pragma unroll
+    for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn) {
+        if (wm * kTM + tm != wn * kTN + tn) continue;
+        const int c = lane & 31, hi = lane >> 5;
+        if (((c & 7) >> 2) != hi) continue;
+        const int vsel = 4 * (c >> 3) + (c & 7) - 4 * hi;
+        double d = 0.0;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (v == vsel) d = acc64[tm][tn][v];
+        s_nn[0][(wm * kTM + tm) * 32 + c] = d;
+      }
+    __syncthreads();
+    for (int i = tid; i < kTile; i += kGramThreads) {
+      const double v = s_nn[0][i];
+      const double iv = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
+      s_inv[0][i] = iv;
+      s_nn[1][i] = v;
+      s_inv[1][i] = iv;
+      if (i < nA) {
+        nn[n0 + rowA0 + i] = v;
+        inv[n0 + rowA0 + i] = iv;
+      }
+    }
+  } else {
+    for (int i = tid; i < 2 * kTile; i += kGramThreads) {
+      const int side = i / kTile, x = i % kTile;
+      const int row = (side ? rowB0 : rowA0) + x;
+      const bool ok = x < (side ? nB : nA);
+      s_nn[side][x] = ok ? nn[n0 + row] : 0.0;
+      s_inv[side][x] = ok ? inv[n0 + row] : 0.0;
+    }
+  }
+  __syncthreads();
+
+  // Coverage distances, written to (i, j) and, off the diagonal, to (j, i).
+  float *D = dmat + d_off[r];
+  const int64_t dlim = d_cap - d_off[r];
+#pragma unroll
+  for (int tm = 0; tm < kTM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < kTN; ++tn) {
+      const int jl = (wn * kTN + tn) * 32 + (lane & 31), j = rowB0 + jl;
+      const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
+#pragma unroll
+      for (int vq = 0; vq < 4; ++vq) {
+        const int il0 = (wm * kTM + tm) * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
+        float dv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int i = i0 + u;
+          dv[u] = (i < N && j < N) ? coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u], nnj,
+                                              s_inv[0][il0 + u], invj)
+                                   : 0.f;
+          if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
+        }
+        if (!DIAG && j < N) {
+          const int64_t o = (int64_t)j * N + i0;
+          if (i0 + 3 < N && ((d_off[r] + o) & 3) == 0 && o + 3 < dlim) {
+            *reinterpret_cast<float4 *>(D + o) = make_float4(dv[0], dv[1], dv[2], dv[3]);
+          } else {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              if (i0 + u < N && o + u < dlim) D[o + u] = dv[u];
           }
         }
       }
@@ -310,23 +602,26 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
 // fp32 features: squared norms and dots in fp64 FMAs over d = 0..Dv-1 in
 // order, the same loop for both, so duplicates again give distance 0.
 __global__ __launch_bounds__(256) void k_sqnorm_f32(const float *__restrict__ X, int64_t N_total,
-                                                    int Dv, double *__restrict__ nn) {
+                                                    int Dv, double *__restrict__ nn,
+                                                    double *__restrict__ inv) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= N_total) return;
   const float *x = X + i * Dv;
   double s = 0.0;
   for (int d = 0; d < Dv; ++d) s = fma((double)x[d], (double)x[d], s);
   nn[i] = s;
+  inv[i] = s > 0.0 ? 1.0 / sqrt(s) : 0.0;
 }
 
 constexpr int kF32Tile = 64;
 constexpr int kF32KS = 32;
 
+template <bool DIAG>
 __global__ __launch_bounds__(256) void k_gram_f32(
     const float *__restrict__ X, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
-    const int64_t *__restrict__ d_off, const double *__restrict__ nn, int Dv, int64_t tiles_total,
-    int64_t d_cap, float *__restrict__ dmat) {
+    const int64_t *__restrict__ d_off, const double *__restrict__ nn, const double *__restrict__ inv,
+    int Dv, int64_t tiles_total, int64_t d_cap, float *__restrict__ dmat) {
   // A 128x128 Gram tile is covered by 2x2 sub-tiles of 64x64, one pass each.
   __shared__ float sA[kF32KS][kF32Tile + 1];
   __shared__ float sB[kF32KS][kF32Tile + 1];
@@ -337,7 +632,10 @@ __global__ __launch_bounds__(256) void k_gram_f32(
   const int N = cu_vis[r + 1] - (int)n0;
   const int nb = (N + kTile - 1) / kTile;
   int I, J;
-  tile_ij((int)(t_glob - tile_off[r]), nb, I, J);
+  if (DIAG)
+    I = J = (int)(t_glob - tile_off[r]);
+  else
+    tile_ij_upper((int)(t_glob - tile_off[r]), nb, I, J);
   float *D = dmat + d_off[r];
   const int64_t dlim = d_cap - d_off[r];
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
@@ -378,7 +676,7 @@ __global__ __launch_bounds__(256) void k_gram_f32(
       for (int b = 0; b < 4; ++b) {
         const int i = rowA0 + ty + 16 * a, j = rowB0 + tx + 16 * b;
         if (i >= N || j >= N) continue;
-        const float dv = coverage(acc[a][b], nn[n0 + i], nn[n0 + j]);
+        const float dv = coverage(acc[a][b], nn[n0 + i], nn[n0 + j], inv[n0 + i], inv[n0 + j]);
         if ((int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv;
         if (I != J && (int64_t)j * N + i < dlim) D[(int64_t)j * N + i] = dv;
       }
@@ -614,7 +912,8 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
     p.N_max = std::max<int32_t>(p.N_max, (int32_t)N);
     p.K_max = std::max<int32_t>(p.K_max, (int32_t)K);
     const int64_t tb = (N + kTile - 1) / kTile;
-    p.tiles_total += tb * (tb + 1) / 2;
+    p.tiles_diag += tb;
+    p.tiles_off += tb * (tb - 1) / 2;
     p.d_elems += N * N;
   }
   p.threads = p.N_max > 1024 ? 1024 : std::max(64, (p.N_max + 63) / 64 * 64);
@@ -628,10 +927,13 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
   Carver cv(ws);
   SelectWs w{};
   if (mode == LAST_SEL_KCENTER) {
-    w.tile_off = cv.take<int32_t>(R + 1);
-    w.tile_req = cv.take<int32_t>(p.tiles_total);
+    w.dtile_off = cv.take<int32_t>(R + 1);
+    w.dtile_req = cv.take<int32_t>(p.tiles_diag);
+    w.otile_off = cv.take<int32_t>(R + 1);
+    w.otile_req = cv.take<int32_t>(p.tiles_off);
     w.d_off = cv.take<int64_t>(R + 1);
     w.nn = cv.take<double>(p.N_total);
+    w.inv = cv.take<double>(p.N_total);
     w.dmat = cv.take<float>(p.d_elems);
   }
   *bytes = cv.size();
@@ -659,32 +961,43 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
   }
 
   launch_begin("select_plan", s);
-  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, p.tiles_total, w.tile_off,
-                     w.tile_req, w.d_off);
+  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, p.tiles_diag, p.tiles_off,
+                     w.dtile_off, w.dtile_req, w.otile_off, w.otile_req, w.d_off);
   if ((e = launch_end(s)) != hipSuccess) return e;
 
   if (fdtype == LAST_BF16) {
-    launch_begin("sqnorm", s);
-    const int64_t nblk = (p.N_total + 127) / 128;
-    hipLaunchKernelGGL(k_sqnorm_bf16, dim3((unsigned)nblk), dim3(256), 0, s,
-                       (const uint16_t *)feats, p.N_total, Dv, w.nn);
+    // the streamed kernel needs an even number of 64-column stages; other widths use the staged one
+    const bool dma = Dv % (2 * kDmaCols) == 0;
+    launch_begin("gram_diag", s);
+    hipLaunchKernelGGL(dma ? k_gram_bf16<true> : k_gram_bf16_staged<true>, dim3((unsigned)p.tiles_diag),
+                       dim3(kGramThreads), 0, s, (const uint16_t *)feats, cu_vis, w.dtile_off,
+                       w.dtile_req, w.d_off, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
-    launch_begin("gram", s);
-    const int64_t grid = (p.tiles_total + 7) / 8 * 8;
-    hipLaunchKernelGGL(k_gram_bf16, dim3((unsigned)grid), dim3(kGramThreads), 0, s,
-                       (const uint16_t *)feats, cu_vis, w.tile_off, w.tile_req, w.d_off, w.nn, Dv,
-                       p.tiles_total, p.d_elems, w.dmat);
-    if ((e = launch_end(s)) != hipSuccess) return e;
+    if (p.tiles_off > 0) {
+      launch_begin("gram", s);
+      const int64_t grid = (p.tiles_off + 7) / 8 * 8;
+      hipLaunchKernelGGL(dma ? k_gram_bf16<false> : k_gram_bf16_staged<false>, dim3((unsigned)grid),
+                         dim3(kGramThreads), 0, s, (const uint16_t *)feats, cu_vis, w.otile_off,
+                         w.otile_req, w.d_off, w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
+      if ((e = launch_end(s)) != hipSuccess) return e;
+    }
   } else {
     launch_begin("sqnorm", s);
     hipLaunchKernelGGL(k_sqnorm_f32, dim3((unsigned)((p.N_total + 255) / 256)), dim3(256), 0, s,
-                       (const float *)feats, p.N_total, Dv, w.nn);
+                       (const float *)feats, p.N_total, Dv, w.nn, w.inv);
     if ((e = launch_end(s)) != hipSuccess) return e;
-    launch_begin("gram", s);
-    hipLaunchKernelGGL(k_gram_f32, dim3((unsigned)p.tiles_total), dim3(256), 0, s,
-                       (const float *)feats, cu_vis, w.tile_off, w.tile_req, w.d_off, w.nn, Dv,
-                       p.tiles_total, p.d_elems, w.dmat);
+    launch_begin("gram_diag", s);
+    hipLaunchKernelGGL(k_gram_f32<true>, dim3((unsigned)p.tiles_diag), dim3(256), 0, s,
+                       (const float *)feats, cu_vis, w.dtile_off, w.dtile_req, w.d_off, w.nn, w.inv,
+                       Dv, p.tiles_diag, p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
+    if (p.tiles_off > 0) {
+      launch_begin("gram", s);
+      hipLaunchKernelGGL(k_gram_f32<false>, dim3((unsigned)p.tiles_off), dim3(256), 0, s,
+                         (const float *)feats, cu_vis, w.otile_off, w.otile_req, w.d_off, w.nn, w.inv,
+                         Dv, p.tiles_off, p.d_elems, w.dmat);
+      if ((e = launch_end(s)) != hipSuccess) return e;
+    }
   }
 
   launch_begin("greedy", s);
