@@ -594,7 +594,7 @@ hipError_t launch_stream_dh(const last_batch *b, const last::ScorePlan &p, const
   const int g = b->Hq / b->Hkv;
   const int64_t blocks = (int64_t)b->G * p.C_total;
   const size_t lds = (size_t)p.chunk_tokens * b->Hq * sizeof(float);
-  last::launch_begin("score_partial", s);
+  last::launch_begin("score_stream", s);
 #define LAST_LAUNCH_GQ(GQV)                                                                        \
   hipLaunchKernelGGL((k_score_stream<T, DH, GQV>), dim3((unsigned)blocks), dim3(kThreads), lds, s, \
                      (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,          \
