@@ -149,6 +149,12 @@ __device__ __forceinline__ float coverage(double dot, double nni, double nnj, do
 #ifndef LAST_GRAM_LAYOUT
 #define LAST_GRAM_LAYOUT 1
 #endif
+#ifndef LAST_GRAM_REVERSE
+#define LAST_GRAM_REVERSE 0
+#endif
+#ifndef LAST_GRAM_SCHED
+#define LAST_GRAM_SCHED 2
+#endif
 #if LAST_GRAM_LAYOUT == 0
 constexpr int kWM = 2, kWN = 2, kTM = 2, kTN = 2;
 #elif LAST_GRAM_LAYOUT == 1
@@ -180,6 +186,11 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
     // go to the same XCD, which receives every 8th block.
     const int64_t per_xcd = gridDim.x / 8;
     t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+#if LAST_GRAM_REVERSE
+    // last requests first: their rows were the most recent reads of the
+    // diagonal launch and are the likeliest to still sit in the last-level cache
+    t = (int64_t)gridDim.x - 1 - t;
+#endif
   }
   if (t >= tiles) return;
   const int r = tile_req[t];
@@ -348,18 +359,25 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
 
 // The same tiles with the operands streamed straight into LDS by
 // global_load_lds_dwordx4 (lane i's 16 bytes land at M0 + 16 i), through a
-// ring of kRing stages of 64 columns: the loads for stage ch + kRing - 1 are
+// ring of kRing stages of 64 columns (kRingOff for off-diagonal tiles,
+// kRingDiag for diagonal ones): the loads for stage ch + kRing - 1 are
 // in flight while stage ch feeds the matrix cores. The loads are issued from
 // inline assembly so that the compiler does not serialise every LDS read
 // behind them; this kernel waits for them itself (s_waitcnt vmcnt) before the
-// block barrier that publishes a stage. Each stage is one fold chunk; two
-// accumulator sets alternate so that folding chunk c - 1 into fp64 can overlap
-// the matrix-core work of chunk c. Needs Dv % 128 == 0 (an even stage count).
+// block barrier that publishes a stage. A fold chunk is two stages (128
+// columns); two accumulator sets alternate so that folding chunk c - 1 into
+// fp64 can overlap the matrix-core work of chunk c. Needs Dv % 256 == 0 (a
+// stage count divisible by 4).
 #ifndef LAST_GRAM_RING
 #define LAST_GRAM_RING 4
 #endif
-constexpr int kRing = LAST_GRAM_RING;
-static_assert((kRing & (kRing - 1)) == 0, "power-of-two ring");
+#ifndef LAST_GRAM_RING_DIAG
+#define LAST_GRAM_RING_DIAG 8
+#endif
+// Diagonal tiles stage one operand (16 KB a stage) and read every row exactly
+// once, straight from HBM, so they keep a deeper ring in flight.
+constexpr int kRingOff = LAST_GRAM_RING, kRingDiag = LAST_GRAM_RING_DIAG;
+static_assert((kRingOff & (kRingOff - 1)) == 0 && (kRingDiag & (kRingDiag - 1)) == 0, "power-of-two ring");
 constexpr int kDmaCols = kKS;                               // columns per ring stage (64)
 constexpr int kDmaPieces = kTile * kDmaCols * 2 / 16;       // 16-byte pieces per operand stage (1024)
 constexpr int kDmaInstr = kDmaPieces / 64;                  // wave instructions per operand stage (16)
@@ -391,11 +409,12 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
     const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv, int Dv,
     int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
   constexpr int kOps = DIAG ? 1 : 2;
+  constexpr int kRing = DIAG ? kRingDiag : kRingOff;
   constexpr int kInstr = kOps * kDmaInstr;                  // per stage, all operands
   static_assert(kInstr % kGramWaves == 0, "even DMA split");
   constexpr int kPerWave = kInstr / kGramWaves;
   constexpr int kSteady = (kRing - 2) * kPerWave;           // loads allowed in flight at a stage boundary
-  static_assert(kSteady <= 15, "vmcnt immediate");
+  static_assert(kSteady <= 63, "vmcnt immediate");
   __shared__ uint4 sbuf[kRing][kOps][kDmaPieces];
   __shared__ double s_nn[2][kTile], s_inv[2][kTile];
 
@@ -405,6 +424,11 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
     // go to the same XCD, which receives every 8th block.
     const int64_t per_xcd = gridDim.x / 8;
     t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+#if LAST_GRAM_REVERSE
+    // last requests first: their rows were the most recent reads of the
+    // diagonal launch and are the likeliest to still sit in the last-level cache
+    t = (int64_t)gridDim.x - 1 - t;
+#endif
   }
   if (t >= tiles) return;
   const int r = tile_req[t];
@@ -473,23 +497,38 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
       for (int v = 0; v < 16; ++v) acc64[tm][tn][v] = 0.0;
   f32x16 accP[kTM][kTN], accQ[kTM][kTN];
 
-  auto fold = [&](const f32x16 (&a)[kTM][kTN]) {
+  // Fold elements [8 h, 8 h + 8) of every tile of `a` into the fp64 totals.
+  auto fold_half = [&](const f32x16 (&a)[kTM][kTN], int h) {
 #pragma unroll
     for (int tm = 0; tm < kTM; ++tm)
 #pragma unroll
       for (int tn = 0; tn < kTN; ++tn)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc64[tm][tn][v] += (double)a[tm][tn][v];
+        for (int v = 0; v < 8; ++v) acc64[tm][tn][8 * h + v] += (double)a[tm][tn][8 * h + v];
   };
-  // One stage: wait for it, publish it, refill the ring, run its four
-  // 16-deep MFMA steps into `cur` (from zero), and fold the previous chunk.
-  auto stage = [&](int ch, f32x16 (&cur)[kTM][kTN], const f32x16 (&prev)[kTM][kTN]) {
-    if (ch + kRing - 2 < nst)
+  // One stage: wait for it, publish it, refill the ring, and run its four
+  // 16-deep MFMA steps into `cur` (from zero when `fresh`); then fold half of
+  // the previous chunk, so that its fp64 adds overlap this chunk's MFMA work.
+  // `pending` is how many later stages may still be in flight when this one
+  // is needed, `refill` whether this stage issues the loads of stage
+  // ch + kRing - 1; both are literals at every call, so the steady-state loop
+  // body has no branches and the fold stays where it is written.
+  auto stage = [&](int ch, int pending, bool refill, f32x16 (&cur)[kTM][kTN], bool fresh,
+                   const f32x16 (&prev)[kTM][kTN], int h) {
+    if (pending >= kRing - 2) {
       vm_wait<kSteady>();
-    else
-      vm_wait<0>();
+    } else {
+      switch (pending) {   // only in the tail
+        case 5: vm_wait<5 * kPerWave>(); break;
+        case 4: vm_wait<4 * kPerWave>(); break;
+        case 3: vm_wait<3 * kPerWave>(); break;
+        case 2: vm_wait<2 * kPerWave>(); break;
+        case 1: vm_wait<kPerWave>(); break;
+        default: vm_wait<0>(); break;
+      }
+    }
     __syncthreads();
-    if (ch + kRing - 1 < nst) issue(ch + kRing - 1);
+    if (refill) issue(ch + kRing - 1);
     const uint4 *pa = sbuf[ch & (kRing - 1)][0];
     const uint4 *pb = sbuf[ch & (kRing - 1)][kOps - 1];
 #pragma unroll
@@ -503,23 +542,57 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
       for (int tm = 0; tm < kTM; ++tm)
 #pragma unroll
         for (int tn = 0; tn < kTN; ++tn)
-          cur[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[tm], b[tn], s == 0 ? f32x16{} : cur[tm][tn],
-                                                                0, 0, 0);
+          cur[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              a[tm], b[tn], (fresh && s == 0) ? f32x16{} : cur[tm][tn], 0, 0, 0);
     }
-    fold(prev);
+    fold_half(prev, h);
+#if LAST_GRAM_SCHED
+    // interleave: fragment reads of two k-steps, then MFMA / fold pairs
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+    for (int i = 0; i < 6; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    }
+#endif
+#if LAST_GRAM_SCHED >= 2
+    __builtin_amdgcn_sched_barrier(0);
+#endif
   };
 
-  // nst is even here (Dv % 128 == 0); the first fold adds zeros, exactly.
+  // A chunk is two stages (128 columns) accumulated in fp32; chunks alternate
+  // between the P and Q sets, and each is folded into fp64 while the next one
+  // runs. nst is a multiple of 4 (Dv % 256 == 0); the first folds add zeros,
+  // exactly. The steady loop runs while all four of its stages refill the
+  // ring; the tail (at most kRing + 3 stages) waits and refills as needed.
+  static_assert(kRing <= 8, "tail waits cover up to 6 pending stages");
 #pragma unroll
   for (int tm = 0; tm < kTM; ++tm)
 #pragma unroll
     for (int tn = 0; tn < kTN; ++tn) accQ[tm][tn] = f32x16{};
   for (int st = 0; st < kRing - 1 && st < nst; ++st) issue(st);
-  for (int ch = 0; ch < nst; ch += 2) {
-    stage(ch, accP, accQ);
-    stage(ch + 1, accQ, accP);
+  int ch = 0;
+  for (; ch + kRing + 2 < nst; ch += 4) {
+    stage(ch, kRing - 2, true, accP, true, accQ, 0);
+    stage(ch + 1, kRing - 2, true, accP, false, accQ, 1);
+    stage(ch + 2, kRing - 2, true, accQ, true, accP, 0);
+    stage(ch + 3, kRing - 2, true, accQ, false, accP, 1);
   }
-  fold(accQ);
+  auto pend = [&](int c) { return min(kRing - 2, nst - 1 - c); };
+  auto refills = [&](int c) { return c + kRing - 1 < nst; };
+  for (; ch < nst; ch += 4) {
+    stage(ch, pend(ch), refills(ch), accP, true, accQ, 0);
+    stage(ch + 1, pend(ch + 1), refills(ch + 1), accP, false, accQ, 1);
+    stage(ch + 2, pend(ch + 2), refills(ch + 2), accQ, true, accP, 0);
+    stage(ch + 3, pend(ch + 3), refills(ch + 3), accQ, false, accP, 1);
+  }
+  fold_half(accQ, 0);
+  fold_half(accQ, 1);
   __syncthreads();
 
   // Squared norms (diagonal tiles) or the norms of both row blocks, into LDS.
@@ -966,8 +1039,8 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
   if ((e = launch_end(s)) != hipSuccess) return e;
 
   if (fdtype == LAST_BF16) {
-    // the streamed kernel needs an even number of 64-column stages; other widths use the staged one
-    const bool dma = Dv % (2 * kDmaCols) == 0;
+    // the streamed kernel needs a multiple of four 64-column stages; other widths use the staged one
+    const bool dma = Dv % (4 * kDmaCols) == 0;
     launch_begin("gram_diag", s);
     hipLaunchKernelGGL(dma ? k_gram_bf16<true> : k_gram_bf16_staged<true>, dim3((unsigned)p.tiles_diag),
                        dim3(kGramThreads), 0, s, (const uint16_t *)feats, cu_vis, w.dtile_off,
