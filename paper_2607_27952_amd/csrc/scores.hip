@@ -45,11 +45,26 @@ namespace {
 #define LAST_SCORE_UNROLL 4
 #endif
 #ifndef LAST_SCORE_WG_KB
-#define LAST_SCORE_WG_KB 192
+#define LAST_SCORE_WG_KB 96
 #endif
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+#ifndef LAST_SCORE_NT
+#define LAST_SCORE_NT 1
+#endif
 constexpr int kUnroll = LAST_SCORE_UNROLL;  // row groups (8 rows each) in flight per wave
+
+// Key rows are read exactly once: non-temporal loads stream them without
+// displacing cache lines that other blocks still use.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 stream_load(const void *p) {
+#if LAST_SCORE_NT
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+#else
+  return *reinterpret_cast<const uint4 *>(p);
+#endif
+}
 constexpr int64_t kWgBytes = (int64_t)LAST_SCORE_WG_KB * 1024;  // key bytes per stream block
 constexpr int kMaxChunk = 4096;             // tokens per chunk (fallback kernel), upper bound
 constexpr int kLdsLogitFloats = 8192;
@@ -277,7 +292,7 @@ __global__ __launch_bounds__(kThreads) void k_score_stream(
       const T *kp = kchunk + (int64_t)row * DH;
 #pragma unroll
       for (int p = 0; p < RS::kNP; ++p)
-        buf[u][p] = *reinterpret_cast<const uint4 *>(kp + (sub + 8 * p) * RS::kEP);
+        buf[u][p] = stream_load(kp + (sub + 8 * p) * RS::kEP);
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
@@ -400,7 +415,7 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
       const T *kp = kbase + (int64_t)t * kstride;
 #pragma unroll
       for (int p = 0; p < RS::kNP; ++p)
-        buf[u][p] = *reinterpret_cast<const uint4 *>(kp + (sub + 8 * p) * RS::kEP);
+        buf[u][p] = stream_load(kp + (sub + 8 * p) * RS::kEP);
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
