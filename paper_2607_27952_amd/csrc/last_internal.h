@@ -124,20 +124,56 @@ __device__ __forceinline__ float sum8(float v) {
   return v;
 }
 
+// Wave-wide max / sum, returned wave-uniform: DPP inside each row of 16
+// lanes, then the four row results in a fixed order (deterministic). Every
+// lane of the wave must be active.
+__device__ __forceinline__ float dpp_mirror(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row_lane15(float v, int row) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16 * row + 15));
+}
 __device__ __forceinline__ float wave_max(float v) {
-  for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m));
-  return v;
+  v = fmaxf(v, dpp_xor1(v));
+  v = fmaxf(v, dpp_xor2(v));
+  v = fmaxf(v, dpp_half_mirror(v));
+  v = fmaxf(v, dpp_mirror(v));
+  return fmaxf(fmaxf(row_lane15(v, 0), row_lane15(v, 1)), fmaxf(row_lane15(v, 2), row_lane15(v, 3)));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-  return v;
+  v += dpp_xor1(v);
+  v += dpp_xor2(v);
+  v += dpp_half_mirror(v);
+  v += dpp_mirror(v);
+  return (row_lane15(v, 0) + row_lane15(v, 1)) + (row_lane15(v, 2) + row_lane15(v, 3));
+}
+// Maximum over the wave of a 64-bit key, returned wave-uniform. DPP exchanges
+// inside each row of 16 lanes (xor 1, xor 2, half-mirror, mirror) leave the
+// row's maximum in every lane of the row; the four rows meet through
+// readlane. Every lane of the wave must be active.
+template <int CTRL>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
+  return ((unsigned long long)hi << 32) | lo;
+}
+__device__ __forceinline__ unsigned long long max_u64(unsigned long long a, unsigned long long b) {
+  return a > b ? a : b;
 }
 __device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
-  for (int m = 32; m >= 1; m >>= 1) {
-    unsigned long long o = __shfl_xor(v, m);
-    v = o > v ? o : v;
+  v = max_u64(v, dpp_u64<0xB1>(v));
+  v = max_u64(v, dpp_u64<0x4E>(v));
+  v = max_u64(v, dpp_u64<0x141>(v));
+  v = max_u64(v, dpp_u64<0x140>(v));
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  unsigned long long r = 0;
+#pragma unroll
+  for (int row = 0; row < 4; ++row) {
+    const uint32_t l = __builtin_amdgcn_readlane(lo, 16 * row + 15);
+    const uint32_t h = __builtin_amdgcn_readlane(hi, 16 * row + 15);
+    r = max_u64(r, ((unsigned long long)h << 32) | l);
   }
-  return v;
+  return r;
 }
 
 }  // namespace last_dev

@@ -810,21 +810,26 @@ __global__ __launch_bounds__(1024) void k_greedy(const float *__restrict__ score
   float w[EPT], dl[EPT];
   bool sel[EPT];
 #pragma unroll
+  for (int e = 0; e < EPT; ++e) w[e] = scores[n0 + min(tid + e * nth, N - 1)];
+#pragma unroll
   for (int e = 0; e < EPT; ++e) {
     const int i = tid + e * nth;
-    w[e] = i < N ? clean_score(scores[n0 + i]) : 0.f;
+    w[e] = i < N ? clean_score(w[e]) : 0.f;
     dl[e] = INFINITY;
     sel[e] = false;
   }
   int j = -1;
   for (int t = 0; t < K; ++t) {
     if (t > 0) {
+      // All EPT loads are issued before any is used (indices clamped into the
+      // row, N >= 1), so a step waits for one memory round trip, not EPT.
       const float *row = D + (int64_t)j * N;
+      float rv[EPT];
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) {
-        const int i = tid + e * nth;
-        if (i < N) dl[e] = fminf(dl[e], row[i]);
-      }
+      for (int e = 0; e < EPT; ++e) rv[e] = row[min(tid + e * nth, N - 1)];
+#pragma unroll
+      for (int e = 0; e < EPT; ++e)
+        if (tid + e * nth < N) dl[e] = fminf(dl[e], rv[e]);
     }
     unsigned long long best = 0;
 #pragma unroll
