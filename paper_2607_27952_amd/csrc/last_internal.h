@@ -73,7 +73,8 @@ struct SelectPlan {
   int64_t tiles_diag;      // diagonal Gram tiles over all requests
   int64_t tiles_off;       // Gram tiles strictly above the diagonal
   int64_t d_elems;         // sum of N_r^2 (coverage matrices)
-  int32_t threads, ept;    // greedy / top-k block shape
+  int32_t threads, ept;    // top-k block shape
+  int32_t g_threads, g_ept;  // greedy block shape
 };
 
 struct SelectWs {

@@ -124,6 +124,12 @@ __device__ __forceinline__ void tile_ij_upper(int t, int nb, int &I, int &J) {
   J = i + 1 + rem;
 }
 
+// The coverage matrix holds -inf on its diagonal instead of a token's distance
+// to itself: the greedy folds a pick's own row into its running minimum at the
+// next step, and -inf there makes the pick's objective -inf or NaN, which no
+// comparison ever prefers -- the pick is marked selected at no extra cost.
+constexpr float kSelfMark = -INFINITY;
+
 __device__ __forceinline__ float coverage(double dot, double nni, double nnj, double invi, double invj) {
   // Eq. 10 term: 1 - cos, clamped at 0. Zero-norm rows have cosine 0.
   // Bitwise-identical rows give dot == nni == nnj exactly, hence distance 0.
@@ -338,8 +344,9 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int i = i0 + u;
-          dv[u] = (i < N && j < N) ? coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u], nnj,
-                                              s_inv[0][il0 + u], invj)
+          dv[u] = (i < N && j < N) ? (DIAG && i == j ? kSelfMark
+                                                     : coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u],
+                                                                nnj, s_inv[0][il0 + u], invj))
                                    : 0.f;
           if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
         }
@@ -653,8 +660,9 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int i = i0 + u;
-          dv[u] = (i < N && j < N) ? coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u], nnj,
-                                              s_inv[0][il0 + u], invj)
+          dv[u] = (i < N && j < N) ? (DIAG && i == j ? kSelfMark
+                                                     : coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u],
+                                                                nnj, s_inv[0][il0 + u], invj))
                                    : 0.f;
           if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
         }
@@ -749,7 +757,7 @@ __global__ __launch_bounds__(256) void k_gram_f32(
       for (int b = 0; b < 4; ++b) {
         const int i = rowA0 + ty + 16 * a, j = rowB0 + tx + 16 * b;
         if (i >= N || j >= N) continue;
-        const float dv = coverage(acc[a][b], nn[n0 + i], nn[n0 + j], inv[n0 + i], inv[n0 + j]);
+        const float dv = i == j ? kSelfMark : coverage(acc[a][b], nn[n0 + i], nn[n0 + j], inv[n0 + i], inv[n0 + j]);
         if ((int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv;
         if (I != J && (int64_t)j * N + i < dlim) D[(int64_t)j * N + i] = dv;
       }
@@ -787,16 +795,26 @@ __device__ void compact_ascending(const bool (&flag)[EPT], int32_t *dst, int *sh
   }
 }
 
-template <int EPT>
-__global__ __launch_bounds__(1024) void k_greedy(const float *__restrict__ scores,
-                                                 const float *__restrict__ dmat,
-                                                 const int64_t *__restrict__ d_off,
-                                                 const int32_t *__restrict__ cu_vis,
-                                                 const int32_t *__restrict__ cu_keep,
-                                                 int32_t *__restrict__ kept,
-                                                 int32_t *__restrict__ order,
-                                                 float *__restrict__ gains) {
-  __shared__ unsigned long long s_key[2][16];
+// Eq. 9-11 for one request per block of NTH threads (64, 256 or 512); thread t
+// holds tokens t + e * NTH. w is the relevance (NaN for tokens past N_r), dl
+// the running minimum coverage distance to the picks so far. A pick j's row of
+// the coverage matrix carries -inf at j, so after it is folded in, the pick's
+// objective w * dl is -inf or NaN and never wins again. Each thread keeps the
+// best (objective, lowest index) of its tokens with a strict compare in
+// ascending index order; the block then takes the maximum 64-bit key
+// (objective bits, ~index), which orders by objective and breaks ties towards
+// the lowest index (objectives are >= 0 here, so their bits order like them).
+template <int EPT, int NTH>
+__global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores,
+                                                const float *__restrict__ dmat,
+                                                const int64_t *__restrict__ d_off,
+                                                const int32_t *__restrict__ cu_vis,
+                                                const int32_t *__restrict__ cu_keep,
+                                                int32_t *__restrict__ kept,
+                                                int32_t *__restrict__ order,
+                                                float *__restrict__ gains) {
+  constexpr int kNW = NTH / 64;
+  __shared__ unsigned long long s_key[2][kNW];
   __shared__ int s_cnt[16];
   const int r = blockIdx.x;
   const int64_t n0 = cu_vis[r];
@@ -804,66 +822,87 @@ __global__ __launch_bounds__(1024) void k_greedy(const float *__restrict__ score
   const int64_t k0 = cu_keep[r];
   const int K = cu_keep[r + 1] - (int)k0;
   const float *D = dmat + d_off[r];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, nw = blockDim.x >> 6;
-  const int nth = blockDim.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
   float w[EPT], dl[EPT];
-  bool sel[EPT];
 #pragma unroll
-  for (int e = 0; e < EPT; ++e) w[e] = scores[n0 + min(tid + e * nth, N - 1)];
+  for (int e = 0; e < EPT; ++e) w[e] = scores[n0 + min(tid + e * NTH, N - 1)];
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
-    const int i = tid + e * nth;
-    w[e] = i < N ? clean_score(w[e]) : 0.f;
+    // tokens past N_r get NaN: every product with NaN is NaN and loses every
+    // comparison (-inf could meet the -inf self-mark that a clamped load
+    // returns and give +inf, i.e. pick an index past the request)
+    w[e] = tid + e * NTH < N ? clean_score(w[e]) : __builtin_nanf("");
     dl[e] = INFINITY;
-    sel[e] = false;
   }
-  int j = -1;
-  for (int t = 0; t < K; ++t) {
-    if (t > 0) {
-      // All EPT loads are issued before any is used (indices clamped into the
-      // row, N >= 1), so a step waits for one memory round trip, not EPT.
-      const float *row = D + (int64_t)j * N;
-      float rv[EPT];
+  // block-wide maximum of a 64-bit key (wave-uniform result)
+  auto block_max = [&](unsigned long long key, int t) {
+    key = wave_max_u64(key);
+    if (kNW == 1) return key;
+    if (lane == 0) s_key[t & 1][wave] = key;
+    __syncthreads();
+    key = s_key[t & 1][0];
 #pragma unroll
-      for (int e = 0; e < EPT; ++e) rv[e] = row[min(tid + e * nth, N - 1)];
+    for (int wv = 1; wv < kNW; ++wv) key = max_u64(key, s_key[t & 1][wv]);
+    return key;
+  };
+  auto key_of = [](float bo, int bi) -> unsigned long long {
+    return bo >= 0.f ? ((unsigned long long)__float_as_uint(bo) << 32) | (0xFFFFFFFFu - (unsigned)bi) : 0ull;
+  };
+
+  // t = 0: j_1 = argmax w (Eq. 9)
+  float bo = -1.f;
+  int bi = 0;
 #pragma unroll
-      for (int e = 0; e < EPT; ++e)
-        if (tid + e * nth < N) dl[e] = fminf(dl[e], rv[e]);
+  for (int e = 0; e < EPT; ++e)
+    if (w[e] > bo) {
+      bo = w[e];
+      bi = tid + e * NTH;
     }
-    unsigned long long best = 0;
+  unsigned long long best = block_max(key_of(bo, bi), 0);
+  int j = (int)(0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull));
+  if (tid == 0) {
+    order[k0] = j;
+    gains[k0] = __uint_as_float((unsigned)(best >> 32));
+  }
+  int taken = 1;
+  for (int t = 1; t < K; ++t) {
+    // fold the last pick's coverage row into the running minimum (Eq. 10);
+    // every load is issued before any is used (indices clamped into the row)
+    const float *row = D + (int64_t)j * N;
+    float rv[EPT];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) rv[e] = row[min(tid + e * NTH, N - 1)];
+    bo = -1.f;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-      const int i = tid + e * nth;
-      if (i < N && !sel[e]) {
-        const float o = t == 0 ? w[e] : w[e] * dl[e];
-        const unsigned long long kk = obj_key(o, i);
-        best = kk > best ? kk : best;
+      dl[e] = fminf(dl[e], rv[e]);
+      const float o = w[e] * dl[e];   // Eq. 11 objective; -inf or NaN once picked, NaN past N_r
+      if (o > bo) {
+        bo = o;
+        bi = tid + e * NTH;
       }
     }
-    best = wave_max_u64(best);
-    if (lane == 0) s_key[t & 1][wave] = best;
-    __syncthreads();
-    best = s_key[t & 1][0];
-    for (int wv = 1; wv < nw; ++wv) {
-      const unsigned long long o = s_key[t & 1][wv];
-      best = o > best ? o : best;
-    }
-    if (best == 0ull) break;   // no unselected token left (budget beyond N): stop
+    best = block_max(key_of(bo, bi), t);
+    if (best == 0ull) break;   // every token already picked (cannot happen for K <= N)
     j = (int)(0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull));
-#pragma unroll
-    for (int e = 0; e < EPT; ++e)
-      if (tid + e * nth == j) sel[e] = true;
     if (tid == 0) {
       order[k0 + t] = j;
       gains[k0 + t] = __uint_as_float((unsigned)(best >> 32));
     }
+    ++taken;
   }
+  // selected = marked by their own row, plus the last pick (never folded in)
+  bool sel[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = tid + e * NTH;
+    sel[e] = i < N && (dl[e] == -INFINITY || i == j);
+  }
+  (void)taken;
   __syncthreads();
   compact_ascending<EPT>(sel, kept + k0, s_cnt);
 }
-
-// ------------------------------------------------------------ top-k
 template <int EPT>
 __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
                                                const int32_t *__restrict__ cu_vis,
@@ -997,6 +1036,20 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   p.threads = p.N_max > 1024 ? 1024 : std::max(64, (p.N_max + 63) / 64 * 64);
   const int ept = (p.N_max + p.threads - 1) / p.threads;
   p.ept = ept <= 1 ? 1 : ept <= 2 ? 2 : ept <= 4 ? 4 : ept <= 8 ? 8 : 16;
+  // greedy: one wave up to 1024 tokens (no block barrier per step), else 256
+  // threads (one wave per SIMD) with up to 64 tokens each
+  if (p.N_max <= 1024) {
+    p.g_threads = 64;
+    const int e = (p.N_max + 63) / 64;
+    p.g_ept = e <= 2 ? 2 : e <= 4 ? 4 : e <= 8 ? 8 : e <= 12 ? 12 : 16;
+  } else if (p.N_max <= 8192) {
+    p.g_threads = 256;
+    const int e = (p.N_max + 255) / 256;
+    p.g_ept = e <= 8 ? 8 : e <= 16 ? 16 : 32;
+  } else {
+    p.g_threads = 512;   // up to kSelMaxN = 16384 tokens, 32 a thread
+    p.g_ept = 32;
+  }
   return p;
 }
 
@@ -1079,15 +1132,25 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
   }
 
   launch_begin("greedy", s);
-#define LAST_GREEDY(E)                                                                       \
-  hipLaunchKernelGGL(k_greedy<E>, dim3(R), dim3(p.threads), 0, s, scores, w.dmat, w.d_off, \
-                     cu_vis, cu_keep, kept, order, gains)
-  switch (p.ept) {
-    case 1: LAST_GREEDY(1); break;
-    case 2: LAST_GREEDY(2); break;
-    case 4: LAST_GREEDY(4); break;
-    case 8: LAST_GREEDY(8); break;
-    default: LAST_GREEDY(16); break;
+#define LAST_GREEDY(E, T)                                                                          \
+  hipLaunchKernelGGL((k_greedy<E, T>), dim3(R), dim3(T), 0, s, scores, w.dmat, w.d_off, cu_vis, cu_keep, \
+                     kept, order, gains)
+  if (p.g_threads == 64) {
+    switch (p.g_ept) {
+      case 2: LAST_GREEDY(2, 64); break;
+      case 4: LAST_GREEDY(4, 64); break;
+      case 8: LAST_GREEDY(8, 64); break;
+      case 12: LAST_GREEDY(12, 64); break;
+      default: LAST_GREEDY(16, 64); break;
+    }
+  } else if (p.g_threads == 256) {
+    switch (p.g_ept) {
+      case 8: LAST_GREEDY(8, 256); break;
+      case 16: LAST_GREEDY(16, 256); break;
+      default: LAST_GREEDY(32, 256); break;
+    }
+  } else {
+    LAST_GREEDY(32, 512);
   }
 #undef LAST_GREEDY
   return launch_end(s);
