@@ -8,13 +8,14 @@
 // cores and each step reads one row of it:
 //
 //   k_select_plan   per-request prefixes of the diagonal and off-diagonal
-//                   Gram tiles, tile -> request maps, and the element offset
-//                   of each request's N_r x N_r block.
+//   k_tile_fill     Gram tiles, the element offset of each request's N_r x N_r
+//                   block, and the tile -> request maps (one block a request).
 //   k_gram_bf16     128x128 tiles of X_r X_r^T on MFMA
 //                   (v_mfma_f32_32x32x16_bf16; bf16 products are exact, the
-//                   fp32 accumulator is folded into fp64 every 64 elements),
+//                   fp32 accumulator is folded into fp64 every 128 elements),
 //                   then delta_ij = max(0, 1 - dot_ij / (|x_i| |x_j|)) in fp64,
-//                   stored as fp32. A first launch over the diagonal tiles also
+//                   stored as fp32, with -inf on the diagonal (a pick's mark,
+//                   see k_greedy). A first launch over the diagonal tiles also
 //                   yields |x_i|^2 from the same arithmetic (so a row and its
 //                   bitwise duplicate get distance exactly 0); a second launch
 //                   covers the tiles above the diagonal and mirrors them.
@@ -23,9 +24,10 @@
 //   k_greedy        one block per request; w and delta live in registers.
 //                   Step t loads row j_{t-1} of the distance block, folds it
 //                   into delta with min, and takes the block-wide argmax of
-//                   w * delta over unselected tokens (ties -> lowest index,
-//                   via a 64-bit key of (value bits, ~index)). The kept set is
-//                   compacted in ascending order at the end (Eq. 12).
+//                   w * delta (ties -> lowest index, via a 64-bit key of
+//                   (value bits, ~index)); picked tokens drop out through the
+//                   -inf diagonal. The kept set is compacted in ascending
+//                   order at the end (Eq. 12).
 //
 // Top-k mode (Table 5): k_topk, one block per request, radix-selects the K
 // largest scores on their fp32 bit patterns (non-negative floats order like
@@ -69,11 +71,8 @@ __device__ void block_excl_scan_i64(int64_t v, int64_t *sh, int64_t *total, int6
 // Per request: nb = ceil(N / 128) row blocks give nb diagonal Gram tiles and
 // nb (nb - 1) / 2 tiles above the diagonal; the N x N block starts at d_off.
 __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__ cu_vis, int R,
-                                                     int64_t diag_cap, int64_t off_cap,
                                                      int32_t *__restrict__ dtile_off,
-                                                     int32_t *__restrict__ dtile_req,
                                                      int32_t *__restrict__ otile_off,
-                                                     int32_t *__restrict__ otile_req,
                                                      int64_t *__restrict__ d_off) {
   __shared__ int64_t sh[4];
   int64_t carry_d = 0, carry_o = 0, carry_m = 0;
@@ -97,10 +96,6 @@ __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__
       dtile_off[r] = (int32_t)pd;
       otile_off[r] = (int32_t)po;
       d_off[r] = pm;
-      for (int64_t c = 0; c < nd; ++c)
-        if (pd + c < diag_cap) dtile_req[pd + c] = r;
-      for (int64_t c = 0; c < no; ++c)
-        if (po + c < off_cap) otile_req[po + c] = r;
     }
     carry_d += td;
     carry_o += to;
@@ -111,6 +106,19 @@ __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__
     otile_off[R] = (int32_t)carry_o;
     d_off[R] = carry_m;
   }
+}
+
+// Tile -> request maps: block r writes r over its request's contiguous ranges
+// of diagonal and off-diagonal tiles (the caps bound every write).
+__global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ dtile_off,
+                                                   const int32_t *__restrict__ otile_off,
+                                                   int64_t diag_cap, int64_t off_cap,
+                                                   int32_t *__restrict__ dtile_req,
+                                                   int32_t *__restrict__ otile_req) {
+  const int r = blockIdx.x;
+  const int64_t d1 = min((int64_t)dtile_off[r + 1], diag_cap), o1 = min((int64_t)otile_off[r + 1], off_cap);
+  for (int64_t t = dtile_off[r] + threadIdx.x; t < d1; t += 256) dtile_req[t] = r;
+  for (int64_t t = otile_off[r] + threadIdx.x; t < o1; t += 256) otile_req[t] = r;
 }
 
 // Map a request-local index of the tiles strictly above the diagonal to (I, J).
@@ -1092,8 +1100,9 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
   }
 
   launch_begin("select_plan", s);
-  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, p.tiles_diag, p.tiles_off,
-                     w.dtile_off, w.dtile_req, w.otile_off, w.otile_req, w.d_off);
+  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, w.dtile_off, w.otile_off, w.d_off);
+  hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, w.dtile_off, w.otile_off, p.tiles_diag,
+                     p.tiles_off, w.dtile_req, w.otile_req);
   if ((e = launch_end(s)) != hipSuccess) return e;
 
   if (fdtype == LAST_BF16) {
