@@ -471,7 +471,7 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
 #pragma unroll
   for (int x = 0; x < kPerWave; ++x) {
     const int q = wave + kGramWaves * x, op = q / kDmaInstr, qi = q % kDmaInstr;
-    const int slot = qi * 64 + lane, row = slot >> 3, piece = (slot & 7) ^ (row & 7);
+    const int slot = qi * 64 + lane, row = slot >> 3, piece = (slot & 7) ^ ((row >> 1) & 7);
     const int rr = min(row, (op ? nB : nA) - 1);
     gbase[x] = uniform_ptr(X + (n0 + (op ? rowB0 : rowA0)) * (int64_t)Dv);
     voff[x] = (uint32_t)((rr * (int64_t)Dv + piece * 8) * 2);
@@ -486,128 +486,180 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
       dma16(dst[x] + off, (const char *)gbase[x] + (int64_t)st * kDmaCols * 2, voff[x]);
   };
 
-  // fragment slots: row (block row) * 8 + (piece ^ (row & 7))
-  int aslot[kTM][4], bslot[kTN][4];
+  // This block's work in pairs of 32 x 32 sub-tiles: A rows [32 a, 32 a + 32)
+  // against B rows [64 c, 64 c + 64). Sub-tile (a, b) is needed iff A row
+  // 32 a and B row 32 b exist (partial tiles at a request's end) and, on a
+  // diagonal tile, b >= a (the lower triangle is the mirror). Pairs needing
+  // both sub-tiles come first, then those needing one, and pair k goes to wave
+  // k; waves k and k + 4 share a SIMD, so each SIMD gets an even share of the
+  // MFMA work. Waves without a pair only issue their share of the loads.
+  static_assert(kTM == 1 && kTN == 2 && kGramWaves == 8, "pair layout of the streamed kernel");
+  int my_a = 0, my_b0 = 0, my_nt = 0;
+  {
+    auto need = [&](int sa, int sb) { return sa * 32 < nA && sb * 32 < nB && (!DIAG || sb >= sa); };
+    int k = 0;
+#pragma unroll
+    for (int pass = 2; pass >= 1; --pass)
+#pragma unroll
+      for (int sa = 0; sa < 4; ++sa)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          const bool n0c = need(sa, 2 * c), n1c = need(sa, 2 * c + 1);
+          if ((int)n0c + (int)n1c != pass) continue;
+          if (k == wave) {
+            my_a = sa;
+            my_b0 = n0c ? 2 * c : 2 * c + 1;   // first needed sub-tile column
+            my_nt = pass;
+          }
+          ++k;
+        }
+  }
+
+  // fragment slots: row (block row) * 8 + (piece ^ ((row >> 1) & 7)); the 16
+  // lanes that the LDS serves together read 16 consecutive rows, whose 16-byte
+  // slots then fall in 16 distinct bank groups (row parity x swizzled piece)
+  int aslot[4], bslot[kTN][4];
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
     const int piece = s * 2 + (lane >> 5);
-#pragma unroll
-    for (int tm = 0; tm < kTM; ++tm) {
-      const int row = (wm * kTM + tm) * 32 + (lane & 31);
-      aslot[tm][s] = row * 8 + (piece ^ (row & 7));
-    }
+    const int row = my_a * 32 + (lane & 31);
+    aslot[s] = row * 8 + (piece ^ ((row >> 1) & 7));
 #pragma unroll
     for (int tn = 0; tn < kTN; ++tn) {
-      const int row = (wn * kTN + tn) * 32 + (lane & 31);
-      bslot[tn][s] = row * 8 + (piece ^ (row & 7));
+      const int brow = min(my_b0 + tn, 3) * 32 + (lane & 31);
+      bslot[tn][s] = brow * 8 + (piece ^ ((brow >> 1) & 7));
     }
   }
 
-  double acc64[kTM][kTN][16];
+  double acc64[kTN][16];
 #pragma unroll
-  for (int tm = 0; tm < kTM; ++tm)
+  for (int tn = 0; tn < kTN; ++tn)
 #pragma unroll
-    for (int tn = 0; tn < kTN; ++tn)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc64[tm][tn][v] = 0.0;
-  f32x16 accP[kTM][kTN], accQ[kTM][kTN];
+    for (int v = 0; v < 16; ++v) acc64[tn][v] = 0.0;
 
-  // Fold elements [8 h, 8 h + 8) of every tile of `a` into the fp64 totals.
-  auto fold_half = [&](const f32x16 (&a)[kTM][kTN], int h) {
-#pragma unroll
-    for (int tm = 0; tm < kTM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < kTN; ++tn)
-#pragma unroll
-        for (int v = 0; v < 8; ++v) acc64[tm][tn][8 * h + v] += (double)a[tm][tn][8 * h + v];
+  // wait until at most n stages of this wave's loads are still in flight
+  // (a literal n folds to one s_waitcnt)
+  auto wait_pending = [&](int n) {
+    static_assert(kRing - 1 <= 7, "cases below");
+    switch (n) {
+      case 7: vm_wait<7 * kPerWave>(); break;
+      case 6: vm_wait<6 * kPerWave>(); break;
+      case 5: vm_wait<5 * kPerWave>(); break;
+      case 4: vm_wait<4 * kPerWave>(); break;
+      case 3: vm_wait<3 * kPerWave>(); break;
+      case 2: vm_wait<2 * kPerWave>(); break;
+      case 1: vm_wait<kPerWave>(); break;
+      default: vm_wait<0>(); break;
+    }
   };
-  // One stage: wait for it, publish it, refill the ring, and run its four
-  // 16-deep MFMA steps into `cur` (from zero when `fresh`); then fold half of
-  // the previous chunk, so that its fp64 adds overlap this chunk's MFMA work.
-  // `pending` is how many later stages may still be in flight when this one
-  // is needed, `refill` whether this stage issues the loads of stage
-  // ch + kRing - 1; both are literals at every call, so the steady-state loop
-  // body has no branches and the fold stays where it is written.
-  auto stage = [&](int ch, int pending, bool refill, f32x16 (&cur)[kTM][kTN], bool fresh,
-                   const f32x16 (&prev)[kTM][kTN], int h) {
-    if (pending >= kRing - 2) {
-      vm_wait<kSteady>();
-    } else {
-      switch (pending) {   // only in the tail
-        case 5: vm_wait<5 * kPerWave>(); break;
-        case 4: vm_wait<4 * kPerWave>(); break;
-        case 3: vm_wait<3 * kPerWave>(); break;
-        case 2: vm_wait<2 * kPerWave>(); break;
-        case 1: vm_wait<kPerWave>(); break;
-        default: vm_wait<0>(); break;
+
+  // The stage loop for a wave with NT sub-tiles (2, 1 or 0), software-
+  // pipelined across the stage barrier. A stage's fragments are read in two
+  // halves (k-steps 0-1 and 2-3). Stage ch reads its second half while its
+  // first half feeds the MFMAs; then it waits for stage ch + 1's loads, meets
+  // the other waves at the block barrier (whose fence also completes every
+  // wave's reads of stage ch), refills stage ch's ring slot with stage
+  // ch + kRing, and reads the first half of stage ch + 1 while its own second
+  // half runs. A chunk is two stages (128 columns) accumulated in fp32; chunks
+  // alternate between the P and Q sets and each is folded into fp64, a
+  // quarter at a time, between the next chunk's MFMAs. nst is a multiple of 4
+  // (Dv % 256 == 0); the first folds add zeros, exactly.
+  auto run = [&](auto nt_const) {
+    constexpr int NT = decltype(nt_const)::value;
+    f32x16 accP[kTN], accQ[kTN];
+    bf16x8 fa0[2], fb0[2][kTN], fa1[2], fb1[2][kTN];
+    auto fold_q = [&](const f32x16 (&a)[kTN], int q) {   // elements [4 q, 4 q + 4)
+#pragma unroll
+      for (int tn = 0; tn < NT; ++tn)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc64[tn][4 * q + v] += (double)a[tn][4 * q + v];
+    };
+    auto read_half = [&](int ch, int half, bf16x8 (&fa)[2], bf16x8 (&fb)[2][kTN]) {
+      if (NT == 0) return;
+      const uint4 *pa = sbuf[ch & (kRing - 1)][0];
+      const uint4 *pb = sbuf[ch & (kRing - 1)][kOps - 1];
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss) {
+        fa[ss] = __builtin_bit_cast(bf16x8, pa[aslot[2 * half + ss]]);
+#pragma unroll
+        for (int tn = 0; tn < NT; ++tn) fb[ss][tn] = __builtin_bit_cast(bf16x8, pb[bslot[tn][2 * half + ss]]);
       }
-    }
-    __syncthreads();
-    if (refill) issue(ch + kRing - 1);
-    const uint4 *pa = sbuf[ch & (kRing - 1)][0];
-    const uint4 *pb = sbuf[ch & (kRing - 1)][kOps - 1];
+    };
+    auto mma_half = [&](f32x16 (&cur)[kTN], bool fresh, const bf16x8 (&fa)[2], const bf16x8 (&fb)[2][kTN]) {
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      bf16x8 a[kTM], b[kTN];
+      for (int ss = 0; ss < 2; ++ss)
 #pragma unroll
-      for (int tm = 0; tm < kTM; ++tm) a[tm] = __builtin_bit_cast(bf16x8, pa[aslot[tm][s]]);
-#pragma unroll
-      for (int tn = 0; tn < kTN; ++tn) b[tn] = __builtin_bit_cast(bf16x8, pb[bslot[tn][s]]);
-#pragma unroll
-      for (int tm = 0; tm < kTM; ++tm)
-#pragma unroll
-        for (int tn = 0; tn < kTN; ++tn)
-          cur[tm][tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              a[tm], b[tn], (fresh && s == 0) ? f32x16{} : cur[tm][tn], 0, 0, 0);
-    }
-    fold_half(prev, h);
+        for (int tn = 0; tn < NT; ++tn)
+          cur[tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ss], fb[ss][tn],
+                                                            (fresh && ss == 0) ? f32x16{} : cur[tn], 0, 0, 0);
+    };
+    auto sched_half = [&]() {
 #if LAST_GRAM_SCHED
-    // interleave: fragment reads of two k-steps, then MFMA / fold pairs
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+      if (NT > 0) {
+        constexpr int kMfmaHalf = 2 * (NT > 0 ? NT : 1);   // MFMAs per half stage
+        constexpr int kFoldHalf = 8 * (NT > 0 ? NT : 1);   // fold instructions per half stage
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * (1 + NT), 0);
 #pragma unroll
-    for (int i = 0; i < 6; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
-    }
+        for (int i = 0; i < kMfmaHalf; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, kFoldHalf / kMfmaHalf, 0);
+        }
+      }
 #endif
 #if LAST_GRAM_SCHED >= 2
-    __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_sched_barrier(0);
 #endif
+    };
+    // `pending`: later stages allowed in flight when stage ch + 1 is needed
+    // (-1: ch is the last stage); `refill`: issue stage ch + kRing. Both are
+    // literals in the steady loop, so its body has no branches.
+    auto stage = [&](int ch, int pending, bool refill, f32x16 (&cur)[kTN], bool fresh,
+                     const f32x16 (&prev)[kTN], int h) {
+      read_half(ch, 1, fa1, fb1);
+      mma_half(cur, fresh, fa0, fb0);
+      fold_q(prev, 2 * h);
+      sched_half();
+      if (pending >= 0) {
+        wait_pending(pending);
+        __syncthreads();
+        if (refill) issue(ch + kRing);
+        read_half(ch + 1, 0, fa0, fb0);
+      }
+      mma_half(cur, false, fa1, fb1);
+      fold_q(prev, 2 * h + 1);
+      sched_half();
+    };
+#pragma unroll
+    for (int tn = 0; tn < kTN; ++tn) accQ[tn] = f32x16{};
+    for (int st = 0; st < kRing && st < nst; ++st) issue(st);
+    wait_pending(min(kRing, nst) - 1);   // stage 0 has landed
+    __syncthreads();
+    read_half(0, 0, fa0, fb0);
+    auto pend = [&](int c) { return c == nst - 1 ? -1 : min(kRing - 2, nst - 2 - c); };
+    auto refills = [&](int c) { return c + kRing < nst; };
+    int ch = 0;
+    for (; ch + kRing + 3 < nst; ch += 4) {
+      stage(ch, kRing - 2, true, accP, true, accQ, 0);
+      stage(ch + 1, kRing - 2, true, accP, false, accQ, 1);
+      stage(ch + 2, kRing - 2, true, accQ, true, accP, 0);
+      stage(ch + 3, kRing - 2, true, accQ, false, accP, 1);
+    }
+    for (; ch < nst; ch += 4) {
+      stage(ch, pend(ch), refills(ch), accP, true, accQ, 0);
+      stage(ch + 1, pend(ch + 1), refills(ch + 1), accP, false, accQ, 1);
+      stage(ch + 2, pend(ch + 2), refills(ch + 2), accQ, true, accP, 0);
+      stage(ch + 3, pend(ch + 3), refills(ch + 3), accQ, false, accP, 1);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) fold_q(accQ, q);
   };
-
-  // A chunk is two stages (128 columns) accumulated in fp32; chunks alternate
-  // between the P and Q sets, and each is folded into fp64 while the next one
-  // runs. nst is a multiple of 4 (Dv % 256 == 0); the first folds add zeros,
-  // exactly. The steady loop runs while all four of its stages refill the
-  // ring; the tail (at most kRing + 3 stages) waits and refills as needed.
-  static_assert(kRing <= 8, "tail waits cover up to 6 pending stages");
-#pragma unroll
-  for (int tm = 0; tm < kTM; ++tm)
-#pragma unroll
-    for (int tn = 0; tn < kTN; ++tn) accQ[tm][tn] = f32x16{};
-  for (int st = 0; st < kRing - 1 && st < nst; ++st) issue(st);
-  int ch = 0;
-  for (; ch + kRing + 2 < nst; ch += 4) {
-    stage(ch, kRing - 2, true, accP, true, accQ, 0);
-    stage(ch + 1, kRing - 2, true, accP, false, accQ, 1);
-    stage(ch + 2, kRing - 2, true, accQ, true, accP, 0);
-    stage(ch + 3, kRing - 2, true, accQ, false, accP, 1);
-  }
-  auto pend = [&](int c) { return min(kRing - 2, nst - 1 - c); };
-  auto refills = [&](int c) { return c + kRing - 1 < nst; };
-  for (; ch < nst; ch += 4) {
-    stage(ch, pend(ch), refills(ch), accP, true, accQ, 0);
-    stage(ch + 1, pend(ch + 1), refills(ch + 1), accP, false, accQ, 1);
-    stage(ch + 2, pend(ch + 2), refills(ch + 2), accQ, true, accP, 0);
-    stage(ch + 3, pend(ch + 3), refills(ch + 3), accQ, false, accP, 1);
-  }
-  fold_half(accQ, 0);
-  fold_half(accQ, 1);
+  static_assert(kRing <= 8, "waits cover up to 7 pending stages");
+  if (my_nt == 2)
+    run(std::integral_constant<int, 2>{});
+  else if (my_nt == 1)
+    run(std::integral_constant<int, 1>{});
+  else
+    run(std::integral_constant<int, 0>{});
   __syncthreads();
 
   // Squared norms (diagonal tiles) or the norms of both row blocks, into LDS.
@@ -615,23 +667,20 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   // (l/32)*4 + (v%4) + 8*(v/4); column c's diagonal element is in half
   // hi = (c%8)/4 at v = 4*(c/8) + (c%8) - 4*hi.
   if (DIAG) {
+    for (int tn = 0; tn < my_nt; ++tn) {
+      if (my_b0 + tn != my_a) continue;
+      const int c = lane & 31, hi = lane >> 5;
+      if (((c & 7) >> 2) != hi) continue;
+      const int vsel = 4 * (c >> 3) + (c & 7) - 4 * hi;
+      double d = 0.0;
 #pragma unroll
-    for (int tm = 0; tm < kTM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < kTN; ++tn) {
-        if (wm * kTM + tm != wn * kTN + tn) continue;
-        const int c = lane & 31, hi = lane >> 5;
-        if (((c & 7) >> 2) != hi) continue;
-        const int vsel = 4 * (c >> 3) + (c & 7) - 4 * hi;
-        double d = 0.0;
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          if (v == vsel) d = acc64[tm][tn][v];
-        s_nn[0][(wm * kTM + tm) * 32 + c] = d;
-      }
+      for (int v = 0; v < 16; ++v)
+        if (v == vsel) d = tn ? acc64[1][v] : acc64[0][v];
+      s_nn[0][my_a * 32 + c] = d;
+    }
     __syncthreads();
     for (int i = tid; i < kTile; i += kGramThreads) {
-      const double v = s_nn[0][i];
+      const double v = i < nA ? s_nn[0][i] : 0.0;
       const double iv = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
       s_inv[0][i] = iv;
       s_nn[1][i] = v;
@@ -652,40 +701,40 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   }
   __syncthreads();
 
-  // Coverage distances, written to (i, j) and, off the diagonal, to (j, i).
+  // Coverage distances, written to (i, j) and, for sub-tiles strictly above
+  // the diagonal, to (j, i).
   float *D = dmat + d_off[r];
   const int64_t dlim = d_cap - d_off[r];
+  for (int tn = 0; tn < my_nt; ++tn) {
+    const int sb = my_b0 + tn;
+    const bool mirror = !DIAG || sb > my_a;
+    const int jl = sb * 32 + (lane & 31), j = rowB0 + jl;
+    const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
 #pragma unroll
-  for (int tm = 0; tm < kTM; ++tm)
+    for (int vq = 0; vq < 4; ++vq) {
+      const int il0 = my_a * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
+      float dv[4];
 #pragma unroll
-    for (int tn = 0; tn < kTN; ++tn) {
-      const int jl = (wn * kTN + tn) * 32 + (lane & 31), j = rowB0 + jl;
-      const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u;
+        const double dot = tn ? acc64[1][4 * vq + u] : acc64[0][4 * vq + u];
+        dv[u] = (i < N && j < N)
+                    ? (DIAG && i == j ? kSelfMark : coverage(dot, s_nn[0][il0 + u], nnj, s_inv[0][il0 + u], invj))
+                    : 0.f;
+        if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
+      }
+      if (mirror && j < N) {
+        const int64_t o = (int64_t)j * N + i0;
+        if (i0 + 3 < N && ((d_off[r] + o) & 3) == 0 && o + 3 < dlim) {
+          *reinterpret_cast<float4 *>(D + o) = make_float4(dv[0], dv[1], dv[2], dv[3]);
+        } else {
 #pragma unroll
-      for (int vq = 0; vq < 4; ++vq) {
-        const int il0 = (wm * kTM + tm) * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
-        float dv[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int i = i0 + u;
-          dv[u] = (i < N && j < N) ? (DIAG && i == j ? kSelfMark
-                                                     : coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u],
-                                                                nnj, s_inv[0][il0 + u], invj))
-                                   : 0.f;
-          if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
-        }
-        if (!DIAG && j < N) {
-          const int64_t o = (int64_t)j * N + i0;
-          if (i0 + 3 < N && ((d_off[r] + o) & 3) == 0 && o + 3 < dlim) {
-            *reinterpret_cast<float4 *>(D + o) = make_float4(dv[0], dv[1], dv[2], dv[3]);
-          } else {
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-              if (i0 + u < N && o + u < dlim) D[o + u] = dv[u];
-          }
+          for (int u = 0; u < 4; ++u)
+            if (i0 + u < N && o + u < dlim) D[o + u] = dv[u];
         }
       }
     }
+  }
 }
 
 // fp32 features: squared norms and dots in fp64 FMAs over d = 0..Dv-1 in
