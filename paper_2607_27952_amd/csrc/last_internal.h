@@ -80,6 +80,7 @@ struct SelectPlan {
 struct SelectWs {
   int32_t *dtile_off, *dtile_req;  // diagonal tile prefix per request, tile -> request
   int32_t *otile_off, *otile_req;  // off-diagonal tile prefix per request, tile -> request
+  int32_t *otile_ij;               // off-diagonal tile -> row blocks I << 16 | J
   int64_t *d_off;                  // [R+1] element offsets of each request's N_r x N_r block
   double *nn, *inv;                // [N_total] squared feature norms and 1 / norm
   float *dmat;                     // coverage distances, sum N_r^2

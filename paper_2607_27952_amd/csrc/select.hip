@@ -108,19 +108,6 @@ __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__
   }
 }
 
-// Tile -> request maps: block r writes r over its request's contiguous ranges
-// of diagonal and off-diagonal tiles (the caps bound every write).
-__global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ dtile_off,
-                                                   const int32_t *__restrict__ otile_off,
-                                                   int64_t diag_cap, int64_t off_cap,
-                                                   int32_t *__restrict__ dtile_req,
-                                                   int32_t *__restrict__ otile_req) {
-  const int r = blockIdx.x;
-  const int64_t d1 = min((int64_t)dtile_off[r + 1], diag_cap), o1 = min((int64_t)otile_off[r + 1], off_cap);
-  for (int64_t t = dtile_off[r] + threadIdx.x; t < d1; t += 256) dtile_req[t] = r;
-  for (int64_t t = otile_off[r] + threadIdx.x; t < o1; t += 256) otile_req[t] = r;
-}
-
 // Map a request-local index of the tiles strictly above the diagonal to (I, J).
 __device__ __forceinline__ void tile_ij_upper(int t, int nb, int &I, int &J) {
   int i = 0, rem = t;
@@ -130,6 +117,48 @@ __device__ __forceinline__ void tile_ij_upper(int t, int nb, int &I, int &J) {
   }
   I = i;
   J = i + 1 + rem;
+}
+
+// Tile maps, one block per request: the request of every diagonal and
+// off-diagonal tile, and the (I, J) row blocks of every off-diagonal tile
+// packed as I << 16 | J. Off-diagonal tiles are listed region by region
+// (kRegion x kRegion row blocks, regions in upper-triangle order, tiles
+// I-major inside), so the tiles that run together share few row blocks and
+// re-read them from cache, not HBM. The caps bound every write.
+constexpr int kRegion = 8;
+__global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ cu_vis,
+                                                   const int32_t *__restrict__ dtile_off,
+                                                   const int32_t *__restrict__ otile_off,
+                                                   int64_t diag_cap, int64_t off_cap,
+                                                   int32_t *__restrict__ dtile_req,
+                                                   int32_t *__restrict__ otile_req,
+                                                   int32_t *__restrict__ otile_ij) {
+  const int r = blockIdx.x;
+  const int64_t d1 = min((int64_t)dtile_off[r + 1], diag_cap), o1 = min((int64_t)otile_off[r + 1], off_cap);
+  for (int64_t t = dtile_off[r] + threadIdx.x; t < d1; t += 256) dtile_req[t] = r;
+  for (int64_t t = otile_off[r] + threadIdx.x; t < o1; t += 256) otile_req[t] = r;
+  const int N = cu_vis[r + 1] - cu_vis[r];
+  const int nb = (N + kTile - 1) / kTile, nR = (nb + kRegion - 1) / kRegion;
+  int64_t base = otile_off[r];
+  for (int P = 0; P < nR; ++P)
+    for (int Q = P; Q < nR; ++Q) {
+      const int i0 = P * kRegion, hI = min(i0 + kRegion, nb) - i0;
+      const int j0 = Q * kRegion, hJ = min(j0 + kRegion, nb) - j0;
+      const int cnt = P < Q ? hI * hJ : hI * (hI - 1) / 2;
+      for (int k = threadIdx.x; k < cnt; k += 256) {
+        int I, J;
+        if (P < Q) {
+          I = i0 + k / hJ;
+          J = j0 + k % hJ;
+        } else {
+          tile_ij_upper(k, hI, I, J);
+          I += i0;
+          J += i0;
+        }
+        if (base + k < o1) otile_ij[base + k] = (I << 16) | J;
+      }
+      base += cnt;
+    }
 }
 
 // The coverage matrix holds -inf on its diagonal instead of a token's distance
@@ -188,6 +217,7 @@ template <bool DIAG>
 __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
     const uint16_t *__restrict__ X, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
+    const int32_t *__restrict__ tile_ij,
     const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv, int Dv,
     int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
   __shared__ uint4 sA[2][kPieces];
@@ -215,7 +245,8 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
   if (DIAG) {
     I = J = (int)(t - tile_off[r]);
   } else {
-    tile_ij_upper((int)(t - tile_off[r]), nb, I, J);
+    I = tile_ij[t] >> 16;
+    J = tile_ij[t] & 0xFFFF;
   }
   const int rowA0 = I * kTile, rowB0 = J * kTile;
   const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
@@ -421,6 +452,7 @@ template <bool DIAG>
 __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
     const uint16_t *__restrict__ X, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
+    const int32_t *__restrict__ tile_ij,
     const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv, int Dv,
     int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
   constexpr int kOps = DIAG ? 1 : 2;
@@ -454,7 +486,8 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   if (DIAG) {
     I = J = (int)(t - tile_off[r]);
   } else {
-    tile_ij_upper((int)(t - tile_off[r]), nb, I, J);
+    I = tile_ij[t] >> 16;
+    J = tile_ij[t] & 0xFFFF;
   }
   const int rowA0 = I * kTile, rowB0 = J * kTile;
   const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
@@ -758,6 +791,7 @@ template <bool DIAG>
 __global__ __launch_bounds__(256) void k_gram_f32(
     const float *__restrict__ X, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
+    const int32_t *__restrict__ tile_ij,
     const int64_t *__restrict__ d_off, const double *__restrict__ nn, const double *__restrict__ inv,
     int Dv, int64_t tiles_total, int64_t d_cap, float *__restrict__ dmat) {
   // A 128x128 Gram tile is covered by 2x2 sub-tiles of 64x64, one pass each.
@@ -770,10 +804,12 @@ __global__ __launch_bounds__(256) void k_gram_f32(
   const int N = cu_vis[r + 1] - (int)n0;
   const int nb = (N + kTile - 1) / kTile;
   int I, J;
-  if (DIAG)
+  if (DIAG) {
     I = J = (int)(t_glob - tile_off[r]);
-  else
-    tile_ij_upper((int)(t_glob - tile_off[r]), nb, I, J);
+  } else {
+    I = tile_ij[t_glob] >> 16;
+    J = tile_ij[t_glob] & 0xFFFF;
+  }
   float *D = dmat + d_off[r];
   const int64_t dlim = d_cap - d_off[r];
   const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
@@ -1119,6 +1155,7 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
     w.dtile_req = cv.take<int32_t>(p.tiles_diag);
     w.otile_off = cv.take<int32_t>(R + 1);
     w.otile_req = cv.take<int32_t>(p.tiles_off);
+    w.otile_ij = cv.take<int32_t>(p.tiles_off);
     w.d_off = cv.take<int64_t>(R + 1);
     w.nn = cv.take<double>(p.N_total);
     w.inv = cv.take<double>(p.N_total);
@@ -1150,8 +1187,8 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
 
   launch_begin("select_plan", s);
   hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, w.dtile_off, w.otile_off, w.d_off);
-  hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, w.dtile_off, w.otile_off, p.tiles_diag,
-                     p.tiles_off, w.dtile_req, w.otile_req);
+  hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, cu_vis, w.dtile_off, w.otile_off, p.tiles_diag,
+                     p.tiles_off, w.dtile_req, w.otile_req, w.otile_ij);
   if ((e = launch_end(s)) != hipSuccess) return e;
 
   if (fdtype == LAST_BF16) {
@@ -1160,14 +1197,14 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
     launch_begin("gram_diag", s);
     hipLaunchKernelGGL(dma ? k_gram_bf16<true> : k_gram_bf16_staged<true>, dim3((unsigned)p.tiles_diag),
                        dim3(kGramThreads), 0, s, (const uint16_t *)feats, cu_vis, w.dtile_off,
-                       w.dtile_req, w.d_off, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
+                       w.dtile_req, nullptr, w.d_off, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
     if (p.tiles_off > 0) {
       launch_begin("gram", s);
       const int64_t grid = (p.tiles_off + 7) / 8 * 8;
       hipLaunchKernelGGL(dma ? k_gram_bf16<false> : k_gram_bf16_staged<false>, dim3((unsigned)grid),
                          dim3(kGramThreads), 0, s, (const uint16_t *)feats, cu_vis, w.otile_off,
-                         w.otile_req, w.d_off, w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
+                         w.otile_req, w.otile_ij, w.d_off, w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
       if ((e = launch_end(s)) != hipSuccess) return e;
     }
   } else {
@@ -1177,14 +1214,14 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
     if ((e = launch_end(s)) != hipSuccess) return e;
     launch_begin("gram_diag", s);
     hipLaunchKernelGGL(k_gram_f32<true>, dim3((unsigned)p.tiles_diag), dim3(256), 0, s,
-                       (const float *)feats, cu_vis, w.dtile_off, w.dtile_req, w.d_off, w.nn, w.inv,
-                       Dv, p.tiles_diag, p.d_elems, w.dmat);
+                       (const float *)feats, cu_vis, w.dtile_off, w.dtile_req, nullptr, w.d_off, w.nn,
+                       w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
     if (p.tiles_off > 0) {
       launch_begin("gram", s);
       hipLaunchKernelGGL(k_gram_f32<false>, dim3((unsigned)p.tiles_off), dim3(256), 0, s,
-                         (const float *)feats, cu_vis, w.otile_off, w.otile_req, w.d_off, w.nn, w.inv,
-                         Dv, p.tiles_off, p.d_elems, w.dmat);
+                         (const float *)feats, cu_vis, w.otile_off, w.otile_req, w.otile_ij, w.d_off,
+                         w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
       if ((e = launch_end(s)) != hipSuccess) return e;
     }
   }
