@@ -19,8 +19,9 @@
 //                   yields |x_i|^2 from the same arithmetic (so a row and its
 //                   bitwise duplicate get distance exactly 0); a second launch
 //                   covers the tiles above the diagonal and mirrors them.
-//   k_sqnorm_f32 / k_gram_f32   the same for fp32 features, in fp64 VALU FMAs
-//                   (norms in a separate pass with the dots' loop order).
+//   k_gram_f32      the same for fp32 features, in fp64 VALU FMAs over
+//                   32 x 32 sub-tiles; the diagonal sub-tiles run first and
+//                   yield the norms from the same FMA chains.
 //   k_greedy        one block per request; w and delta live in registers.
 //                   Step t loads row j_{t-1} of the distance block, folds it
 //                   into delta with min, and takes the block-wide argmax of
@@ -197,6 +198,9 @@ __device__ __forceinline__ float coverage(double dot, double nni, double nnj, do
 #endif
 #ifndef LAST_GRAM_SCHED
 #define LAST_GRAM_SCHED 2
+#endif
+#ifndef LAST_GRAM_DMA_SPREAD
+#define LAST_GRAM_DMA_SPREAD 1
 #endif
 #if LAST_GRAM_LAYOUT == 0
 constexpr int kWM = 2, kWN = 2, kTM = 2, kTN = 2;
@@ -512,11 +516,13 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   }
   constexpr uint32_t kStageBytes = kOps * kDmaPieces * 16;
   const int nst = Dv / kDmaCols;
+  auto issue_one = [&](int st, int x) {
+    dma16(dst[x] + (uint32_t)(st & (kRing - 1)) * kStageBytes, (const char *)gbase[x] + (int64_t)st * kDmaCols * 2,
+          voff[x]);
+  };
   auto issue = [&](int st) {
-    const uint32_t off = (uint32_t)(st & (kRing - 1)) * kStageBytes;
 #pragma unroll
-    for (int x = 0; x < kPerWave; ++x)
-      dma16(dst[x] + off, (const char *)gbase[x] + (int64_t)st * kDmaCols * 2, voff[x]);
+    for (int x = 0; x < kPerWave; ++x) issue_one(st, x);
   };
 
   // This block's work in pairs of 32 x 32 sub-tiles: A rows [32 a, 32 a + 32)
@@ -652,6 +658,35 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
       mma_half(cur, fresh, fa0, fb0);
       fold_q(prev, 2 * h);
       sched_half();
+#if LAST_GRAM_DMA_SPREAD
+      // second half: after the barrier, each MFMA is followed by a share of
+      // this wave's loads of stage ch + kRing and two fold elements, in that
+      // order, so the load issue does not hold the wave at the barrier
+      if (pending >= 0) {
+        wait_pending(pending);
+        __syncthreads();
+        read_half(ch + 1, 0, fa0, fb0);
+      }
+      if (NT == 0) {
+        if (refill) issue(ch + kRing);
+      } else {
+        constexpr int kM = 2 * (NT > 0 ? NT : 1);
+#pragma unroll
+        for (int m = 0; m < kM; ++m) {
+          const int ss = m / (NT > 0 ? NT : 1), tn = m % (NT > 0 ? NT : 1);
+          cur[tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[ss], fb1[ss][tn], cur[tn], 0, 0, 0);
+          if (refill)
+#pragma unroll
+            for (int x = m * kPerWave / kM; x < (m + 1) * kPerWave / kM; ++x) issue_one(ch + kRing, x);
+#pragma unroll
+          for (int e = 2 * m; e < 2 * m + 2; ++e) {
+            const int et = e / 4, ev = 4 * (2 * h + 1) + e % 4;
+            acc64[et][ev] += (double)prev[et][ev];
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+#else
       if (pending >= 0) {
         wait_pending(pending);
         __syncthreads();
@@ -661,6 +696,7 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
       mma_half(cur, false, fa1, fb1);
       fold_q(prev, 2 * h + 1);
       sched_half();
+#endif
     };
 #pragma unroll
     for (int tn = 0; tn < kTN; ++tn) accQ[tn] = f32x16{};
@@ -770,91 +806,115 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   }
 }
 
-// fp32 features: squared norms and dots in fp64 FMAs over d = 0..Dv-1 in
-// order, the same loop for both, so duplicates again give distance 0.
-__global__ __launch_bounds__(256) void k_sqnorm_f32(const float *__restrict__ X, int64_t N_total,
-                                                    int Dv, double *__restrict__ nn,
-                                                    double *__restrict__ inv) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= N_total) return;
-  const float *x = X + i * Dv;
-  double s = 0.0;
-  for (int d = 0; d < Dv; ++d) s = fma((double)x[d], (double)x[d], s);
-  nn[i] = s;
-  inv[i] = s > 0.0 ? 1.0 / sqrt(s) : 0.0;
-}
+// fp32 features: every dot product, squared norms included, is one fp64 FMA
+// chain over d = 0..Dv-1 in order, so a row and its bitwise duplicate get
+// distance exactly 0. Block b computes 32 x 32 sub-tile b % 16 of 128 x 128
+// tile b / 16 (4 x 4 sub-tiles), 2 x 2 outputs a thread, over 64-column
+// chunks staged through LDS; the next chunk is loaded into registers while
+// the current one is used. Three launches:
+//   kF32Self   sub-tiles on the diagonal of the diagonal tiles: their own
+//              diagonal gives the squared norms of their 32 rows (written
+//              out for the other launches) and their coverage values;
+//   kF32Upper  sub-tiles above the diagonal of the diagonal tiles (each
+//              also writes its mirror);
+//   kF32Off    every sub-tile of the off-diagonal tiles (mirrored).
+constexpr int kF32Sub = 32, kF32KS = 64, kF32Subs = (kTile / kF32Sub) * (kTile / kF32Sub);
+constexpr int kF32Self = 0, kF32Upper = 1, kF32Off = 2;
+constexpr int kF32Per = kF32Sub * kF32KS / 256;   // staged elements per thread and operand
 
-constexpr int kF32Tile = 64;
-constexpr int kF32KS = 32;
-
-template <bool DIAG>
+template <int MODE>
 __global__ __launch_bounds__(256) void k_gram_f32(
     const float *__restrict__ X, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
     const int32_t *__restrict__ tile_ij,
-    const int64_t *__restrict__ d_off, const double *__restrict__ nn, const double *__restrict__ inv,
+    const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv,
     int Dv, int64_t tiles_total, int64_t d_cap, float *__restrict__ dmat) {
-  // A 128x128 Gram tile is covered by 2x2 sub-tiles of 64x64, one pass each.
-  __shared__ float sA[kF32KS][kF32Tile + 1];
-  __shared__ float sB[kF32KS][kF32Tile + 1];
-  const int64_t t_glob = blockIdx.x;
+  __shared__ float sA[kF32KS][kF32Sub + 1];
+  __shared__ float sB[kF32KS][kF32Sub + 1];
+  __shared__ double s_nn[kF32Sub], s_inv[kF32Sub];
+  const int64_t t_glob = blockIdx.x / kF32Subs;
+  const int sub = blockIdx.x % kF32Subs, sa = sub / (kTile / kF32Sub), sb = sub % (kTile / kF32Sub);
   if (t_glob >= tiles_total) return;
+  if (MODE == kF32Self && sb != sa) return;
+  if (MODE == kF32Upper && sb <= sa) return;
   const int r = tile_req[t_glob];
   const int64_t n0 = cu_vis[r];
   const int N = cu_vis[r + 1] - (int)n0;
-  const int nb = (N + kTile - 1) / kTile;
   int I, J;
-  if (DIAG) {
+  if (MODE != kF32Off) {
     I = J = (int)(t_glob - tile_off[r]);
   } else {
     I = tile_ij[t_glob] >> 16;
     J = tile_ij[t_glob] & 0xFFFF;
   }
+  const int rowA0 = I * kTile + sa * kF32Sub, rowB0 = J * kTile + sb * kF32Sub;
+  if (rowA0 >= N || rowB0 >= N) return;
   float *D = dmat + d_off[r];
   const int64_t dlim = d_cap - d_off[r];
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  for (int sub = 0; sub < 4; ++sub) {
-    const int rowA0 = I * kTile + (sub >> 1) * kF32Tile;
-    const int rowB0 = J * kTile + (sub & 1) * kF32Tile;
-    if (rowA0 >= N || rowB0 >= N) continue;
-    double acc[4][4];
+  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+
+  float pa[kF32Per], pb[kF32Per];
+  auto fetch = [&](int k0) {
 #pragma unroll
-    for (int a = 0; a < 4; ++a)
+    for (int q = 0; q < kF32Per; ++q) {
+      const int e = tid + 256 * q, row = e / kF32KS, kk = e % kF32KS;
+      const int ia = rowA0 + row, ib = rowB0 + row;
+      pa[q] = (ia < N && k0 + kk < Dv) ? X[(n0 + ia) * Dv + k0 + kk] : 0.f;
+      pb[q] = (ib < N && k0 + kk < Dv) ? X[(n0 + ib) * Dv + k0 + kk] : 0.f;
+    }
+  };
+  double acc[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
+  fetch(0);
+  for (int k0 = 0; k0 < Dv; k0 += kF32KS) {
+    __syncthreads();
 #pragma unroll
-      for (int b = 0; b < 4; ++b) acc[a][b] = 0.0;
-    for (int k0 = 0; k0 < Dv; k0 += kF32KS) {
-      __syncthreads();
-      for (int e = threadIdx.x; e < kF32KS * kF32Tile; e += 256) {
-        const int row = e / kF32KS, kk = e % kF32KS;
-        const int ia = rowA0 + row, ib = rowB0 + row;
-        sA[kk][row] = (ia < N && k0 + kk < Dv) ? X[(n0 + ia) * Dv + k0 + kk] : 0.f;
-        sB[kk][row] = (ib < N && k0 + kk < Dv) ? X[(n0 + ib) * Dv + k0 + kk] : 0.f;
-      }
-      __syncthreads();
-      const int kmax = min(kF32KS, Dv - k0);
-      for (int kk = 0; kk < kmax; ++kk) {
-        double av[4], bv[4];
-#pragma unroll
-        for (int a = 0; a < 4; ++a) av[a] = sA[kk][ty + 16 * a];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) bv[b] = sB[kk][tx + 16 * b];
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-#pragma unroll
-          for (int b = 0; b < 4; ++b) acc[a][b] = fma(av[a], bv[b], acc[a][b]);
+    for (int q = 0; q < kF32Per; ++q) {
+      const int e = tid + 256 * q, row = e / kF32KS, kk = e % kF32KS;
+      sA[kk][row] = pa[q];
+      sB[kk][row] = pb[q];
+    }
+    __syncthreads();
+    if (k0 + kF32KS < Dv) fetch(k0 + kF32KS);
+    const int kmax = min(kF32KS, Dv - k0);
+    for (int kk = 0; kk < kmax; ++kk) {
+      const double a0 = sA[kk][ty], a1 = sA[kk][ty + 16];
+      const double b0 = sB[kk][tx], b1 = sB[kk][tx + 16];
+      acc[0][0] = fma(a0, b0, acc[0][0]);
+      acc[0][1] = fma(a0, b1, acc[0][1]);
+      acc[1][0] = fma(a1, b0, acc[1][0]);
+      acc[1][1] = fma(a1, b1, acc[1][1]);
+    }
+  }
+  // norms of the rows (MODE kF32Self: from this block's own diagonal)
+  const double *nnA, *nnB, *invA, *invB;
+  if (MODE == kF32Self) {
+    if (tx == ty) {
+      s_nn[ty] = acc[0][0];
+      s_nn[ty + 16] = acc[1][1];
+    }
+    __syncthreads();
+    if (tid < kF32Sub) {
+      const double v = s_nn[tid];
+      s_inv[tid] = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
+      if (rowA0 + tid < N) {
+        nn[n0 + rowA0 + tid] = v;
+        inv[n0 + rowA0 + tid] = s_inv[tid];
       }
     }
-#pragma unroll
-    for (int a = 0; a < 4; ++a)
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int i = rowA0 + ty + 16 * a, j = rowB0 + tx + 16 * b;
-        if (i >= N || j >= N) continue;
-        const float dv = i == j ? kSelfMark : coverage(acc[a][b], nn[n0 + i], nn[n0 + j], inv[n0 + i], inv[n0 + j]);
-        if ((int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv;
-        if (I != J && (int64_t)j * N + i < dlim) D[(int64_t)j * N + i] = dv;
-      }
+    __syncthreads();
   }
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int il = ty + 16 * a, jl = tx + 16 * b, i = rowA0 + il, j = rowB0 + jl;
+      if (i >= N || j >= N) continue;
+      const double nni = MODE == kF32Self ? s_nn[il] : nn[n0 + i], nnj = MODE == kF32Self ? s_nn[jl] : nn[n0 + j];
+      const double ivi = MODE == kF32Self ? s_inv[il] : inv[n0 + i], ivj = MODE == kF32Self ? s_inv[jl] : inv[n0 + j];
+      const float dv = i == j ? kSelfMark : coverage(acc[a][b], nni, nnj, ivi, ivj);
+      if ((int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv;
+      if (MODE != kF32Self && (int64_t)j * N + i < dlim) D[(int64_t)j * N + i] = dv;
+    }
 }
 
 // ------------------------------------------------------------ greedy
@@ -1208,18 +1268,17 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
       if ((e = launch_end(s)) != hipSuccess) return e;
     }
   } else {
-    launch_begin("sqnorm", s);
-    hipLaunchKernelGGL(k_sqnorm_f32, dim3((unsigned)((p.N_total + 255) / 256)), dim3(256), 0, s,
-                       (const float *)feats, p.N_total, Dv, w.nn, w.inv);
-    if ((e = launch_end(s)) != hipSuccess) return e;
     launch_begin("gram_diag", s);
-    hipLaunchKernelGGL(k_gram_f32<true>, dim3((unsigned)p.tiles_diag), dim3(256), 0, s,
+    hipLaunchKernelGGL(k_gram_f32<kF32Self>, dim3((unsigned)(p.tiles_diag * kF32Subs)), dim3(256), 0, s,
+                       (const float *)feats, cu_vis, w.dtile_off, w.dtile_req, nullptr, w.d_off, w.nn,
+                       w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
+    hipLaunchKernelGGL(k_gram_f32<kF32Upper>, dim3((unsigned)(p.tiles_diag * kF32Subs)), dim3(256), 0, s,
                        (const float *)feats, cu_vis, w.dtile_off, w.dtile_req, nullptr, w.d_off, w.nn,
                        w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
     if (p.tiles_off > 0) {
       launch_begin("gram", s);
-      hipLaunchKernelGGL(k_gram_f32<false>, dim3((unsigned)p.tiles_off), dim3(256), 0, s,
+      hipLaunchKernelGGL(k_gram_f32<kF32Off>, dim3((unsigned)(p.tiles_off * kF32Subs)), dim3(256), 0, s,
                          (const float *)feats, cu_vis, w.otile_off, w.otile_req, w.otile_ij, w.d_off,
                          w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
       if ((e = launch_end(s)) != hipSuccess) return e;
