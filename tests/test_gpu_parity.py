@@ -147,6 +147,10 @@ SELECT_CASES = [
     (23, 2, (300, 640), 136, W.BF16, 0.5, 5),      # Dv not a multiple of 64
     (24, 3, (50, 500), 96, W.F32, 0.2, 6),
     (25, 1, (1500, 2100), 512, W.BF16, 0.1, 24),
+    (26, 7, (1, 260), 256, W.BF16, 0.3, 3),        # four 64-column stages only; one-block requests
+    (27, 2, (1025, 1100), 768, W.BF16, None, 12),  # greedy blocks of 256 threads
+    (28, 1, (8193, 8300), 256, W.BF16, 0.05, 32),  # greedy blocks of 512 threads
+    (29, 5, (1, 200), 32, W.F32, 0.5, 3),          # fp32 rows shorter than one staged chunk
 ]
 
 
