@@ -1,0 +1,38 @@
+"""The bench's algorithmic work figures (no GPU): the Gram's diagonal and
+off-diagonal blocks together count every unordered pair of a request once,
+diagonal included, and the score pass counts every key row once."""
+import os
+import sys
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+from paper_2607_27952_amd import workloads as W  # noqa: E402
+
+
+def test_gram_flops_cover_each_pair_once():
+    for n in [1, 5, 127, 128, 129, 576, 1000, 2880]:
+        d, o = bench.gram_flops(np.array([n]), 16)
+        assert d + o == n * (n + 1) * 16          # N(N+1)/2 pairs x 2 flops x Dv
+        if n <= 128:
+            assert o == 0
+
+
+def test_kernel_work_matches_shapes():
+    wl = W.tiny(3, R=3, G=2, Hq=8, Hkv=2, Dh=64, n_range=(100, 300), t_range=(5, 40), Dv=256)
+    work = bench.kernel_work(wl)
+    elt = 2 if wl.qk_dtype == W.BF16 else 4
+    assert work["score_stream"] == ("hbm", wl.G * wl.T_total * wl.Hkv * wl.Dh * elt + wl.G * wl.R * wl.Hq * wl.Dh * elt)
+    n = np.diff(wl.cu_vis)
+    assert work["gram_diag"][1] + work["gram"][1] == float(np.sum(n * (n + 1))) * wl.Dv
+    felt = 2 if wl.f_dtype == W.BF16 else 4
+    assert work["gather"] == ("hbm", 2 * wl.K_total * wl.Dv * felt)
+    assert work["gram"][0] == ("mfma" if felt == 2 else "alu")
+
+
+def test_multi_gpu_request_exits():
+    import subprocess
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True)
+    assert r.returncode == 2 and "one GPU" in r.stderr
