@@ -519,33 +519,47 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
 
 // Per request: merge the chunk statistics of every (layer, head) row into its
 // max M and 1/Z, and the total visual mass S = sum_{l,h} V / Z (= sum_i s_i).
-__global__ __launch_bounds__(kThreads) void k_score_merge(
+constexpr int kMergeThreads = 1024;
+__global__ __launch_bounds__(kMergeThreads) void k_score_merge(
     const float4 *__restrict__ stats, const int32_t *__restrict__ chunk_off, int GH,
     int64_t C_total, float2 *__restrict__ rowstat, float *__restrict__ mass) {
-  __shared__ float s_red[kWaves];
+  // One wave per (layer, head) row at a time: lanes merge the row's chunks
+  // lane-strided with the online rule, then the wave combines the lanes
+  // (log-sum-exp over (max, sum) pairs). The visual mass adds V / Z over the
+  // rows, per wave and then over the waves, in a fixed order.
+  constexpr int kNW = kMergeThreads / 64;
+  __shared__ float s_red[kNW];
   const int r = blockIdx.x;
   const int c0 = chunk_off[r], c1 = chunk_off[r + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float part = 0.f;
-  for (int p = threadIdx.x; p < GH; p += kThreads) {
+  for (int p = wave; p < GH; p += kNW) {
     const float4 *st = stats + (int64_t)p * C_total;
-    float M = -INFINITY;
-    for (int c = c0; c < c1; ++c) M = fmaxf(M, st[c].x);
-    float Z = 0.f, V = 0.f;
-    for (int c = c0; c < c1; ++c) {
-      const float4 s = st[c];
-      const float e = expf(s.x - M);
-      Z = fmaf(s.y, e, Z);
-      V = fmaf(s.z, e, V);
+    float m = -INFINITY, z = 0.f, v = 0.f;
+    for (int c = c0 + lane; c < c1; c += 64) {
+      const float4 e = st[c];
+      if (e.x > m) {
+        const float f = m == -INFINITY ? 0.f : expf(m - e.x);
+        z = fmaf(z, f, e.y);
+        v = fmaf(v, f, e.z);
+        m = e.x;
+      } else {
+        const float f = expf(e.x - m);
+        z = fmaf(e.y, f, z);
+        v = fmaf(e.z, f, v);
+      }
     }
-    rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
+    const float M = wave_max(m);
+    const float f = m == -INFINITY ? 0.f : expf(m - M);
+    const float Z = wave_sum(z * f), V = wave_sum(v * f);
+    if (lane == 0) rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
     part += V / Z;
   }
-  part = wave_sum(part);
-  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = part;
+  if (lane == 0) s_red[wave] = part;
   __syncthreads();
   if (threadIdx.x == 0) {
     float S = 0.f;
-    for (int w = 0; w < kWaves; ++w) S += s_red[w];
+    for (int w = 0; w < kNW; ++w) S += s_red[w];
     mass[r] = S;
   }
 }
@@ -736,7 +750,7 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
   if (e != hipSuccess) return e;
 
   launch_begin("score_merge", s);
-  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)b->R), dim3(kThreads), 0, s, w.stats, w.chunk_off,
+  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)b->R), dim3(kMergeThreads), 0, s, w.stats, w.chunk_off,
                      b->G * b->Hq, p.C_total, w.rowstat, w.mass);
   e = launch_end(s);
   if (e != hipSuccess) return e;

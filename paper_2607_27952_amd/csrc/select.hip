@@ -244,7 +244,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
   const int r = tile_req[t];
   const int64_t n0 = cu_vis[r];
   const int N = cu_vis[r + 1] - (int)n0;
-  const int nb = (N + kTile - 1) / kTile;
   int I, J;
   if (DIAG) {
     I = J = (int)(t - tile_off[r]);
@@ -485,7 +484,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   const int r = tile_req[t];
   const int64_t n0 = cu_vis[r];
   const int N = cu_vis[r + 1] - (int)n0;
-  const int nb = (N + kTile - 1) / kTile;
   int I, J;
   if (DIAG) {
     I = J = (int)(t - tile_off[r]);
@@ -497,7 +495,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / kWN, wn = wave % kWN;
 
   // This wave's DMA instructions: q = wave + kGramWaves * x, operand q / 16,
   // LDS slots (q % 16) * 64 + lane of the stage. The operand's row-block base
@@ -886,7 +883,6 @@ __global__ __launch_bounds__(256) void k_gram_f32(
     }
   }
   // norms of the rows (MODE kF32Self: from this block's own diagonal)
-  const double *nnA, *nnB, *invA, *invB;
   if (MODE == kF32Self) {
     if (tx == ty) {
       s_nn[ty] = acc[0][0];
