@@ -190,25 +190,8 @@ __device__ __forceinline__ float coverage(double dot, double nni, double nnj, do
 // so that the fragment reads of 16 consecutive rows hit distinct banks. Two
 // stages alternate; the next stage is fetched into registers while the
 // current one feeds the matrix cores.
-#ifndef LAST_GRAM_LAYOUT
-#define LAST_GRAM_LAYOUT 1
-#endif
-#ifndef LAST_GRAM_REVERSE
-#define LAST_GRAM_REVERSE 0
-#endif
-#ifndef LAST_GRAM_SCHED
-#define LAST_GRAM_SCHED 2
-#endif
-#ifndef LAST_GRAM_DMA_SPREAD
-#define LAST_GRAM_DMA_SPREAD 1
-#endif
-#if LAST_GRAM_LAYOUT == 0
-constexpr int kWM = 2, kWN = 2, kTM = 2, kTN = 2;
-#elif LAST_GRAM_LAYOUT == 1
+// Block tile 128 x 128: 4 x 2 waves, each 1 x 2 MFMA tiles of 32 x 32.
 constexpr int kWM = 4, kWN = 2, kTM = 1, kTN = 2;
-#else
-constexpr int kWM = 4, kWN = 4, kTM = 1, kTN = 1;
-#endif
 constexpr int kGramWaves = kWM * kWN;
 constexpr int kGramThreads = 64 * kGramWaves;
 constexpr int kPieces = kTile * 8;                     // 16-byte pieces per operand stage
@@ -234,11 +217,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
     // go to the same XCD, which receives every 8th block.
     const int64_t per_xcd = gridDim.x / 8;
     t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-#if LAST_GRAM_REVERSE
-    // last requests first: their rows were the most recent reads of the
-    // diagonal launch and are the likeliest to still sit in the last-level cache
-    t = (int64_t)gridDim.x - 1 - t;
-#endif
   }
   if (t >= tiles) return;
   const int r = tile_req[t];
@@ -417,15 +395,9 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
 // columns); two accumulator sets alternate so that folding chunk c - 1 into
 // fp64 can overlap the matrix-core work of chunk c. Needs Dv % 256 == 0 (a
 // stage count divisible by 4).
-#ifndef LAST_GRAM_RING
-#define LAST_GRAM_RING 4
-#endif
-#ifndef LAST_GRAM_RING_DIAG
-#define LAST_GRAM_RING_DIAG 8
-#endif
 // Diagonal tiles stage one operand (16 KB a stage) and read every row exactly
 // once, straight from HBM, so they keep a deeper ring in flight.
-constexpr int kRingOff = LAST_GRAM_RING, kRingDiag = LAST_GRAM_RING_DIAG;
+constexpr int kRingOff = 4, kRingDiag = 8;
 static_assert((kRingOff & (kRingOff - 1)) == 0 && (kRingDiag & (kRingDiag - 1)) == 0, "power-of-two ring");
 constexpr int kDmaCols = kKS;                               // columns per ring stage (64)
 constexpr int kDmaPieces = kTile * kDmaCols * 2 / 16;       // 16-byte pieces per operand stage (1024)
@@ -474,11 +446,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
     // go to the same XCD, which receives every 8th block.
     const int64_t per_xcd = gridDim.x / 8;
     t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-#if LAST_GRAM_REVERSE
-    // last requests first: their rows were the most recent reads of the
-    // diagonal launch and are the likeliest to still sit in the last-level cache
-    t = (int64_t)gridDim.x - 1 - t;
-#endif
   }
   if (t >= tiles) return;
   const int r = tile_req[t];
@@ -630,7 +597,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
                                                             (fresh && ss == 0) ? f32x16{} : cur[tn], 0, 0, 0);
     };
     auto sched_half = [&]() {
-#if LAST_GRAM_SCHED
       if (NT > 0) {
         constexpr int kMfmaHalf = 2 * (NT > 0 ? NT : 1);   // MFMAs per half stage
         constexpr int kFoldHalf = 8 * (NT > 0 ? NT : 1);   // fold instructions per half stage
@@ -641,10 +607,7 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
           __builtin_amdgcn_sched_group_barrier(0x002, kFoldHalf / kMfmaHalf, 0);
         }
       }
-#endif
-#if LAST_GRAM_SCHED >= 2
       __builtin_amdgcn_sched_barrier(0);
-#endif
     };
     // `pending`: later stages allowed in flight when stage ch + 1 is needed
     // (-1: ch is the last stage); `refill`: issue stage ch + kRing. Both are
@@ -655,7 +618,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
       mma_half(cur, fresh, fa0, fb0);
       fold_q(prev, 2 * h);
       sched_half();
-#if LAST_GRAM_DMA_SPREAD
       // second half: after the barrier, each MFMA is followed by a share of
       // this wave's loads of stage ch + kRing and two fold elements, in that
       // order, so the load issue does not hold the wave at the barrier
@@ -683,17 +645,6 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
           __builtin_amdgcn_sched_barrier(0);
         }
       }
-#else
-      if (pending >= 0) {
-        wait_pending(pending);
-        __syncthreads();
-        if (refill) issue(ch + kRing);
-        read_half(ch + 1, 0, fa0, fb0);
-      }
-      mma_half(cur, false, fa1, fb1);
-      fold_q(prev, 2 * h + 1);
-      sched_half();
-#endif
     };
 #pragma unroll
     for (int tn = 0; tn < kTN; ++tn) accQ[tn] = f32x16{};
