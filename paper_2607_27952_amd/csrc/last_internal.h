@@ -67,23 +67,44 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
 constexpr int kGramTile = 128;       // Gram tile edge (rows of X per side)
 constexpr int kSelMaxN = 16384;      // largest request the register-resident greedy holds
 
+// A request's coverage matrix is stored as nb x nb tiles of 128 x 128 floats
+// (nb = ceil(N_r / 128)), tile (I, J) at element (I * nb + J) * 128 * 128 and
+// row-major inside. A Gram tile then writes two contiguous 64 KB blocks (its
+// own and the mirror), and the greedy reads row j as nb pieces of 512 bytes.
+// Entries past N_r in the last row or column block are padding, never read.
+constexpr int64_t kCovTileElems = (int64_t)kGramTile * kGramTile;
+__host__ __device__ inline int64_t cov_blocks(int64_t n) { return (n + kGramTile - 1) / kGramTile; }
+__host__ __device__ inline int64_t cov_elems(int64_t n) { return cov_blocks(n) * cov_blocks(n) * kCovTileElems; }
+// element (i, j) of a matrix with nb row blocks
+__host__ __device__ inline int64_t cov_index(int64_t i, int64_t j, int64_t nb) {
+  return ((i / kGramTile) * nb + j / kGramTile) * kCovTileElems + (i % kGramTile) * kGramTile + j % kGramTile;
+}
+
+// One Gram tile: the request's first feature row, N_r, the row blocks
+// I << 16 | J, the request, and the element offset of its coverage matrix.
+struct alignas(16) TileMeta {
+  int32_t n0, n, ij, r;
+  int64_t doff, pad;
+};
+static_assert(sizeof(TileMeta) == 32, "two 16-byte pieces");
+
 struct SelectPlan {
   int64_t N_total, K_total;
   int32_t N_max, K_max;
   int64_t tiles_diag;      // diagonal Gram tiles over all requests
   int64_t tiles_off;       // Gram tiles strictly above the diagonal
-  int64_t d_elems;         // sum of N_r^2 (coverage matrices)
+  int64_t d_elems;         // sum of cov_elems(N_r) (coverage matrices)
   int32_t threads, ept;    // top-k block shape
   int32_t g_threads, g_ept;  // greedy block shape
 };
 
 struct SelectWs {
-  int32_t *dtile_off, *dtile_req;  // diagonal tile prefix per request, tile -> request
-  int32_t *otile_off, *otile_req;  // off-diagonal tile prefix per request, tile -> request
-  int32_t *otile_ij;               // off-diagonal tile -> row blocks I << 16 | J
-  int64_t *d_off;                  // [R+1] element offsets of each request's N_r x N_r block
-  double *nn, *inv;                // [N_total] squared feature norms and 1 / norm
-  float *dmat;                     // coverage distances, sum N_r^2
+  int32_t *dtile_off, *otile_off;  // [R+1] diagonal / off-diagonal tile prefixes per request
+  TileMeta *dtile, *otile;         // every diagonal / off-diagonal tile
+  int64_t *d_off;                  // [R+1] element offsets of each request's coverage matrix
+  double *nn, *inv;                // [N_total + 128] squared feature norms and 1 / norm
+                                   // (the tail lets a tile read 128 entries from any row)
+  float *dmat;                     // coverage distances, tile-major per request (cov_index)
 };
 
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,

@@ -35,6 +35,7 @@
 // their bits), breaks ties at the threshold towards the lowest index, and
 // ranks the kept tokens for the pick order.
 #include <algorithm>
+#include <atomic>
 #include <math.h>
 
 #include "last_internal.h"
@@ -45,6 +46,12 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+using last::TileMeta;
+using last::cov_blocks;
+using last::cov_elems;
+using last::cov_index;
+using last::kCovTileElems;
 
 constexpr int kTile = last::kGramTile;   // 128
 constexpr int kKS = 64;                  // elements per k stage = one fp64 fold chunk
@@ -70,7 +77,8 @@ __device__ void block_excl_scan_i64(int64_t v, int64_t *sh, int64_t *total, int6
 }
 
 // Per request: nb = ceil(N / 128) row blocks give nb diagonal Gram tiles and
-// nb (nb - 1) / 2 tiles above the diagonal; the N x N block starts at d_off.
+// nb (nb - 1) / 2 tiles above the diagonal; the coverage matrix (nb x nb
+// tiles of 128 x 128) starts at d_off.
 __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__ cu_vis, int R,
                                                      int32_t *__restrict__ dtile_off,
                                                      int32_t *__restrict__ otile_off,
@@ -84,7 +92,7 @@ __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__
       const int64_t N = cu_vis[r + 1] - cu_vis[r];
       nd = (N + kTile - 1) / kTile;
       no = nd * (nd - 1) / 2;
-      nm = N * N;
+      nm = cov_elems(N);
     }
     int64_t td, to, tm, pd, po, pm;
     block_excl_scan_i64(nd, sh, &td, &pd);
@@ -120,25 +128,38 @@ __device__ __forceinline__ void tile_ij_upper(int t, int nb, int &I, int &J) {
   J = i + 1 + rem;
 }
 
-// Tile maps, one block per request: the request of every diagonal and
-// off-diagonal tile, and the (I, J) row blocks of every off-diagonal tile
-// packed as I << 16 | J. Off-diagonal tiles are listed region by region
-// (kRegion x kRegion row blocks, regions in upper-triangle order, tiles
-// I-major inside), so the tiles that run together share few row blocks and
-// re-read them from cache, not HBM. The caps bound every write.
+// Tile descriptions, one block per request: every diagonal tile and every
+// tile strictly above the diagonal, with its row blocks packed as I << 16 | J.
+// Off-diagonal tiles are listed region by region (kRegion x kRegion row
+// blocks, regions in upper-triangle order, tiles I-major inside), so the
+// tiles that run together share few row blocks and re-read them from cache,
+// not HBM. The caps bound every write.
 constexpr int kRegion = 8;
 __global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ cu_vis,
                                                    const int32_t *__restrict__ dtile_off,
                                                    const int32_t *__restrict__ otile_off,
+                                                   const int64_t *__restrict__ d_off,
                                                    int64_t diag_cap, int64_t off_cap,
-                                                   int32_t *__restrict__ dtile_req,
-                                                   int32_t *__restrict__ otile_req,
-                                                   int32_t *__restrict__ otile_ij) {
+                                                   TileMeta *__restrict__ dtile,
+                                                   TileMeta *__restrict__ otile) {
   const int r = blockIdx.x;
+  const int n0 = cu_vis[r], N = cu_vis[r + 1] - n0;
+  const int64_t doff = d_off[r];
+  auto meta = [&](int I, int J) {
+    TileMeta m;
+    m.n0 = n0;
+    m.n = N;
+    m.ij = (I << 16) | J;
+    m.r = r;
+    m.doff = doff;
+    m.pad = 0;
+    return m;
+  };
   const int64_t d1 = min((int64_t)dtile_off[r + 1], diag_cap), o1 = min((int64_t)otile_off[r + 1], off_cap);
-  for (int64_t t = dtile_off[r] + threadIdx.x; t < d1; t += 256) dtile_req[t] = r;
-  for (int64_t t = otile_off[r] + threadIdx.x; t < o1; t += 256) otile_req[t] = r;
-  const int N = cu_vis[r + 1] - cu_vis[r];
+  for (int64_t t = dtile_off[r] + threadIdx.x; t < d1; t += 256) {
+    const int I = (int)(t - dtile_off[r]);
+    dtile[t] = meta(I, I);
+  }
   const int nb = (N + kTile - 1) / kTile, nR = (nb + kRegion - 1) / kRegion;
   int64_t base = otile_off[r];
   for (int P = 0; P < nR; ++P)
@@ -156,7 +177,7 @@ __global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ c
           I += i0;
           J += i0;
         }
-        if (base + k < o1) otile_ij[base + k] = (I << 16) | J;
+        if (base + k < o1) otile[base + k] = meta(I, J);
       }
       base += cnt;
     }
@@ -169,12 +190,15 @@ __global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ c
 constexpr float kSelfMark = -INFINITY;
 
 __device__ __forceinline__ float coverage(double dot, double nni, double nnj, double invi, double invj) {
-  // Eq. 10 term: 1 - cos, clamped at 0. Zero-norm rows have cosine 0.
-  // Bitwise-identical rows give dot == nni == nnj exactly, hence distance 0.
-  if (nni <= 0.0 || nnj <= 0.0) return 1.0f;
-  if (dot == nni && nni == nnj) return 0.0f;
+  // Eq. 10 term: 1 - cos, clamped at 0. Zero-norm rows have cosine 0 (distance
+  // 1); bitwise-identical rows give dot == nni == nnj exactly, hence distance
+  // 0. Written as selects, in that order of precedence, so that it compiles
+  // without branches.
   const double t = 1.0 - dot * invi * invj;
-  return t > 0.0 ? (float)t : 0.0f;
+  float c = t > 0.0 ? (float)t : 0.0f;
+  c = (dot == nni && nni == nnj) ? 0.0f : c;
+  c = (nni <= 0.0 || nnj <= 0.0) ? 1.0f : c;
+  return c;
 }
 
 // ------------------------------------------------- Gram on the matrix cores
@@ -202,11 +226,8 @@ __device__ __forceinline__ int lds_slot(int row, int piece) { return row * 8 + (
 
 template <bool DIAG>
 __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
-    const uint16_t *__restrict__ X, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
-    const int32_t *__restrict__ tile_ij,
-    const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv, int Dv,
-    int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
+    const uint16_t *__restrict__ X, const TileMeta *__restrict__ meta, double *__restrict__ nn,
+    double *__restrict__ inv, int Dv, int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
   __shared__ uint4 sA[2][kPieces];
   __shared__ uint4 sB[DIAG ? 1 : 2][DIAG ? 1 : kPieces];
   __shared__ double s_nn[2][kTile], s_inv[2][kTile];   // [0]: rows of A, [1]: rows of B
@@ -219,16 +240,9 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
     t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
   }
   if (t >= tiles) return;
-  const int r = tile_req[t];
-  const int64_t n0 = cu_vis[r];
-  const int N = cu_vis[r + 1] - (int)n0;
-  int I, J;
-  if (DIAG) {
-    I = J = (int)(t - tile_off[r]);
-  } else {
-    I = tile_ij[t] >> 16;
-    J = tile_ij[t] & 0xFFFF;
-  }
+  const TileMeta m = meta[t];
+  const int64_t n0 = m.n0;
+  const int N = m.n, I = m.ij >> 16, J = m.ij & 0xFFFF;
   const int rowA0 = I * kTile, rowB0 = J * kTile;
   const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
   const uint16_t *XA = X + (n0 + rowA0) * Dv;
@@ -348,40 +362,37 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
   }
   __syncthreads();
 
-  // Coverage distances, written to (i, j) and, off the diagonal, to (j, i).
-  float *D = dmat + d_off[r];
-  const int64_t dlim = d_cap - d_off[r];
+  // Coverage distances into the tile's 128 x 128 block and, off the diagonal,
+  // the transposed values into the mirror block (J, I). Entries past N are
+  // padding (written as 0). One uniform check guards the request's matrix.
+  const int64_t nbr = cov_blocks(N);
+  if (m.doff + nbr * nbr * kCovTileElems <= d_cap) {
+    float *DA = dmat + m.doff + ((int64_t)I * nbr + J) * kCovTileElems;
+    float *DB = dmat + m.doff + ((int64_t)J * nbr + I) * kCovTileElems;
 #pragma unroll
-  for (int tm = 0; tm < kTM; ++tm)
+    for (int tm = 0; tm < kTM; ++tm)
 #pragma unroll
-    for (int tn = 0; tn < kTN; ++tn) {
-      const int jl = (wn * kTN + tn) * 32 + (lane & 31), j = rowB0 + jl;
-      const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
+      for (int tn = 0; tn < kTN; ++tn) {
+        const int jl = (wn * kTN + tn) * 32 + (lane & 31), j = rowB0 + jl;
+        const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
 #pragma unroll
-      for (int vq = 0; vq < 4; ++vq) {
-        const int il0 = (wm * kTM + tm) * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
-        float dv[4];
+        for (int vq = 0; vq < 4; ++vq) {
+          const int il0 = (wm * kTM + tm) * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
+          float dv[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int i = i0 + u;
-          dv[u] = (i < N && j < N) ? (DIAG && i == j ? kSelfMark
-                                                     : coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u],
-                                                                nnj, s_inv[0][il0 + u], invj))
-                                   : 0.f;
-          if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
-        }
-        if (!DIAG && j < N) {
-          const int64_t o = (int64_t)j * N + i0;
-          if (i0 + 3 < N && ((d_off[r] + o) & 3) == 0 && o + 3 < dlim) {
-            *reinterpret_cast<float4 *>(D + o) = make_float4(dv[0], dv[1], dv[2], dv[3]);
-          } else {
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-              if (i0 + u < N && o + u < dlim) D[o + u] = dv[u];
+          for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u;
+            const float c = DIAG && i == j ? kSelfMark
+                                           : coverage(acc64[tm][tn][4 * vq + u], s_nn[0][il0 + u], nnj,
+                                                      s_inv[0][il0 + u], invj);
+            dv[u] = (i < N && j < N) ? c : 0.f;
+            DA[(il0 + u) * kTile + jl] = dv[u];
           }
+          if (!DIAG)
+            *reinterpret_cast<float4 *>(DB + jl * kTile + il0) = make_float4(dv[0], dv[1], dv[2], dv[3]);
         }
       }
-    }
+  }
 }
 
 // The same tiles with the operands streamed straight into LDS by
@@ -397,6 +408,13 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
 // stage count divisible by 4).
 // Diagonal tiles stage one operand (16 KB a stage) and read every row exactly
 // once, straight from HBM, so they keep a deeper ring in flight.
+//
+// The blocks are persistent, one per CU, and walk a list of tiles. While a
+// tile's stages run, the block also fetches (by the same LDS DMA, so no
+// registers are held) the description of its next tile and, off the
+// diagonal, the norms its epilogue needs; the first ring stages of the next
+// tile are issued before the epilogue of the current one, so their latency
+// hides behind the epilogue's arithmetic and stores.
 constexpr int kRingOff = 4, kRingDiag = 8;
 static_assert((kRingOff & (kRingOff - 1)) == 0 && (kRingDiag & (kRingDiag - 1)) == 0, "power-of-two ring");
 constexpr int kDmaCols = kKS;                               // columns per ring stage (64)
@@ -418,18 +436,27 @@ __device__ __forceinline__ const void *uniform_ptr(const void *p) {
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
   return (const void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
 }
+__device__ __forceinline__ int64_t uniform_i64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
 template <int N>
 __device__ __forceinline__ void vm_wait() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// Persistent grid for `tiles` tiles on `cus` compute units: a multiple of 8
+// (one share per XCD), at most one block per CU.
+inline int64_t persistent_grid(int64_t tiles, int cus) {
+  const int64_t cap = std::max(8, cus / 8 * 8);
+  return std::min(cap, (tiles + 7) / 8 * 8);
+}
+
 template <bool DIAG>
 __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
-    const uint16_t *__restrict__ X, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
-    const int32_t *__restrict__ tile_ij,
-    const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv, int Dv,
-    int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
+    const uint16_t *__restrict__ X, const TileMeta *__restrict__ meta, double *__restrict__ nn,
+    double *__restrict__ inv, int Dv, int64_t tiles, int64_t d_cap, float *__restrict__ dmat) {
   constexpr int kOps = DIAG ? 1 : 2;
   constexpr int kRing = DIAG ? kRingDiag : kRingOff;
   constexpr int kInstr = kOps * kDmaInstr;                  // per stage, all operands
@@ -438,48 +465,45 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   constexpr int kSteady = (kRing - 2) * kPerWave;           // loads allowed in flight at a stage boundary
   static_assert(kSteady <= 63, "vmcnt immediate");
   __shared__ uint4 sbuf[kRing][kOps][kDmaPieces];
-  __shared__ double s_nn[2][kTile], s_inv[2][kTile];
+  __shared__ __align__(16) double s_nn[2][kTile];   // [0]: rows of A, [1]: rows of B
+  __shared__ __align__(16) double s_inv[2][kTile];
+  __shared__ TileMeta s_next;                        // the next tile, fetched during this one
 
-  int64_t t = blockIdx.x;
-  if (!DIAG) {
-    // XCD-aware order: consecutive tiles (same request, shared row blocks)
-    // go to the same XCD, which receives every 8th block.
-    const int64_t per_xcd = gridDim.x / 8;
-    t = (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-  }
-  if (t >= tiles) return;
-  const int r = tile_req[t];
-  const int64_t n0 = cu_vis[r];
-  const int N = cu_vis[r + 1] - (int)n0;
-  int I, J;
-  if (DIAG) {
-    I = J = (int)(t - tile_off[r]);
-  } else {
-    I = tile_ij[t] >> 16;
-    J = tile_ij[t] & 0xFFFF;
-  }
-  const int rowA0 = I * kTile, rowB0 = J * kTile;
-  const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
+  // XCD x receives blocks x, x + 8, ... (gridDim.x is a multiple of 8) and
+  // owns the contiguous range [lo, hi) of the region-ordered tile list; its
+  // blocks take every per-th tile of it, so the tiles that run together on
+  // one XCD are neighbours and share row blocks in that XCD's L2.
+  const int per = (int)(gridDim.x / 8), xcd = (int)(blockIdx.x % 8);
+  const int64_t lo = tiles * xcd / 8, hi = tiles * (xcd + 1) / 8;
+  int64_t t = lo + (int64_t)(blockIdx.x / 8);
+  if (t >= hi) return;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the wave index is uniform: keep it (and all that derives from it) scalar
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int nst = Dv / kDmaCols;
+  constexpr uint32_t kStageBytes = kOps * kDmaPieces * 16;
 
   // This wave's DMA instructions: q = wave + kGramWaves * x, operand q / 16,
   // LDS slots (q % 16) * 64 + lane of the stage. The operand's row-block base
   // and the LDS address are wave-uniform (scalar); each lane's byte offset
-  // within the row block is fixed for the whole loop.
+  // within the row block is fixed for a tile.
   const void *gbase[kPerWave];
   uint32_t voff[kPerWave], dst[kPerWave];
 #pragma unroll
   for (int x = 0; x < kPerWave; ++x) {
     const int q = wave + kGramWaves * x, op = q / kDmaInstr, qi = q % kDmaInstr;
-    const int slot = qi * 64 + lane, row = slot >> 3, piece = (slot & 7) ^ ((row >> 1) & 7);
-    const int rr = min(row, (op ? nB : nA) - 1);
-    gbase[x] = uniform_ptr(X + (n0 + (op ? rowB0 : rowA0)) * (int64_t)Dv);
-    voff[x] = (uint32_t)((rr * (int64_t)Dv + piece * 8) * 2);
     dst[x] = __builtin_amdgcn_readfirstlane(lds_u32(&sbuf[0][op][qi * 64]));
   }
-  constexpr uint32_t kStageBytes = kOps * kDmaPieces * 16;
-  const int nst = Dv / kDmaCols;
+  auto aim = [&](int lane, int64_t n0_, int rowA0_, int rowB0_, int nA_, int nB_) {
+#pragma unroll
+    for (int x = 0; x < kPerWave; ++x) {
+      const int q = wave + kGramWaves * x, op = q / kDmaInstr, qi = q % kDmaInstr;
+      const int slot = qi * 64 + lane, row = slot >> 3, piece = (slot & 7) ^ ((row >> 1) & 7);
+      const int rr = min(row, (op ? nB_ : nA_) - 1);
+      gbase[x] = uniform_ptr(X + (n0_ + (op ? rowB0_ : rowA0_)) * (int64_t)Dv);
+      voff[x] = (uint32_t)((rr * (int64_t)Dv + piece * 8) * 2);
+    }
+  };
   auto issue_one = [&](int st, int x) {
     dma16(dst[x] + (uint32_t)(st & (kRing - 1)) * kStageBytes, (const char *)gbase[x] + (int64_t)st * kDmaCols * 2,
           voff[x]);
@@ -488,60 +512,14 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
 #pragma unroll
     for (int x = 0; x < kPerWave; ++x) issue_one(st, x);
   };
-
-  // This block's work in pairs of 32 x 32 sub-tiles: A rows [32 a, 32 a + 32)
-  // against B rows [64 c, 64 c + 64). Sub-tile (a, b) is needed iff A row
-  // 32 a and B row 32 b exist (partial tiles at a request's end) and, on a
-  // diagonal tile, b >= a (the lower triangle is the mirror). Pairs needing
-  // both sub-tiles come first, then those needing one, and pair k goes to wave
-  // k; waves k and k + 4 share a SIMD, so each SIMD gets an even share of the
-  // MFMA work. Waves without a pair only issue their share of the loads.
-  static_assert(kTM == 1 && kTN == 2 && kGramWaves == 8, "pair layout of the streamed kernel");
-  int my_a = 0, my_b0 = 0, my_nt = 0;
-  {
-    auto need = [&](int sa, int sb) { return sa * 32 < nA && sb * 32 < nB && (!DIAG || sb >= sa); };
-    int k = 0;
-#pragma unroll
-    for (int pass = 2; pass >= 1; --pass)
-#pragma unroll
-      for (int sa = 0; sa < 4; ++sa)
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          const bool n0c = need(sa, 2 * c), n1c = need(sa, 2 * c + 1);
-          if ((int)n0c + (int)n1c != pass) continue;
-          if (k == wave) {
-            my_a = sa;
-            my_b0 = n0c ? 2 * c : 2 * c + 1;   // first needed sub-tile column
-            my_nt = pass;
-          }
-          ++k;
-        }
-  }
-
-  // fragment slots: row (block row) * 8 + (piece ^ ((row >> 1) & 7)); the 16
-  // lanes that the LDS serves together read 16 consecutive rows, whose 16-byte
-  // slots then fall in 16 distinct bank groups (row parity x swizzled piece)
-  int aslot[4], bslot[kTN][4];
-#pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const int piece = s * 2 + (lane >> 5);
-    const int row = my_a * 32 + (lane & 31);
-    aslot[s] = row * 8 + (piece ^ ((row >> 1) & 7));
-#pragma unroll
-    for (int tn = 0; tn < kTN; ++tn) {
-      const int brow = min(my_b0 + tn, 3) * 32 + (lane & 31);
-      bslot[tn][s] = brow * 8 + (piece ^ ((brow >> 1) & 7));
-    }
-  }
-
-  double acc64[kTN][16];
-#pragma unroll
-  for (int tn = 0; tn < kTN; ++tn)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc64[tn][v] = 0.0;
+  auto prologue = [&]() {
+    for (int st = 0; st < kRing && st < nst; ++st) issue(st);
+  };
 
   // wait until at most n stages of this wave's loads are still in flight
-  // (a literal n folds to one s_waitcnt)
+  // (a literal n folds to one s_waitcnt). Other memory operations issued
+  // after those loads (the prefetches, the previous tile's stores) only add
+  // to the count, so every wait stays at least as strict.
   auto wait_pending = [&](int n) {
     static_assert(kRing - 1 <= 7, "cases below");
     switch (n) {
@@ -556,201 +534,313 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
     }
   };
 
-  // The stage loop for a wave with NT sub-tiles (2, 1 or 0), software-
-  // pipelined across the stage barrier. A stage's fragments are read in two
-  // halves (k-steps 0-1 and 2-3). Stage ch reads its second half while its
-  // first half feeds the MFMAs; then it waits for stage ch + 1's loads, meets
-  // the other waves at the block barrier (whose fence also completes every
-  // wave's reads of stage ch), refills stage ch's ring slot with stage
-  // ch + kRing, and reads the first half of stage ch + 1 while its own second
-  // half runs. A chunk is two stages (128 columns) accumulated in fp32; chunks
-  // alternate between the P and Q sets and each is folded into fp64, a
-  // quarter at a time, between the next chunk's MFMAs. nst is a multiple of 4
-  // (Dv % 256 == 0); the first folds add zeros, exactly.
-  auto run = [&](auto nt_const) {
-    constexpr int NT = decltype(nt_const)::value;
-    f32x16 accP[kTN], accQ[kTN];
-    bf16x8 fa0[2], fb0[2][kTN], fa1[2], fb1[2][kTN];
-    auto fold_q = [&](const f32x16 (&a)[kTN], int q) {   // elements [4 q, 4 q + 4)
+  // the first tile's description and ring stages
+  int64_t n0, doff;
+  int N, I, J;
+  {
+    const TileMeta m = meta[t];
+    n0 = m.n0;
+    doff = m.doff;
+    N = m.n;
+    I = m.ij >> 16;
+    J = m.ij & 0xFFFF;
+  }
+  aim((int)threadIdx.x & 63, n0, I * kTile, J * kTile, min(kTile, N - I * kTile), min(kTile, N - J * kTile));
+  prologue();
+
+  for (;;) {
+    // Lane-dependent values are rebuilt every tile instead of being hoisted
+    // out of the tile loop and held (or spilled) across it.
+    int tid = (int)threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
+    const int rowA0 = I * kTile, rowB0 = J * kTile;
+    const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
+    // (recomputed rather than kept alive through the previous epilogue)
+    aim(lane, n0, rowA0, rowB0, nA, nB);
+    const int64_t t_next = t + per;
+    const bool has_next = t_next < hi;
+
+    // This tile's work in pairs of 32 x 32 sub-tiles: A rows [32 a, 32 a + 32)
+    // against B rows [64 c, 64 c + 64). Sub-tile (a, b) is needed iff A row
+    // 32 a and B row 32 b exist (partial tiles at a request's end) and, on a
+    // diagonal tile, b >= a (the lower triangle is the mirror). Pairs needing
+    // both sub-tiles come first, then those needing one, and pair k goes to
+    // wave k; waves k and k + 4 share a SIMD, so each SIMD gets an even share
+    // of the MFMA work. Waves without a pair only issue their share of the loads.
+    static_assert(kTM == 1 && kTN == 2 && kGramWaves == 8, "pair layout of the streamed kernel");
+    int my_a = 0, my_b0 = 0, my_nt = 0;
+    {
+      auto need = [&](int sa, int sb) { return sa * 32 < nA && sb * 32 < nB && (!DIAG || sb >= sa); };
+      int k = 0;
 #pragma unroll
-      for (int tn = 0; tn < NT; ++tn)
+      for (int pass = 2; pass >= 1; --pass)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) acc64[tn][4 * q + v] += (double)a[tn][4 * q + v];
-    };
-    auto read_half = [&](int ch, int half, bf16x8 (&fa)[2], bf16x8 (&fb)[2][kTN]) {
-      if (NT == 0) return;
-      const uint4 *pa = sbuf[ch & (kRing - 1)][0];
-      const uint4 *pb = sbuf[ch & (kRing - 1)][kOps - 1];
+        for (int sa = 0; sa < 4; ++sa)
 #pragma unroll
-      for (int ss = 0; ss < 2; ++ss) {
-        fa[ss] = __builtin_bit_cast(bf16x8, pa[aslot[2 * half + ss]]);
+          for (int c = 0; c < 2; ++c) {
+            const bool n0c = need(sa, 2 * c), n1c = need(sa, 2 * c + 1);
+            if ((int)n0c + (int)n1c != pass) continue;
+            if (k == wave) {
+              my_a = sa;
+              my_b0 = n0c ? 2 * c : 2 * c + 1;   // first needed sub-tile column
+              my_nt = pass;
+            }
+            ++k;
+          }
+    }
+
+    // fragment slots: row (block row) * 8 + (piece ^ ((row >> 1) & 7)); the 16
+    // lanes that the LDS serves together read 16 consecutive rows, whose 16-byte
+    // slots then fall in 16 distinct bank groups (row parity x swizzled piece)
+    int aslot[4], bslot[kTN][4];
 #pragma unroll
-        for (int tn = 0; tn < NT; ++tn) fb[ss][tn] = __builtin_bit_cast(bf16x8, pb[bslot[tn][2 * half + ss]]);
+    for (int s = 0; s < 4; ++s) {
+      const int piece = s * 2 + (lane >> 5);
+      const int row = my_a * 32 + (lane & 31);
+      aslot[s] = row * 8 + (piece ^ ((row >> 1) & 7));
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn) {
+        const int brow = min(my_b0 + tn, 3) * 32 + (lane & 31);
+        bslot[tn][s] = brow * 8 + (piece ^ ((brow >> 1) & 7));
+      }
+    }
+
+    double acc64[kTN][16];
+#pragma unroll
+    for (int tn = 0; tn < kTN; ++tn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc64[tn][v] = 0.0;
+
+    // Fetches issued once the tile's first stage has landed (every wave has
+    // then finished the previous epilogue, which read s_nn, s_inv and s_next):
+    // wave 0 the next tile's 32-byte description, and off the diagonal waves
+    // 1-4 this tile's norms (128 doubles a side; the arrays carry 128 entries
+    // of slack, so a partial row block reads no further than that).
+    auto prefetch = [&]() {
+      if (wave == 0 && has_next && lane < 2)
+        dma16(__builtin_amdgcn_readfirstlane(lds_u32(&s_next)), uniform_ptr(meta + t_next), (uint32_t)lane * 16);
+      if (!DIAG && wave >= 1 && wave <= 4) {
+        const int w = wave - 1, side = w >> 1;
+        const double *src = ((w & 1) ? inv : nn) + n0 + (side ? rowB0 : rowA0);
+        const double *to = (w & 1) ? s_inv[side] : s_nn[side];
+        dma16(__builtin_amdgcn_readfirstlane(lds_u32(to)), uniform_ptr(src), (uint32_t)lane * 16);
       }
     };
-    auto mma_half = [&](f32x16 (&cur)[kTN], bool fresh, const bf16x8 (&fa)[2], const bf16x8 (&fb)[2][kTN]) {
-#pragma unroll
-      for (int ss = 0; ss < 2; ++ss)
+
+    // The stage loop for a wave with NT sub-tiles (2, 1 or 0), software-
+    // pipelined across the stage barrier. A stage's fragments are read in two
+    // halves (k-steps 0-1 and 2-3). Stage ch reads its second half while its
+    // first half feeds the MFMAs; then it waits for stage ch + 1's loads, meets
+    // the other waves at the block barrier (whose fence also completes every
+    // wave's reads of stage ch), refills stage ch's ring slot with stage
+    // ch + kRing, and reads the first half of stage ch + 1 while its own second
+    // half runs. A chunk is two stages (128 columns) accumulated in fp32; chunks
+    // alternate between the P and Q sets and each is folded into fp64, a
+    // quarter at a time, between the next chunk's MFMAs. nst is a multiple of 4
+    // (Dv % 256 == 0); the first folds add zeros, exactly. The ring's first
+    // stages were issued before the loop starts.
+    auto run = [&](auto nt_const) {
+      constexpr int NT = decltype(nt_const)::value;
+      f32x16 accP[kTN], accQ[kTN];
+      bf16x8 fa0[2], fb0[2][kTN], fa1[2], fb1[2][kTN];
+      auto fold_q = [&](const f32x16 (&a)[kTN], int q) {   // elements [4 q, 4 q + 4)
 #pragma unroll
         for (int tn = 0; tn < NT; ++tn)
-          cur[tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ss], fb[ss][tn],
-                                                            (fresh && ss == 0) ? f32x16{} : cur[tn], 0, 0, 0);
-    };
-    auto sched_half = [&]() {
-      if (NT > 0) {
-        constexpr int kMfmaHalf = 2 * (NT > 0 ? NT : 1);   // MFMAs per half stage
-        constexpr int kFoldHalf = 8 * (NT > 0 ? NT : 1);   // fold instructions per half stage
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * (1 + NT), 0);
 #pragma unroll
-        for (int i = 0; i < kMfmaHalf; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x002, kFoldHalf / kMfmaHalf, 0);
+          for (int v = 0; v < 4; ++v) acc64[tn][4 * q + v] += (double)a[tn][4 * q + v];
+      };
+      auto read_half = [&](int ch, int half, bf16x8 (&fa)[2], bf16x8 (&fb)[2][kTN]) {
+        if (NT == 0) return;
+        const uint4 *pa = sbuf[ch & (kRing - 1)][0];
+        const uint4 *pb = sbuf[ch & (kRing - 1)][kOps - 1];
+#pragma unroll
+        for (int ss = 0; ss < 2; ++ss) {
+          fa[ss] = __builtin_bit_cast(bf16x8, pa[aslot[2 * half + ss]]);
+#pragma unroll
+          for (int tn = 0; tn < NT; ++tn) fb[ss][tn] = __builtin_bit_cast(bf16x8, pb[bslot[tn][2 * half + ss]]);
         }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    };
-    // `pending`: later stages allowed in flight when stage ch + 1 is needed
-    // (-1: ch is the last stage); `refill`: issue stage ch + kRing. Both are
-    // literals in the steady loop, so its body has no branches.
-    auto stage = [&](int ch, int pending, bool refill, f32x16 (&cur)[kTN], bool fresh,
-                     const f32x16 (&prev)[kTN], int h) {
-      read_half(ch, 1, fa1, fb1);
-      mma_half(cur, fresh, fa0, fb0);
-      fold_q(prev, 2 * h);
-      sched_half();
-      // second half: after the barrier, each MFMA is followed by a share of
-      // this wave's loads of stage ch + kRing and two fold elements, in that
-      // order, so the load issue does not hold the wave at the barrier
-      if (pending >= 0) {
-        wait_pending(pending);
-        __syncthreads();
-        read_half(ch + 1, 0, fa0, fb0);
-      }
-      if (NT == 0) {
-        if (refill) issue(ch + kRing);
-      } else {
-        constexpr int kM = 2 * (NT > 0 ? NT : 1);
+      };
+      auto mma_half = [&](f32x16 (&cur)[kTN], bool fresh, const bf16x8 (&fa)[2], const bf16x8 (&fb)[2][kTN]) {
 #pragma unroll
-        for (int m = 0; m < kM; ++m) {
-          const int ss = m / (NT > 0 ? NT : 1), tn = m % (NT > 0 ? NT : 1);
-          cur[tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[ss], fb1[ss][tn], cur[tn], 0, 0, 0);
-          if (refill)
+        for (int ss = 0; ss < 2; ++ss)
 #pragma unroll
-            for (int x = m * kPerWave / kM; x < (m + 1) * kPerWave / kM; ++x) issue_one(ch + kRing, x);
+          for (int tn = 0; tn < NT; ++tn)
+            cur[tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[ss], fb[ss][tn],
+                                                              (fresh && ss == 0) ? f32x16{} : cur[tn], 0, 0, 0);
+      };
+      auto sched_half = [&]() {
+        if (NT > 0) {
+          constexpr int kMfmaHalf = 2 * (NT > 0 ? NT : 1);   // MFMAs per half stage
+          constexpr int kFoldHalf = 8 * (NT > 0 ? NT : 1);   // fold instructions per half stage
+          __builtin_amdgcn_sched_group_barrier(0x100, 2 * (1 + NT), 0);
 #pragma unroll
-          for (int e = 2 * m; e < 2 * m + 2; ++e) {
-            const int et = e / 4, ev = 4 * (2 * h + 1) + e % 4;
-            acc64[et][ev] += (double)prev[et][ev];
+          for (int i = 0; i < kMfmaHalf; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, kFoldHalf / kMfmaHalf, 0);
           }
-          __builtin_amdgcn_sched_barrier(0);
         }
-      }
-    };
-#pragma unroll
-    for (int tn = 0; tn < kTN; ++tn) accQ[tn] = f32x16{};
-    for (int st = 0; st < kRing && st < nst; ++st) issue(st);
-    wait_pending(min(kRing, nst) - 1);   // stage 0 has landed
-    __syncthreads();
-    read_half(0, 0, fa0, fb0);
-    auto pend = [&](int c) { return c == nst - 1 ? -1 : min(kRing - 2, nst - 2 - c); };
-    auto refills = [&](int c) { return c + kRing < nst; };
-    int ch = 0;
-    for (; ch + kRing + 3 < nst; ch += 4) {
-      stage(ch, kRing - 2, true, accP, true, accQ, 0);
-      stage(ch + 1, kRing - 2, true, accP, false, accQ, 1);
-      stage(ch + 2, kRing - 2, true, accQ, true, accP, 0);
-      stage(ch + 3, kRing - 2, true, accQ, false, accP, 1);
-    }
-    for (; ch < nst; ch += 4) {
-      stage(ch, pend(ch), refills(ch), accP, true, accQ, 0);
-      stage(ch + 1, pend(ch + 1), refills(ch + 1), accP, false, accQ, 1);
-      stage(ch + 2, pend(ch + 2), refills(ch + 2), accQ, true, accP, 0);
-      stage(ch + 3, pend(ch + 3), refills(ch + 3), accQ, false, accP, 1);
-    }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) fold_q(accQ, q);
-  };
-  static_assert(kRing <= 8, "waits cover up to 7 pending stages");
-  if (my_nt == 2)
-    run(std::integral_constant<int, 2>{});
-  else if (my_nt == 1)
-    run(std::integral_constant<int, 1>{});
-  else
-    run(std::integral_constant<int, 0>{});
-  __syncthreads();
-
-  // Squared norms (diagonal tiles) or the norms of both row blocks, into LDS.
-  // In a 32 x 32 MFMA tile, lane l holds column l%32 and rows
-  // (l/32)*4 + (v%4) + 8*(v/4); column c's diagonal element is in half
-  // hi = (c%8)/4 at v = 4*(c/8) + (c%8) - 4*hi.
-  if (DIAG) {
-    for (int tn = 0; tn < my_nt; ++tn) {
-      if (my_b0 + tn != my_a) continue;
-      const int c = lane & 31, hi = lane >> 5;
-      if (((c & 7) >> 2) != hi) continue;
-      const int vsel = 4 * (c >> 3) + (c & 7) - 4 * hi;
-      double d = 0.0;
-#pragma unroll
-      for (int v = 0; v < 16; ++v)
-        if (v == vsel) d = tn ? acc64[1][v] : acc64[0][v];
-      s_nn[0][my_a * 32 + c] = d;
-    }
-    __syncthreads();
-    for (int i = tid; i < kTile; i += kGramThreads) {
-      const double v = i < nA ? s_nn[0][i] : 0.0;
-      const double iv = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
-      s_inv[0][i] = iv;
-      s_nn[1][i] = v;
-      s_inv[1][i] = iv;
-      if (i < nA) {
-        nn[n0 + rowA0 + i] = v;
-        inv[n0 + rowA0 + i] = iv;
-      }
-    }
-  } else {
-    for (int i = tid; i < 2 * kTile; i += kGramThreads) {
-      const int side = i / kTile, x = i % kTile;
-      const int row = (side ? rowB0 : rowA0) + x;
-      const bool ok = x < (side ? nB : nA);
-      s_nn[side][x] = ok ? nn[n0 + row] : 0.0;
-      s_inv[side][x] = ok ? inv[n0 + row] : 0.0;
-    }
-  }
-  __syncthreads();
-
-  // Coverage distances, written to (i, j) and, for sub-tiles strictly above
-  // the diagonal, to (j, i).
-  float *D = dmat + d_off[r];
-  const int64_t dlim = d_cap - d_off[r];
-  for (int tn = 0; tn < my_nt; ++tn) {
-    const int sb = my_b0 + tn;
-    const bool mirror = !DIAG || sb > my_a;
-    const int jl = sb * 32 + (lane & 31), j = rowB0 + jl;
-    const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
-#pragma unroll
-    for (int vq = 0; vq < 4; ++vq) {
-      const int il0 = my_a * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
-      float dv[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = i0 + u;
-        const double dot = tn ? acc64[1][4 * vq + u] : acc64[0][4 * vq + u];
-        dv[u] = (i < N && j < N)
-                    ? (DIAG && i == j ? kSelfMark : coverage(dot, s_nn[0][il0 + u], nnj, s_inv[0][il0 + u], invj))
-                    : 0.f;
-        if (i < N && j < N && (int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv[u];
-      }
-      if (mirror && j < N) {
-        const int64_t o = (int64_t)j * N + i0;
-        if (i0 + 3 < N && ((d_off[r] + o) & 3) == 0 && o + 3 < dlim) {
-          *reinterpret_cast<float4 *>(D + o) = make_float4(dv[0], dv[1], dv[2], dv[3]);
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      // `pending`: later stages allowed in flight when stage ch + 1 is needed
+      // (-1: ch is the last stage); `refill`: issue stage ch + kRing. Both are
+      // literals in the steady loop, so its body has no branches.
+      auto stage = [&](int ch, int pending, bool refill, f32x16 (&cur)[kTN], bool fresh,
+                       const f32x16 (&prev)[kTN], int h) {
+        read_half(ch, 1, fa1, fb1);
+        mma_half(cur, fresh, fa0, fb0);
+        fold_q(prev, 2 * h);
+        sched_half();
+        // second half: after the barrier, each MFMA is followed by a share of
+        // this wave's loads of stage ch + kRing and two fold elements, in that
+        // order, so the load issue does not hold the wave at the barrier
+        if (pending >= 0) {
+          wait_pending(pending);
+          __syncthreads();
+          read_half(ch + 1, 0, fa0, fb0);
+        }
+        if (NT == 0) {
+          if (refill) issue(ch + kRing);
         } else {
+          constexpr int kM = 2 * (NT > 0 ? NT : 1);
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            if (i0 + u < N && o + u < dlim) D[o + u] = dv[u];
+          for (int m = 0; m < kM; ++m) {
+            const int ss = m / (NT > 0 ? NT : 1), tn = m % (NT > 0 ? NT : 1);
+            cur[tn] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa1[ss], fb1[ss][tn], cur[tn], 0, 0, 0);
+            if (refill)
+#pragma unroll
+              for (int x = m * kPerWave / kM; x < (m + 1) * kPerWave / kM; ++x) issue_one(ch + kRing, x);
+#pragma unroll
+            for (int e = 2 * m; e < 2 * m + 2; ++e) {
+              const int et = e / 4, ev = 4 * (2 * h + 1) + e % 4;
+              acc64[et][ev] += (double)prev[et][ev];
+            }
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      };
+#pragma unroll
+      for (int tn = 0; tn < kTN; ++tn) accQ[tn] = f32x16{};
+      wait_pending(min(kRing, nst) - 1);   // stage 0 has landed
+      __syncthreads();
+      prefetch();
+      read_half(0, 0, fa0, fb0);
+      auto pend = [&](int c) { return c == nst - 1 ? -1 : min(kRing - 2, nst - 2 - c); };
+      auto refills = [&](int c) { return c + kRing < nst; };
+      int ch = 0;
+      for (; ch + kRing + 3 < nst; ch += 4) {
+        stage(ch, kRing - 2, true, accP, true, accQ, 0);
+        stage(ch + 1, kRing - 2, true, accP, false, accQ, 1);
+        stage(ch + 2, kRing - 2, true, accQ, true, accP, 0);
+        stage(ch + 3, kRing - 2, true, accQ, false, accP, 1);
+      }
+      for (; ch < nst; ch += 4) {
+        stage(ch, pend(ch), refills(ch), accP, true, accQ, 0);
+        stage(ch + 1, pend(ch + 1), refills(ch + 1), accP, false, accQ, 1);
+        stage(ch + 2, pend(ch + 2), refills(ch + 2), accQ, true, accP, 0);
+        stage(ch + 3, pend(ch + 3), refills(ch + 3), accQ, false, accP, 1);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) fold_q(accQ, q);
+    };
+    static_assert(kRing <= 8, "waits cover up to 7 pending stages");
+    if (my_nt == 2)
+      run(std::integral_constant<int, 2>{});
+    else if (my_nt == 1)
+      run(std::integral_constant<int, 1>{});
+    else
+      run(std::integral_constant<int, 0>{});
+    // Every wave is past its last ring read, and the wait before the last
+    // stage covered the prefetches, so s_next, s_nn and s_inv are complete.
+    __syncthreads();
+
+    // The next tile: its description, its operand addresses and its first
+    // ring stages, in flight during this tile's epilogue.
+    int64_t n0_next = 0, doff_next = 0;
+    int N_next = 0, I_next = 0, J_next = 0;
+    if (has_next) {
+      n0_next = __builtin_amdgcn_readfirstlane(s_next.n0);
+      doff_next = uniform_i64(s_next.doff);
+      N_next = __builtin_amdgcn_readfirstlane(s_next.n);
+      const int ij = __builtin_amdgcn_readfirstlane(s_next.ij);
+      I_next = ij >> 16;
+      J_next = ij & 0xFFFF;
+      aim(lane, n0_next, I_next * kTile, J_next * kTile, min(kTile, N_next - I_next * kTile),
+          min(kTile, N_next - J_next * kTile));
+      prologue();
+    }
+
+    // Squared norms of a diagonal tile's rows, from its own diagonal. In a
+    // 32 x 32 MFMA tile, lane l holds column l%32 and rows
+    // (l/32)*4 + (v%4) + 8*(v/4); column c's diagonal element is in half
+    // hi = (c%8)/4 at v = 4*(c/8) + (c%8) - 4*hi.
+    if (DIAG) {
+      for (int tn = 0; tn < my_nt; ++tn) {
+        if (my_b0 + tn != my_a) continue;
+        const int c = lane & 31, hi2 = lane >> 5;
+        if (((c & 7) >> 2) != hi2) continue;
+        const int vsel = 4 * (c >> 3) + (c & 7) - 4 * hi2;
+        double d = 0.0;
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (v == vsel) d = tn ? acc64[1][v] : acc64[0][v];
+        s_nn[0][my_a * 32 + c] = d;
+      }
+      __syncthreads();
+      for (int i = tid; i < kTile; i += kGramThreads) {
+        const double v = i < nA ? s_nn[0][i] : 0.0;
+        const double iv = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
+        s_inv[0][i] = iv;
+        s_nn[1][i] = v;
+        s_inv[1][i] = iv;
+        if (i < nA) {
+          nn[n0 + rowA0 + i] = v;
+          inv[n0 + rowA0 + i] = iv;
+        }
+      }
+      __syncthreads();
+    }
+
+    // Coverage distances into the tile's 128 x 128 block (I, J) and, for
+    // sub-tiles strictly above the diagonal, the transposed values into block
+    // (J, I): two contiguous 64 KB blocks, every store inside them (entries
+    // past N are padding, written as 0). One uniform check guards the
+    // request's matrix.
+    const int64_t nbr = cov_blocks(N);
+    if (doff + nbr * nbr * kCovTileElems <= d_cap) {
+      float *DA = dmat + doff + ((int64_t)I * nbr + J) * kCovTileElems;
+      float *DB = dmat + doff + ((int64_t)J * nbr + I) * kCovTileElems;
+      for (int tn = 0; tn < my_nt; ++tn) {
+        const int sb = my_b0 + tn;
+        const bool mirror = !DIAG || sb > my_a;
+        const int jl = sb * 32 + (lane & 31), j = rowB0 + jl;
+        const double nnj = s_nn[1][jl], invj = s_inv[1][jl];
+#pragma unroll
+        for (int vq = 0; vq < 4; ++vq) {
+          const int il0 = my_a * 32 + (lane >> 5) * 4 + 8 * vq, i0 = rowA0 + il0;
+          float dv[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int i = i0 + u;
+            const double dot = tn ? acc64[1][4 * vq + u] : acc64[0][4 * vq + u];
+            const float c = DIAG && i == j ? kSelfMark
+                                           : coverage(dot, s_nn[0][il0 + u], nnj, s_inv[0][il0 + u], invj);
+            dv[u] = (i < N && j < N) ? c : 0.f;
+            DA[(il0 + u) * kTile + jl] = dv[u];
+          }
+          if (mirror)
+            *reinterpret_cast<float4 *>(DB + jl * kTile + il0) = make_float4(dv[0], dv[1], dv[2], dv[3]);
         }
       }
     }
+
+    if (!has_next) break;
+    t = t_next;
+    n0 = n0_next;
+    doff = doff_next;
+    N = N_next;
+    I = I_next;
+    J = J_next;
   }
 }
 
@@ -772,11 +862,8 @@ constexpr int kF32Per = kF32Sub * kF32KS / 256;   // staged elements per thread 
 
 template <int MODE>
 __global__ __launch_bounds__(256) void k_gram_f32(
-    const float *__restrict__ X, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ tile_off, const int32_t *__restrict__ tile_req,
-    const int32_t *__restrict__ tile_ij,
-    const int64_t *__restrict__ d_off, double *__restrict__ nn, double *__restrict__ inv,
-    int Dv, int64_t tiles_total, int64_t d_cap, float *__restrict__ dmat) {
+    const float *__restrict__ X, const TileMeta *__restrict__ meta, double *__restrict__ nn,
+    double *__restrict__ inv, int Dv, int64_t tiles_total, int64_t d_cap, float *__restrict__ dmat) {
   __shared__ float sA[kF32KS][kF32Sub + 1];
   __shared__ float sB[kF32KS][kF32Sub + 1];
   __shared__ double s_nn[kF32Sub], s_inv[kF32Sub];
@@ -785,20 +872,13 @@ __global__ __launch_bounds__(256) void k_gram_f32(
   if (t_glob >= tiles_total) return;
   if (MODE == kF32Self && sb != sa) return;
   if (MODE == kF32Upper && sb <= sa) return;
-  const int r = tile_req[t_glob];
-  const int64_t n0 = cu_vis[r];
-  const int N = cu_vis[r + 1] - (int)n0;
-  int I, J;
-  if (MODE != kF32Off) {
-    I = J = (int)(t_glob - tile_off[r]);
-  } else {
-    I = tile_ij[t_glob] >> 16;
-    J = tile_ij[t_glob] & 0xFFFF;
-  }
+  const TileMeta m = meta[t_glob];
+  const int64_t n0 = m.n0;
+  const int N = m.n, I = m.ij >> 16, J = m.ij & 0xFFFF;
   const int rowA0 = I * kTile + sa * kF32Sub, rowB0 = J * kTile + sb * kF32Sub;
   if (rowA0 >= N || rowB0 >= N) return;
-  float *D = dmat + d_off[r];
-  const int64_t dlim = d_cap - d_off[r];
+  float *D = dmat + m.doff;
+  const int64_t nbr = cov_blocks(N), dlim = d_cap - m.doff;
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
 
   float pa[kF32Per], pb[kF32Per];
@@ -859,8 +939,9 @@ __global__ __launch_bounds__(256) void k_gram_f32(
       const double nni = MODE == kF32Self ? s_nn[il] : nn[n0 + i], nnj = MODE == kF32Self ? s_nn[jl] : nn[n0 + j];
       const double ivi = MODE == kF32Self ? s_inv[il] : inv[n0 + i], ivj = MODE == kF32Self ? s_inv[jl] : inv[n0 + j];
       const float dv = i == j ? kSelfMark : coverage(acc[a][b], nni, nnj, ivi, ivj);
-      if ((int64_t)i * N + j < dlim) D[(int64_t)i * N + j] = dv;
-      if (MODE != kF32Self && (int64_t)j * N + i < dlim) D[(int64_t)j * N + i] = dv;
+      const int64_t oij = cov_index(i, j, nbr), oji = cov_index(j, i, nbr);
+      if (oij < dlim) D[oij] = dv;
+      if (MODE != kF32Self && oji < dlim) D[oji] = dv;
     }
 }
 
@@ -922,7 +1003,17 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
   const int64_t k0 = cu_keep[r];
   const int K = cu_keep[r + 1] - (int)k0;
   const float *D = dmat + d_off[r];
+  const int64_t nbr = cov_blocks(N);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // offset of this thread's element e within a row of the tile-major
+  // coverage matrix (index clamped into the request, so the tail re-reads
+  // element N - 1; those lanes carry NaN relevance and never win)
+  int32_t coff[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = min(tid + e * NTH, N - 1);
+    coff[e] = (int32_t)((i / kTile) * kCovTileElems + i % kTile);
+  }
 
   float w[EPT], dl[EPT];
 #pragma unroll
@@ -968,11 +1059,11 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
   int taken = 1;
   for (int t = 1; t < K; ++t) {
     // fold the last pick's coverage row into the running minimum (Eq. 10);
-    // every load is issued before any is used (indices clamped into the row)
-    const float *row = D + (int64_t)j * N;
+    // every load is issued before any is used
+    const float *row = D + ((int64_t)(j / kTile) * nbr) * kCovTileElems + (j % kTile) * kTile;
     float rv[EPT];
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) rv[e] = row[min(tid + e * NTH, N - 1)];
+    for (int e = 0; e < EPT; ++e) rv[e] = row[coff[e]];
     bo = -1.f;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
@@ -1117,6 +1208,18 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
 
 namespace last {
 
+// Compute units of the current device, queried once per device.
+static int device_cus() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+  cache[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
+
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,
                             last_sel_mode mode) {
   (void)mode;
@@ -1131,7 +1234,7 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
     const int64_t tb = (N + kTile - 1) / kTile;
     p.tiles_diag += tb;
     p.tiles_off += tb * (tb - 1) / 2;
-    p.d_elems += N * N;
+    p.d_elems += cov_elems(N);
   }
   p.threads = p.N_max > 1024 ? 1024 : std::max(64, (p.N_max + 63) / 64 * 64);
   const int ept = (p.N_max + p.threads - 1) / p.threads;
@@ -1159,13 +1262,12 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
   SelectWs w{};
   if (mode == LAST_SEL_KCENTER) {
     w.dtile_off = cv.take<int32_t>(R + 1);
-    w.dtile_req = cv.take<int32_t>(p.tiles_diag);
     w.otile_off = cv.take<int32_t>(R + 1);
-    w.otile_req = cv.take<int32_t>(p.tiles_off);
-    w.otile_ij = cv.take<int32_t>(p.tiles_off);
+    w.dtile = cv.take<TileMeta>(p.tiles_diag);
+    w.otile = cv.take<TileMeta>(p.tiles_off);
     w.d_off = cv.take<int64_t>(R + 1);
-    w.nn = cv.take<double>(p.N_total);
-    w.inv = cv.take<double>(p.N_total);
+    w.nn = cv.take<double>(p.N_total + kTile);
+    w.inv = cv.take<double>(p.N_total + kTile);
     w.dmat = cv.take<float>(p.d_elems);
   }
   *bytes = cv.size();
@@ -1194,40 +1296,49 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
 
   launch_begin("select_plan", s);
   hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, w.dtile_off, w.otile_off, w.d_off);
-  hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, cu_vis, w.dtile_off, w.otile_off, p.tiles_diag,
-                     p.tiles_off, w.dtile_req, w.otile_req, w.otile_ij);
+  hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, cu_vis, w.dtile_off, w.otile_off, w.d_off,
+                     p.tiles_diag, p.tiles_off, w.dtile, w.otile);
   if ((e = launch_end(s)) != hipSuccess) return e;
 
   if (fdtype == LAST_BF16) {
     // the streamed kernel needs a multiple of four 64-column stages; other widths use the staged one
-    const bool dma = Dv % (4 * kDmaCols) == 0;
-    launch_begin("gram_diag", s);
-    hipLaunchKernelGGL(dma ? k_gram_bf16<true> : k_gram_bf16_staged<true>, dim3((unsigned)p.tiles_diag),
-                       dim3(kGramThreads), 0, s, (const uint16_t *)feats, cu_vis, w.dtile_off,
-                       w.dtile_req, nullptr, w.d_off, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
-    if ((e = launch_end(s)) != hipSuccess) return e;
-    if (p.tiles_off > 0) {
-      launch_begin("gram", s);
-      const int64_t grid = (p.tiles_off + 7) / 8 * 8;
-      hipLaunchKernelGGL(dma ? k_gram_bf16<false> : k_gram_bf16_staged<false>, dim3((unsigned)grid),
-                         dim3(kGramThreads), 0, s, (const uint16_t *)feats, cu_vis, w.otile_off,
-                         w.otile_req, w.otile_ij, w.d_off, w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
+    if (Dv % (4 * kDmaCols) == 0) {
+      const int cus = device_cus();
+      launch_begin("gram_diag", s);
+      hipLaunchKernelGGL(k_gram_bf16<true>, dim3((unsigned)persistent_grid(p.tiles_diag, cus)), dim3(kGramThreads),
+                         0, s, (const uint16_t *)feats, w.dtile, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
       if ((e = launch_end(s)) != hipSuccess) return e;
+      if (p.tiles_off > 0) {
+        launch_begin("gram", s);
+        hipLaunchKernelGGL(k_gram_bf16<false>, dim3((unsigned)persistent_grid(p.tiles_off, cus)),
+                           dim3(kGramThreads), 0, s, (const uint16_t *)feats, w.otile, w.nn, w.inv, Dv,
+                           p.tiles_off, p.d_elems, w.dmat);
+        if ((e = launch_end(s)) != hipSuccess) return e;
+      }
+    } else {
+      launch_begin("gram_diag", s);
+      hipLaunchKernelGGL(k_gram_bf16_staged<true>, dim3((unsigned)p.tiles_diag), dim3(kGramThreads), 0, s,
+                         (const uint16_t *)feats, w.dtile, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
+      if ((e = launch_end(s)) != hipSuccess) return e;
+      if (p.tiles_off > 0) {
+        launch_begin("gram", s);
+        const int64_t grid = (p.tiles_off + 7) / 8 * 8;
+        hipLaunchKernelGGL(k_gram_bf16_staged<false>, dim3((unsigned)grid), dim3(kGramThreads), 0, s,
+                           (const uint16_t *)feats, w.otile, w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
+        if ((e = launch_end(s)) != hipSuccess) return e;
+      }
     }
   } else {
     launch_begin("gram_diag", s);
     hipLaunchKernelGGL(k_gram_f32<kF32Self>, dim3((unsigned)(p.tiles_diag * kF32Subs)), dim3(256), 0, s,
-                       (const float *)feats, cu_vis, w.dtile_off, w.dtile_req, nullptr, w.d_off, w.nn,
-                       w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
+                       (const float *)feats, w.dtile, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
     hipLaunchKernelGGL(k_gram_f32<kF32Upper>, dim3((unsigned)(p.tiles_diag * kF32Subs)), dim3(256), 0, s,
-                       (const float *)feats, cu_vis, w.dtile_off, w.dtile_req, nullptr, w.d_off, w.nn,
-                       w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
+                       (const float *)feats, w.dtile, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
     if (p.tiles_off > 0) {
       launch_begin("gram", s);
       hipLaunchKernelGGL(k_gram_f32<kF32Off>, dim3((unsigned)(p.tiles_off * kF32Subs)), dim3(256), 0, s,
-                         (const float *)feats, cu_vis, w.otile_off, w.otile_req, w.otile_ij, w.d_off,
-                         w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
+                         (const float *)feats, w.otile, w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
       if ((e = launch_end(s)) != hipSuccess) return e;
     }
   }
