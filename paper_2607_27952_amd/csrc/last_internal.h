@@ -170,33 +170,34 @@ __device__ __forceinline__ float wave_sum(float v) {
   v += dpp_mirror(v);
   return (row_lane15(v, 0) + row_lane15(v, 1)) + (row_lane15(v, 2) + row_lane15(v, 3));
 }
-// Maximum over the wave of a 64-bit key, returned wave-uniform. DPP exchanges
-// inside each row of 16 lanes (xor 1, xor 2, half-mirror, mirror) leave the
-// row's maximum in every lane of the row; the four rows meet through
-// readlane. Every lane of the wave must be active.
+// Wave-wide maximum of the 64-bit key (hi << 32) | lo, returned
+// wave-uniform, in two 32-bit passes: the maximum hi by DPP exchanges inside
+// each row of 16 lanes (xor 1, xor 2, half-mirror, mirror) and a readlane of
+// the four rows; then the lo of the lanes holding that hi. A single such lane
+// (the usual case) gives its lo directly; ties take a second pass over lo.
+// Every lane of the wave must be active.
 template <int CTRL>
-__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long v) {
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xF, 0xF, false);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
-  return ((unsigned long long)hi << 32) | lo;
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
 }
-__device__ __forceinline__ unsigned long long max_u64(unsigned long long a, unsigned long long b) {
-  return a > b ? a : b;
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dpp_u32<0xB1>(v));
+  v = max(v, dpp_u32<0x4E>(v));
+  v = max(v, dpp_u32<0x141>(v));
+  v = max(v, dpp_u32<0x140>(v));
+  const uint32_t a = max((uint32_t)__builtin_amdgcn_readlane(v, 15), (uint32_t)__builtin_amdgcn_readlane(v, 31));
+  const uint32_t b = max((uint32_t)__builtin_amdgcn_readlane(v, 47), (uint32_t)__builtin_amdgcn_readlane(v, 63));
+  return max(a, b);
 }
-__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long v) {
-  v = max_u64(v, dpp_u64<0xB1>(v));
-  v = max_u64(v, dpp_u64<0x4E>(v));
-  v = max_u64(v, dpp_u64<0x141>(v));
-  v = max_u64(v, dpp_u64<0x140>(v));
-  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
-  unsigned long long r = 0;
-#pragma unroll
-  for (int row = 0; row < 4; ++row) {
-    const uint32_t l = __builtin_amdgcn_readlane(lo, 16 * row + 15);
-    const uint32_t h = __builtin_amdgcn_readlane(hi, 16 * row + 15);
-    r = max_u64(r, ((unsigned long long)h << 32) | l);
-  }
-  return r;
+__device__ __forceinline__ unsigned long long wave_max_key(uint32_t hi, uint32_t lo) {
+  const uint32_t mh = wave_max_u32(hi);
+  const unsigned long long tied = __ballot(hi == mh);
+  uint32_t ml;
+  if (__popcll(tied) == 1)
+    ml = (uint32_t)__builtin_amdgcn_readlane(lo, (int)__ffsll((long long)tied) - 1);
+  else
+    ml = wave_max_u32(hi == mh ? lo : 0u);
+  return ((unsigned long long)mh << 32) | ml;
 }
 
 }  // namespace last_dev

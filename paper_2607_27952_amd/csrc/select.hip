@@ -1027,29 +1027,49 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
     dl[e] = INFINITY;
   }
   // block-wide maximum of a 64-bit key (wave-uniform result)
-  auto block_max = [&](unsigned long long key, int t) {
-    key = wave_max_u64(key);
+  auto block_max = [&](unsigned long long k, int t) {
+    unsigned long long key = wave_max_key((uint32_t)(k >> 32), (uint32_t)k);
     if (kNW == 1) return key;
     if (lane == 0) s_key[t & 1][wave] = key;
     __syncthreads();
     key = s_key[t & 1][0];
 #pragma unroll
-    for (int wv = 1; wv < kNW; ++wv) key = max_u64(key, s_key[t & 1][wv]);
+    for (int wv = 1; wv < kNW; ++wv) {
+      const unsigned long long other = s_key[t & 1][wv];
+      key = other > key ? other : key;
+    }
     return key;
   };
   auto key_of = [](float bo, int bi) -> unsigned long long {
     return bo >= 0.f ? ((unsigned long long)__float_as_uint(bo) << 32) | (0xFFFFFFFFu - (unsigned)bi) : 0ull;
   };
 
-  // t = 0: j_1 = argmax w (Eq. 9)
-  float bo = -1.f;
-  int bi = 0;
+  // The best (value, lowest index) of this thread's values v[e], in two
+  // independent chains (even and odd e, ascending) merged at the end, so that
+  // a single wave is not held up by one long chain of dependent compares.
+  auto thread_best = [&](const float (&v)[EPT], float &bo, int &bi) {
+    float b0 = -1.f, b1 = -1.f;
+    int i0 = 0, i1 = 0;
 #pragma unroll
-  for (int e = 0; e < EPT; ++e)
-    if (w[e] > bo) {
-      bo = w[e];
-      bi = tid + e * NTH;
+    for (int e = 0; e < EPT; e += 2) {
+      if (v[e] > b0) {
+        b0 = v[e];
+        i0 = tid + e * NTH;
+      }
+      if (e + 1 < EPT && v[e + 1] > b1) {
+        b1 = v[e + 1];
+        i1 = tid + (e + 1) * NTH;
+      }
     }
+    const bool take1 = b1 > b0 || (b1 == b0 && i1 < i0);
+    bo = take1 ? b1 : b0;
+    bi = take1 ? i1 : i0;
+  };
+
+  // t = 0: j_1 = argmax w (Eq. 9)
+  float bo;
+  int bi;
+  thread_best(w, bo, bi);
   unsigned long long best = block_max(key_of(bo, bi), 0);
   int j = (int)(0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull));
   if (tid == 0) {
@@ -1064,16 +1084,13 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
     float rv[EPT];
 #pragma unroll
     for (int e = 0; e < EPT; ++e) rv[e] = row[coff[e]];
-    bo = -1.f;
+    float o[EPT];
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
       dl[e] = fminf(dl[e], rv[e]);
-      const float o = w[e] * dl[e];   // Eq. 11 objective; -inf or NaN once picked, NaN past N_r
-      if (o > bo) {
-        bo = o;
-        bi = tid + e * NTH;
-      }
+      o[e] = w[e] * dl[e];   // Eq. 11 objective; -inf or NaN once picked, NaN past N_r
     }
+    thread_best(o, bo, bi);
     best = block_max(key_of(bo, bi), t);
     if (best == 0ull) break;   // every token already picked (cannot happen for K <= N)
     j = (int)(0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull));
