@@ -52,7 +52,7 @@ struct ScorePlan {
 struct ScoreWs {
   int32_t *chunk_off, *chunk_req, *slice_off, *slice_req;
   float4 *stats;  // [G][Hq][C_total] (chunk max, sum exp, visual sum exp, 0)
-  float *vlog;    // [N_total][G * Hq] scaled logits of visual columns, token-major
+  float *vlog;    // [G][N_total][Hq] scaled logits of visual columns, layer-major
   float2 *rowstat;  // [R][G * Hq] merged (max, 1 / sum exp) of every row
   float *mass;      // [R] total visual mass sum_{l,h} V / Z
 };

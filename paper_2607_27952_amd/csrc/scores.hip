@@ -212,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void k_score_stream(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req, int R, int Hq,
-    int Hkv, int CH, int64_t C_total, int64_t T_total, int GL, float scale,
+    int Hkv, int CH, int64_t C_total, int64_t T_total, float scale,
     float *__restrict__ vlog, float4 *__restrict__ stats, float *__restrict__ rows) {
   using RS = RowShape<T, DH>;
   extern __shared__ float s_log[];          // [CH][Hq]
@@ -299,13 +299,13 @@ __global__ __launch_bounds__(kThreads) void k_score_stream(
     __syncthreads();
   }
 
-  // Visual logits, token-major, coalesced; and every logit if rows are asked.
-  const int GH = GL * Hq;
+  // Visual logits, layer-major ([layer][visual token][head]): this block's
+  // are one contiguous run of whole cache lines. Every logit if rows are asked.
   const int vb = max(0, v_lo), ve = min(nt, v_hi);
   const int64_t vtok0 = (int64_t)cu_vis[r] - vis_start[r] + t_begin;
   for (int e = vb * Hq + (int)threadIdx.x; e < ve * Hq; e += kThreads) {
     const int t = e / Hq, h = e - t * Hq;
-    vlog[(vtok0 + t) * GH + (int64_t)l * Hq + h] = s_log[e];
+    vlog[((int64_t)l * cu_vis[R] + vtok0 + t) * Hq + h] = s_log[e];
   }
   if (rows)
     for (int e = threadIdx.x; e < nt * Hq; e += kThreads) {
@@ -319,7 +319,7 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req, int R, int Hq,
-    int Hkv, int g, int HG, int CH, int64_t C_total, int64_t T_total, int GL, float scale,
+    int Hkv, int g, int HG, int CH, int64_t C_total, int64_t T_total, float scale,
     float *__restrict__ vlog, float4 *__restrict__ stats, float *__restrict__ rows) {
   using RS = RowShape<T, DH>;
   extern __shared__ float s_logit[];   // [GM][CH]
@@ -459,11 +459,10 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
     stats[((int64_t)l * Hq + h0 + hh) * C_total + c] = make_float4(mm, zz, x, 0.f);
   }
 
-  const int GH = GL * Hq;
   const int64_t vtok0 = (int64_t)cu_vis[r] + t_begin - v_r;
   for (int hh = 0; hh < gh; ++hh) {
     for (int t = vb + threadIdx.x; t < ve; t += kThreads)
-      vlog[(vtok0 + t) * GH + (int64_t)l * Hq + h0 + hh] = s_logit[hh * CH + t];
+      vlog[((int64_t)l * cu_vis[R] + vtok0 + t) * Hq + h0 + hh] = s_logit[hh * CH + t];
     if (rows) {
       float *rd = rows + ((int64_t)l * Hq + h0 + hh) * T_total + tok0 + t_begin;
       for (int t = threadIdx.x; t < nt; t += kThreads) rd[t] = s_logit[hh * CH + t];
@@ -522,8 +521,9 @@ __global__ __launch_bounds__(kMergeThreads) void k_score_merge(
 __global__ __launch_bounds__(kThreads) void k_score_finalize(
     const float *__restrict__ vlog, const float2 *__restrict__ rowstat,
     const float *__restrict__ mass, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ slice_off, const int32_t *__restrict__ slice_req, int GH, int SL,
-    float *__restrict__ scores) {
+    const int32_t *__restrict__ slice_off, const int32_t *__restrict__ slice_req, int G, int Hq,
+    int64_t N_total, int SL, float *__restrict__ scores) {
+  const int GH = G * Hq;
   __shared__ float2 sMZ[kMaxPairs];
   const int b = blockIdx.x;
   const int r = slice_req[b];
@@ -535,18 +535,23 @@ __global__ __launch_bounds__(kThreads) void k_score_finalize(
   const int N_r = cu_vis[r + 1] - (int)n0;
   const int end = min(N_r, (sl + 1) * SL);
   for (int i = sl * SL + threadIdx.x; i < end; i += kThreads) {
-    const float *lg = vlog + (n0 + i) * GH;
+    // (layer, head) pairs p = l * Hq + h in increasing order; layer l's logits
+    // of this token are Hq contiguous floats
     float acc = 0.f;
-    if ((GH & 3) == 0) {
-      for (int p = 0; p < GH; p += 4) {
-        const float4 x = *reinterpret_cast<const float4 *>(lg + p);
-        acc = fmaf(expf(x.x - sMZ[p].x), sMZ[p].y, acc);
-        acc = fmaf(expf(x.y - sMZ[p + 1].x), sMZ[p + 1].y, acc);
-        acc = fmaf(expf(x.z - sMZ[p + 2].x), sMZ[p + 2].y, acc);
-        acc = fmaf(expf(x.w - sMZ[p + 3].x), sMZ[p + 3].y, acc);
+    for (int l = 0; l < G; ++l) {
+      const float *lg = vlog + ((int64_t)l * N_total + n0 + i) * Hq;
+      const float2 *mz = sMZ + l * Hq;
+      if ((Hq & 3) == 0) {
+        for (int h = 0; h < Hq; h += 4) {
+          const float4 x = *reinterpret_cast<const float4 *>(lg + h);
+          acc = fmaf(expf(x.x - mz[h].x), mz[h].y, acc);
+          acc = fmaf(expf(x.y - mz[h + 1].x), mz[h + 1].y, acc);
+          acc = fmaf(expf(x.z - mz[h + 2].x), mz[h + 2].y, acc);
+          acc = fmaf(expf(x.w - mz[h + 3].x), mz[h + 3].y, acc);
+        }
+      } else {
+        for (int h = 0; h < Hq; ++h) acc = fmaf(expf(lg[h] - mz[h].x), mz[h].y, acc);
       }
-    } else {
-      for (int p = 0; p < GH; ++p) acc = fmaf(expf(lg[p] - sMZ[p].x), sMZ[p].y, acc);
     }
     scores[n0 + i] = acc * invS;
   }
@@ -582,7 +587,7 @@ hipError_t launch_stream_dh(const last_batch *b, const last::ScorePlan &p, const
   hipLaunchKernelGGL((k_score_stream<T, DH, GQV>), dim3((unsigned)blocks), dim3(kThreads), lds, s, \
                      (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,          \
                      w.chunk_off, w.chunk_req, b->R, b->Hq, b->Hkv, p.chunk_tokens, p.C_total,   \
-                     p.T_total, b->G, scale, w.vlog, w.stats, attn_rows)
+                     p.T_total, scale, w.vlog, w.stats, attn_rows)
   switch (g) {
     case 1: LAST_LAUNCH_GQ(1); break;
     case 2: LAST_LAUNCH_GQ(2); break;
@@ -609,7 +614,7 @@ hipError_t launch_partial_dh(const last_batch *b, const last::ScorePlan &p,
   hipLaunchKernelGGL((k_score_partial<T, DH, GMV>), dim3((unsigned)blocks), dim3(kThreads), lds, \
                      s, (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,      \
                      w.chunk_off, w.chunk_req, b->R, b->Hq, b->Hkv, g, p.head_groups,           \
-                     p.chunk_tokens, p.C_total, p.T_total, b->G, scale, w.vlog, w.stats,         \
+                     p.chunk_tokens, p.C_total, p.T_total, scale, w.vlog, w.stats,               \
                      attn_rows)
   switch (p.g_max) {
     case 1: LAST_LAUNCH_GM(1); break;
@@ -711,7 +716,7 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
 
   launch_begin("score_finalize", s);
   hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog,
-                     w.rowstat, w.mass, b->cu_vis, w.slice_off, w.slice_req, b->G * b->Hq,
+                     w.rowstat, w.mass, b->cu_vis, w.slice_off, w.slice_req, b->G, b->Hq, p.N_total,
                      p.slice_tokens, scores);
   e = launch_end(s);
   if (e != hipSuccess || !attn_rows) return e;
