@@ -12,6 +12,9 @@ Each function names the paper passage it follows (arXiv 2607.27952, Sec. 3):
   replay  -- teacher-forced check of a candidate pick sequence under Eq. 9-11
   gather  -- Eq. 12 (rows of X in ascending kept order)
   budget  -- Eq. 2 (K = ceil(rho * N))
+  rows_scores -- Table 4 attention sources: Eq. 6-8 over any set of causal
+             query rows per request (first / middle / every query token)
+  source_rows -- the row positions of each Table 4 attention source
 """
 import ctypes
 import os
@@ -45,6 +48,10 @@ def lib():
         L.oracle_gather.restype = I
         L.oracle_budget.argtypes = [I64, I64, I64]
         L.oracle_budget.restype = I64
+        L.oracle_rows_scores.argtypes = [I, I, I, I, I, I, D, P, P, P, P, P, P, P, P, P, I]
+        L.oracle_rows_scores.restype = I
+        L.oracle_source_rows.argtypes = [I, ctypes.c_int32, ctypes.c_int32, P]
+        L.oracle_source_rows.restype = I
         L.oracle_max_threads.argtypes = []
         L.oracle_max_threads.restype = I
         _lib = L
@@ -88,6 +95,39 @@ def scores(R, G, Hq, Hkv, Dh, q, k, cu_seqlens, vis_start, cu_vis, dtype,
     if rc != 0:
         raise RuntimeError(f"oracle_scores failed ({rc})")
     return (w, rows) if want_rows else w
+
+
+def rows_scores(R, G, Hq, Hkv, Dh, q, k, cu_seqlens, vis_start, cu_vis, cu_rows, row_pos, dtype,
+                scale=0.0, want_sums=False, nthreads=0):
+    """Table 4 sources: Eq. 6-8 summed over the causal rows at row_pos (CSR by cu_rows).
+
+    q is [G][M_total][Hq][Dh]. Returns w [N_total] (fp64) and, if asked, the
+    unnormalised sums s [N_total].
+    """
+    cu_seqlens, vis_start, cu_vis = _i32(cu_seqlens), _i32(vis_start), _i32(cu_vis)
+    cu_rows, row_pos = _i32(cu_rows), _i32(row_pos)
+    q, qd = _storage(q, dtype)
+    k, _ = _storage(k, dtype)
+    w = np.zeros(int(cu_vis[R]), dtype=np.float64)
+    s = np.zeros(int(cu_vis[R]), dtype=np.float64) if want_sums else None
+    rc = lib().oracle_rows_scores(R, G, Hq, Hkv, Dh, qd, float(scale), _ptr(cu_seqlens),
+                                  _ptr(vis_start), _ptr(cu_vis), _ptr(cu_rows), _ptr(row_pos),
+                                  _ptr(q), _ptr(k), _ptr(w), _ptr(s), nthreads)
+    if rc != 0:
+        raise RuntimeError(f"oracle_rows_scores failed ({rc})")
+    return (w, s) if want_sums else w
+
+
+SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
+
+
+def source_rows(src, qb, qe):
+    """Table 4: positions of the rows of attention source `src` for a query at [qb, qe)."""
+    pos = np.zeros(max(1, qe - qb), np.int32)
+    n = lib().oracle_source_rows(int(src), int(qb), int(qe), _ptr(pos))
+    if n < 0:
+        raise ValueError("empty query or unknown source")
+    return pos[:n].copy()
 
 
 def select(R, Dv, w32, feats, cu_vis, cu_keep, dtype, mode=KCENTER, nthreads=0):

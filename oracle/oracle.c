@@ -26,6 +26,8 @@
  *     gathered in that order.
  *   - Sec. 4.3, Table 5: the "Top-k" ablation keeps the K largest w.
  *   - Sec. 3.2, Eq. 2: K = ceil(rho * N).
+ *   - Sec. 4.3, Table 4: other attention sources (first, middle or every
+ *     query token instead of the last), each row causal.
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   - softmax scale sigma is an explicit argument (1/sqrt(Dh) when <= 0);
@@ -148,6 +150,110 @@ int oracle_scores(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
     free(s);
   }
   return bad ? 2 : 0;
+}
+
+/*
+ * Sec. 4.3, Table 4 (which attention rows supply the relevance). Eq. 7 with
+ * its single row p* replaced by a set of query rows per request: request r
+ * uses the rows at positions row_pos[cu_rows[r] .. cu_rows[r+1]), and their
+ * attention over the visual tokens is summed over rows, layers and heads
+ * ("All Mean" averages the rows; a common factor cancels in Eq. 8). Under the
+ * causal mask of Eq. 6 the row at position p attends to keys 0..p only: its
+ * softmax runs over those p + 1 keys, and visual tokens after p get nothing
+ * from it. With one row at P_r - 1 per request this is oracle_scores.
+ * q: [G][M_total][Hq][Dh] (the queries of those rows, M_total = cu_rows[R]),
+ * k: [G][T_total][Hkv][Dh]. w_out: [N_total] normalised scores (Eq. 8);
+ * s_out (nullable): [N_total] the sums s_i before normalisation.
+ * Returns 1 for malformed arguments (a row outside [0, P_r)), 3 if a request's
+ * rows see no visual token (Eq. 8 undefined).
+ */
+int oracle_rows_scores(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
+                       double scale, const int32_t *cu_seqlens,
+                       const int32_t *vis_start, const int32_t *cu_vis,
+                       const int32_t *cu_rows, const int32_t *row_pos,
+                       const void *q, const void *k, double *w_out,
+                       double *s_out, int nthreads) {
+  if (R < 0 || G < 1 || Hq < 1 || Hkv < 1 || Dh < 1 || Hq % Hkv != 0)
+    return 1;
+  const int g = Hq / Hkv;
+  const int64_t T_total = cu_seqlens[R];
+  const int64_t M_total = cu_rows[R];
+  if (scale <= 0.0) scale = 1.0 / sqrt((double)Dh);
+  for (int r = 0; r < R; ++r)
+    for (int64_t m = cu_rows[r]; m < cu_rows[r + 1]; ++m)
+      if (row_pos[m] < 0 || row_pos[m] >= cu_seqlens[r + 1] - cu_seqlens[r]) return 1;
+  orc_set_threads(nthreads);
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+  for (int r = 0; r < R; ++r) {
+    const int64_t tok0 = cu_seqlens[r];
+    const int64_t P = (int64_t)cu_seqlens[r + 1] - tok0;
+    const int64_t v0 = vis_start[r];
+    const int64_t N = (int64_t)cu_vis[r + 1] - cu_vis[r];
+    double *logit = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+    double *s = (double *)calloc((size_t)(N > 0 ? N : 1), sizeof(double));
+    if (!logit || !s) {
+      bad |= 2;
+      free(logit);
+      free(s);
+      continue;
+    }
+    for (int l = 0; l < G; ++l) {
+      for (int h = 0; h < Hq; ++h) {
+        const int kv = h / g;
+        for (int64_t m = cu_rows[r]; m < cu_rows[r + 1]; ++m) {
+          const int64_t p = row_pos[m];
+          const int64_t qoff = (((int64_t)l * M_total + m) * Hq + h) * Dh;
+          /* the row sees keys 0..p (causal mask, Eq. 6) */
+          for (int64_t j = 0; j <= p; ++j) {
+            const int64_t koff = (((int64_t)l * T_total + tok0 + j) * Hkv + kv) * Dh;
+            double acc = 0.0;
+            for (int d = 0; d < Dh; ++d)
+              acc += orc_widen(q, qoff + d, qk_dtype) * orc_widen(k, koff + d, qk_dtype);
+            logit[j] = scale * acc;
+          }
+          double mx = -INFINITY;
+          for (int64_t j = 0; j <= p; ++j)
+            if (logit[j] > mx) mx = logit[j];
+          double Z = 0.0;
+          for (int64_t j = 0; j <= p; ++j) Z += exp(logit[j] - mx);
+          /* visual columns the row can see, summed over rows, layers, heads */
+          for (int64_t i = 0; i < N && v0 + i <= p; ++i) s[i] += exp(logit[v0 + i] - mx) / Z;
+        }
+      }
+    }
+    double tot = 0.0;
+    for (int64_t i = 0; i < N; ++i) tot += s[i];
+    if (!(tot > 0.0)) bad |= 1;
+    for (int64_t i = 0; i < N; ++i) {
+      w_out[cu_vis[r] + i] = tot > 0.0 ? s[i] / tot : 0.0;
+      if (s_out) s_out[cu_vis[r] + i] = s[i];
+    }
+    free(logit);
+    free(s);
+  }
+  return (bad & 2) ? 2 : (bad & 1) ? 3 : 0;
+}
+
+/*
+ * Sec. 4.3, Table 4: the attention sources compared there, for a text query
+ * of M = qe - qb tokens q_1 .. q_M at positions qb .. qe - 1 (q_M is the last
+ * query token p*). Writes the positions of the source's rows to pos and
+ * returns how many: 0 Last -> q_M; 1 First -> q_1; 2 Middle -> q_ceil(M/2);
+ * 3 All Mean -> q_1 .. q_M. Returns -1 for an empty query or an unknown source.
+ */
+int oracle_source_rows(int src, int32_t qb, int32_t qe, int32_t *pos) {
+  const int32_t M = qe - qb;
+  if (M < 1 || qb < 0) return -1;
+  switch (src) {
+    case 0: pos[0] = qb + M - 1; return 1;
+    case 1: pos[0] = qb; return 1;
+    case 2: pos[0] = qb + (M + 1) / 2 - 1; return 1;
+    case 3:
+      for (int32_t m = 0; m < M; ++m) pos[m] = qb + m;
+      return M;
+    default: return -1;
+  }
 }
 
 /*

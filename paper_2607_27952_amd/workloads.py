@@ -95,6 +95,7 @@ class Workload:
     cu_keep: np.ndarray
     planted: Optional[List[np.ndarray]] = None
     notes: str = ""
+    qk_std: float = 0.0          # element std of q and k as drawn (0: 1/sqrt(Dh))
 
     @property
     def T_total(self) -> int:
@@ -335,7 +336,7 @@ def make(name: str, budget: Optional[int] = None, sharp: bool = False, seed: int
     return Workload(name=name + ("_sharp" if sharp else ""), R=R, G=G, Hq=Hq, Hkv=Hkv, Dh=Dh,
                     qk_dtype=qkd, scale=scale, cu_seqlens=cu_seqlens, vis_start=vis_start,
                     cu_vis=cu_vis, q=_store(q32, qkd), k=k_out, Dv=Dv, f_dtype=fd,
-                    feats=f_out, cu_keep=cu_keep, planted=planted)
+                    feats=f_out, cu_keep=cu_keep, planted=planted, qk_std=float(std))
 
 
 def tiny(seed: int, R: int = 2, G: int = 1, Hq: int = 4, Hkv: int = 2, Dh: int = 64,
@@ -360,4 +361,57 @@ def tiny(seed: int, R: int = 2, G: int = 1, Hq: int = 4, Hkv: int = 2, Dh: int =
     return Workload(name=f"tiny{seed}", R=R, G=G, Hq=Hq, Hkv=Hkv, Dh=Dh, qk_dtype=qk_dtype,
                     scale=1.0 / math.sqrt(Dh), cu_seqlens=cu_seqlens, vis_start=vis_start,
                     cu_vis=cu_vis, q=_store(q32, qk_dtype), k=_store(k32, qk_dtype), Dv=Dv,
-                    f_dtype=f_dtype, feats=_store(feats, f_dtype), cu_keep=_cu(Kr))
+                    f_dtype=f_dtype, feats=_store(feats, f_dtype), cu_keep=_cu(Kr), qk_std=float(std))
+
+
+@dataclasses.dataclass
+class QueryRows:
+    """Queries of every text-query token of a batch: the tokens after each
+    request's visual span, positions [q_begin[r], q_end[r]) with
+    q_end[r] = P_r (the last of them is the last query token).
+
+      q_begin, q_end  [R] request-local positions
+      cu_q            [R+1] CSR offsets of the rows in q
+      q               [G][Q_total][Hq][Dh], the workload's storage dtype
+    """
+    q_begin: np.ndarray
+    q_end: np.ndarray
+    cu_q: np.ndarray
+    q: np.ndarray
+
+    def rows(self, r: int) -> np.ndarray:
+        """q of request r's query tokens: [G][M_r][Hq][Dh]."""
+        return self.q[:, int(self.cu_q[r]):int(self.cu_q[r + 1])]
+
+    def subset(self, reqs) -> "QueryRows":
+        reqs = [int(r) for r in reqs]
+        return QueryRows(q_begin=self.q_begin[reqs].copy(), q_end=self.q_end[reqs].copy(),
+                         cu_q=_cu([int(self.cu_q[r + 1] - self.cu_q[r]) for r in reqs]),
+                         q=np.ascontiguousarray(np.concatenate([self.rows(r) for r in reqs], axis=1)))
+
+
+def query_rows(wl: Workload, seed: int = 0) -> QueryRows:
+    """Queries for every text token after the visual span of each request.
+
+    The row of the last token is the workload's own q (so a source made of
+    that row alone is the last-token path); the others are fresh draws with
+    the same element distribution, from SeedSequence([2607, 27952, 1000 +
+    seed, r]) for request r. Nothing here depends on how rows are chosen."""
+    N = np.diff(wl.cu_vis).astype(np.int64)
+    P = np.diff(wl.cu_seqlens).astype(np.int64)
+    qb = (wl.vis_start.astype(np.int64) + N).astype(np.int32)
+    qe = P.astype(np.int32)
+    M = (qe - qb).astype(np.int64)
+    if np.any(M < 1):
+        raise ValueError("every request needs at least one text token after its visual span")
+    cu_q = _cu(M)
+    std = np.float32(wl.qk_std if wl.qk_std > 0 else 1.0 / math.sqrt(wl.Dh))
+    dt = np.uint16 if wl.qk_dtype == BF16 else np.float32
+    out = np.empty((wl.G, int(cu_q[-1]), wl.Hq, wl.Dh), dtype=dt)
+    for r in range(wl.R):
+        rng = np.random.default_rng(np.random.SeedSequence([2607, 27952, 1000 + seed, r]))
+        x = rng.standard_normal((wl.G, int(M[r]), wl.Hq, wl.Dh), dtype=np.float32) * std
+        a = int(cu_q[r])
+        out[:, a:a + int(M[r]) - 1] = _store(x[:, :-1], wl.qk_dtype)
+        out[:, a + int(M[r]) - 1] = wl.q[:, r]
+    return QueryRows(q_begin=qb, q_end=qe, cu_q=cu_q, q=out)

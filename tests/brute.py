@@ -77,3 +77,36 @@ def gonzalez(X, K):
         d[S] = -np.inf
         S.append(int(np.argmax(d)))
     return np.array(S)
+
+
+def rows_scores(wl, cu_rows, row_pos, q_rows, rng=None, want_sums=False):
+    """Table 4 sources by brute force: the full P x P causal attention matrix of
+    every layer and head, with the given queries placed at their positions
+    (random queries elsewhere); the listed rows are read out and summed, then
+    normalised over the visual tokens (Eq. 7-8)."""
+    rng = rng or np.random.default_rng(0)
+    qr = _f64(q_rows, wl.qk_dtype)
+    k = _f64(wl.k, wl.qk_dtype)
+    g = wl.Hq // wl.Hkv
+    w = np.zeros(wl.N_total)
+    sums = np.zeros(wl.N_total)
+    for r in range(wl.R):
+        a, b = int(wl.cu_seqlens[r]), int(wl.cu_seqlens[r + 1])
+        P = b - a
+        v0, N = int(wl.vis_start[r]), wl.n(r)
+        rows = list(range(int(cu_rows[r]), int(cu_rows[r + 1])))
+        s = np.zeros(N)
+        for l in range(wl.G):
+            for h in range(wl.Hq):
+                Kmat = k[l, a:b, h // g, :]
+                Q = rng.standard_normal((P, wl.Dh))
+                for m in rows:
+                    Q[int(row_pos[m])] = qr[l, m, h]
+                logits = wl.scale * (Q @ Kmat.T)
+                logits[np.triu_indices(P, 1)] = -np.inf
+                A = scipy.special.softmax(logits, axis=1)
+                for m in rows:
+                    s += A[int(row_pos[m]), v0:v0 + N]
+        sums[int(wl.cu_vis[r]):int(wl.cu_vis[r + 1])] = s
+        w[int(wl.cu_vis[r]):int(wl.cu_vis[r + 1])] = s / s.sum()
+    return (w, sums) if want_sums else w

@@ -7,6 +7,7 @@ mutation tests at the end plant plausible mistakes in a temporary copy of
 the oracle's C source and check that these pins catch every one of them.
 """
 import ctypes
+import dataclasses
 import json
 import math
 import os
@@ -382,13 +383,131 @@ def test_budget_golden_and_exact():
             assert oracle.budget(n, num, den) == math.ceil(Fraction(n * num, den))
 
 
+
+# ------------------------------------------------- attention sources (Table 4)
+
+def _orc_rows(wl, cu_rows, row_pos, q_rows, **kw):
+    return oracle.rows_scores(wl.R, wl.G, wl.Hq, wl.Hkv, wl.Dh, q_rows, wl.k, wl.cu_seqlens,
+                              wl.vis_start, wl.cu_vis, cu_rows, row_pos, _fcode(wl.qk_dtype),
+                              scale=wl.scale, **kw)
+
+
+def _random_rows(wl, rng, max_rows=4):
+    """Random row sets per request: positions anywhere from the visual span's start
+    to the last token, with queries drawn fresh (sharp, so the rows differ)."""
+    counts, pos = [], []
+    for r in range(wl.R):
+        lo, hi = int(wl.vis_start[r]), wl.p(r)
+        m = int(rng.integers(1, min(max_rows, hi - lo) + 1))
+        pos.extend(sorted(rng.choice(np.arange(lo, hi), size=m, replace=False).tolist()))
+        counts.append(m)
+    cu_rows = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    q = rng.standard_normal((wl.G, int(cu_rows[-1]), wl.Hq, wl.Dh)).astype(np.float32)
+    q = W.to_bf16_bits(q) if wl.qk_dtype == W.BF16 else q
+    return cu_rows, np.asarray(pos, np.int32), q
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_rows_scores_match_bruteforce(seed):
+    wl = W.tiny(300 + seed, R=3, G=1 + seed % 2, Hq=4, Hkv=1 + seed % 2 * 1, Dh=8 if seed % 2 else 16,
+                n_range=(1, 20), t_range=(2, 12), qk_dtype=W.BF16 if seed % 3 else W.F32)
+    rng = np.random.default_rng(seed)
+    cu_rows, pos, q = _random_rows(wl, rng)
+    w, s = _orc_rows(wl, cu_rows, pos, q, want_sums=True)
+    wb, sb = brute.rows_scores(wl, cu_rows, pos, q, want_sums=True)
+    np.testing.assert_allclose(w, wb, rtol=1e-10, atol=1e-15)
+    np.testing.assert_allclose(s, sb, rtol=1e-10, atol=1e-15)
+
+
+def test_rows_golden_causal():
+    gold = _load("rows_causal.json")
+    P, v0, N, Dh = gold["P"], gold["vis_start"], gold["N"], gold["Dh"]
+    k = np.ones((1, P, 1, Dh), np.float32)
+    wl = _make_wl(np.zeros((1, 1, 1, Dh)), k, [0, P], [v0], [0, N], 1, 1, 0.5)
+    for case in gold["cases"]:
+        rows = np.asarray(case["rows"], np.int32)
+        q = np.random.default_rng(len(rows)).standard_normal((1, len(rows), 1, Dh)).astype(np.float32)
+        w = _orc_rows(wl, [0, len(rows)], rows, q)
+        exp = np.array([float(Fraction(x)) for x in case["w"]])
+        np.testing.assert_allclose(w, exp, rtol=1e-13, atol=1e-15)
+
+
+def test_rows_of_last_token_is_token_scores():
+    for seed in range(4):
+        wl = W.tiny(320 + seed, R=3, G=2, Hq=4, Hkv=2, Dh=16, n_range=(1, 30), t_range=(1, 10))
+        cu_rows = np.arange(wl.R + 1, dtype=np.int32)
+        pos = np.array([wl.p(r) - 1 for r in range(wl.R)], np.int32)
+        np.testing.assert_allclose(_orc_rows(wl, cu_rows, pos, wl.q), _orc_scores(wl), rtol=1e-13)
+
+
+def test_rows_keys_after_the_rows_are_invisible():
+    wl = W.tiny(330, R=2, G=1, Hq=2, Hkv=1, Dh=16, n_range=(8, 20), t_range=(8, 12), qk_dtype=W.F32)
+    rng = np.random.default_rng(3)
+    # rows end before the last few tokens; keys after the last row get huge values
+    counts, pos = [], []
+    for r in range(wl.R):
+        lo, hi = int(wl.vis_start[r]) + 2, wl.p(r) - 3
+        pos.extend([lo, (lo + hi) // 2, hi])
+        counts.append(3)
+    cu_rows = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    q = rng.standard_normal((1, 6, 2, 16)).astype(np.float32)
+    w0 = _orc_rows(wl, cu_rows, pos, q)
+    k2 = wl.k.copy()
+    for r in range(wl.R):
+        a = int(wl.cu_seqlens[r])
+        k2[:, a + int(pos[3 * r + 2]) + 1:int(wl.cu_seqlens[r + 1])] = 50.0
+    w1 = _orc_rows(dataclasses.replace(wl, k=k2), cu_rows, pos, q)
+    assert np.array_equal(w0, w1)
+
+
+def test_rows_sums_add_over_row_sets():
+    """Eq. 7 sums rows: the unnormalised sums of a union are the sums of the parts."""
+    wl = W.tiny(340, R=3, G=2, Hq=4, Hkv=2, Dh=16, n_range=(4, 25), t_range=(4, 12))
+    rng = np.random.default_rng(7)
+    cu_a, pos_a, q_a = _random_rows(wl, rng, 3)
+    cu_b, pos_b, q_b = _random_rows(wl, rng, 3)
+    _, sa = _orc_rows(wl, cu_a, pos_a, q_a, want_sums=True)
+    _, sb = _orc_rows(wl, cu_b, pos_b, q_b, want_sums=True)
+    pos, qs, cnt = [], [], []
+    for r in range(wl.R):
+        ia = slice(int(cu_a[r]), int(cu_a[r + 1]))
+        ib = slice(int(cu_b[r]), int(cu_b[r + 1]))
+        pos.extend(list(pos_a[ia]) + list(pos_b[ib]))
+        qs.append(np.concatenate([q_a[:, ia], q_b[:, ib]], axis=1))
+        cnt.append(int(cu_a[r + 1] - cu_a[r] + cu_b[r + 1] - cu_b[r]))
+    cu = np.concatenate([[0], np.cumsum(cnt)]).astype(np.int32)
+    _, s = _orc_rows(wl, cu, np.asarray(pos, np.int32), np.concatenate(qs, axis=1), want_sums=True)
+    np.testing.assert_allclose(s, sa + sb, rtol=1e-12)
+
+
+def test_rows_reject_invisible_or_out_of_range_rows():
+    wl = W.tiny(350, R=1, n_range=(5, 5), t_range=(8, 8))
+    q = wl.q[:, :1]
+    with pytest.raises(RuntimeError):
+        _orc_rows(wl, [0, 1], [wl.p(0)], q)           # past the last token
+    with pytest.raises(RuntimeError):
+        _orc_rows(wl, [0, 1], [int(wl.vis_start[0]) - 1], q) if wl.vis_start[0] > 0 else \
+            _orc_rows(wl, [0, 1], [-1], q)             # sees no visual token / negative
+
+
+def test_source_rows_golden():
+    gold = _load("source_rows.json")
+    for case in gold["cases"]:
+        for name, code in gold["sources"].items():
+            got = oracle.source_rows(code, case["q_begin"], case["q_end"])
+            assert got.tolist() == case[name], (name, case)
+    with pytest.raises(ValueError):
+        oracle.source_rows(0, 5, 5)
+
+
 # ---------------------------------------------------------------- planted mistakes
 
 MUTANTS = {
     # dropped term: the last layer is never summed (Eq. 7)
-    "drop_layer": ("for (int l = 0; l < G; ++l) {", "for (int l = 0; l < G - 1 + (G == 1); ++l) {"),
+    "drop_layer": ("for (int l = 0; l < G; ++l) {\n      for (int h = 0; h < Hq; ++h) {\n        const int kv = h / g;\n        const int64_t qoff",
+                   "for (int l = 0; l < G - 1 + (G == 1); ++l) {\n      for (int h = 0; h < Hq; ++h) {\n        const int kv = h / g;\n        const int64_t qoff"),
     # wrong index: query head h reads KV head h % Hkv instead of h / g
-    "kv_index": ("const int kv = h / g;", "const int kv = h % Hkv;"),
+    "kv_index": ("const int kv = h / g;\n        const int64_t qoff", "const int kv = h % Hkv;\n        const int64_t qoff"),
     # softmax over the visual span only instead of the whole row (Eq. 6)
     "visual_softmax": ("for (int64_t j = 0; j < P; ++j) Z += exp(logit[j] - m);",
                        "for (int64_t j = v0; j < v0 + N; ++j) Z += exp(logit[j] - m);"),
@@ -412,6 +531,16 @@ MUTANTS = {
     # kept indices left in pick order instead of ascending (Eq. 12)
     "unsorted_kept": ("if (sel[i]) kept[out0 + c++] = (int32_t)i;",
                       "if (sel[i]) { kept[out0 + c] = order[out0 + c]; ++c; }"),
+    # Table 4 rows scored as if they were the last token (causal mask ignored)
+    "rows_no_causal": ("const int64_t p = row_pos[m];", "const int64_t p = P - 1; (void)row_pos;"),
+    # off by one in the causal softmax: the row's own key left out of Z
+    "rows_off_by_one": ("for (int64_t j = 0; j <= p; ++j) Z += exp(logit[j] - mx);",
+                        "for (int64_t j = 0; j < p; ++j) Z += exp(logit[j] - mx);"),
+    # every row renormalised over the visual tokens it sees
+    "rows_renormalise": ("for (int64_t j = 0; j <= p; ++j) Z += exp(logit[j] - mx);",
+                         "for (int64_t j = v0; j <= p && j < v0 + N; ++j) Z += exp(logit[j] - mx);"),
+    # Middle taken as q_(floor(M/2)+1) instead of q_ceil(M/2)
+    "middle_floor": ("case 2: pos[0] = qb + (M + 1) / 2 - 1; return 1;", "case 2: pos[0] = qb + M / 2; return 1;"),
 }
 
 
@@ -434,7 +563,9 @@ def _pins_pass():
               lambda: test_scores_match_bruteforce(2), lambda: test_scores_planted_key_closed_form(3.0),
               test_select_golden_cases, lambda: test_select_matches_bruteforce(0),
               lambda: test_select_matches_bruteforce(5), test_select_orthogonal_features_is_topk,
-              test_select_uniform_weights_is_farthest_point, lambda: test_select_invariants(0)]
+              test_select_uniform_weights_is_farthest_point, lambda: test_select_invariants(0),
+              lambda: test_rows_scores_match_bruteforce(1), lambda: test_rows_scores_match_bruteforce(2),
+              test_rows_golden_causal, test_source_rows_golden]
     for c in checks:
         try:
             c()
