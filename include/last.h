@@ -9,6 +9,8 @@
  *                      (softmax over the whole visual + text context), its
  *                      visual columns summed over guidance layers and heads,
  *                      normalised over the visual tokens.
+ *   last_rows_scores   Sec. 4.3, Table 4: the same scores from other causal
+ *                      query rows (first, middle or every query token).
  *   diverse_select     Sec. 3.4, Eq. 9-12: importance-weighted greedy k-center
  *                      over unit-normalised encoder features under a budget
  *                      K = ceil(rho N) (Eq. 2); or the Top-k ablation of
@@ -110,6 +112,56 @@ size_t last_token_scores_workspace(const last_batch *b);
 last_status last_token_scores(const last_batch *b, const void *q, const void *k,
                               float *scores, float *attn_rows, void *ws,
                               size_t ws_bytes, void *stream);
+
+/*
+ * Sec. 4.3, Table 4 (attention-source ablation): the sources compared there,
+ * for a text query of M tokens q_1 .. q_M at positions q_begin .. q_end - 1
+ * of a request (M = q_end - q_begin; q_M is the last query token p*).
+ *   LAST_SRC_LAST      q_M            (the method's choice, Eq. 7)
+ *   LAST_SRC_FIRST     q_1
+ *   LAST_SRC_MIDDLE    q_ceil(M/2)    (indices count query tokens)
+ *   LAST_SRC_ALL_MEAN  q_1 .. q_M     (rows averaged; the average and the sum
+ *                                      give the same scores after Eq. 8)
+ */
+typedef enum {
+  LAST_SRC_LAST = 0,
+  LAST_SRC_FIRST = 1,
+  LAST_SRC_MIDDLE = 2,
+  LAST_SRC_ALL_MEAN = 3
+} last_source;
+
+/* Host helper: writes the request-local positions of source `src`'s rows to
+ * pos_h (room for q_end - q_begin entries) in increasing order and returns
+ * how many; -1 for q_begin < 0, q_end <= q_begin or an unknown source. */
+int32_t last_source_rows(last_source src, int32_t q_begin, int32_t q_end, int32_t *pos_h);
+
+/* Workspace bytes last_rows_scores needs (0 if the arguments are invalid). */
+size_t last_rows_scores_workspace(const last_batch *b, const int32_t *cu_rows_h,
+                                  const int32_t *row_pos_h);
+
+/*
+ * Sec. 4.3, Table 4, generalising Eq. 6-8 from the last query token's row to
+ * any set of query rows per request:
+ *   s_i = sum_l sum_h sum_{m in rows(r)} A^(l,h)[p_m, v_r + i],  w~ = s / sum s
+ * Under the causal mask the row at position p attends to keys 0 .. p only:
+ * its softmax runs over those p + 1 keys and visual tokens after p get
+ * nothing from it.
+ *   b          as for last_token_scores
+ *   cu_rows    [R+1] CSR offsets of each request's rows; M_r >= 1
+ *   row_pos    [M_total] request-local position of each row, with
+ *              vis_start[r] <= p < P_r (every row sees a visual token)
+ *   q          [G][M_total][Hq][Dh] the queries of those rows (after rotary
+ *              embedding), same dtype as k
+ *   k, scores, ws, stream   as for last_token_scores
+ * One row per request (Last, First, Middle) runs the streamed single-row
+ * kernels; several rows (All Mean) run two matrix-core passes over the keys:
+ * row statistics, then the visual probabilities summed over rows and heads.
+ * The result with one row per request at P_r - 1 equals last_token_scores.
+ */
+last_status last_rows_scores(const last_batch *b, const int32_t *cu_rows,
+                             const int32_t *cu_rows_h, const int32_t *row_pos,
+                             const int32_t *row_pos_h, const void *q, const void *k,
+                             float *scores, void *ws, size_t ws_bytes, void *stream);
 
 /* Workspace bytes diverse_select needs (0 if the arguments are invalid). */
 size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,

@@ -192,24 +192,32 @@ int oracle_rows_scores(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
     const int64_t N = (int64_t)cu_vis[r + 1] - cu_vis[r];
     double *logit = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
     double *s = (double *)calloc((size_t)(N > 0 ? N : 1), sizeof(double));
-    if (!logit || !s) {
+    /* one layer's keys of one KV head, and one query row, widened to fp64 */
+    double *kx = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1) * (size_t)Dh);
+    double *qx = (double *)malloc(sizeof(double) * (size_t)Dh);
+    if (!logit || !s || !kx || !qx) {
       bad |= 2;
       free(logit);
       free(s);
+      free(kx);
+      free(qx);
       continue;
     }
     for (int l = 0; l < G; ++l) {
       for (int h = 0; h < Hq; ++h) {
         const int kv = h / g;
+        if (h % g == 0)
+          for (int64_t j = 0; j < P; ++j)
+            for (int d = 0; d < Dh; ++d)
+              kx[j * Dh + d] = orc_widen(k, (((int64_t)l * T_total + tok0 + j) * Hkv + kv) * Dh + d, qk_dtype);
         for (int64_t m = cu_rows[r]; m < cu_rows[r + 1]; ++m) {
           const int64_t p = row_pos[m];
           const int64_t qoff = (((int64_t)l * M_total + m) * Hq + h) * Dh;
+          for (int d = 0; d < Dh; ++d) qx[d] = orc_widen(q, qoff + d, qk_dtype);
           /* the row sees keys 0..p (causal mask, Eq. 6) */
           for (int64_t j = 0; j <= p; ++j) {
-            const int64_t koff = (((int64_t)l * T_total + tok0 + j) * Hkv + kv) * Dh;
             double acc = 0.0;
-            for (int d = 0; d < Dh; ++d)
-              acc += orc_widen(q, qoff + d, qk_dtype) * orc_widen(k, koff + d, qk_dtype);
+            for (int d = 0; d < Dh; ++d) acc += qx[d] * kx[j * Dh + d];
             logit[j] = scale * acc;
           }
           double mx = -INFINITY;
@@ -231,6 +239,8 @@ int oracle_rows_scores(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
     }
     free(logit);
     free(s);
+    free(kx);
+    free(qx);
   }
   return (bad & 2) ? 2 : (bad & 1) ? 3 : 0;
 }

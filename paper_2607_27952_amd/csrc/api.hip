@@ -149,6 +149,24 @@ static last_status check_select(int32_t R, const int32_t *cu_vis_h, int32_t Dv, 
 
 static bool aligned(const void *p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
+// Query rows of last_rows_scores: at least one per request, each between the
+// start of its request's visual span and the last token.
+static last_status check_rows(const last_batch *b, const int32_t *cu_rows_h, const int32_t *row_pos_h) {
+  if (!csr_ok(cu_rows_h, b->R, 1) || !row_pos_h) return LAST_ERR_INVALID;
+  for (int32_t r = 0; r < b->R; ++r) {
+    const int64_t P = (int64_t)b->cu_seqlens_h[r + 1] - b->cu_seqlens_h[r];
+    for (int32_t m = cu_rows_h[r]; m < cu_rows_h[r + 1]; ++m)
+      if (row_pos_h[m] < b->vis_start_h[r] || row_pos_h[m] >= P) return LAST_ERR_INVALID;
+  }
+  return LAST_OK;
+}
+
+static bool one_row_each(const last_batch *b, const int32_t *cu_rows_h) {
+  for (int32_t r = 0; r < b->R; ++r)
+    if (cu_rows_h[r + 1] - cu_rows_h[r] != 1) return false;
+  return true;
+}
+
 }  // namespace last
 
 using namespace last;
@@ -176,7 +194,61 @@ last_status last_token_scores(const last_batch *b, const void *q, const void *k,
   if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
   const ScoreWs w = carve_score_ws(ws, b, p, &need);
   const float scale = b->softmax_scale > 0.f ? b->softmax_scale : 1.0f / sqrtf((float)b->Dh);
-  const hipError_t e = launch_scores(b, p, w, q, k, scores, attn_rows, scale, (hipStream_t)stream);
+  const hipError_t e = launch_scores(b, p, w, q, k, nullptr, scores, attn_rows, scale, (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+int32_t last_source_rows(last_source src, int32_t q_begin, int32_t q_end, int32_t *pos_h) {
+  if (q_begin < 0 || q_end <= q_begin || !pos_h) return -1;
+  const int32_t M = q_end - q_begin;
+  switch (src) {
+    case LAST_SRC_LAST: pos_h[0] = q_end - 1; return 1;
+    case LAST_SRC_FIRST: pos_h[0] = q_begin; return 1;
+    case LAST_SRC_MIDDLE: pos_h[0] = q_begin + (M - 1) / 2; return 1;   // q_ceil(M/2), 1-based
+    case LAST_SRC_ALL_MEAN:
+      for (int32_t m = 0; m < M; ++m) pos_h[m] = q_begin + m;
+      return M;
+  }
+  return -1;
+}
+
+size_t last_rows_scores_workspace(const last_batch *b, const int32_t *cu_rows_h, const int32_t *row_pos_h) {
+  if (check_batch(b) != LAST_OK || check_rows(b, cu_rows_h, row_pos_h) != LAST_OK) return 0;
+  size_t bytes = 0;
+  if (one_row_each(b, cu_rows_h)) {
+    const ScorePlan p = make_score_plan(b, row_pos_h);
+    carve_score_ws(nullptr, b, p, &bytes);
+  } else {
+    const RowsPlan p = make_rows_plan(b, cu_rows_h, row_pos_h);
+    carve_rows_ws(nullptr, b, p, &bytes);
+  }
+  return bytes;
+}
+
+last_status last_rows_scores(const last_batch *b, const int32_t *cu_rows, const int32_t *cu_rows_h,
+                             const int32_t *row_pos, const int32_t *row_pos_h, const void *q,
+                             const void *k, float *scores, void *ws, size_t ws_bytes, void *stream) {
+  last_status st = check_batch(b);
+  if (st != LAST_OK) return st;
+  st = check_rows(b, cu_rows_h, row_pos_h);
+  if (st != LAST_OK) return st;
+  if (!cu_rows || !row_pos || !q || !k || !scores) return LAST_ERR_INVALID;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(scores, 4)) return LAST_ERR_INVALID;
+  const size_t need = last_rows_scores_workspace(b, cu_rows_h, row_pos_h);
+  if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
+  const float scale = b->softmax_scale > 0.f ? b->softmax_scale : 1.0f / sqrtf((float)b->Dh);
+  hipError_t e;
+  size_t used = 0;
+  if (one_row_each(b, cu_rows_h)) {
+    // one row per request: q is [G][R][Hq][Dh], the streamed single-row kernels
+    const ScorePlan p = make_score_plan(b, row_pos_h);
+    const ScoreWs w = carve_score_ws(ws, b, p, &used);
+    e = launch_scores(b, p, w, q, k, row_pos, scores, nullptr, scale, (hipStream_t)stream);
+  } else {
+    const RowsPlan p = make_rows_plan(b, cu_rows_h, row_pos_h);
+    const RowsWs w = carve_rows_ws(ws, b, p, &used);
+    e = launch_rows(b, p, w, cu_rows, row_pos, q, k, scores, scale, (hipStream_t)stream);
+  }
   return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
 }
 

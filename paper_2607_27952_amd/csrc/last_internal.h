@@ -57,11 +57,43 @@ struct ScoreWs {
   float *mass;      // [R] total visual mass sum_{l,h} V / Z
 };
 
-ScorePlan make_score_plan(const last_batch *b);
+// row_pos (nullable, one entry per request): score the causal row at that
+// position instead of the last token's; the row sees keys 0 .. row_pos[r].
+ScorePlan make_score_plan(const last_batch *b, const int32_t *row_pos_h = nullptr);
 ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t *bytes);
 hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
-                         const void *q, const void *k, float *scores, float *attn_rows,
-                         float scale, hipStream_t s);
+                         const void *q, const void *k, const int32_t *row_pos, float *scores,
+                         float *attn_rows, float scale, hipStream_t s);
+
+// ------------------------------------------------ several rows per request
+// Query rows are taken 32 at a time (one matrix-core tile per wave), a block
+// of kRowWaves waves forms a row group; keys go in chunks of kRowChunk.
+constexpr int kRowWaves = 4;
+constexpr int kRowChunk = 1024;
+
+struct RowsPlan {
+  int64_t M_total, N_total, T_total;
+  int64_t items1, items2;   // (request, row group, key chunk) and (.., visual chunk) work items
+  int64_t SC_total;         // per layer: sum_r Hq * M_r * key chunks_r row statistics
+  int32_t RG_max;           // most row groups of any request
+};
+
+struct RowsWs {
+  int32_t *off1, *off2;     // [R+1] item prefixes per request
+  int64_t *sc_off;          // [R+1] statistics prefixes per request
+  int4 *rinfo;              // [R] (key chunks, visual chunks, row groups, last row position)
+  int4 *items1, *items2;    // (request, row group, chunk, 0)
+  float4 *stats;            // [G][SC_total] (max, sum exp, visual sum exp, 0) per row and chunk
+  float2 *rowstat;          // [G][Hq][M_total] (max, 1 / sum exp) per row
+  float *mass;              // [R] sum over rows of visual mass V / Z
+  float *part;              // [G][Hkv][RG_max][N_total] visual probability sums per row group
+};
+
+RowsPlan make_rows_plan(const last_batch *b, const int32_t *cu_rows_h, const int32_t *row_pos_h);
+RowsWs carve_rows_ws(void *ws, const last_batch *b, const RowsPlan &p, size_t *bytes);
+hipError_t launch_rows(const last_batch *b, const RowsPlan &p, const RowsWs &w,
+                       const int32_t *cu_rows, const int32_t *row_pos, const void *q,
+                       const void *k, float *scores, float scale, hipStream_t s);
 
 // ------------------------------------------------------------ selection
 constexpr int kGramTile = 128;       // Gram tile edge (rows of X per side)
@@ -198,6 +230,28 @@ __device__ __forceinline__ unsigned long long wave_max_key(uint32_t hi, uint32_t
   else
     ml = wave_max_u32(hi == mh ? lo : 0u);
   return ((unsigned long long)mh << 32) | ml;
+}
+
+// Exclusive scan of one int per thread over the block; returns the prefix and
+// writes the block total. `sh` needs blockDim/64 ints.
+__device__ inline int block_exclusive_scan(int v, int *sh, int *total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[wave] = x;
+  __syncthreads();
+  int before = 0, tot = 0;
+  for (int w = 0; w < nw; ++w) {
+    const int s = sh[w];
+    if (w < wave) before += s;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return before + x - v;
 }
 
 }  // namespace last_dev

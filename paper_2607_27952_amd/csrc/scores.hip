@@ -85,30 +85,9 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
                                          c, false);
 }
 
-// Exclusive scan of one int per thread over the block; returns the prefix and
-// writes the block total. `sh` needs blockDim/64 ints.
-__device__ int block_exclusive_scan(int v, int *sh, int *total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  int x = v;
-  for (int o = 1; o < 64; o <<= 1) {
-    int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
-  }
-  if (lane == 63) sh[wave] = x;
-  __syncthreads();
-  int before = 0, tot = 0;
-  for (int w = 0; w < nw; ++w) {
-    const int s = sh[w];
-    if (w < wave) before += s;
-    tot += s;
-  }
-  __syncthreads();
-  *total = tot;
-  return before + x - v;
-}
-
 __global__ __launch_bounds__(kThreads) void k_score_plan(
-    const int32_t *__restrict__ cu_seqlens, const int32_t *__restrict__ cu_vis, int R, int CH,
+    const int32_t *__restrict__ cu_seqlens, const int32_t *__restrict__ cu_vis,
+    const int32_t *__restrict__ row_pos, int R, int CH,
     int SL, int64_t C_cap, int64_t S_cap, int32_t *__restrict__ chunk_off,
     int32_t *__restrict__ chunk_req, int32_t *__restrict__ slice_off,
     int32_t *__restrict__ slice_req) {
@@ -118,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void k_score_plan(
     const int r = base + (int)threadIdx.x;
     int nc = 0, ns = 0;
     if (r < R) {
-      const int P = cu_seqlens[r + 1] - cu_seqlens[r];
+      const int P = row_pos ? row_pos[r] + 1 : cu_seqlens[r + 1] - cu_seqlens[r];
       const int N = cu_vis[r + 1] - cu_vis[r];
       nc = (P + CH - 1) / CH;
       ns = (N + SL - 1) / SL;
@@ -211,9 +190,10 @@ template <typename T, int DH, int GQ>
 __global__ __launch_bounds__(kThreads) void k_score_stream(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req, int R, int Hq,
-    int Hkv, int CH, int64_t C_total, int64_t T_total, float scale,
-    float *__restrict__ vlog, float4 *__restrict__ stats, float *__restrict__ rows) {
+    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req,
+    const int32_t *__restrict__ row_pos, int R, int Hq, int Hkv, int CH, int64_t C_total,
+    int64_t T_total, float scale, float *__restrict__ vlog, float4 *__restrict__ stats,
+    float *__restrict__ rows) {
   using RS = RowShape<T, DH>;
   extern __shared__ float s_log[];          // [CH][Hq]
   __shared__ float4 s_part[kThreads];
@@ -223,7 +203,8 @@ __global__ __launch_bounds__(kThreads) void k_score_stream(
   const int r = chunk_req[c];
   const int c_local = (int)(c - chunk_off[r]);
   const int64_t tok0 = cu_seqlens[r];
-  const int P = cu_seqlens[r + 1] - (int)tok0;
+  // the scored row sits at position P - 1 and sees keys 0 .. P - 1 (causal)
+  const int P = row_pos ? row_pos[r] + 1 : cu_seqlens[r + 1] - (int)tok0;
   const int t_begin = c_local * CH;
   const int nt = min(P - t_begin, CH);
   if (nt <= 0) return;
@@ -318,9 +299,10 @@ template <typename T, int DH, int GM>
 __global__ __launch_bounds__(kThreads) void k_score_partial(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req, int R, int Hq,
-    int Hkv, int g, int HG, int CH, int64_t C_total, int64_t T_total, float scale,
-    float *__restrict__ vlog, float4 *__restrict__ stats, float *__restrict__ rows) {
+    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req,
+    const int32_t *__restrict__ row_pos, int R, int Hq, int Hkv, int g, int HG, int CH,
+    int64_t C_total, int64_t T_total, float scale, float *__restrict__ vlog,
+    float4 *__restrict__ stats, float *__restrict__ rows) {
   using RS = RowShape<T, DH>;
   extern __shared__ float s_logit[];   // [GM][CH]
   __shared__ float s_red[kWaves][GM];
@@ -335,7 +317,7 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
   const int r = chunk_req[c];
   const int c_local = (int)(c - chunk_off[r]);
   const int64_t tok0 = cu_seqlens[r];
-  const int P = cu_seqlens[r + 1] - (int)tok0;
+  const int P = row_pos ? row_pos[r] + 1 : cu_seqlens[r + 1] - (int)tok0;
   const int t_begin = c_local * CH;
   const int nt = min(P - t_begin, CH);
   if (nt <= 0) return;
@@ -521,6 +503,7 @@ __global__ __launch_bounds__(kMergeThreads) void k_score_merge(
 __global__ __launch_bounds__(kThreads) void k_score_finalize(
     const float *__restrict__ vlog, const float2 *__restrict__ rowstat,
     const float *__restrict__ mass, const int32_t *__restrict__ cu_vis,
+    const int32_t *__restrict__ vis_start, const int32_t *__restrict__ row_pos,
     const int32_t *__restrict__ slice_off, const int32_t *__restrict__ slice_req, int G, int Hq,
     int64_t N_total, int SL, float *__restrict__ scores) {
   const int GH = G * Hq;
@@ -534,7 +517,13 @@ __global__ __launch_bounds__(kThreads) void k_score_finalize(
   const int64_t n0 = cu_vis[r];
   const int N_r = cu_vis[r + 1] - (int)n0;
   const int end = min(N_r, (sl + 1) * SL);
+  // a row before the end of the visual span sees only the tokens up to itself
+  const int seen = row_pos ? min(N_r, row_pos[r] - vis_start[r] + 1) : N_r;
   for (int i = sl * SL + threadIdx.x; i < end; i += kThreads) {
+    if (i >= seen) {
+      scores[n0 + i] = 0.f;
+      continue;
+    }
     // (layer, head) pairs p = l * Hq + h in increasing order; layer l's logits
     // of this token are Hq contiguous floats
     float acc = 0.f;
@@ -577,8 +566,8 @@ __global__ __launch_bounds__(kThreads) void k_rows_finalize(
 
 template <typename T, int DH>
 hipError_t launch_stream_dh(const last_batch *b, const last::ScorePlan &p, const last::ScoreWs &w,
-                            const void *q, const void *k, float *attn_rows, float scale,
-                            hipStream_t s) {
+                            const void *q, const void *k, const int32_t *row_pos, float *attn_rows,
+                            float scale, hipStream_t s) {
   const int g = b->Hq / b->Hkv;
   const int64_t blocks = (int64_t)b->G * p.C_total;
   const size_t lds = (size_t)p.chunk_tokens * b->Hq * sizeof(float);
@@ -586,8 +575,8 @@ hipError_t launch_stream_dh(const last_batch *b, const last::ScorePlan &p, const
 #define LAST_LAUNCH_GQ(GQV)                                                                        \
   hipLaunchKernelGGL((k_score_stream<T, DH, GQV>), dim3((unsigned)blocks), dim3(kThreads), lds, s, \
                      (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,          \
-                     w.chunk_off, w.chunk_req, b->R, b->Hq, b->Hkv, p.chunk_tokens, p.C_total,   \
-                     p.T_total, scale, w.vlog, w.stats, attn_rows)
+                     w.chunk_off, w.chunk_req, row_pos, b->R, b->Hq, b->Hkv, p.chunk_tokens,     \
+                     p.C_total, p.T_total, scale, w.vlog, w.stats, attn_rows)
   switch (g) {
     case 1: LAST_LAUNCH_GQ(1); break;
     case 2: LAST_LAUNCH_GQ(2); break;
@@ -605,7 +594,7 @@ hipError_t launch_stream_dh(const last_batch *b, const last::ScorePlan &p, const
 template <typename T, int DH>
 hipError_t launch_partial_dh(const last_batch *b, const last::ScorePlan &p,
                              const last::ScoreWs &w, const void *q, const void *k,
-                             float *attn_rows, float scale, hipStream_t s) {
+                             const int32_t *row_pos, float *attn_rows, float scale, hipStream_t s) {
   const int g = b->Hq / b->Hkv;
   const int64_t blocks = (int64_t)b->G * p.C_total * b->Hkv * p.head_groups;
   const size_t lds = (size_t)p.g_max * p.chunk_tokens * sizeof(float);
@@ -613,7 +602,7 @@ hipError_t launch_partial_dh(const last_batch *b, const last::ScorePlan &p,
 #define LAST_LAUNCH_GM(GMV)                                                                     \
   hipLaunchKernelGGL((k_score_partial<T, DH, GMV>), dim3((unsigned)blocks), dim3(kThreads), lds, \
                      s, (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,      \
-                     w.chunk_off, w.chunk_req, b->R, b->Hq, b->Hkv, g, p.head_groups,           \
+                     w.chunk_off, w.chunk_req, row_pos, b->R, b->Hq, b->Hkv, g, p.head_groups,  \
                      p.chunk_tokens, p.C_total, p.T_total, scale, w.vlog, w.stats,               \
                      attn_rows)
   switch (p.g_max) {
@@ -630,7 +619,7 @@ hipError_t launch_partial_dh(const last_batch *b, const last::ScorePlan &p,
 
 namespace last {
 
-ScorePlan make_score_plan(const last_batch *b) {
+ScorePlan make_score_plan(const last_batch *b, const int32_t *row_pos_h) {
   ScorePlan p{};
   const int g = b->Hq / b->Hkv;
   p.T_total = b->cu_seqlens_h[b->R];
@@ -660,7 +649,7 @@ ScorePlan make_score_plan(const last_batch *b) {
   p.C_total = 0;
   p.S_total = 0;
   for (int r = 0; r < b->R; ++r) {
-    const int64_t P = b->cu_seqlens_h[r + 1] - b->cu_seqlens_h[r];
+    const int64_t P = row_pos_h ? (int64_t)row_pos_h[r] + 1 : b->cu_seqlens_h[r + 1] - b->cu_seqlens_h[r];
     const int64_t N = b->cu_vis_h[r + 1] - b->cu_vis_h[r];
     p.C_total += (P + p.chunk_tokens - 1) / p.chunk_tokens;
     p.S_total += (N + p.slice_tokens - 1) / p.slice_tokens;
@@ -686,26 +675,26 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
 int score_max_pairs() { return kMaxPairs; }
 
 hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
-                         const void *q, const void *k, float *scores, float *attn_rows,
-                         float scale, hipStream_t s) {
+                         const void *q, const void *k, const int32_t *row_pos, float *scores,
+                         float *attn_rows, float scale, hipStream_t s) {
   launch_begin("score_plan", s);
   hipLaunchKernelGGL(k_score_plan, dim3(1), dim3(kThreads), 0, s, b->cu_seqlens, b->cu_vis,
-                     b->R, p.chunk_tokens, p.slice_tokens, p.C_total, p.S_total, w.chunk_off,
+                     row_pos, b->R, p.chunk_tokens, p.slice_tokens, p.C_total, p.S_total, w.chunk_off,
                      w.chunk_req, w.slice_off, w.slice_req);
   hipError_t e = launch_end(s);
   if (e != hipSuccess) return e;
 
   const bool bf = b->qk_dtype == LAST_BF16;
   if (p.stream)
-    e = bf ? (b->Dh == 64 ? launch_stream_dh<uint16_t, 64>(b, p, w, q, k, attn_rows, scale, s)
-                          : launch_stream_dh<uint16_t, 128>(b, p, w, q, k, attn_rows, scale, s))
-           : (b->Dh == 64 ? launch_stream_dh<float, 64>(b, p, w, q, k, attn_rows, scale, s)
-                          : launch_stream_dh<float, 128>(b, p, w, q, k, attn_rows, scale, s));
+    e = bf ? (b->Dh == 64 ? launch_stream_dh<uint16_t, 64>(b, p, w, q, k, row_pos, attn_rows, scale, s)
+                          : launch_stream_dh<uint16_t, 128>(b, p, w, q, k, row_pos, attn_rows, scale, s))
+           : (b->Dh == 64 ? launch_stream_dh<float, 64>(b, p, w, q, k, row_pos, attn_rows, scale, s)
+                          : launch_stream_dh<float, 128>(b, p, w, q, k, row_pos, attn_rows, scale, s));
   else
-    e = bf ? (b->Dh == 64 ? launch_partial_dh<uint16_t, 64>(b, p, w, q, k, attn_rows, scale, s)
-                          : launch_partial_dh<uint16_t, 128>(b, p, w, q, k, attn_rows, scale, s))
-           : (b->Dh == 64 ? launch_partial_dh<float, 64>(b, p, w, q, k, attn_rows, scale, s)
-                          : launch_partial_dh<float, 128>(b, p, w, q, k, attn_rows, scale, s));
+    e = bf ? (b->Dh == 64 ? launch_partial_dh<uint16_t, 64>(b, p, w, q, k, row_pos, attn_rows, scale, s)
+                          : launch_partial_dh<uint16_t, 128>(b, p, w, q, k, row_pos, attn_rows, scale, s))
+           : (b->Dh == 64 ? launch_partial_dh<float, 64>(b, p, w, q, k, row_pos, attn_rows, scale, s)
+                          : launch_partial_dh<float, 128>(b, p, w, q, k, row_pos, attn_rows, scale, s));
   if (e != hipSuccess) return e;
 
   launch_begin("score_merge", s);
@@ -716,7 +705,7 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
 
   launch_begin("score_finalize", s);
   hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog,
-                     w.rowstat, w.mass, b->cu_vis, w.slice_off, w.slice_req, b->G, b->Hq, p.N_total,
+                     w.rowstat, w.mass, b->cu_vis, b->vis_start, row_pos, w.slice_off, w.slice_req, b->G, b->Hq, p.N_total,
                      p.slice_tokens, scores);
   e = launch_end(s);
   if (e != hipSuccess || !attn_rows) return e;

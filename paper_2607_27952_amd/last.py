@@ -21,8 +21,10 @@ LIB_PATH = os.path.join(PKG, "liblast.so")
 LAST_OK, LAST_ERR_INVALID, LAST_ERR_UNSUPPORTED, LAST_ERR_WORKSPACE, LAST_ERR_DEVICE = range(5)
 LAST_F32, LAST_BF16 = 0, 1
 KCENTER, TOPK = 0, 1
+SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
 
-EXPORTS = ("last_token_scores_workspace", "last_token_scores", "diverse_select_workspace",
+EXPORTS = ("last_token_scores_workspace", "last_token_scores", "last_source_rows",
+           "last_rows_scores_workspace", "last_rows_scores", "diverse_select_workspace",
            "diverse_select", "gather_kept", "last_budget", "last_status_string", "last_version",
            "last_profile_enable", "last_profile_collect", "last_profile_reset",
            "last_profile_count", "last_profile_kernel")
@@ -59,6 +61,12 @@ def lib():
         L.last_token_scores_workspace.restype = SZ
         L.last_token_scores.argtypes = [ctypes.POINTER(_Batch), P, P, P, P, P, SZ, P]
         L.last_token_scores.restype = I32
+        L.last_source_rows.argtypes = [I32, I32, I32, P]
+        L.last_source_rows.restype = I32
+        L.last_rows_scores_workspace.argtypes = [ctypes.POINTER(_Batch), P, P]
+        L.last_rows_scores_workspace.restype = SZ
+        L.last_rows_scores.argtypes = [ctypes.POINTER(_Batch), P, P, P, P, P, P, P, P, SZ, P]
+        L.last_rows_scores.restype = I32
         L.diverse_select_workspace.argtypes = [I32, P, I32, I32, I32]
         L.diverse_select_workspace.restype = SZ
         L.diverse_select.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
@@ -186,6 +194,56 @@ def token_scores(batch: Batch, q: torch.Tensor, k: torch.Tensor, scores=None, at
     if st != LAST_OK:
         raise LastError(st, "last_token_scores")
     return (scores, attn_rows) if want_rows else scores
+
+
+def source_rows(src: int, q_begin: int, q_end: int) -> np.ndarray:
+    """last_source_rows (Table 4): positions of the rows of attention source `src`."""
+    pos = np.zeros(max(1, int(q_end) - int(q_begin)), np.int32)
+    n = lib().last_source_rows(int(src), int(q_begin), int(q_end), _ptr(pos))
+    if n < 0:
+        raise ValueError("empty query or unknown attention source")
+    return pos[:n].copy()
+
+
+@dataclass
+class Rows:
+    """Query rows per request (CSR): host and device copies."""
+    cu_rows_h: np.ndarray
+    row_pos_h: np.ndarray
+    cu_rows: torch.Tensor
+    row_pos: torch.Tensor
+
+    @staticmethod
+    def make(cu_rows, row_pos, device="cuda") -> "Rows":
+        cr, rp = _i32_host(cu_rows), _i32_host(row_pos)
+        return Rows(cu_rows_h=cr, row_pos_h=rp, cu_rows=_i32_dev(cr, device), row_pos=_i32_dev(rp, device))
+
+
+def rows_scores_workspace(batch: Batch, rows: Rows, qk_dtype=torch.bfloat16) -> int:
+    code = LAST_BF16 if qk_dtype == torch.bfloat16 else LAST_F32
+    b = batch.struct(code)
+    return int(lib().last_rows_scores_workspace(ctypes.byref(b), _ptr(rows.cu_rows_h), _ptr(rows.row_pos_h)))
+
+
+def rows_scores(batch: Batch, rows: Rows, q: torch.Tensor, k: torch.Tensor, scores=None, ws=None,
+                stream=None):
+    """last_rows_scores (Table 4 sources): scores [N_total] fp32 from the causal rows
+    at rows.row_pos; q is [G][M_total][Hq][Dh]."""
+    code = _dtype_code(q)
+    if k.dtype != q.dtype:
+        raise TypeError("q and k must share a dtype")
+    b = batch.struct(code)
+    if scores is None:
+        scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
+    need = int(lib().last_rows_scores_workspace(ctypes.byref(b), _ptr(rows.cu_rows_h), _ptr(rows.row_pos_h)))
+    if ws is None:
+        ws = _workspace(need, q.device)
+    st = lib().last_rows_scores(ctypes.byref(b), _ptr(rows.cu_rows), _ptr(rows.cu_rows_h), _ptr(rows.row_pos),
+                                _ptr(rows.row_pos_h), _ptr(q), _ptr(k), _ptr(scores), _ptr(ws), ws.numel(),
+                                _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "last_rows_scores")
+    return scores
 
 
 def select_workspace(cu_vis_h, Dv: int, f_dtype=torch.bfloat16, mode: int = KCENTER) -> int:

@@ -187,3 +187,53 @@ def test_gather_rejects_bad_arguments():
     assert L.gather_kept(2, 64, 2, dev.p, dev.p, cv.ctypes.data, dev.p, dev.p, bad.ctypes.data, out.p, None) == last.LAST_ERR_INVALID
     assert L.gather_kept(2, 64, 2, None, dev.p, cv.ctypes.data, dev.p, dev.p, ck.ctypes.data, out.p, None) == last.LAST_ERR_INVALID
     assert out.untouched()
+
+
+# ------------------------------------------------- attention sources (Table 4)
+
+def _rows_call(b, cu_rows, row_pos, ws_bytes=1 << 30):
+    cr = None if cu_rows is None else np.asarray(cu_rows, np.int32)
+    rp = None if row_pos is None else np.asarray(row_pos, np.int32)
+    dev, q, k, out, ws = Fake(), Fake(), Fake(), Fake(), Fake()
+    st = last.lib().last_rows_scores(ctypes.byref(b), dev.p, None if cr is None else cr.ctypes.data, dev.p,
+                                     None if rp is None else rp.ctypes.data, q.p, k.p, out.p, ws.p,
+                                     ws_bytes, None)
+    assert out.untouched() and ws.untouched()
+    return st
+
+
+def test_rows_reject_bad_row_sets():
+    b, keep = _batch(P=(20, 30), N=(10, 12), vis=(2, 3))
+    E = last.LAST_ERR_INVALID
+    assert _rows_call(b, [0, 1, 2], [1, 29]) == E          # row before the visual span (sees no visual token)
+    assert _rows_call(b, [0, 1, 2], [20, 29]) == E         # row past the last token
+    assert _rows_call(b, [0, 0, 2], [5, 29]) == E          # a request without rows
+    assert _rows_call(b, [0, 2, 3], [5, 19, 30]) == E      # second request: row past its last token
+    assert _rows_call(b, None, [5, 29]) == E
+    assert _rows_call(b, [0, 1, 2], None) == E
+    b.Dh = 96
+    assert _rows_call(b, [0, 1, 2], [5, 29]) == last.LAST_ERR_UNSUPPORTED
+
+
+def test_rows_workspace_query_and_small_workspace():
+    b, keep = _batch(P=(20, 30), N=(10, 12), vis=(2, 3))
+    L = last.lib()
+    one = np.array([0, 1, 2], np.int32), np.array([19, 29], np.int32)
+    many = np.array([0, 3, 5], np.int32), np.array([2, 12, 19, 15, 29], np.int32)
+    for cr, rp in (one, many):
+        need = L.last_rows_scores_workspace(ctypes.byref(b), cr.ctypes.data, rp.ctypes.data)
+        assert need > 0
+        assert _rows_call(b, cr, rp, ws_bytes=need - 1) == last.LAST_ERR_WORKSPACE
+    bad = np.array([0, 3, 5], np.int32), np.array([2, 12, 19, 15, 30], np.int32)
+    assert L.last_rows_scores_workspace(ctypes.byref(b), bad[0].ctypes.data, bad[1].ctypes.data) == 0
+
+
+def test_source_rows_match_golden():
+    import json
+    gold = json.load(open(os.path.join(ROOT, "tests", "golden", "source_rows.json")))
+    for case in gold["cases"]:
+        for name, code in gold["sources"].items():
+            assert last.source_rows(code, case["q_begin"], case["q_end"]).tolist() == case[name], (name, case)
+    for qb, qe, src in ((5, 5, 0), (-1, 3, 1), (0, 4, 9)):
+        with pytest.raises(ValueError):
+            last.source_rows(src, qb, qe)
