@@ -1,7 +1,9 @@
 """Benchmark of the LAST token-selection path on one MI355X.
 
 A step is one pass of the whole path over one batch that is already resident
-in HBM: last_token_scores -> diverse_select (k-center) -> gather_kept.
+in HBM: last_token_scores -> diverse_select (k-center) -> gather_kept. With
+--source first|middle|all_mean the scores come from those query rows instead
+(last_rows_scores, the attention sources of the paper's Table 4).
 
 Default workload: the LLaVA-1.5-shaped batch (64 requests of 576 visual +
 64 text tokens, 2 guidance layers of 32 heads, head_dim 128, bf16; budget
@@ -42,6 +44,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="c2_llava15")
     ap.add_argument("--budget", type=int, default=None)
+    ap.add_argument("--source", default="last", choices=("last", "first", "middle", "all_mean"),
+                    help="attention rows the scores come from (Table 4)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time for the oracle sample")
@@ -77,13 +81,47 @@ def gram_flops(n, dv):
     return diag, off
 
 
-def kernel_work(wl):
-    """Algorithmic bytes / flops per launch of each kernel, and its bound."""
+HBM_BYTES_PER_S = HBM_PEAK_GBS * 1e9
+MFMA_FLOPS_PER_S = MFMA_BF16_PEAK_TFLOPS * 1e12
+
+
+def rows_work(wl, cu_rows, row_pos):
+    """Algorithmic work of the attention-source passes. Pass 1 reads every key up
+    to the last row of its request once and forms one logit per (row, head, key
+    the row sees); pass 2 reads the visual keys the rows see and forms their
+    logits again. A pass is bound by whichever of HBM bytes and MFMA flops takes
+    longer at the peaks."""
+    elt = 2 if wl.qk_dtype == "bf16" else 4
+    keys1 = keys2 = logits1 = logits2 = 0
+    for r in range(wl.R):
+        pos = np.asarray(row_pos[int(cu_rows[r]):int(cu_rows[r + 1])], np.int64)
+        v0, n = int(wl.vis_start[r]), wl.n(r)
+        keys1 += int(pos.max()) + 1
+        keys2 += min(n, int(pos.max()) - v0 + 1)
+        logits1 += int(np.sum(pos + 1))
+        logits2 += int(np.sum(np.clip(pos - v0 + 1, 0, n)))
+    q_bytes = wl.G * int(cu_rows[-1]) * wl.Hq * wl.Dh * elt
+    b1 = wl.G * keys1 * wl.Hkv * wl.Dh * elt + q_bytes
+    b2 = wl.G * keys2 * wl.Hkv * wl.Dh * elt + q_bytes
+    f1 = 2.0 * wl.G * wl.Hq * logits1 * wl.Dh
+    f2 = 2.0 * wl.G * wl.Hq * logits2 * wl.Dh
+
+    def bound(b, f):
+        return ("hbm", b) if b / HBM_BYTES_PER_S >= f / MFMA_FLOPS_PER_S else ("mfma", f)
+    return {"rows_stats": bound(b1, f1), "rows_visual": bound(b2, f2),
+            "rows_stats_bytes": b1, "rows_stats_flops": f1, "rows_visual_bytes": b2, "rows_visual_flops": f2}
+
+
+def kernel_work(wl, row_pos=None):
+    """Algorithmic bytes / flops per launch of each kernel, and its bound.
+    row_pos: one scored row per request (a single-row attention source), whose
+    causal prefix is what the score pass reads; None for the last token."""
     elt = 2 if wl.qk_dtype == "bf16" else 4
     felt = 2 if wl.f_dtype == "bf16" else 4
     n = np.diff(wl.cu_vis).astype(np.int64)
     kk = np.diff(wl.cu_keep).astype(np.int64)
-    k_bytes = wl.G * wl.T_total * wl.Hkv * wl.Dh * elt
+    tokens = wl.T_total if row_pos is None else int(np.sum(np.asarray(row_pos, np.int64) + 1))
+    k_bytes = wl.G * tokens * wl.Hkv * wl.Dh * elt
     q_bytes = wl.G * wl.R * wl.Hq * wl.Dh * elt
     vlog = wl.G * wl.Hq * wl.N_total * 4
     g_diag, g_off = gram_flops(n, wl.Dv)
@@ -185,7 +223,22 @@ def main():
     order = torch.empty(wl.K_total, dtype=torch.int32, device=dev)
     gains = torch.empty(wl.K_total, dtype=torch.float32, device=dev)
     out = torch.empty((wl.K_total, wl.Dv), dtype=dw.feats.dtype, device=dev)
-    ws_s = torch.empty(last.token_scores_workspace(b, dw.q.dtype), dtype=torch.uint8, device=dev)
+    rows = q_rows = None
+    if args.source != "last":
+        qr = W.query_rows(wl)
+        src = {"first": last.SRC_FIRST, "middle": last.SRC_MIDDLE, "all_mean": last.SRC_ALL_MEAN}[args.source]
+        counts, pos, qs = [], [], []
+        for r in range(wl.R):
+            p = last.source_rows(src, int(qr.q_begin[r]), int(qr.q_end[r]))
+            counts.append(len(p))
+            pos.extend(p.tolist())
+            qs.append(qr.rows(r)[:, p - int(qr.q_begin[r])])
+        rows = last.Rows.make(np.concatenate([[0], np.cumsum(counts)]), pos, device=dev)
+        q_rows = last.to_torch(np.ascontiguousarray(np.concatenate(qs, axis=1)), wl.qk_dtype, dev)
+        ws_s = torch.empty(last.rows_scores_workspace(b, rows, dw.q.dtype), dtype=torch.uint8, device=dev)
+        log(f"[bench] scores from the {args.source} rows: {int(rows.cu_rows_h[-1])} query rows")
+    else:
+        ws_s = torch.empty(last.token_scores_workspace(b, dw.q.dtype), dtype=torch.uint8, device=dev)
     ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8, device=dev)
 
     if args.copy_calibration_mib > 0:
@@ -199,7 +252,10 @@ def main():
         del src, dst
 
     def step():
-        last.token_scores(b, dw.q, dw.k, scores=scores, ws=ws_s)
+        if rows is None:
+            last.token_scores(b, dw.q, dw.k, scores=scores, ws=ws_s)
+        else:
+            last.rows_scores(b, rows, q_rows, dw.k, scores=scores, ws=ws_s)
         last.diverse_select(scores, dw.feats, wl.cu_vis, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep,
                             kept=kept, order=order, gains=gains, ws=ws_k)
         last.gather_kept(dw.feats, wl.cu_vis, kept, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep, out=out)
@@ -232,7 +288,11 @@ def main():
     elapsed_prof, step_ms_prof, prof = timed(True)
     ms_per_step = elapsed / args.steps * 1e3
 
-    work = kernel_work(wl)
+    single = rows is not None and int(rows.cu_rows_h[-1]) == wl.R
+    work = kernel_work(wl, rows.row_pos_h if single else None)
+    if rows is not None and not single:
+        work.update({k: v for k, v in rows_work(wl, rows.cu_rows_h, rows.row_pos_h).items()
+                     if k in ("rows_stats", "rows_visual")})
     kernels = {}
     for name, (launches, total_ms) in prof.items():
         kernels[name] = {"launches": launches, "avg_ms": round(total_ms / max(launches, 1), 5),
@@ -244,7 +304,7 @@ def main():
     dominant = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])[0]
     main_roof = next((r for r in rooflines if r["kernel"] == dominant), None)
     if main_roof is not None:
-        tr = traffic_for(dominant, args.workload)
+        tr = traffic_for(dominant, args.workload if args.source == "last" else f"{args.workload}_{args.source}")
         main_roof = {k: main_roof[k] for k in ("bound", "achieved", "peak", "unit", "frac")} | {
             "traffic": tr, "kernel": dominant}
     # the paper's own similarity work (Sec. 3.4: one x_j^T X product per pick,
@@ -260,7 +320,7 @@ def main():
                       "gram_ms_per_step": round(gram_ms, 4),
                       "tflops_on_paper_work": round(paper_flops / (gram_ms * 1e-3) / 1e12, 2),
                       "tflops_on_gram_work": round(exec_flops / (gram_ms * 1e-3) / 1e12, 2)}
-    score_ms = sum(kernels[k]["ms_per_step"] for k in kernels if k.startswith("score"))
+    score_ms = sum(kernels[k]["ms_per_step"] for k in kernels if k.startswith("score") or k.startswith("rows"))
     select_ms = sum(kernels[k]["ms_per_step"] for k in kernels
                     if k in ("select_plan", "sqnorm", "gram_diag", "gram", "greedy", "topk"))
     gather_ms = kernels.get("gather", {}).get("ms_per_step", 0.0)
@@ -278,9 +338,13 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": describe(wl, args.budget), "requests": wl.R, "visual_tokens": wl.N_total,
-                   "kept_tokens": wl.K_total, "arithmetic": "bf16 inputs, fp32 FMA score pass, bf16 MFMA "
-                   "Gram with fp32 partial sums folded into fp64, fp32 objective"},
+        "config": {"workload": describe(wl, args.budget) + ("" if args.source == "last" else
+                                                             f"; scores from the {args.source} query rows"),
+                   "requests": wl.R, "visual_tokens": wl.N_total,
+                   "kept_tokens": wl.K_total, "arithmetic": (
+                       "bf16 inputs, " + ("fp32 FMA score pass" if args.source != "all_mean" else
+                                          "bf16 MFMA score passes with fp32 accumulation")
+                       + ", bf16 MFMA Gram with fp32 partial sums folded into fp64, fp32 objective")},
         "visual_tokens_scored_per_s": round(wl.N_total / (score_ms * 1e-3), 1) if score_ms > 0 else None,
         "p50_select_latency_ms": round(float(np.median(step_ms)), 4),
         "p90_select_latency_ms": round(float(np.percentile(step_ms, 90)), 4),

@@ -36,3 +36,24 @@ def test_multi_gpu_request_exits():
     import subprocess
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True, text=True)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_rows_work_counts_causal_prefixes():
+    wl = W.tiny(4, R=2, G=2, Hq=8, Hkv=2, Dh=64, n_range=(50, 80), t_range=(10, 20), Dv=64)
+    elt = 2 if wl.qk_dtype == W.BF16 else 4
+    # one row at the last token per request: pass 1 reads every key, pass 2 every visual key
+    cu = np.arange(wl.R + 1)
+    pos = np.array([wl.p(r) - 1 for r in range(wl.R)])
+    w = bench.rows_work(wl, cu, pos)
+    q_bytes = wl.G * wl.R * wl.Hq * wl.Dh * elt
+    assert w["rows_stats_bytes"] == wl.G * wl.T_total * wl.Hkv * wl.Dh * elt + q_bytes
+    assert w["rows_visual_bytes"] == wl.G * wl.N_total * wl.Hkv * wl.Dh * elt + q_bytes
+    assert w["rows_stats_flops"] == 2.0 * wl.G * wl.Hq * wl.T_total * wl.Dh
+    # a row at the first visual token sees that token and everything before it
+    pos2 = np.array([[int(wl.vis_start[r]), wl.p(r) - 1] for r in range(wl.R)]).ravel()
+    w2 = bench.rows_work(wl, np.arange(0, 2 * wl.R + 1, 2), pos2)
+    assert w2["rows_visual_flops"] == 2.0 * wl.G * wl.Hq * (wl.N_total + wl.R) * wl.Dh
+    assert w2["rows_stats_flops"] == 2.0 * wl.G * wl.Hq * (wl.T_total + int(np.sum(wl.vis_start + 1))) * wl.Dh
+    # single-row sources: the score pass reads each request's causal prefix
+    kw = bench.kernel_work(wl, pos - 3)
+    assert kw["score_stream"][1] == wl.G * (wl.T_total - wl.R * 3) * wl.Hkv * wl.Dh * elt + q_bytes
