@@ -66,8 +66,10 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
                          float *attn_rows, float scale, hipStream_t s);
 
 // ------------------------------------------------ several rows per request
-// Query rows are taken 32 at a time (one matrix-core tile per wave), a block
-// of kRowWaves waves forms a row group; keys go in chunks of kRowChunk.
+// Query rows are taken 32 at a time (one matrix-core tile). A block of
+// kRowWaves waves takes RT such row tiles (a row group) and splits each stage
+// of keys among the kRowWaves / RT waves that share a row tile; RT is 4, 2 or
+// 1, from the largest request's tile count. Keys go in chunks of kRowChunk.
 constexpr int kRowWaves = 4;
 constexpr int kRowChunk = 1024;
 
@@ -76,6 +78,7 @@ struct RowsPlan {
   int64_t items1, items2;   // (request, row group, key chunk) and (.., visual chunk) work items
   int64_t SC_total;         // per layer: sum_r Hq * M_r * key chunks_r row statistics
   int32_t RG_max;           // most row groups of any request
+  int32_t RT;               // row tiles per block
 };
 
 struct RowsWs {
@@ -230,6 +233,37 @@ __device__ __forceinline__ unsigned long long wave_max_key(uint32_t hi, uint32_t
   else
     ml = wave_max_u32(hi == mh ? lo : 0u);
   return ((unsigned long long)mh << 32) | ml;
+}
+
+// LDS byte address of a __shared__ object.
+__device__ __forceinline__ uint32_t lds_u32(const void *p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void *)p);
+}
+
+// global_load_lds_dwordx4: lane i's 16 bytes at base + voff land in LDS at
+// lds + 16 i. lds: wave-uniform LDS byte address (goes to M0); base:
+// wave-uniform global address; voff: this lane's byte offset from base. The
+// load is issued from inline assembly so that the compiler does not order LDS
+// reads behind it; the caller waits for it (vm_wait) before publishing the
+// LDS it wrote.
+__device__ __forceinline__ void dma16(uint32_t lds, const void *base, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory");
+}
+__device__ __forceinline__ const void *uniform_ptr(const void *p) {
+  const uint64_t v = (uint64_t)(uintptr_t)p;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+  return (const void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ int64_t uniform_i64(int64_t v) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+// Wait until at most N vector memory loads of this wave are outstanding.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
 // Exclusive scan of one int per thread over the block; returns the prefix and

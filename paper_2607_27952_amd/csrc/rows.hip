@@ -16,22 +16,29 @@
 //   k_rows_plan      one block: per request the row groups, key chunks and
 //                    visual chunks, the work-item lists and their prefixes.
 //   k_rows_stats     one block per (layer, KV head, request, row group, key
-//                    chunk): 32 query rows per wave against the chunk's keys,
-//                    staged through LDS 64 keys at a time. Each lane keeps, for
-//                    the 16 rows of its accumulator, a running max and the sums
-//                    of exp(l - max) over all keys and over the visual ones
-//                    (one exponential per logit), merged over the wave's lanes
-//                    at the end of the chunk.
-//   k_rows_merge     one block per request: every row's chunks merged into its
-//                    max M and 1/Z, and the visual mass S = sum V / Z over the
-//                    request's rows (= sum_i s_i).
+//                    chunk): the chunk's keys staged into LDS 128 at a time by
+//                    LDS DMA, one stage in flight while the other is used;
+//                    each wave multiplies one 32-row query tile by its share of
+//                    every stage. Each lane keeps, for the 16 rows of its
+//                    accumulator, a reference r and the sums of 2^(x - r) over
+//                    all keys and over the visual ones, x being the logit in
+//                    base-2 units (the softmax scale times log2 e folded into
+//                    one multiply). The reference only moves when a logit
+//                    exceeds it by 64 (sums stay far from overflow), so a logit
+//                    costs one exponential and no rescaling.
+//   k_rows_merge     one block per request: every row's chunks merged into one
+//                    reference and 1/Z, and the visual mass S = sum V / Z over
+//                    the request's rows (= sum_i s_i).
 //   k_rows_visual    one block per (layer, KV head, request, row group, visual
-//                    chunk): the visual logits again, exp(l - M) / Z summed over
+//                    chunk): the visual logits again, 2^(x - r) / Z summed over
 //                    the block's rows per key, written per row group.
 //   k_rows_finalize  one thread per visual token: the row-group sums over
 //                    layers and KV heads in a fixed order, divided by S.
 //
-// Every reduction has a fixed order, so results are bitwise reproducible.
+// Stages whose keys every row of a wave sees (all of them except near the
+// rows themselves) skip the causal mask; stages wholly inside or outside the
+// visual span skip the per-key visual test. Every reduction has a fixed
+// order, so results are bitwise reproducible.
 #include <algorithm>
 #include <math.h>
 
@@ -44,9 +51,13 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 64 * last::kRowWaves;
-constexpr int kSub = 64;                      // keys per LDS stage: two 32-key tiles
+constexpr int kW = last::kRowWaves;
+constexpr int kThreads = 64 * kW;
+constexpr int kSub = 128;                     // keys per LDS stage: four 32-key tiles
 constexpr int kCH = last::kRowChunk;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kSlack = 64.f;                // a reference may trail its row's max by this much
+constexpr float kNoRef = -1e30f;              // the reference of a row that has seen no key yet
 static_assert(kCH % kSub == 0, "whole stages per chunk");
 
 // A key (or query) row of DH elements as 16-byte pieces. One matrix-core step
@@ -57,8 +68,7 @@ struct KeyRow {
   static constexpr int kPieces = DH * (int)sizeof(T) / 16;
   static constexpr int kSteps = kPieces / 2;
   static constexpr int kStage = kSub * kPieces;           // pieces per LDS stage
-  static constexpr int kPer = kStage / kThreads;          // pieces each thread stages
-  static_assert(kPieces >= 8 && kStage % kThreads == 0, "row shape");
+  static_assert(kPieces >= 8 && kStage % (64 * kW) == 0, "row shape");
 };
 
 // LDS slot of piece p of stage row j: the 16 rows a fragment read serves
@@ -79,38 +89,43 @@ __device__ __forceinline__ void mma_piece(f32x16_t &acc, const uint4 &a, const u
   acc = __builtin_amdgcn_mfma_f32_32x32x2f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
 }
 
+// 2^x on the transcendental unit (results below 2^-126 flush to zero).
+__device__ __forceinline__ float pow2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // In a 32 x 32 accumulator lane l holds column l % 32 and, at element v, row
 // 4 * (l / 32) + (v % 4) + 8 * (v / 4).
 __device__ __forceinline__ int acc_row(int lane, int v) { return 4 * (lane >> 5) + (v & 3) + 8 * (v >> 2); }
 
-// What a block works on: its request's rows split into the (head, row) pairs
-// of one KV head, 32 per wave.
-struct RowSet {
-  int r, m0, M, nrows, tile0;
-  bool active;   // the wave has at least one real row
+// The block's place in its request: wave w multiplies row tile w % RT of the
+// row group and key tiles w / RT, w / RT + KS, ... of every stage
+// (KS = kW / RT waves share a row tile). Row rho of a KV head's set is query
+// head kv * g + rho / M, query row rho % M.
+template <int RT>
+struct Place {
+  static constexpr int KS = kW / RT;
+  int m0, M, nrows, rt, ks, tile0;
+  bool active;   // the wave's row tile has at least one real row
+  __device__ Place(const int32_t *cu_rows, int r, int rg, int g) {
+    m0 = cu_rows[r];
+    M = cu_rows[r + 1] - m0;
+    nrows = g * M;
+    const int w = (int)(threadIdx.x >> 6);
+    rt = w % RT;
+    ks = w / RT;
+    tile0 = (rg * RT + rt) * 32;
+    active = tile0 < nrows;
+  }
 };
 
-__device__ __forceinline__ RowSet row_set(const int32_t *cu_rows, int r, int rg, int g) {
-  RowSet s;
-  s.r = r;
-  s.m0 = cu_rows[r];
-  s.M = cu_rows[r + 1] - s.m0;
-  s.nrows = g * s.M;
-  s.tile0 = (rg * last::kRowWaves + (int)(threadIdx.x >> 6)) * 32;
-  s.active = s.tile0 < s.nrows;
-  return s;
-}
-
-// Row rho of a KV head's set is query head kv * g + rho / M, row rho % M.
-template <typename T, int DH>
-__device__ __forceinline__ void load_query_frags(const T *q, const RowSet &s, int l, int kv, int g,
+template <typename T, int DH, int RT>
+__device__ __forceinline__ void load_query_frags(const T *q, const Place<RT> &pl, int l, int kv, int g,
                                                  int Hq, int64_t M_total,
                                                  uint4 (&a)[KeyRow<T, DH>::kSteps]) {
   const int lane = threadIdx.x & 63;
-  const int rho = s.tile0 + (lane & 31);
-  if (rho < s.nrows) {
-    const int hh = rho / s.M, m = rho - hh * s.M;
-    const char *qp = reinterpret_cast<const char *>(q + (((int64_t)l * M_total + s.m0 + m) * Hq + kv * g + hh) * DH);
+  const int rho = pl.tile0 + (lane & 31);
+  if (rho < pl.nrows) {
+    const int hh = rho / pl.M, m = rho - hh * pl.M;
+    const char *qp = reinterpret_cast<const char *>(q + (((int64_t)l * M_total + pl.m0 + m) * Hq + kv * g + hh) * DH);
 #pragma unroll
     for (int st = 0; st < KeyRow<T, DH>::kSteps; ++st)
       a[st] = *reinterpret_cast<const uint4 *>(qp + (2 * st + (lane >> 5)) * 16);
@@ -120,90 +135,94 @@ __device__ __forceinline__ void load_query_frags(const T *q, const RowSet &s, in
   }
 }
 
-// Keys [j0, j0 + nk) of one KV head staged in registers, then in LDS.
+// Keys [j0, j0 + nk) of one KV head into an LDS stage by LDS DMA (no
+// registers held): wave w issues instructions w, w + kW, ... of the stage,
+// each filling 64 consecutive 16-byte slots; a slot's lane fetches the piece
+// the swizzle puts there. Slots past the last key repeat key nk - 1 (callers
+// never use them). kbase must be wave-uniform.
 template <typename T, int DH>
-struct Stager {
+__device__ __forceinline__ void stage_dma(uint4 *buf, const char *kbase, int64_t kstride, int j0, int nk) {
   using KR = KeyRow<T, DH>;
-  uint4 v[KR::kPer];
-  __device__ __forceinline__ void load(const char *kbase, int64_t kstride, int j0, int nk) {
+  constexpr int NP = KR::kPieces;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int i = 0; i < KR::kPer; ++i) {
-      const int e = (int)threadIdx.x + kThreads * i, j = e / KR::kPieces, p = e - j * KR::kPieces;
-      v[i] = j < nk ? *reinterpret_cast<const uint4 *>(kbase + (int64_t)(j0 + j) * kstride + p * 16)
-                    : make_uint4(0, 0, 0, 0);
-    }
+  for (int n = 0; n < KR::kStage / 64 / kW; ++n) {
+    const int ins = wave + kW * n;
+    const int sl = ins * 64 + lane, j = sl / NP;
+    const int p = (sl % NP) ^ (NP >= 16 ? (j & 15) : ((j >> 1) & 7));
+    const uint32_t voff = (uint32_t)((int64_t)(j0 + min(j, nk - 1)) * kstride + p * 16);
+    dma16(__builtin_amdgcn_readfirstlane(lds_u32(buf + ins * 64)), kbase, voff);
   }
-  __device__ __forceinline__ void store(uint4 *buf) const {
-#pragma unroll
-    for (int i = 0; i < KR::kPer; ++i) {
-      const int e = (int)threadIdx.x + kThreads * i, j = e / KR::kPieces, p = e - j * KR::kPieces;
-      buf[slot<KR::kPieces>(j, p)] = v[i];
-    }
-  }
-};
+}
 
-// Logits of the wave's 32 rows against the stage's 64 keys (unscaled):
-// c0 for keys 0-31, c1 for keys 32-63.
+// Dots (unscaled logits) of the wave's 32 query rows with the 32 keys of
+// stage key tile kt.
 template <typename T, int DH>
-__device__ __forceinline__ void stage_dots(const uint4 *buf, const uint4 (&a)[KeyRow<T, DH>::kSteps],
-                                           f32x16_t &c0, f32x16_t &c1) {
+__device__ __forceinline__ void tile_dots(const uint4 *buf, const uint4 (&a)[KeyRow<T, DH>::kSteps], int kt,
+                                          f32x16_t &c) {
   using KR = KeyRow<T, DH>;
   const int lane = threadIdx.x & 63, col = lane & 31, half = lane >> 5;
-  c0 = f32x16_t{};
-  c1 = f32x16_t{};
+  c = f32x16_t{};
 #pragma unroll
-  for (int st = 0; st < KR::kSteps; ++st) {
-    const uint4 b0 = buf[slot<KR::kPieces>(col, 2 * st + half)];
-    const uint4 b1 = buf[slot<KR::kPieces>(32 + col, 2 * st + half)];
-    mma_piece(c0, a[st], b0, T());
-    mma_piece(c1, a[st], b1, T());
+  for (int st = 0; st < KR::kSteps; ++st) mma_piece(c, a[st], buf[slot<KR::kPieces>(kt * 32 + col, 2 * st + half)], T());
+}
+
+// Scheduling of one pipelined tile: the next tile's fragment reads and
+// matrix-core steps spread through this tile's vector work (NV vector
+// instructions per step), so that the two overlap.
+template <typename T, int DH, int NV>
+__device__ __forceinline__ void interleave_hint() {
+  constexpr int kMfma = KeyRow<T, DH>::kSteps * (sizeof(T) == 2 ? 1 : 4);
+  constexpr int kDs = KeyRow<T, DH>::kSteps;
+  __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+  for (int i = 0; i < kMfma; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if (i * kDs / kMfma + 2 < kDs && (i * kDs) % kMfma == 0) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, NV, 0);
   }
 }
 
-// Running (max, sum exp, visual sum exp) with one exponential per logit: the
-// smaller of the new logit and the running max is scaled against the larger.
-__device__ __forceinline__ void online_add(float x, bool vis, float &m, float &z, float &vz) {
-  const float d = x - m;
-  const float e = expf(-fabsf(d));
-  const bool up = d > 0.f;
-  const float nz = up ? fmaf(z, e, 1.f) : z + e;
-  const float nv = up ? fmaf(vz, e, vis ? 1.f : 0.f) : vz + (vis ? e : 0.f);
-  const bool live = x != -INFINITY;
-  z = live ? nz : z;
-  vz = live ? nv : vz;
-  m = live ? fmaxf(m, x) : m;
-}
-
-__device__ __forceinline__ void online_merge(float &m, float &z, float &vz, float m2, float z2, float v2) {
+// Combine two (reference, sum, visual sum) triples in base 2. References are
+// finite (kNoRef for a row that has seen no key: its sums are 0).
+__device__ __forceinline__ void merge2(float &m, float &z, float &vz, float m2, float z2, float v2) {
   const float M = fmaxf(m, m2);
-  const float f1 = m == -INFINITY ? 0.f : expf(m - M);
-  const float f2 = m2 == -INFINITY ? 0.f : expf(m2 - M);
+  const float f1 = pow2(m - M), f2 = pow2(m2 - M);
   z = z * f1 + z2 * f2;
   vz = vz * f1 + v2 * f2;
   m = M;
+}
+
+// Wave-uniform minimum of the real row positions in this lane's accumulator
+// rows (positions are < 2^24, exact in fp32).
+__device__ __forceinline__ int wave_min_pos(const int (&prow)[16]) {
+  int mn = 1 << 24;
+#pragma unroll
+  for (int v = 0; v < 16; ++v)
+    if (prow[v] >= 0) mn = min(mn, prow[v]);
+  return (int)(-wave_max(-(float)mn));
 }
 
 // ---------------------------------------------------------------- plan
 __global__ __launch_bounds__(256) void k_rows_plan(
     const int32_t *__restrict__ cu_seqlens, const int32_t *__restrict__ vis_start,
     const int32_t *__restrict__ cu_vis, const int32_t *__restrict__ cu_rows,
-    const int32_t *__restrict__ row_pos, int R, int Hq, int g, int64_t cap1, int64_t cap2,
+    const int32_t *__restrict__ row_pos, int R, int Hq, int g, int RT, int64_t cap1, int64_t cap2,
     int32_t *__restrict__ off1, int32_t *__restrict__ off2, int64_t *__restrict__ sc_off,
     int4 *__restrict__ rinfo, int4 *__restrict__ items1, int4 *__restrict__ items2) {
   __shared__ int sh[4];
-  int carry1 = 0, carry2 = 0;
-  int64_t carry_sc = 0;
   __shared__ long long s_sc[256];
+  int carry1 = 0, carry2 = 0;
+  long long carry_sc = 0;
   for (int base = 0; base < R; base += 256) {
     const int r = base + (int)threadIdx.x;
     int n1 = 0, n2 = 0, KC = 0, VC = 0, RG = 0, pmax = 0;
     long long nsc = 0;
     if (r < R) {
       const int m0 = cu_rows[r], M = cu_rows[r + 1] - m0;
-      pmax = 0;
       for (int m = 0; m < M; ++m) pmax = max(pmax, row_pos[m0 + m]);
       const int tiles = (g * M + 31) / 32;
-      RG = (tiles + last::kRowWaves - 1) / last::kRowWaves;
+      RG = (tiles + RT - 1) / RT;
       KC = (pmax + 1 + kCH - 1) / kCH;
       const int N = cu_vis[r + 1] - cu_vis[r];
       const int seen = min(N, pmax - vis_start[r] + 1);
@@ -248,16 +267,19 @@ __global__ __launch_bounds__(256) void k_rows_plan(
 }
 
 // ---------------------------------------------------------------- pass 1
-template <typename T, int DH>
-__global__ __launch_bounds__(kThreads) void k_rows_stats(
+template <typename T, int DH, int RT>
+__global__ __launch_bounds__(kThreads, 2) void k_rows_stats(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ cu_rows, const int32_t *__restrict__ row_pos,
     const int4 *__restrict__ items, const int4 *__restrict__ rinfo,
     const int64_t *__restrict__ sc_off, int64_t n_items, int Hq, int Hkv, int64_t T_total,
-    int64_t M_total, int64_t SC_total, float scale, float4 *__restrict__ stats) {
+    int64_t M_total, int64_t SC_total, float scale2, float4 *__restrict__ stats) {
   using KR = KeyRow<T, DH>;
+  constexpr int KS = kW / RT;
   __shared__ uint4 s_k[2][KR::kStage];
+  __shared__ float4 s_st[kW][32];
+  __shared__ int s_pos[kW][32];     // position of each row of a wave's tile (-1: none)
   const int64_t item = blockIdx.x % n_items;
   const int lk = (int)(blockIdx.x / n_items);
   const int kv = lk % Hkv, l = lk / Hkv;
@@ -266,16 +288,24 @@ __global__ __launch_bounds__(kThreads) void k_rows_stats(
   const int4 info = rinfo[r];
   const int KC = info.x, pmax = info.w;
   const int g = Hq / Hkv;
-  const RowSet rs = row_set(cu_rows, r, rg, g);
-  const int lane = threadIdx.x & 63, col = lane & 31;
+  const Place<RT> pl(cu_rows, r, rg, g);
+  const int lane = threadIdx.x & 63, col = lane & 31, wave = threadIdx.x >> 6;
 
   uint4 a[KR::kSteps];
-  load_query_frags<T, DH>(q, rs, l, kv, g, Hq, M_total, a);
-  int prow[16];
+  load_query_frags<T, DH, RT>(q, pl, l, kv, g, Hq, M_total, a);
+  int pmin;
+  {
+    int prow[16];
 #pragma unroll
-  for (int v = 0; v < 16; ++v) {
-    const int rho = rs.tile0 + acc_row(lane, v);
-    prow[v] = rho < rs.nrows ? row_pos[rs.m0 + rho % rs.M] : -1;
+    for (int v = 0; v < 16; ++v) {
+      const int rho = pl.tile0 + acc_row(lane, v);
+      prow[v] = rho < pl.nrows ? row_pos[pl.m0 + rho % pl.M] : -1;
+    }
+    pmin = wave_min_pos(prow);
+    if (lane < 32) {
+      const int rho = pl.tile0 + lane;
+      s_pos[wave][lane] = rho < pl.nrows ? row_pos[pl.m0 + rho % pl.M] : -1;
+    }
   }
 
   const int64_t tok0 = cu_seqlens[r];
@@ -284,59 +314,123 @@ __global__ __launch_bounds__(kThreads) void k_rows_stats(
   const int nk = ke - kb;
   const int vlo = vis_start[r], vhi = vlo + (cu_vis[r + 1] - cu_vis[r]);
   const int64_t kstride = (int64_t)Hkv * DH * sizeof(T);
-  const char *kbase = reinterpret_cast<const char *>(k + (((int64_t)l * T_total + tok0 + kb) * Hkv + kv) * DH);
+  const char *kbase = (const char *)uniform_ptr(k + (((int64_t)l * T_total + tok0 + kb) * Hkv + kv) * DH);
 
-  float mx[16], z[16], vz[16];
+  float mr[16], z[16], vz[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    mx[v] = -INFINITY;
+    mr[v] = kNoRef;
     z[v] = 0.f;
     vz[v] = 0.f;
   }
 
-  Stager<T, DH> stg;
-  stg.load(kbase, kstride, 0, nk);
-  stg.store(s_k[0]);
+  stage_dma<T, DH>(s_k[0], kbase, kstride, 0, nk);
+  vm_wait<0>();
   __syncthreads();
   const int nst = (nk + kSub - 1) / kSub;
   for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) stg.load(kbase, kstride, (st + 1) * kSub, nk - (st + 1) * kSub);
-    if (rs.active) {
-      f32x16_t c0, c1;
-      stage_dots<T, DH>(s_k[st & 1], a, c0, c1);
-      const int j0 = kb + st * kSub + col, j1 = j0 + 32;
-      const bool v0 = j0 >= vlo && j0 < vhi, v1 = j1 >= vlo && j1 < vhi;
+    if (st + 1 < nst) stage_dma<T, DH>(s_k[(st + 1) & 1], kbase, kstride, (st + 1) * kSub, nk - (st + 1) * kSub);
+    if (pl.active) {
+      const int s0 = kb + st * kSub;                         // first key position of the stage
+      const int s1 = s0 + kSub - 1;                          // last
+      // every row of the wave sees every key of the stage, all keys exist
+      const bool full = s1 <= pmin && s1 < ke;
+      const bool allvis = s0 >= vlo && s1 < vhi, novis = s1 < vlo || s0 >= vhi;
+      const uint4 *buf = s_k[st & 1];
+      f32x16_t cur, nxt;
+      tile_dots<T, DH>(buf, a, pl.ks, cur);
+      // Per tile: the next tile's matrix-core steps run under this tile's
+      // exponentials. A term whose logit passes its row's reference by more
+      // than the slack is held back and folded in afterwards with a new
+      // reference (rare: the first key a row sees, or a jump of 2^64). The
+      // masked and unmasked loops are separate, so that neither branches.
+      auto fold_big = [&](int j, float vis) {
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float x0 = (j0 <= prow[v] && j0 < ke) ? c0[v] * scale : -INFINITY;
-        const float x1 = (j1 <= prow[v] && j1 < ke) ? c1[v] * scale : -INFINITY;
-        online_add(x0, v0, mx[v], z[v], vz[v]);
-        online_add(x1, v1, mx[v], z[v], vz[v]);
+        for (int v = 0; v < 16; ++v) {
+          const bool live = full || (j <= s_pos[wave][acc_row(lane, v)] && j < ke);
+          const float x = cur[v] * scale2;
+          const bool b = live && x - mr[v] > kSlack;
+          const float f = pow2(mr[v] - x);
+          z[v] = b ? fmaf(z[v], f, 1.f) : z[v];
+          vz[v] = b ? fmaf(vz[v], f, vis) : vz[v];
+          mr[v] = b ? x : mr[v];
+        }
+      };
+      if (full) {
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+          const int j = s0 + (pl.ks + KS * i) * 32 + col;
+          const float vis = allvis ? 1.f : (novis ? 0.f : ((j >= vlo && j < vhi) ? 1.f : 0.f));
+          if (i + 1 < RT) tile_dots<T, DH>(buf, a, pl.ks + KS * (i + 1), nxt);
+          bool big = false;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float d = fmaf(cur[v], scale2, -mr[v]);
+            const bool b = d > kSlack;
+            const float e = pow2(b ? -INFINITY : d);
+            z[v] += e;
+            vz[v] = fmaf(e, vis, vz[v]);
+            big |= b;
+          }
+          if (i + 1 < RT) interleave_hint<T, DH, 8>();
+          if (__any(big)) fold_big(j, vis);
+          if (i + 1 < RT) cur = nxt;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+          const int j = s0 + (pl.ks + KS * i) * 32 + col;
+          const float vis = (j >= vlo && j < vhi) ? 1.f : 0.f;
+          if (i + 1 < RT) tile_dots<T, DH>(buf, a, pl.ks + KS * (i + 1), nxt);
+          bool big = false;
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const bool live = j <= s_pos[wave][acc_row(lane, v)] && j < ke;
+            const float d = live ? fmaf(cur[v], scale2, -mr[v]) : -INFINITY;
+            const bool b = d > kSlack;
+            const float e = pow2(b ? -INFINITY : d);
+            z[v] += e;
+            vz[v] = fmaf(e, vis, vz[v]);
+            big |= b;
+          }
+          if (i + 1 < RT) interleave_hint<T, DH, 10>();
+          if (__any(big)) fold_big(j, vis);
+          if (i + 1 < RT) cur = nxt;
+        }
       }
     }
-    if (st + 1 < nst) stg.store(s_k[(st + 1) & 1]);
+    vm_wait<0>();
     __syncthreads();
   }
-  if (!rs.active) return;
 
-  // merge the 32 lanes of each half (they hold the same rows, other keys)
-#pragma unroll
-  for (int v = 0; v < 16; ++v) {
-#pragma unroll
-    for (int o = 1; o < 32; o <<= 1) {
-      const float m2 = __shfl_xor(mx[v], o), z2 = __shfl_xor(z[v], o), v2 = __shfl_xor(vz[v], o);
-      online_merge(mx[v], z[v], vz[v], m2, z2, v2);
-    }
-  }
-  if (col == 0) {
-    float4 *st_base = stats + (int64_t)l * SC_total + sc_off[r];
+  // merge the 32 lanes of each half (same rows, other keys), then the KS
+  // waves that share a row tile, in a fixed order
+  if (pl.active) {
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      const int rho = rs.tile0 + acc_row(lane, v);
-      if (rho < rs.nrows) {
-        const int hh = rho / rs.M, m = rho - hh * rs.M;
-        st_base[((int64_t)(kv * g + hh) * rs.M + m) * KC + c] = make_float4(mx[v], z[v], vz[v], 0.f);
+#pragma unroll
+      for (int o = 1; o < 32; o <<= 1) {
+        const float m2 = __shfl_xor(mr[v], o), z2 = __shfl_xor(z[v], o), v2 = __shfl_xor(vz[v], o);
+        merge2(mr[v], z[v], vz[v], m2, z2, v2);
       }
+    }
+    if (col == 0)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s_st[wave][acc_row(lane, v)] = make_float4(mr[v], z[v], vz[v], 0.f);
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < RT * 32) {
+    const int rt = threadIdx.x / 32, x = threadIdx.x % 32;
+    const int rho = (rg * RT + rt) * 32 + x;
+    if (rho < pl.nrows) {
+      float4 acc = s_st[rt][x];
+#pragma unroll
+      for (int s = 1; s < KS; ++s) {
+        const float4 e = s_st[rt + RT * s][x];
+        merge2(acc.x, acc.y, acc.z, e.x, e.y, e.z);
+      }
+      const int hh = rho / pl.M, m = rho - hh * pl.M;
+      stats[(int64_t)l * SC_total + sc_off[r] + ((int64_t)(kv * g + hh) * pl.M + m) * KC + c] = acc;
     }
   }
 }
@@ -356,10 +450,10 @@ __global__ __launch_bounds__(256) void k_rows_merge(
     const int l = e / per_layer, rem = e - l * per_layer;
     const int h = rem / M, m = rem - h * M;
     const float4 *st = stats + (int64_t)l * SC_total + sc_off[r] + (int64_t)rem * KC;
-    float mx = -INFINITY, z = 0.f, vz = 0.f;
+    float mx = kNoRef, z = 0.f, vz = 0.f;
     for (int c = 0; c < KC; ++c) {
       const float4 x = st[c];
-      online_merge(mx, z, vz, x.x, x.y, x.z);
+      merge2(mx, z, vz, x.x, x.y, x.z);
     }
     rowstat[((int64_t)l * Hq + h) * M_total + m0 + m] = make_float2(mx, 1.0f / z);
     part += vz / z;
@@ -371,17 +465,18 @@ __global__ __launch_bounds__(256) void k_rows_merge(
 }
 
 // ---------------------------------------------------------------- pass 2
-template <typename T, int DH>
-__global__ __launch_bounds__(kThreads) void k_rows_visual(
+template <typename T, int DH, int RT>
+__global__ __launch_bounds__(kThreads, 2) void k_rows_visual(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ cu_rows, const int32_t *__restrict__ row_pos,
     const int4 *__restrict__ items, const int4 *__restrict__ rinfo, int64_t n_items, int Hq,
-    int Hkv, int64_t T_total, int64_t M_total, int64_t N_total, int RG_max, float scale,
+    int Hkv, int64_t T_total, int64_t M_total, int64_t N_total, int RG_max, float scale2,
     const float2 *__restrict__ rowstat, float *__restrict__ part) {
   using KR = KeyRow<T, DH>;
+  constexpr int KS = kW / RT;
   __shared__ uint4 s_k[2][KR::kStage];
-  __shared__ float s_col[last::kRowWaves][kCH];
+  __shared__ float s_col[RT][kCH];
   const int64_t item = blockIdx.x % n_items;
   const int lk = (int)(blockIdx.x / n_items);
   const int kv = lk % Hkv, l = lk / Hkv;
@@ -389,27 +484,30 @@ __global__ __launch_bounds__(kThreads) void k_rows_visual(
   const int r = it.x, rg = it.y, c = it.z;
   const int pmax = rinfo[r].w;
   const int g = Hq / Hkv;
-  const RowSet rs = row_set(cu_rows, r, rg, g);
-  const int lane = threadIdx.x & 63, col = lane & 31, wave = threadIdx.x >> 6;
+  const Place<RT> pl(cu_rows, r, rg, g);
+  const int lane = threadIdx.x & 63, col = lane & 31;
 
   uint4 a[KR::kSteps];
-  load_query_frags<T, DH>(q, rs, l, kv, g, Hq, M_total, a);
+  load_query_frags<T, DH, RT>(q, pl, l, kv, g, Hq, M_total, a);
+  // per accumulator row: position, reference and 1/Z; a missing row gets an
+  // infinite reference, so its terms are exactly 0
   int prow[16];
   float rm[16], riz[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    const int rho = rs.tile0 + acc_row(lane, v);
+    const int rho = pl.tile0 + acc_row(lane, v);
     prow[v] = -1;
-    rm[v] = 0.f;
+    rm[v] = INFINITY;
     riz[v] = 0.f;
-    if (rho < rs.nrows) {
-      const int hh = rho / rs.M, m = rho - hh * rs.M;
-      prow[v] = row_pos[rs.m0 + m];
-      const float2 x = rowstat[((int64_t)l * Hq + kv * g + hh) * M_total + rs.m0 + m];
+    if (rho < pl.nrows) {
+      const int hh = rho / pl.M, m = rho - hh * pl.M;
+      prow[v] = row_pos[pl.m0 + m];
+      const float2 x = rowstat[((int64_t)l * Hq + kv * g + hh) * M_total + pl.m0 + m];
       rm[v] = x.x;
       riz[v] = x.y;
     }
   }
+  const int pmin = wave_min_pos(prow);
 
   const int vlo = vis_start[r];
   const int64_t n0 = cu_vis[r];
@@ -419,39 +517,67 @@ __global__ __launch_bounds__(kThreads) void k_rows_visual(
   const int nk = min(kCH, seen - ib);
   const int64_t tok0 = cu_seqlens[r];
   const int64_t kstride = (int64_t)Hkv * DH * sizeof(T);
-  const char *kbase =
-      reinterpret_cast<const char *>(k + (((int64_t)l * T_total + tok0 + vlo + ib) * Hkv + kv) * DH);
+  const char *kbase = (const char *)uniform_ptr(k + (((int64_t)l * T_total + tok0 + vlo + ib) * Hkv + kv) * DH);
 
-  Stager<T, DH> stg;
-  stg.load(kbase, kstride, 0, nk);
-  stg.store(s_k[0]);
+  stage_dma<T, DH>(s_k[0], kbase, kstride, 0, nk);
+  vm_wait<0>();
   __syncthreads();
   const int nst = (nk + kSub - 1) / kSub;
   for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) stg.load(kbase, kstride, (st + 1) * kSub, nk - (st + 1) * kSub);
-    float s0 = 0.f, s1 = 0.f;
-    if (rs.active) {
-      f32x16_t c0, c1;
-      stage_dots<T, DH>(s_k[st & 1], a, c0, c1);
-      const int j0 = vlo + ib + st * kSub + col, j1 = j0 + 32;   // key positions
+    if (st + 1 < nst) stage_dma<T, DH>(s_k[(st + 1) & 1], kbase, kstride, (st + 1) * kSub, nk - (st + 1) * kSub);
+    float sum[RT];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        s0 += j0 <= prow[v] ? expf(c0[v] * scale - rm[v]) * riz[v] : 0.f;
-        s1 += j1 <= prow[v] ? expf(c1[v] * scale - rm[v]) * riz[v] : 0.f;
+    for (int i = 0; i < RT; ++i) sum[i] = 0.f;
+    if (pl.active) {
+      const int s0 = vlo + ib + st * kSub;                   // key position of the stage's first key
+      const bool full = s0 + kSub - 1 <= pmin;               // every row of the wave sees every key
+      const uint4 *buf = s_k[st & 1];
+      f32x16_t cur, nxt;
+      tile_dots<T, DH>(buf, a, pl.ks, cur);
+      // the next tile's matrix-core steps run under this tile's exponentials;
+      // the two loops differ only in the causal mask, so that neither branches
+      if (full) {
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+          if (i + 1 < RT) tile_dots<T, DH>(buf, a, pl.ks + KS * (i + 1), nxt);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sum[i] = fmaf(pow2(fmaf(cur[v], scale2, -rm[v])), riz[v], sum[i]);
+          if (i + 1 < RT) {
+            interleave_hint<T, DH, 6>();
+            cur = nxt;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < RT; ++i) {
+          const int j = s0 + (pl.ks + KS * i) * 32 + col;
+          if (i + 1 < RT) tile_dots<T, DH>(buf, a, pl.ks + KS * (i + 1), nxt);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const float x = j <= prow[v] ? fmaf(cur[v], scale2, -rm[v]) : -INFINITY;
+            sum[i] = fmaf(pow2(x), riz[v], sum[i]);
+          }
+          if (i + 1 < RT) {
+            interleave_hint<T, DH, 8>();
+            cur = nxt;
+          }
+        }
       }
       // the other half of the wave holds the other 16 rows of the same keys
-      s0 += __shfl_xor(s0, 32);
-      s1 += __shfl_xor(s1, 32);
+#pragma unroll
+      for (int i = 0; i < RT; ++i) sum[i] += __shfl_xor(sum[i], 32);
     }
-    s_col[wave][st * kSub + lane] = (lane < 32) ? s0 : s1;
-    if (st + 1 < nst) stg.store(s_k[(st + 1) & 1]);
+    if (lane < 32)
+#pragma unroll
+      for (int i = 0; i < RT; ++i) s_col[pl.rt][st * kSub + (pl.ks + KS * i) * 32 + col] = sum[i];
+    vm_wait<0>();
     __syncthreads();
   }
   float *out = part + (((int64_t)l * Hkv + kv) * RG_max + rg) * N_total + n0 + ib;
   for (int t = threadIdx.x; t < nk; t += kThreads) {
     float x = s_col[0][t];
 #pragma unroll
-    for (int w = 1; w < last::kRowWaves; ++w) x += s_col[w][t];
+    for (int w = 1; w < RT; ++w) x += s_col[w][t];
     out[t] = x;
   }
 }
@@ -485,17 +611,17 @@ __global__ __launch_bounds__(256) void k_rows_finalize(
   scores[n] = s / mass[r];
 }
 
-template <typename T, int DH>
+template <typename T, int DH, int RT>
 hipError_t launch_passes(const last_batch *b, const last::RowsPlan &p, const last::RowsWs &w,
                          const int32_t *cu_rows, const int32_t *row_pos, const void *q,
-                         const void *k, float scale, hipStream_t s) {
+                         const void *k, float scale2, hipStream_t s) {
   const int64_t blocks1 = (int64_t)b->G * b->Hkv * p.items1;
   const int64_t blocks2 = (int64_t)b->G * b->Hkv * p.items2;
   last::launch_begin("rows_stats", s);
-  hipLaunchKernelGGL((k_rows_stats<T, DH>), dim3((unsigned)blocks1), dim3(kThreads), 0, s,
+  hipLaunchKernelGGL((k_rows_stats<T, DH, RT>), dim3((unsigned)blocks1), dim3(kThreads), 0, s,
                      (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis, cu_rows,
                      row_pos, w.items1, w.rinfo, w.sc_off, p.items1, b->Hq, b->Hkv, p.T_total,
-                     p.M_total, p.SC_total, scale, w.stats);
+                     p.M_total, p.SC_total, scale2, w.stats);
   hipError_t e = last::launch_end(s);
   if (e != hipSuccess) return e;
 
@@ -506,11 +632,22 @@ hipError_t launch_passes(const last_batch *b, const last::RowsPlan &p, const las
   if (e != hipSuccess) return e;
 
   last::launch_begin("rows_visual", s);
-  hipLaunchKernelGGL((k_rows_visual<T, DH>), dim3((unsigned)blocks2), dim3(kThreads), 0, s,
+  hipLaunchKernelGGL((k_rows_visual<T, DH, RT>), dim3((unsigned)blocks2), dim3(kThreads), 0, s,
                      (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis, cu_rows,
                      row_pos, w.items2, w.rinfo, p.items2, b->Hq, b->Hkv, p.T_total, p.M_total,
-                     p.N_total, p.RG_max, scale, w.rowstat, w.part);
+                     p.N_total, p.RG_max, scale2, w.rowstat, w.part);
   return last::launch_end(s);
+}
+
+template <typename T, int DH>
+hipError_t launch_rt(const last_batch *b, const last::RowsPlan &p, const last::RowsWs &w,
+                     const int32_t *cu_rows, const int32_t *row_pos, const void *q, const void *k,
+                     float scale2, hipStream_t s) {
+  switch (p.RT) {
+    case 1: return launch_passes<T, DH, 1>(b, p, w, cu_rows, row_pos, q, k, scale2, s);
+    case 2: return launch_passes<T, DH, 2>(b, p, w, cu_rows, row_pos, q, k, scale2, s);
+    default: return launch_passes<T, DH, 4>(b, p, w, cu_rows, row_pos, q, k, scale2, s);
+  }
 }
 
 }  // namespace
@@ -523,12 +660,16 @@ RowsPlan make_rows_plan(const last_batch *b, const int32_t *cu_rows_h, const int
   p.M_total = cu_rows_h[b->R];
   p.N_total = b->cu_vis_h[b->R];
   p.T_total = b->cu_seqlens_h[b->R];
+  int max_tiles = 1;
+  for (int r = 0; r < b->R; ++r)
+    max_tiles = std::max(max_tiles, (g * (cu_rows_h[r + 1] - cu_rows_h[r]) + 31) / 32);
+  p.RT = max_tiles >= 3 ? 4 : max_tiles;
   for (int r = 0; r < b->R; ++r) {
     const int M = cu_rows_h[r + 1] - cu_rows_h[r];
     int pmax = 0;
     for (int m = 0; m < M; ++m) pmax = std::max(pmax, row_pos_h[cu_rows_h[r] + m]);
     const int tiles = (g * M + 31) / 32;
-    const int RG = (tiles + kRowWaves - 1) / kRowWaves;
+    const int RG = (tiles + p.RT - 1) / p.RT;
     const int KC = (pmax + 1 + kRowChunk - 1) / kRowChunk;
     const int N = b->cu_vis_h[r + 1] - b->cu_vis_h[r];
     const int seen = std::min(N, pmax - b->vis_start_h[r] + 1);
@@ -564,16 +705,18 @@ hipError_t launch_rows(const last_batch *b, const RowsPlan &p, const RowsWs &w,
   const int g = b->Hq / b->Hkv;
   launch_begin("rows_plan", s);
   hipLaunchKernelGGL(k_rows_plan, dim3(1), dim3(256), 0, s, b->cu_seqlens, b->vis_start, b->cu_vis,
-                     cu_rows, row_pos, b->R, b->Hq, g, p.items1, p.items2, w.off1, w.off2, w.sc_off,
-                     w.rinfo, w.items1, w.items2);
+                     cu_rows, row_pos, b->R, b->Hq, g, p.RT, p.items1, p.items2, w.off1, w.off2,
+                     w.sc_off, w.rinfo, w.items1, w.items2);
   hipError_t e = launch_end(s);
   if (e != hipSuccess) return e;
 
+  // logits in base-2 units: sigma * log2(e) * q.k
+  const float scale2 = scale * kLog2e;
   const bool bf = b->qk_dtype == LAST_BF16;
-  e = bf ? (b->Dh == 64 ? launch_passes<uint16_t, 64>(b, p, w, cu_rows, row_pos, q, k, scale, s)
-                        : launch_passes<uint16_t, 128>(b, p, w, cu_rows, row_pos, q, k, scale, s))
-         : (b->Dh == 64 ? launch_passes<float, 64>(b, p, w, cu_rows, row_pos, q, k, scale, s)
-                        : launch_passes<float, 128>(b, p, w, cu_rows, row_pos, q, k, scale, s));
+  e = bf ? (b->Dh == 64 ? launch_rt<uint16_t, 64>(b, p, w, cu_rows, row_pos, q, k, scale2, s)
+                        : launch_rt<uint16_t, 128>(b, p, w, cu_rows, row_pos, q, k, scale2, s))
+         : (b->Dh == 64 ? launch_rt<float, 64>(b, p, w, cu_rows, row_pos, q, k, scale2, s)
+                        : launch_rt<float, 128>(b, p, w, cu_rows, row_pos, q, k, scale2, s));
   if (e != hipSuccess) return e;
 
   launch_begin("rows_finalize", s);

@@ -421,30 +421,6 @@ constexpr int kDmaCols = kKS;                               // columns per ring 
 constexpr int kDmaPieces = kTile * kDmaCols * 2 / 16;       // 16-byte pieces per operand stage (1024)
 constexpr int kDmaInstr = kDmaPieces / 64;                  // wave instructions per operand stage (16)
 
-__device__ __forceinline__ uint32_t lds_u32(const void *p) {
-  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) void *)p);
-}
-
-// lds: wave-uniform LDS byte address (goes to M0); base: wave-uniform global
-// address; voff: this lane's byte offset from base.
-__device__ __forceinline__ void dma16(uint32_t lds, const void *base, uint32_t voff) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory");
-}
-__device__ __forceinline__ const void *uniform_ptr(const void *p) {
-  const uint64_t v = (uint64_t)(uintptr_t)p;
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
-  return (const void *)(uintptr_t)(((uint64_t)hi << 32) | lo);
-}
-__device__ __forceinline__ int64_t uniform_i64(int64_t v) {
-  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
-  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
-  return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-template <int N>
-__device__ __forceinline__ void vm_wait() {
-  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
 
 // Persistent grid for `tiles` tiles on `cus` compute units: a multiple of 8
 // (one share per XCD), at most one block per CU.
