@@ -20,6 +20,9 @@ hipError_t launch_end(hipStream_t s);
 // Remember the last HIP error text for last_status_string (thread-local).
 void note_hip_error(hipError_t e);
 
+// Compute units of the current device (cached per device).
+int device_cus();
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // Workspace carving: consecutive 256-byte aligned segments.

@@ -155,10 +155,17 @@ __global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ c
     m.pad = 0;
     return m;
   };
-  const int64_t d1 = min((int64_t)dtile_off[r + 1], diag_cap), o1 = min((int64_t)otile_off[r + 1], off_cap);
-  for (int64_t t = dtile_off[r] + threadIdx.x; t < d1; t += 256) {
-    const int I = (int)(t - dtile_off[r]);
-    dtile[t] = meta(I, I);
+  const int64_t o1 = min((int64_t)otile_off[r + 1], off_cap);
+  // Diagonal tiles: the first nb - 1 row blocks of every request in request
+  // order, then the last row block of every request (it may be partial), so
+  // that a grid-stride walk meets the full tiles first.
+  {
+    const int nbd = dtile_off[r + 1] - dtile_off[r];
+    const int64_t head = dtile_off[r] - r, tail = (int64_t)dtile_off[gridDim.x] - gridDim.x;
+    for (int I = threadIdx.x; I < nbd; I += 256) {
+      const int64_t t = I + 1 < nbd ? head + I : tail + r;
+      if (t < diag_cap) dtile[t] = meta(I, I);
+    }
   }
   const int nb = (N + kTile - 1) / kTile, nR = (nb + kRegion - 1) / kRegion;
   int64_t base = otile_off[r];
@@ -445,13 +452,17 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   __shared__ __align__(16) double s_inv[2][kTile];
   __shared__ TileMeta s_next;                        // the next tile, fetched during this one
 
-  // XCD x receives blocks x, x + 8, ... (gridDim.x is a multiple of 8) and
-  // owns the contiguous range [lo, hi) of the region-ordered tile list; its
-  // blocks take every per-th tile of it, so the tiles that run together on
-  // one XCD are neighbours and share row blocks in that XCD's L2.
-  const int per = (int)(gridDim.x / 8), xcd = (int)(blockIdx.x % 8);
-  const int64_t lo = tiles * xcd / 8, hi = tiles * (xcd + 1) / 8;
-  int64_t t = lo + (int64_t)(blockIdx.x / 8);
+  // Off the diagonal, XCD x receives blocks x, x + 8, ... (gridDim.x is a
+  // multiple of 8) and owns the contiguous range [lo, hi) of the
+  // region-ordered tile list; its blocks take every per-th tile of it, so the
+  // tiles that run together on one XCD are neighbours and share row blocks in
+  // that XCD's L2. Diagonal tiles share nothing: blocks take them with a plain
+  // grid stride, and the list puts every request's last (possibly partial)
+  // row block at its tail, so a block takes at most one full tile and one
+  // last-block tile before a second full one.
+  const int per = DIAG ? (int)gridDim.x : (int)(gridDim.x / 8), xcd = (int)(blockIdx.x % 8);
+  const int64_t lo = DIAG ? 0 : tiles * xcd / 8, hi = DIAG ? tiles : tiles * (xcd + 1) / 8;
+  int64_t t = lo + (int64_t)(DIAG ? blockIdx.x : blockIdx.x / 8);
   if (t >= hi) return;
 
   // the wave index is uniform: keep it (and all that derives from it) scalar
@@ -1200,18 +1211,6 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
 }  // namespace
 
 namespace last {
-
-// Compute units of the current device, queried once per device.
-static int device_cus() {
-  static std::atomic<int> cache[64];
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  int v = cache[dev].load(std::memory_order_relaxed);
-  if (v > 0) return v;
-  if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-  cache[dev].store(v, std::memory_order_relaxed);
-  return v;
-}
 
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,
                             last_sel_mode mode) {
