@@ -15,6 +15,8 @@ Each function names the paper passage it follows (arXiv 2607.27952, Sec. 3):
   rows_scores -- Table 4 attention sources: Eq. 6-8 over any set of causal
              query rows per request (first / middle / every query token)
   source_rows -- the row positions of each Table 4 attention source
+  prefill -- Sec. 3.3: the guidance model's causal prefill attention
+             (every query row), whose last row Eq. 7 reads
 """
 import ctypes
 import os
@@ -52,6 +54,8 @@ def lib():
         L.oracle_rows_scores.restype = I
         L.oracle_source_rows.argtypes = [I, ctypes.c_int32, ctypes.c_int32, P]
         L.oracle_source_rows.restype = I
+        L.oracle_prefill.argtypes = [I, I, I, I, I, I, D, P, P, P, P, P, I]
+        L.oracle_prefill.restype = I
         L.oracle_max_threads.argtypes = []
         L.oracle_max_threads.restype = I
         _lib = L
@@ -119,6 +123,21 @@ def rows_scores(R, G, Hq, Hkv, Dh, q, k, cu_seqlens, vis_start, cu_vis, cu_rows,
 
 
 SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
+
+
+def prefill(R, G, Hq, Hkv, Dh, q, k, v, cu_seqlens, dtype, scale=0.0, nthreads=0):
+    """Causal prefill attention (Eq. 6, every row) in fp64: out [G][T_total][Hq][Dh]."""
+    cu_seqlens = _i32(cu_seqlens)
+    q, qd = _storage(q, dtype)
+    k, _ = _storage(k, dtype)
+    v, _ = _storage(v, dtype)
+    T = int(cu_seqlens[R])
+    out = np.zeros((G, T, Hq, Dh), dtype=np.float64)
+    rc = lib().oracle_prefill(R, G, Hq, Hkv, Dh, qd, float(scale), _ptr(cu_seqlens), _ptr(q), _ptr(k),
+                              _ptr(v), _ptr(out), nthreads)
+    if rc != 0:
+        raise RuntimeError(f"oracle_prefill failed ({rc})")
+    return out
 
 
 def source_rows(src, qb, qe):

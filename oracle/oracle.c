@@ -28,6 +28,9 @@
  *   - Sec. 3.2, Eq. 2: K = ceil(rho * N).
  *   - Sec. 4.3, Table 4: other attention sources (first, middle or every
  *     query token instead of the last), each row causal.
+ *   - Sec. 3.3: the causal prefill attention of the guidance model itself
+ *     (every query row, softmax-weighted sum of the values), whose last row
+ *     is the one Eq. 7 reads.
  *
  * Readings where the paper is silent (each listed in the design notes):
  *   - softmax scale sigma is an explicit argument (1/sqrt(Dh) when <= 0);
@@ -243,6 +246,82 @@ int oracle_rows_scores(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
     free(qx);
   }
   return (bad & 2) ? 2 : (bad & 1) ? 3 : 0;
+}
+
+/*
+ * Sec. 3.3, Eq. 6: the causal self-attention of the guidance model's prefill,
+ * whose attention tensors LAST reads (Sec. 3.3 reads row p* of A from the
+ * same prefill pass). For every request, layer, query head h and position p:
+ *   a_j = softmax_j(sigma q_p . k_j) over j = 0..p (causal mask),
+ *   out_p = sum_j a_j v_j.
+ * q: [G][T_total][Hq][Dh] (every position), k and v: [G][T_total][Hkv][Dh];
+ * out: [G][T_total][Hq][Dh] in fp64. Query head h reads KV head h / (Hq/Hkv).
+ */
+int oracle_prefill(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
+                   double scale, const int32_t *cu_seqlens, const void *q,
+                   const void *k, const void *v, double *out, int nthreads) {
+  if (R < 0 || G < 1 || Hq < 1 || Hkv < 1 || Dh < 1 || Hq % Hkv != 0)
+    return 1;
+  const int g = Hq / Hkv;
+  const int64_t T_total = cu_seqlens[R];
+  if (scale <= 0.0) scale = 1.0 / sqrt((double)Dh);
+  orc_set_threads(nthreads);
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+  for (int r = 0; r < R; ++r) {
+    const int64_t tok0 = cu_seqlens[r];
+    const int64_t P = (int64_t)cu_seqlens[r + 1] - tok0;
+    double *logit = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1));
+    double *kx = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1) * (size_t)Dh);
+    double *vx = (double *)malloc(sizeof(double) * (size_t)(P > 0 ? P : 1) * (size_t)Dh);
+    double *qx = (double *)malloc(sizeof(double) * (size_t)Dh);
+    if (!logit || !kx || !vx || !qx) {
+      bad = 1;
+      free(logit);
+      free(kx);
+      free(vx);
+      free(qx);
+      continue;
+    }
+    for (int l = 0; l < G; ++l) {
+      for (int h = 0; h < Hq; ++h) {
+        const int kv = h / g;
+        if (h % g == 0)
+          for (int64_t j = 0; j < P; ++j)
+            for (int d = 0; d < Dh; ++d) {
+              const int64_t off = (((int64_t)l * T_total + tok0 + j) * Hkv + kv) * Dh + d;
+              kx[j * Dh + d] = orc_widen(k, off, qk_dtype);
+              vx[j * Dh + d] = orc_widen(v, off, qk_dtype);
+            }
+        for (int64_t p = 0; p < P; ++p) {
+          const int64_t qoff = (((int64_t)l * T_total + tok0 + p) * Hq + h) * Dh;
+          for (int d = 0; d < Dh; ++d) qx[d] = orc_widen(q, qoff + d, qk_dtype);
+          /* row p sees keys 0..seen (causal mask: seen = p) */
+          const int64_t seen = p;
+          double rmax = -INFINITY;
+          for (int64_t j = 0; j <= seen; ++j) {
+            double acc = 0.0;
+            for (int d = 0; d < Dh; ++d) acc += qx[d] * kx[j * Dh + d];
+            logit[j] = scale * acc;
+            if (logit[j] > rmax) rmax = logit[j];
+          }
+          double rsum = 0.0;
+          for (int64_t j = 0; j <= seen; ++j) rsum += exp(logit[j] - rmax);
+          double *o = out + qoff;
+          for (int d = 0; d < Dh; ++d) o[d] = 0.0;
+          for (int64_t j = 0; j <= seen; ++j) {
+            const double a = exp(logit[j] - rmax) / rsum;
+            for (int d = 0; d < Dh; ++d) o[d] += a * vx[j * Dh + d];
+          }
+        }
+      }
+    }
+    free(logit);
+    free(kx);
+    free(vx);
+    free(qx);
+  }
+  return bad ? 2 : 0;
 }
 
 /*

@@ -415,3 +415,41 @@ def query_rows(wl: Workload, seed: int = 0) -> QueryRows:
         out[:, a:a + int(M[r]) - 1] = _store(x[:, :-1], wl.qk_dtype)
         out[:, a + int(M[r]) - 1] = wl.q[:, r]
     return QueryRows(q_begin=qb, q_end=qe, cu_q=cu_q, q=out)
+
+
+@dataclasses.dataclass
+class PrefillInputs:
+    """Queries and values of every prefill position, for the guidance model's
+    causal prefill attention.
+
+      q  [G][T_total][Hq][Dh]   queries of every position; each request's last
+                                position holds the workload's own last query
+      v  [G][T_total][Hkv][Dh]  values, drawn N(0, 1)
+    Both in the workload's storage dtype."""
+    q: np.ndarray
+    v: np.ndarray
+
+
+def prefill_inputs(wl: Workload, seed: int = 0, ids=None) -> PrefillInputs:
+    """Draw prefill queries and values. Request r draws from SeedSequence([2607,
+    27952, 2000 + seed, ids[r], layer]) (ids defaults to 0..R-1, so that a
+    subset can reproduce the rows of the batch it came from)."""
+    ids = list(range(wl.R)) if ids is None else [int(i) for i in ids]
+    std = np.float32(wl.qk_std if wl.qk_std > 0 else 1.0 / math.sqrt(wl.Dh))
+    dt = np.uint16 if wl.qk_dtype == BF16 else np.float32
+    T = wl.T_total
+    q_out = np.empty((wl.G, T, wl.Hq, wl.Dh), dtype=dt)
+    v_out = np.empty((wl.G, T, wl.Hkv, wl.Dh), dtype=dt)
+
+    def fill(item):
+        l, r = item
+        a, b = int(wl.cu_seqlens[r]), int(wl.cu_seqlens[r + 1])
+        rng = np.random.default_rng(np.random.SeedSequence([2607, 27952, 2000 + seed, ids[r], l]))
+        qq = rng.standard_normal((b - a, wl.Hq, wl.Dh), dtype=np.float32) * std
+        vv = rng.standard_normal((b - a, wl.Hkv, wl.Dh), dtype=np.float32)
+        q_out[l, a:b - 1] = _store(qq[:-1], wl.qk_dtype)
+        q_out[l, b - 1] = wl.q[l, r]
+        v_out[l, a:b] = _store(vv, wl.qk_dtype)
+
+    _pool_map(fill, [(l, r) for l in range(wl.G) for r in range(wl.R)])
+    return PrefillInputs(q=q_out, v=v_out)

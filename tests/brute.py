@@ -110,3 +110,22 @@ def rows_scores(wl, cu_rows, row_pos, q_rows, rng=None, want_sums=False):
         sums[int(wl.cu_vis[r]):int(wl.cu_vis[r + 1])] = s
         w[int(wl.cu_vis[r]):int(wl.cu_vis[r + 1])] = s / s.sum()
     return (w, sums) if want_sums else w
+
+
+def prefill(wl, q_all, v):
+    """Causal prefill attention in matrix form: softmax(sigma Q K^T + causal mask) V
+    for every layer, head and request (NumPy fp64)."""
+    q = _f64(q_all, wl.qk_dtype)
+    k = _f64(wl.k, wl.qk_dtype)
+    vv = _f64(v, wl.qk_dtype)
+    g = wl.Hq // wl.Hkv
+    out = np.zeros(q.shape)
+    for r in range(wl.R):
+        a, b = int(wl.cu_seqlens[r]), int(wl.cu_seqlens[r + 1])
+        P = b - a
+        for l in range(wl.G):
+            for h in range(wl.Hq):
+                S = wl.scale * (q[l, a:b, h] @ k[l, a:b, h // g].T)
+                S[np.triu_indices(P, 1)] = -np.inf
+                out[l, a:b, h] = scipy.special.softmax(S, axis=1) @ vv[l, a:b, h // g]
+    return out

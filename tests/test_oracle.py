@@ -500,6 +500,56 @@ def test_source_rows_golden():
         oracle.source_rows(0, 5, 5)
 
 
+
+# ------------------------------------------------- prefill attention (Sec. 3.3)
+
+def _orc_prefill(wl, pi):
+    return oracle.prefill(wl.R, wl.G, wl.Hq, wl.Hkv, wl.Dh, pi.q, wl.k, pi.v, wl.cu_seqlens,
+                          _fcode(wl.qk_dtype), scale=wl.scale)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_prefill_matches_bruteforce(seed):
+    wl = W.tiny(400 + seed, R=2 + seed % 2, G=1 + seed % 2, Hq=4, Hkv=1 + seed % 2 * 1, Dh=8 if seed % 2 else 16,
+                n_range=(1, 20), t_range=(2, 12), qk_dtype=W.BF16 if seed % 3 else W.F32)
+    pi = W.prefill_inputs(wl, seed)
+    np.testing.assert_allclose(_orc_prefill(wl, pi), brute.prefill(wl, pi.q, pi.v), rtol=1e-10, atol=1e-13)
+
+
+def test_prefill_equal_keys_give_prefix_means():
+    wl = W.tiny(410, R=2, G=1, Hq=2, Hkv=1, Dh=8, n_range=(3, 9), t_range=(2, 6), qk_dtype=W.F32)
+    wl = dataclasses.replace(wl, k=np.ones_like(wl.k))
+    pi = W.prefill_inputs(wl)
+    out = _orc_prefill(wl, pi)
+    v = pi.v.astype(np.float64)
+    for r in range(wl.R):
+        a, b = int(wl.cu_seqlens[r]), int(wl.cu_seqlens[r + 1])
+        prefix = np.cumsum(v[0, a:b, 0], axis=0) / np.arange(1, b - a + 1)[:, None]
+        for h in range(wl.Hq):
+            np.testing.assert_allclose(out[0, a:b, h], prefix, rtol=1e-13, atol=1e-15)
+        # the first position sees only itself
+        np.testing.assert_array_equal(out[0, a, 0], v[0, a, 0])
+
+
+def test_prefill_last_row_weights_are_the_token_scores_rows():
+    """With one-hot values the last row's output is its attention row, which the
+    last-token scores see as well (Sec. 3.3 reads row p* of the same map)."""
+    wl = W.tiny(420, R=2, G=1, Hq=2, Hkv=2, Dh=64, n_range=(5, 20), t_range=(3, 20), qk_dtype=W.F32)
+    assert int(np.diff(wl.cu_seqlens).max()) <= wl.Dh
+    pi = W.prefill_inputs(wl)
+    v = np.zeros_like(pi.v)
+    for r in range(wl.R):
+        a, b = int(wl.cu_seqlens[r]), int(wl.cu_seqlens[r + 1])
+        for j in range(b - a):
+            v[0, a + j, :, j] = 1.0
+    out = _orc_prefill(wl, W.PrefillInputs(q=pi.q, v=v))
+    _, rows = _orc_scores(wl, want_rows=True)
+    for r in range(wl.R):
+        a, b = int(wl.cu_seqlens[r]), int(wl.cu_seqlens[r + 1])
+        for h in range(wl.Hq):
+            np.testing.assert_allclose(out[0, b - 1, h, :b - a], rows[0, h, a:b], rtol=1e-12, atol=1e-15)
+
+
 # ---------------------------------------------------------------- planted mistakes
 
 MUTANTS = {
@@ -539,6 +589,11 @@ MUTANTS = {
     # every row renormalised over the visual tokens it sees
     "rows_renormalise": ("for (int64_t j = 0; j <= p; ++j) Z += exp(logit[j] - mx);",
                          "for (int64_t j = v0; j <= p && j < v0 + N; ++j) Z += exp(logit[j] - mx);"),
+    # prefill rows that see the whole request (no causal mask)
+    "prefill_no_mask": ("const int64_t seen = p;", "const int64_t seen = P - 1; (void)p;"),
+    # prefill values read from the wrong KV head
+    "prefill_v_head": ("vx[j * Dh + d] = orc_widen(v, off, qk_dtype);",
+                       "vx[j * Dh + d] = orc_widen(v, off + (Hkv > 1 ? Dh : 0) * (kv + 1 < Hkv ? 1 : -1), qk_dtype);"),
     # Middle taken as q_(floor(M/2)+1) instead of q_ceil(M/2)
     "middle_floor": ("case 2: pos[0] = qb + (M + 1) / 2 - 1; return 1;", "case 2: pos[0] = qb + M / 2; return 1;"),
 }
@@ -565,7 +620,8 @@ def _pins_pass():
               lambda: test_select_matches_bruteforce(5), test_select_orthogonal_features_is_topk,
               test_select_uniform_weights_is_farthest_point, lambda: test_select_invariants(0),
               lambda: test_rows_scores_match_bruteforce(1), lambda: test_rows_scores_match_bruteforce(2),
-              test_rows_golden_causal, test_source_rows_golden]
+              test_rows_golden_causal, test_source_rows_golden,
+              lambda: test_prefill_matches_bruteforce(1), test_prefill_equal_keys_give_prefix_means]
     for c in checks:
         try:
             c()
