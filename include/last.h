@@ -11,6 +11,8 @@
  *                      normalised over the visual tokens.
  *   last_rows_scores   Sec. 4.3, Table 4: the same scores from other causal
  *                      query rows (first, middle or every query token).
+ *   last_prefill_attention  Sec. 3.3: the guidance model's causal prefill
+ *                      attention, with the same scores read from its last row.
  *   diverse_select     Sec. 3.4, Eq. 9-12: importance-weighted greedy k-center
  *                      over unit-normalised encoder features under a budget
  *                      K = ceil(rho N) (Eq. 2); or the Top-k ablation of
@@ -162,6 +164,31 @@ last_status last_rows_scores(const last_batch *b, const int32_t *cu_rows,
                              const int32_t *cu_rows_h, const int32_t *row_pos,
                              const int32_t *row_pos_h, const void *q, const void *k,
                              float *scores, void *ws, size_t ws_bytes, void *stream);
+
+/* Workspace bytes last_prefill_attention needs (0 if invalid). */
+size_t last_prefill_attention_workspace(const last_batch *b);
+
+/*
+ * Sec. 3.3: the guidance model's causal prefill attention, whose attention
+ * tensors LAST reads, with the relevance of Eq. 6-8 taken from the same pass
+ * (no second pass over the keys):
+ *   out_p = sum_{j <= p} softmax_j(sigma q_p . k_j) v_j   for every position p
+ *   scores = w~ from the rows of the last position of each request, exactly
+ *            as last_token_scores computes them.
+ *   b          as for last_token_scores; qk_dtype must be LAST_BF16 (others:
+ *              LAST_ERR_UNSUPPORTED)
+ *   q          [G][T_total][Hq][Dh] queries of every prefill position (after
+ *              rotary embedding); each request's last position is its last
+ *              query token
+ *   k, v       [G][T_total][Hkv][Dh] keys and values
+ *   out        [G][T_total][Hq][Dh] out, bf16 (rounded to nearest even)
+ *   scores     [N_total] out, as for last_token_scores
+ * The products use bf16 inputs with fp32 accumulation; the probabilities
+ * enter the value product rounded to bf16 (relative error <= 2^-9 each).
+ */
+last_status last_prefill_attention(const last_batch *b, const void *q, const void *k,
+                                   const void *v, void *out, float *scores, void *ws,
+                                   size_t ws_bytes, void *stream);
 
 /* Workspace bytes diverse_select needs (0 if the arguments are invalid). */
 size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,

@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <string>
 #include <vector>
@@ -262,6 +263,58 @@ last_status last_rows_scores(const last_batch *b, const int32_t *cu_rows, const 
     const RowsWs w = carve_rows_ws(ws, b, p, &used);
     e = launch_rows(b, p, w, cu_rows, row_pos, q, k, scores, scale, (hipStream_t)stream);
   }
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+// The prefill's score-pass plan: one chunk per request (the prefill kernel
+// writes each request's last-row statistics as a single chunk).
+static ScorePlan prefill_score_plan(const last_batch *b) {
+  ScorePlan p = make_score_plan(b);
+  int32_t pmax = 1;
+  for (int32_t r = 0; r < b->R; ++r) pmax = std::max(pmax, b->cu_seqlens_h[r + 1] - b->cu_seqlens_h[r]);
+  p.chunk_tokens = pmax;
+  p.C_total = b->R;
+  return p;
+}
+
+static size_t prefill_ws(const last_batch *b, void *ws, ScoreWs *sw, int32_t **qb_off, int32_t **qb_req) {
+  const ScorePlan p = prefill_score_plan(b);
+  size_t used = 0;
+  const ScoreWs w = carve_score_ws(ws, b, p, &used);
+  if (sw) *sw = w;
+  Carver cv(ws ? static_cast<char *>(ws) + used : nullptr);
+  int32_t *a = cv.take<int32_t>(b->R + 1);
+  int32_t *c = cv.take<int32_t>(prefill_query_blocks(b));
+  if (qb_off) *qb_off = a;
+  if (qb_req) *qb_req = c;
+  return used + cv.size();
+}
+
+size_t last_prefill_attention_workspace(const last_batch *b) {
+  if (check_batch(b) != LAST_OK || b->qk_dtype != LAST_BF16) return 0;
+  return prefill_ws(b, nullptr, nullptr, nullptr, nullptr);
+}
+
+last_status last_prefill_attention(const last_batch *b, const void *q, const void *k, const void *v,
+                                   void *out, float *scores, void *ws, size_t ws_bytes, void *stream) {
+  last_status st = check_batch(b);
+  if (st != LAST_OK) return st;
+  if (!q || !k || !v || !out || !scores) return LAST_ERR_INVALID;
+  if (b->qk_dtype != LAST_BF16) return LAST_ERR_UNSUPPORTED;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) || !aligned(scores, 4))
+    return LAST_ERR_INVALID;
+  const size_t need = prefill_ws(b, nullptr, nullptr, nullptr, nullptr);
+  if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
+  ScoreWs w;
+  int32_t *qb_off = nullptr, *qb_req = nullptr;
+  prefill_ws(b, ws, &w, &qb_off, &qb_req);
+  const ScorePlan p = prefill_score_plan(b);
+  const float scale = b->softmax_scale > 0.f ? b->softmax_scale : 1.0f / sqrtf((float)b->Dh);
+  const hipStream_t s = (hipStream_t)stream;
+  hipError_t e = launch_score_plan(b, p, w, nullptr, s);
+  if (e == hipSuccess)
+    e = launch_prefill(b, prefill_query_blocks(b), qb_off, qb_req, q, k, v, out, w.vlog, w.stats, scale, s);
+  if (e == hipSuccess) e = launch_score_tail(b, p, w, nullptr, scores, s);
   return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
 }
 

@@ -67,6 +67,21 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
 hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
                          const void *q, const void *k, const int32_t *row_pos, float *scores,
                          float *attn_rows, float scale, hipStream_t s);
+// The plan kernel alone, and merge + finalize alone (for scores whose chunk
+// statistics and visual logits another kernel wrote).
+hipError_t launch_score_plan(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
+                             const int32_t *row_pos, hipStream_t s);
+hipError_t launch_score_tail(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
+                             const int32_t *row_pos, float *scores, hipStream_t s);
+
+// ------------------------------------------------ prefill attention
+// Query blocks of 128 positions over all requests.
+int64_t prefill_query_blocks(const last_batch *b);
+// Causal attention of every position (bf16), and the last row's score-pass
+// statistics as one chunk per request (stats[(l * Hq + h) * R + r], vlog).
+hipError_t launch_prefill(const last_batch *b, int64_t QB_total, int32_t *qb_off, int32_t *qb_req,
+                          const void *q, const void *k, const void *v, void *out, float *vlog,
+                          float4 *stats, float scale, hipStream_t s);
 
 // ------------------------------------------------ several rows per request
 // Query rows are taken 32 at a time (one matrix-core tile). A block of

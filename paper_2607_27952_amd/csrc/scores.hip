@@ -674,14 +674,33 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
 
 int score_max_pairs() { return kMaxPairs; }
 
-hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
-                         const void *q, const void *k, const int32_t *row_pos, float *scores,
-                         float *attn_rows, float scale, hipStream_t s) {
+hipError_t launch_score_plan(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
+                             const int32_t *row_pos, hipStream_t s) {
   launch_begin("score_plan", s);
   hipLaunchKernelGGL(k_score_plan, dim3(1), dim3(kThreads), 0, s, b->cu_seqlens, b->cu_vis,
                      row_pos, b->R, p.chunk_tokens, p.slice_tokens, p.C_total, p.S_total, w.chunk_off,
                      w.chunk_req, w.slice_off, w.slice_req);
+  return launch_end(s);
+}
+
+hipError_t launch_score_tail(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
+                             const int32_t *row_pos, float *scores, hipStream_t s) {
+  launch_begin("score_merge", s);
+  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)b->R), dim3(kMergeThreads), 0, s, w.stats, w.chunk_off,
+                     b->G * b->Hq, p.C_total, w.rowstat, w.mass);
   hipError_t e = launch_end(s);
+  if (e != hipSuccess) return e;
+  launch_begin("score_finalize", s);
+  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog,
+                     w.rowstat, w.mass, b->cu_vis, b->vis_start, row_pos, w.slice_off, w.slice_req, b->G,
+                     b->Hq, p.N_total, p.slice_tokens, scores);
+  return launch_end(s);
+}
+
+hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
+                         const void *q, const void *k, const int32_t *row_pos, float *scores,
+                         float *attn_rows, float scale, hipStream_t s) {
+  hipError_t e = launch_score_plan(b, p, w, row_pos, s);
   if (e != hipSuccess) return e;
 
   const bool bf = b->qk_dtype == LAST_BF16;
@@ -697,17 +716,7 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
                           : launch_partial_dh<float, 128>(b, p, w, q, k, row_pos, attn_rows, scale, s));
   if (e != hipSuccess) return e;
 
-  launch_begin("score_merge", s);
-  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)b->R), dim3(kMergeThreads), 0, s, w.stats, w.chunk_off,
-                     b->G * b->Hq, p.C_total, w.rowstat, w.mass);
-  e = launch_end(s);
-  if (e != hipSuccess) return e;
-
-  launch_begin("score_finalize", s);
-  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog,
-                     w.rowstat, w.mass, b->cu_vis, b->vis_start, row_pos, w.slice_off, w.slice_req, b->G, b->Hq, p.N_total,
-                     p.slice_tokens, scores);
-  e = launch_end(s);
+  e = launch_score_tail(b, p, w, row_pos, scores, s);
   if (e != hipSuccess || !attn_rows) return e;
 
   launch_begin("score_rows", s);

@@ -24,7 +24,8 @@ KCENTER, TOPK = 0, 1
 SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
 
 EXPORTS = ("last_token_scores_workspace", "last_token_scores", "last_source_rows",
-           "last_rows_scores_workspace", "last_rows_scores", "diverse_select_workspace",
+           "last_rows_scores_workspace", "last_rows_scores", "last_prefill_attention_workspace",
+           "last_prefill_attention", "diverse_select_workspace",
            "diverse_select", "gather_kept", "last_budget", "last_status_string", "last_version",
            "last_profile_enable", "last_profile_collect", "last_profile_reset",
            "last_profile_count", "last_profile_kernel")
@@ -67,6 +68,10 @@ def lib():
         L.last_rows_scores_workspace.restype = SZ
         L.last_rows_scores.argtypes = [ctypes.POINTER(_Batch), P, P, P, P, P, P, P, P, SZ, P]
         L.last_rows_scores.restype = I32
+        L.last_prefill_attention_workspace.argtypes = [ctypes.POINTER(_Batch)]
+        L.last_prefill_attention_workspace.restype = SZ
+        L.last_prefill_attention.argtypes = [ctypes.POINTER(_Batch), P, P, P, P, P, P, SZ, P]
+        L.last_prefill_attention.restype = I32
         L.diverse_select_workspace.argtypes = [I32, P, I32, I32, I32]
         L.diverse_select_workspace.restype = SZ
         L.diverse_select.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
@@ -244,6 +249,32 @@ def rows_scores(batch: Batch, rows: Rows, q: torch.Tensor, k: torch.Tensor, scor
     if st != LAST_OK:
         raise LastError(st, "last_rows_scores")
     return scores
+
+
+def prefill_attention_workspace(batch: Batch) -> int:
+    b = batch.struct(LAST_BF16)
+    return int(lib().last_prefill_attention_workspace(ctypes.byref(b)))
+
+
+def prefill_attention(batch: Batch, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, out=None, scores=None,
+                      ws=None, stream=None):
+    """last_prefill_attention (Sec. 3.3): causal attention of every position,
+    out [G][T_total][Hq][Dh] bf16, and the last-row scores [N_total] fp32."""
+    code = _dtype_code(q)
+    if k.dtype != q.dtype or v.dtype != q.dtype:
+        raise TypeError("q, k and v must share a dtype")
+    b = batch.struct(code)
+    if out is None:
+        out = torch.empty(q.shape, dtype=q.dtype, device=q.device)
+    if scores is None:
+        scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = _workspace(lib().last_prefill_attention_workspace(ctypes.byref(b)), q.device)
+    st = lib().last_prefill_attention(ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(scores),
+                                      _ptr(ws), ws.numel(), _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "last_prefill_attention")
+    return out, scores
 
 
 def select_workspace(cu_vis_h, Dv: int, f_dtype=torch.bfloat16, mode: int = KCENTER) -> int:
