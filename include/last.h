@@ -184,7 +184,7 @@ size_t last_prefill_attention_workspace(const last_batch *b);
  *   out        [G][T_total][Hq][Dh] out, bf16 (rounded to nearest even)
  *   scores     [N_total] out, as for last_token_scores
  * The products use bf16 inputs with fp32 accumulation; the probabilities
- * enter the value product rounded to bf16 (relative error <= 2^-9 each).
+ * enter the value product rounded to bf16 (relative error <= 2^-8 each).
  */
 last_status last_prefill_attention(const last_batch *b, const void *q, const void *k,
                                    const void *v, void *out, float *scores, void *ws,

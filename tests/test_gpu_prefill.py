@@ -5,10 +5,13 @@ Bars:
   * scores: element-wise within 1e-5 relative of the oracle (FLT_MIN floor),
     as for last_token_scores;
   * out: the kernel rounds every probability to bf16 before the value
-    product (relative error <= 2^-9 each) and rounds the output to bf16
-    (<= 2^-9 relative), with fp32 accumulation elsewhere. So for row p and
-    dimension d, |out - oracle| <= 2^-9 (max_{j<=p} |v_jd| + |oracle|), plus
-    1e-5 max |v_jd| for the fp32 logits and exponentials.
+    product (relative error <= 2^-8 each) and rounds the output to bf16
+    (<= 2^-8 relative). The matrix cores accumulate in fp32 without a
+    round-to-nearest guarantee per addition; allow 2 ulps of the running
+    magnitude per key (2^-22 (p + 1) max |v_jd|). So for row p and
+    dimension d, with V = max_{j<=p} |v_jd|:
+      |out - oracle| <= 2^-8 (V + |oracle|) + 2^-22 (p + 1) V + 1e-5 V,
+    the last term for the fp32 logits and exponentials.
 Small cases span several 128-position query blocks and 64-key stages with
 ragged tails; the workloads run at full size, checked on sampled requests
 (C4 and C5 on a prefix of one request, which its causal rows make
@@ -26,7 +29,7 @@ pytestmark = pytest.mark.gpu
 
 FLT_MIN = np.finfo(np.float32).tiny
 SCORE_RTOL = 1e-5
-U = 2.0 ** -9
+U = 2.0 ** -8   # unit roundoff of bf16 (8 significant bits)
 
 
 def bf16_to_f64(t):
@@ -50,7 +53,8 @@ def assert_out(wl, v_bits, got, exp, what=""):
         vmax = np.maximum.accumulate(np.abs(v[:, a:b]), axis=1)          # [G][P][Hkv][Dh], prefix max
         vmax = np.repeat(vmax, g, axis=2)                                # per query head
         e = exp[:, a:b]
-        bound = U * (vmax + np.abs(e)) + 1e-5 * vmax
+        keys = np.arange(1, b - a + 1, dtype=np.float64)[None, :, None, None]
+        bound = U * (vmax + np.abs(e)) + (2.0 ** -22 * keys + 1e-5) * vmax
         err = np.abs(got[:, a:b] - e)
         bad = err > bound
         assert not bad.any(), (f"{what} request {r}: {bad.sum()} of {bad.size} outputs off; worst "
