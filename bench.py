@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--budget", type=int, default=None)
     ap.add_argument("--source", default="last", choices=("last", "first", "middle", "all_mean"),
                     help="attention rows the scores come from (Table 4)")
+    ap.add_argument("--prefill", action="store_true",
+                    help="take the scores from the guidance model's causal prefill attention of every "
+                         "position (last_prefill_attention) instead of recomputing the last row")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time for the oracle sample")
@@ -112,6 +115,13 @@ def rows_work(wl, cu_rows, row_pos):
             "rows_stats_bytes": b1, "rows_stats_flops": f1, "rows_visual_bytes": b2, "rows_visual_flops": f2}
 
 
+def prefill_flops(wl):
+    """Causal attention of every position: row p takes p + 1 keys, 2 Dh flops
+    each for the logits and 2 Dh for the value product."""
+    P = np.diff(wl.cu_seqlens).astype(np.float64)
+    return 4.0 * wl.Dh * wl.G * wl.Hq * float(np.sum(P * (P + 1) / 2))
+
+
 def kernel_work(wl, row_pos=None):
     """Algorithmic bytes / flops per launch of each kernel, and its bound.
     row_pos: one scored row per request (a single-row attention source), whose
@@ -140,6 +150,7 @@ def kernel_work(wl, row_pos=None):
         "topk": ("hbm", wl.N_total * 4 + wl.K_total * 4),
         # kept rows read and written
         "gather": ("hbm", 2 * wl.K_total * wl.Dv * felt),
+        "prefill": ("mfma", prefill_flops(wl)),
     }
 
 
@@ -224,6 +235,15 @@ def main():
     gains = torch.empty(wl.K_total, dtype=torch.float32, device=dev)
     out = torch.empty((wl.K_total, wl.Dv), dtype=dw.feats.dtype, device=dev)
     rows = q_rows = None
+    pre = None
+    if args.prefill:
+        if args.source != "last":
+            raise SystemExit("--prefill takes the scores from the last rows; --source must be last")
+        pin = W.prefill_inputs(wl)
+        pre = (last.to_torch(pin.q, wl.qk_dtype, dev), last.to_torch(pin.v, wl.qk_dtype, dev))
+        pre_out = torch.empty(pre[0].shape, dtype=pre[0].dtype, device=dev)
+        del pin
+        log(f"[bench] scores from the causal prefill attention of all {wl.T_total} positions")
     if args.source != "last":
         qr = W.query_rows(wl)
         src = {"first": last.SRC_FIRST, "middle": last.SRC_MIDDLE, "all_mean": last.SRC_ALL_MEAN}[args.source]
@@ -237,6 +257,8 @@ def main():
         q_rows = last.to_torch(np.ascontiguousarray(np.concatenate(qs, axis=1)), wl.qk_dtype, dev)
         ws_s = torch.empty(last.rows_scores_workspace(b, rows, dw.q.dtype), dtype=torch.uint8, device=dev)
         log(f"[bench] scores from the {args.source} rows: {int(rows.cu_rows_h[-1])} query rows")
+    elif pre is not None:
+        ws_s = torch.empty(last.prefill_attention_workspace(b), dtype=torch.uint8, device=dev)
     else:
         ws_s = torch.empty(last.token_scores_workspace(b, dw.q.dtype), dtype=torch.uint8, device=dev)
     ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8, device=dev)
@@ -252,7 +274,9 @@ def main():
         del src, dst
 
     def step():
-        if rows is None:
+        if pre is not None:
+            last.prefill_attention(b, pre[0], dw.k, pre[1], out=pre_out, scores=scores, ws=ws_s)
+        elif rows is None:
             last.token_scores(b, dw.q, dw.k, scores=scores, ws=ws_s)
         else:
             last.rows_scores(b, rows, q_rows, dw.k, scores=scores, ws=ws_s)
@@ -304,7 +328,8 @@ def main():
     dominant = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])[0]
     main_roof = next((r for r in rooflines if r["kernel"] == dominant), None)
     if main_roof is not None:
-        tr = traffic_for(dominant, args.workload if args.source == "last" else f"{args.workload}_{args.source}")
+        tr = traffic_for(dominant, args.workload if args.source == "last" and pre is None else
+                         f"{args.workload}_{'prefill' if pre is not None else args.source}")
         main_roof = {k: main_roof[k] for k in ("bound", "achieved", "peak", "unit", "frac")} | {
             "traffic": tr, "kernel": dominant}
     # the paper's own similarity work (Sec. 3.4: one x_j^T X product per pick,
@@ -320,7 +345,8 @@ def main():
                       "gram_ms_per_step": round(gram_ms, 4),
                       "tflops_on_paper_work": round(paper_flops / (gram_ms * 1e-3) / 1e12, 2),
                       "tflops_on_gram_work": round(exec_flops / (gram_ms * 1e-3) / 1e12, 2)}
-    score_ms = sum(kernels[k]["ms_per_step"] for k in kernels if k.startswith("score") or k.startswith("rows"))
+    score_ms = sum(kernels[k]["ms_per_step"] for k in kernels
+                   if k.startswith("score") or k.startswith("rows") or k.startswith("prefill"))
     select_ms = sum(kernels[k]["ms_per_step"] for k in kernels
                     if k in ("select_plan", "sqnorm", "gram_diag", "gram", "greedy", "topk"))
     gather_ms = kernels.get("gather", {}).get("ms_per_step", 0.0)
@@ -339,7 +365,8 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": describe(wl, args.budget) + ("" if args.source == "last" else
-                                                             f"; scores from the {args.source} query rows"),
+                                                             f"; scores from the {args.source} query rows")
+                   + ("; scores from the causal prefill attention of every position" if pre is not None else ""),
                    "requests": wl.R, "visual_tokens": wl.N_total,
                    "kept_tokens": wl.K_total, "arithmetic": (
                        "bf16 inputs, " + ("fp32 FMA score pass" if args.source != "all_mean" else

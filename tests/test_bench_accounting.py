@@ -57,3 +57,10 @@ def test_rows_work_counts_causal_prefixes():
     # single-row sources: the score pass reads each request's causal prefix
     kw = bench.kernel_work(wl, pos - 3)
     assert kw["score_stream"][1] == wl.G * (wl.T_total - wl.R * 3) * wl.Hkv * wl.Dh * elt + q_bytes
+
+
+def test_prefill_flops_count_causal_rows():
+    wl = W.tiny(5, R=3, G=2, Hq=4, Hkv=2, Dh=64, n_range=(10, 40), t_range=(2, 9), Dv=64)
+    P = np.diff(wl.cu_seqlens)
+    expect = sum(4 * wl.Dh * wl.G * wl.Hq * sum(p + 1 for p in range(n)) for n in P)
+    assert bench.prefill_flops(wl) == expect
