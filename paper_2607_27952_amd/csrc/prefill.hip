@@ -27,8 +27,9 @@
 //                  the permutation above makes each lane's probabilities
 //                  exactly the keys its half of the B operand needs.
 // The softmax runs online per lane in base-2 units (the scale times log2 e
-// folded into one multiply): the stage's row max and sum take one exchange
-// with the partner lane, and the lane's O^T column is rescaled in place.
+// folded into the exponent's fma): the stage's row max and sum take one
+// exchange with the partner lane, and the lane's O^T column is rescaled in
+// place when some lane's max has moved.
 #include <algorithm>
 #include <math.h>
 
@@ -73,12 +74,12 @@ __device__ __forceinline__ int perm_key(int i) {
 }
 __device__ __forceinline__ int acc_key(int half, int v) { return 8 * half + v + (v >= 8 ? 8 : 0); }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// two floats to bf16, round to nearest even (v_cvt_pk_bf16_f32)
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
-  // round to nearest even (finite inputs)
-  uint32_t x = __float_as_uint(a), y = __float_as_uint(b);
-  x += 0x7fffu + ((x >> 16) & 1u);
-  y += 0x7fffu + ((y >> 16) & 1u);
-  return (x >> 16) | (y & 0xffff0000u);
+  const f32x2_t x = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2_t));
 }
 
 // One (layer, request, head, 128-position block) per block.
@@ -194,30 +195,38 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
               __builtin_bit_cast(bf16x8_t, kb[kslot<SH::kPieces>(krow, 2 * s + half)]),
               __builtin_bit_cast(bf16x8_t, bq[s]), sc[t], 0, 0, 0);
       }
-      // base-2 logits, causal mask and the keys past the block's end
+      // base-2 logits: the raw dots stay in place and the scale goes into the
+      // exponent (s2 > 0, so the largest dot gives the largest logit); keys a
+      // query does not see (causal mask, past the block's end) are -inf
       const bool full = k0 + kKS - 1 <= q0;   // every query of the wave sees every key
-      float mx = -INFINITY;
+      if (!full) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int key = k0 + t * 32 + acc_key(half, e);
+            sc[t][e] = (key <= qpos && key < kend) ? sc[t][e] : -INFINITY;
+          }
+      }
+      float mx = sc[0][0];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int key = k0 + t * 32 + acc_key(half, e);
-          const float x = sc[t][e] * s2;
-          sc[t][e] = (full || (key <= qpos && key < kend)) ? x : -INFINITY;
-          mx = fmaxf(mx, sc[t][e]);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[t][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32)) * s2;
       const float mnew = fmaxf(m, mx);
-      // a query with no key seen yet keeps -inf; its terms and factor are 0
-      const float alpha = mnew == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(m - mnew);
+      // a query with no key seen yet keeps -inf; its terms are 0 and its
+      // factor 1 (its sums are still 0)
+      const float mref = mnew == -INFINITY ? 0.f : mnew;
+      const float alpha = __builtin_amdgcn_exp2f(m - mref);
       float ps = 0.f, pv = 0.f;
       uint32_t pb[2][8];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int e = 0; e < 16; e += 2) {
-          const float p0 = mnew == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[t][e] - mnew);
-          const float p1 = mnew == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sc[t][e + 1] - mnew);
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[t][e], s2, -mref));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[t][e + 1], s2, -mref));
           ps += p0 + p1;
           if (has_last) {
             const int key = k0 + t * 32 + acc_key(half, e);
@@ -231,9 +240,12 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
         pv += __shfl_xor(pv, 32);
         vsum = vsum * alpha + pv;
       }
-      m = mnew;
+      // the running max moves rarely after the first stages: rescale only then
+      if (__any(mnew != m)) {
 #pragma unroll
-      for (int dt = 0; dt < SH::kDT; ++dt) o[dt] *= alpha;
+        for (int dt = 0; dt < SH::kDT; ++dt) o[dt] *= alpha;
+      }
+      m = mnew;
       // O^T += V^T P^T: four 16-key steps, each lane's B operand being 8 of
       // its own probabilities (keys 16s + 8 half .. + 7 of the stage)
 #pragma unroll
@@ -255,7 +267,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
           for (int e = 0; e < 16; ++e) {
             const int key = k0 + t * 32 + acc_key(half, e);
             if (key >= vlo && key < vhi && key < kend)
-              vlog[((int64_t)l * N_total + cu_vis[r] + key - vlo) * Hq + h] = sc[t][e] * kLn2;
+              vlog[((int64_t)l * N_total + cu_vis[r] + key - vlo) * Hq + h] = sc[t][e] * scale;
           }
       }
     }
