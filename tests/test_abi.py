@@ -237,3 +237,27 @@ def test_source_rows_match_golden():
     for qb, qe, src in ((5, 5, 0), (-1, 3, 1), (0, 4, 9)):
         with pytest.raises(ValueError):
             last.source_rows(src, qb, qe)
+
+
+# ------------------------------------------------- prefill attention (Sec. 3.3)
+
+def _prefill_call(b, ws_bytes=1 << 34, v_null=False):
+    q, k, v, out, sc, ws = Fake(), Fake(), Fake(), Fake(), Fake(), Fake()
+    st = last.lib().last_prefill_attention(ctypes.byref(b), q.p, k.p, None if v_null else v.p, out.p, sc.p,
+                                           ws.p, ws_bytes, None)
+    assert out.untouched() and sc.untouched() and ws.untouched()
+    return st
+
+
+def test_prefill_rejects_bad_calls_on_the_host():
+    b, keep = _batch(dtype=last.LAST_BF16)
+    L = last.lib()
+    need = L.last_prefill_attention_workspace(ctypes.byref(b))
+    assert need > 0
+    assert _prefill_call(b, ws_bytes=need - 1) == last.LAST_ERR_WORKSPACE
+    assert _prefill_call(b, v_null=True) == last.LAST_ERR_INVALID
+    b32, keep32 = _batch(dtype=last.LAST_F32)
+    assert _prefill_call(b32) == last.LAST_ERR_UNSUPPORTED
+    assert L.last_prefill_attention_workspace(ctypes.byref(b32)) == 0
+    b.Dh = 96
+    assert _prefill_call(b) == last.LAST_ERR_UNSUPPORTED
