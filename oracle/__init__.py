@@ -15,6 +15,7 @@ Each function names the paper passage it follows (arXiv 2607.27952, Sec. 3):
   rows_scores -- Table 4 attention sources: Eq. 6-8 over any set of causal
              query rows per request (first / middle / every query token)
   source_rows -- the row positions of each Table 4 attention source
+  connector -- Sec. 3.4, Eq. 12: the cloud's token-wise connector on X_S
   prefill -- Sec. 3.3: the guidance model's causal prefill attention
              (every query row), whose last row Eq. 7 reads
 """
@@ -56,6 +57,8 @@ def lib():
         L.oracle_source_rows.restype = I
         L.oracle_prefill.argtypes = [I, I, I, I, I, I, D, P, P, P, P, P, I]
         L.oracle_prefill.restype = I
+        L.oracle_connector.argtypes = [I64, I, I, I, I, D, P, P, P, P, P, P, P, P, P, P, I]
+        L.oracle_connector.restype = I
         L.oracle_max_threads.argtypes = []
         L.oracle_max_threads.restype = I
         _lib = L
@@ -123,6 +126,25 @@ def rows_scores(R, G, Hq, Hkv, Dh, q, k, cu_seqlens, vis_start, cu_vis, cu_rows,
 
 
 SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
+
+
+def connector(x, gamma, beta, w1, b1, w2, b2, dtype, eps=1e-5, want_intermediate=False, nthreads=0):
+    """Eq. 12's phi_c in fp64: y [K][Do] (and xhat [K][Dv], h [K][Dh] if asked)."""
+    x, xd = _storage(x, dtype)
+    w1, _ = _storage(w1, dtype)
+    w2, _ = _storage(w2, dtype)
+    K, Dv = x.shape
+    Dh, Do = w1.shape[0], w2.shape[0]
+    f = lambda a: np.ascontiguousarray(a, dtype=np.float32)
+    gamma, beta, b1, b2 = f(gamma), f(beta), f(b1), f(b2)
+    y = np.zeros((K, Do))
+    xh = np.zeros((K, Dv)) if want_intermediate else None
+    h = np.zeros((K, Dh)) if want_intermediate else None
+    rc = lib().oracle_connector(K, Dv, Dh, Do, xd, float(eps), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(w1),
+                                _ptr(b1), _ptr(w2), _ptr(b2), _ptr(y), _ptr(xh), _ptr(h), nthreads)
+    if rc != 0:
+        raise RuntimeError(f"oracle_connector failed ({rc})")
+    return (y, xh, h) if want_intermediate else y
 
 
 def prefill(R, G, Hq, Hkv, Dh, q, k, v, cu_seqlens, dtype, scale=0.0, nthreads=0):

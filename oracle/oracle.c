@@ -28,6 +28,8 @@
  *   - Sec. 3.2, Eq. 2: K = ceil(rho * N).
  *   - Sec. 4.3, Table 4: other attention sources (first, middle or every
  *     query token instead of the last), each row causal.
+ *   - Sec. 3.4, Eq. 12: the cloud's token-wise connector on the kept rows
+ *     (a LayerNorm and a two-layer GELU MLP; a reading of the model family).
  *   - Sec. 3.3: the causal prefill attention of the guidance model itself
  *     (every query row, softmax-weighted sum of the values), whose last row
  *     is the one Eq. 7 reads.
@@ -320,6 +322,67 @@ int oracle_prefill(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
     free(kx);
     free(vx);
     free(qx);
+  }
+  return bad ? 2 : 0;
+}
+
+/*
+ * Sec. 3.4, Eq. 12: the cloud applies its token-wise connector to the
+ * transmitted rows, H_S = phi_c(X_S). Reading (the paper gives no formula;
+ * this is the token-wise connector structure of the InternVL models it uses):
+ *   xhat = (x - mean(x)) / sqrt(var(x) + eps) * gamma + beta     (LayerNorm)
+ *   h    = W1 xhat + b1,   g = GELU(h) = h/2 (1 + erf(h / sqrt 2)),
+ *   y    = W2 g + b2
+ * for every row x of X_S. x: [K][Dv] (bf16 bits or fp32), W1: [Dh][Dv],
+ * W2: [Do][Dh] (same storage type, one output feature per row); gamma, beta
+ * [Dv], b1 [Dh], b2 [Do] fp32. y_out [K][Do]; xhat_out [K][Dv] and h_out
+ * [K][Dh] (nullable) return the intermediate values. All in fp64.
+ */
+int oracle_connector(int64_t K, int Dv, int Dh, int Do, int dtype, double eps,
+                     const void *x, const float *gamma, const float *beta,
+                     const void *w1, const float *b1, const void *w2,
+                     const float *b2, double *y_out, double *xhat_out,
+                     double *h_out, int nthreads) {
+  if (K < 0 || Dv < 1 || Dh < 1 || Do < 1) return 1;
+  orc_set_threads(nthreads);
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic, 16) reduction(| : bad)
+  for (int64_t t = 0; t < K; ++t) {
+    double *xh = (double *)malloc(sizeof(double) * (size_t)Dv);
+    double *g = (double *)malloc(sizeof(double) * (size_t)Dh);
+    if (!xh || !g) {
+      bad = 1;
+      free(xh);
+      free(g);
+      continue;
+    }
+    double mean = 0.0;
+    for (int d = 0; d < Dv; ++d) mean += orc_widen(x, t * Dv + d, dtype);
+    mean /= Dv;
+    double var = 0.0;
+    for (int d = 0; d < Dv; ++d) {
+      const double c = orc_widen(x, t * Dv + d, dtype) - mean;
+      var += c * c;
+    }
+    var /= Dv;
+    const double rstd = 1.0 / sqrt(var + eps);
+    for (int d = 0; d < Dv; ++d)
+      xh[d] = (orc_widen(x, t * Dv + d, dtype) - mean) * rstd * gamma[d] + beta[d];
+    for (int j = 0; j < Dh; ++j) {
+      double acc = b1[j];
+      for (int d = 0; d < Dv; ++d) acc += orc_widen(w1, (int64_t)j * Dv + d, dtype) * xh[d];
+      if (h_out) h_out[t * Dh + j] = acc;
+      g[j] = 0.5 * acc * (1.0 + erf(acc / sqrt(2.0)));
+    }
+    for (int o = 0; o < Do; ++o) {
+      double acc = b2[o];
+      for (int j = 0; j < Dh; ++j) acc += orc_widen(w2, (int64_t)o * Dh + j, dtype) * g[j];
+      y_out[t * Do + o] = acc;
+    }
+    if (xhat_out)
+      for (int d = 0; d < Dv; ++d) xhat_out[t * Dv + d] = xh[d];
+    free(xh);
+    free(g);
   }
   return bad ? 2 : 0;
 }

@@ -453,3 +453,32 @@ def prefill_inputs(wl: Workload, seed: int = 0, ids=None) -> PrefillInputs:
 
     _pool_map(fill, [(l, r) for l in range(wl.G) for r in range(wl.R)])
     return PrefillInputs(q=q_out, v=v_out)
+
+
+@dataclasses.dataclass
+class ConnectorWeights:
+    """Synthetic weights of a token-wise connector: LayerNorm(Dv) -> Linear(Dv, Dh)
+    -> GELU -> Linear(Dh, Do). w1 [Dh][Dv] and w2 [Do][Dh] in the storage dtype
+    (one output feature per row), the rest fp32."""
+    gamma: np.ndarray
+    beta: np.ndarray
+    w1: np.ndarray
+    b1: np.ndarray
+    w2: np.ndarray
+    b2: np.ndarray
+    dtype: str
+
+
+def connector_weights(Dv: int, Dh: int, Do: int, dtype: str = BF16, seed: int = 0) -> ConnectorWeights:
+    """Draw from SeedSequence([2607, 27952, 3000 + seed]): weights N(0, 1/fan_in),
+    biases N(0, 0.02^2), gamma 1 + N(0, 0.1^2), beta N(0, 0.1^2)."""
+    rng = np.random.default_rng(np.random.SeedSequence([2607, 27952, 3000 + seed]))
+    f32 = np.float32
+    gamma = (1.0 + 0.1 * rng.standard_normal(Dv, dtype=f32)).astype(f32)
+    beta = (0.1 * rng.standard_normal(Dv, dtype=f32)).astype(f32)
+    w1 = rng.standard_normal((Dh, Dv), dtype=f32) * f32(1.0 / math.sqrt(Dv))
+    b1 = (0.02 * rng.standard_normal(Dh, dtype=f32)).astype(f32)
+    w2 = rng.standard_normal((Do, Dh), dtype=f32) * f32(1.0 / math.sqrt(Dh))
+    b2 = (0.02 * rng.standard_normal(Do, dtype=f32)).astype(f32)
+    return ConnectorWeights(gamma=gamma, beta=beta, w1=_store(w1, dtype), b1=b1, w2=_store(w2, dtype), b2=b2,
+                            dtype=dtype)

@@ -550,6 +550,60 @@ def test_prefill_last_row_weights_are_the_token_scores_rows():
             np.testing.assert_allclose(out[0, b - 1, h, :b - a], rows[0, h, a:b], rtol=1e-12, atol=1e-15)
 
 
+
+# ------------------------------------------------- cloud connector (Eq. 12)
+
+def _orc_connector(x, cw, eps=1e-5, **kw):
+    return oracle.connector(x, cw.gamma, cw.beta, cw.w1, cw.b1, cw.w2, cw.b2, _fcode(cw.dtype), eps=eps, **kw)
+
+
+def _np_connector(x, cw, eps=1e-5):
+    """LayerNorm, GELU (erf) and the two products in NumPy/SciPy matrix form."""
+    X = W.as_f32(x, cw.dtype).astype(np.float64)
+    W1 = W.as_f32(cw.w1, cw.dtype).astype(np.float64)
+    W2 = W.as_f32(cw.w2, cw.dtype).astype(np.float64)
+    mu = X.mean(axis=1, keepdims=True)
+    var = X.var(axis=1, keepdims=True)
+    xh = (X - mu) / np.sqrt(var + eps) * cw.gamma.astype(np.float64) + cw.beta.astype(np.float64)
+    h = xh @ W1.T + cw.b1.astype(np.float64)
+    g = 0.5 * h * (1.0 + scipy.special.erf(h / np.sqrt(2.0)))
+    return g @ W2.T + cw.b2.astype(np.float64)
+
+
+@pytest.mark.parametrize("dtype", [W.BF16, W.F32])
+def test_connector_matches_matrix_form(dtype):
+    rng = np.random.default_rng(5)
+    cw = W.connector_weights(48, 80, 32, dtype, seed=1)
+    x = rng.standard_normal((37, 48)).astype(np.float32)
+    x = W.to_bf16_bits(x) if dtype == W.BF16 else x
+    np.testing.assert_allclose(_orc_connector(x, cw), _np_connector(x, cw), rtol=1e-11, atol=1e-12)
+
+
+def test_connector_identity_weights_give_gelu_of_layernorm():
+    n = 16
+    eye = np.eye(n, dtype=np.float32)
+    cw = W.ConnectorWeights(gamma=np.ones(n, np.float32), beta=np.zeros(n, np.float32), w1=eye,
+                            b1=np.zeros(n, np.float32), w2=eye, b2=np.zeros(n, np.float32), dtype=W.F32)
+    # a row with mean 0 and variance 1 is its own LayerNorm (eps aside)
+    base = np.array([1.0, -1.0] * (n // 2), np.float32)
+    y = _orc_connector(base[None], cw, eps=0.0)
+    # GELU(1) = Phi(1), GELU(-1) = -Phi(-1)
+    phi1 = 0.5 * (1 + math.erf(1 / math.sqrt(2)))
+    np.testing.assert_allclose(y[0], [phi1, -(1 - phi1)] * (n // 2), rtol=1e-14)
+    # a constant row normalises to 0 and GELU(0) = 0
+    np.testing.assert_array_equal(_orc_connector(np.full((1, n), 3.0, np.float32), cw), np.zeros((1, n)))
+
+
+def test_connector_layernorm_is_shift_and_scale_invariant():
+    rng = np.random.default_rng(6)
+    cw = W.connector_weights(32, 24, 16, W.F32, seed=2)
+    # multiples of 2^-10, so that x + 4 and 8 x are exact in fp32
+    x = (np.round(rng.standard_normal((9, 32)) * 1024) / 1024).astype(np.float32)
+    y = _orc_connector(x, cw, eps=0.0)
+    np.testing.assert_allclose(_orc_connector(x + np.float32(4.0), cw, eps=0.0), y, rtol=1e-9, atol=1e-11)
+    np.testing.assert_allclose(_orc_connector(x * np.float32(8.0), cw, eps=0.0), y, rtol=1e-12, atol=1e-14)
+
+
 # ---------------------------------------------------------------- planted mistakes
 
 MUTANTS = {
@@ -594,6 +648,13 @@ MUTANTS = {
     # prefill values read from the wrong KV head
     "prefill_v_head": ("vx[j * Dh + d] = orc_widen(v, off, qk_dtype);",
                        "vx[j * Dh + d] = orc_widen(v, off + (Hkv > 1 ? Dh : 0) * (kv + 1 < Hkv ? 1 : -1), qk_dtype);"),
+    # connector: GELU's tanh approximation instead of erf
+    "gelu_tanh": ("g[j] = 0.5 * acc * (1.0 + erf(acc / sqrt(2.0)));",
+                  "g[j] = 0.5 * acc * (1.0 + tanh(0.7978845608 * (acc + 0.044715 * acc * acc * acc)));"),
+    # connector: LayerNorm without its mean
+    "ln_no_mean": ("mean /= Dv;", "mean = 0.0;"),
+    # connector: first bias dropped
+    "no_b1": ("double acc = b1[j];", "double acc = 0.0 * b1[j];"),
     # Middle taken as q_(floor(M/2)+1) instead of q_ceil(M/2)
     "middle_floor": ("case 2: pos[0] = qb + (M + 1) / 2 - 1; return 1;", "case 2: pos[0] = qb + M / 2; return 1;"),
 }
@@ -621,7 +682,9 @@ def _pins_pass():
               test_select_uniform_weights_is_farthest_point, lambda: test_select_invariants(0),
               lambda: test_rows_scores_match_bruteforce(1), lambda: test_rows_scores_match_bruteforce(2),
               test_rows_golden_causal, test_source_rows_golden,
-              lambda: test_prefill_matches_bruteforce(1), test_prefill_equal_keys_give_prefix_means]
+              lambda: test_prefill_matches_bruteforce(1), test_prefill_equal_keys_give_prefix_means,
+              lambda: test_connector_matches_matrix_form(W.F32), test_connector_identity_weights_give_gelu_of_layernorm,
+              test_connector_layernorm_is_shift_and_scale_invariant]
     for c in checks:
         try:
             c()
