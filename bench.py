@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--prefill", action="store_true",
                     help="take the scores from the guidance model's causal prefill attention of every "
                          "position (last_prefill_attention) instead of recomputing the last row")
+    ap.add_argument("--connector", action="store_true",
+                    help="apply the cloud connector (last_connector: LayerNorm, Linear, GELU, Linear, "
+                         "Dv -> Dv -> Dv, seeded weights) to the gathered rows in every step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time for the oracle sample")
@@ -120,6 +123,16 @@ def prefill_flops(wl):
     each for the logits and 2 Dh for the value product."""
     P = np.diff(wl.cu_seqlens).astype(np.float64)
     return 4.0 * wl.Dh * wl.G * wl.Hq * float(np.sum(P * (P + 1) / 2))
+
+
+def connector_work(wl):
+    """The cloud connector on the K_total kept rows: LayerNorm reads and writes
+    K Dv bf16 values; the two products take 2 K Dv Dh and 2 K Dh Do flops."""
+    Dh, Do = wl.Dv, wl.Dv
+    K = wl.K_total
+    return {"connector_layernorm": ("hbm", 4 * K * wl.Dv + 8 * wl.Dv),
+            "connector_gemm1": ("mfma", 2.0 * K * wl.Dv * Dh),
+            "connector_gemm2": ("mfma", 2.0 * K * Dh * Do)}
 
 
 def kernel_work(wl, row_pos=None):
@@ -263,6 +276,20 @@ def main():
         ws_s = torch.empty(last.token_scores_workspace(b, dw.q.dtype), dtype=torch.uint8, device=dev)
     ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8, device=dev)
 
+    conn = None
+    if args.connector:
+        if wl.f_dtype != "bf16":
+            raise SystemExit("--connector runs on bf16 features")
+        Dh, Do = W.connector_dims(wl)
+        cw = W.connector_weights(wl.Dv, Dh, Do, W.BF16)
+        f32 = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+        conn = dict(gamma=f32(cw.gamma), beta=f32(cw.beta), w1=last.to_torch(cw.w1, W.BF16, dev), b1=f32(cw.b1),
+                    w2=last.to_torch(cw.w2, W.BF16, dev), b2=f32(cw.b2))
+        conn_out = torch.empty((wl.K_total, Do), dtype=torch.bfloat16, device=dev)
+        ws_c = torch.empty(max(256, last.connector_workspace(wl.K_total, wl.Dv, Dh)), dtype=torch.uint8, device=dev)
+        del cw
+        log(f"[bench] cloud connector {wl.Dv} -> {Dh} -> {Do} on the {wl.K_total} kept rows")
+
     if args.copy_calibration_mib > 0:
         nbytes = args.copy_calibration_mib << 20
         src = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
@@ -283,6 +310,9 @@ def main():
         last.diverse_select(scores, dw.feats, wl.cu_vis, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep,
                             kept=kept, order=order, gains=gains, ws=ws_k)
         last.gather_kept(dw.feats, wl.cu_vis, kept, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep, out=out)
+        if conn is not None:
+            last.connector(out, conn["gamma"], conn["beta"], conn["w1"], conn["b1"], conn["w2"], conn["b2"],
+                           out=conn_out, ws=ws_c)
 
     for _ in range(args.warmup):
         step()
@@ -317,6 +347,8 @@ def main():
     if rows is not None and not single:
         work.update({k: v for k, v in rows_work(wl, rows.cu_rows_h, rows.row_pos_h).items()
                      if k in ("rows_stats", "rows_visual")})
+    if conn is not None:
+        work.update(connector_work(wl))
     kernels = {}
     for name, (launches, total_ms) in prof.items():
         kernels[name] = {"launches": launches, "avg_ms": round(total_ms / max(launches, 1), 5),
@@ -350,6 +382,7 @@ def main():
     select_ms = sum(kernels[k]["ms_per_step"] for k in kernels
                     if k in ("select_plan", "sqnorm", "gram_diag", "gram", "greedy", "topk"))
     gather_ms = kernels.get("gather", {}).get("ms_per_step", 0.0)
+    conn_ms = sum(kernels[k]["ms_per_step"] for k in kernels if k.startswith("connector"))
 
     res = {
         "metric": "requests/sec and visual tokens scored/sec per GPU; p50 select latency",
@@ -366,7 +399,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": describe(wl, args.budget) + ("" if args.source == "last" else
                                                              f"; scores from the {args.source} query rows")
-                   + ("; scores from the causal prefill attention of every position" if pre is not None else ""),
+                   + ("; scores from the causal prefill attention of every position" if pre is not None else "")
+                   + (f"; cloud connector {wl.Dv}->{wl.Dv}->{wl.Dv} on the kept rows" if conn is not None else ""),
                    "requests": wl.R, "visual_tokens": wl.N_total,
                    "kept_tokens": wl.K_total, "arithmetic": (
                        "bf16 inputs, " + ("fp32 FMA score pass" if args.source != "all_mean" else
@@ -377,7 +411,8 @@ def main():
         "p90_select_latency_ms": round(float(np.percentile(step_ms, 90)), 4),
         "ms_per_step_with_kernel_events": round(elapsed_prof / args.steps * 1e3, 4),
         "stage_ms_per_step": {"scores": round(score_ms, 4), "select": round(select_ms, 4),
-                              "gather": round(gather_ms, 4)},
+                              "gather": round(gather_ms, 4)} | (
+                                  {"connector": round(conn_ms, 4)} if conn is not None else {}),
         "kernels": kernels,
         "roofline": main_roof,
         "rooflines": rooflines,

@@ -236,6 +236,39 @@ last_status gather_kept(int32_t R, int32_t Dv, size_t elem_bytes,
                         const int32_t *cu_keep, const int32_t *cu_keep_h,
                         void *out, void *stream);
 
+/* Workspace bytes last_connector needs for K rows: the normalised rows and
+ * the hidden activations, bf16 (0 if the arguments are invalid). */
+size_t last_connector_workspace(int64_t K, int32_t Dv, int32_t Dh);
+
+/*
+ * Sec. 3.4, Eq. 12 (H_S = phi_c(X_S)) and Sec. 3.1: the cloud connector
+ * applied token by token to the K rows the edge transmitted. The paper names
+ * phi_c without a formula; this is the token-wise connector of the model
+ * family it builds on:
+ *   xhat = (x - mean(x)) / sqrt(var(x) + eps) * gamma + beta   (biased var)
+ *   h    = GELU(W1 xhat + b1),  GELU(u) = u (1 + erf(u / sqrt 2)) / 2
+ *   y    = W2 h + b2
+ *   dtype      LAST_BF16 (others: LAST_ERR_UNSUPPORTED)
+ *   K          rows, 0 <= K < 2^31 (0: nothing to do)
+ *   x          [K][Dv] transmitted rows X_S (normally gather_kept's out)
+ *   gamma,beta [Dv] fp32 LayerNorm scale and shift
+ *   w1, b1     [Dh][Dv] (one hidden feature per row, dtype) and [Dh] fp32
+ *   w2, b2     [Do][Dh] (one output feature per row, dtype) and [Do] fp32
+ *   out        [K][Do] out, dtype (rounded to nearest even)
+ *   eps        > 0 and finite (LAST_ERR_INVALID otherwise)
+ * Dv and Dh must be multiples of 64 and Do of 4, each in [64, 65536], and
+ * ceil(K / 128) ceil(max(Dh, Do) / 256) below 2^31 (LAST_ERR_UNSUPPORTED
+ * otherwise). x, w1, w2, b1, b2 and out must be
+ * 16-byte aligned (LAST_ERR_INVALID). xhat and h are rounded to bf16 before
+ * the products, which accumulate in fp32. The workspace (256-byte aligned,
+ * last_connector_workspace bytes) holds xhat and h; the caller owns every
+ * buffer.
+ */
+last_status last_connector(last_dtype dtype, int64_t K, int32_t Dv, int32_t Dh, int32_t Do,
+                           float eps, const void *x, const float *gamma, const float *beta,
+                           const void *w1, const float *b1, const void *w2, const float *b2,
+                           void *out, void *ws, size_t ws_bytes, void *stream);
+
 /* Sec. 3.2, Eq. 2: K = ceil(N * rho_num / rho_den), integer-exact, clamped
  * to [1, N]; returns -1 for N < 1 or a ratio outside (0, 1]. */
 int32_t last_budget(int32_t N, int32_t rho_num, int32_t rho_den);

@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <atomic>
 #include <string>
 #include <vector>
@@ -366,6 +367,46 @@ last_status gather_kept(int32_t R, int32_t Dv, size_t elem_bytes, const void *fe
   if (K_total > 0 && (!feats || !kept || !out)) return LAST_ERR_INVALID;
   const hipError_t e = launch_gather(R, (int64_t)Dv * (int64_t)elem_bytes, K_total, cu_vis_h[R],
                                      feats, cu_vis, kept, cu_keep, out, (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+static bool connector_dims_ok(int64_t K, int32_t Dv, int32_t Dh) {
+  return K >= 0 && K < ((int64_t)1 << 31) && Dv >= 1 && Dh >= 1 && Dv <= 65536 && Dh <= 65536;
+}
+
+static size_t connector_ws(int64_t K, int32_t Dv, int32_t Dh) {
+  Carver c(nullptr);
+  c.take<uint16_t>((size_t)K * Dv);
+  c.take<uint16_t>((size_t)K * Dh);
+  return c.size();
+}
+
+size_t last_connector_workspace(int64_t K, int32_t Dv, int32_t Dh) {
+  if (!connector_dims_ok(K, Dv, Dh)) return 0;
+  return connector_ws(K, Dv, Dh);
+}
+
+last_status last_connector(last_dtype dtype, int64_t K, int32_t Dv, int32_t Dh, int32_t Do, float eps,
+                           const void *x, const float *gamma, const float *beta, const void *w1,
+                           const float *b1, const void *w2, const float *b2, void *out, void *ws,
+                           size_t ws_bytes, void *stream) {
+  if (!connector_dims_ok(K, Dv, Dh) || Do < 1 || Do > 65536) return LAST_ERR_INVALID;
+  if (!(eps > 0.0f) || !std::isfinite(eps)) return LAST_ERR_INVALID;
+  if (dtype != LAST_BF16 && dtype != LAST_F32) return LAST_ERR_INVALID;
+  if (dtype != LAST_BF16 || Dv < 64 || Dh < 64 || Do < 64 || !connector_shape_ok(K, Dv, Dh, Do))
+    return LAST_ERR_UNSUPPORTED;
+  if (K == 0) return LAST_OK;
+  if (!x || !gamma || !beta || !w1 || !b1 || !w2 || !b2 || !out) return LAST_ERR_INVALID;
+  if (!aligned(x, 16) || !aligned(w1, 16) || !aligned(w2, 16) || !aligned(b1, 16) || !aligned(b2, 16) ||
+      !aligned(out, 16) || !aligned(gamma, 4) || !aligned(beta, 4))
+    return LAST_ERR_INVALID;
+  const size_t need = connector_ws(K, Dv, Dh);
+  if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
+  Carver c(ws);
+  void *xn = c.take<uint16_t>((size_t)K * Dv);
+  void *hid = c.take<uint16_t>((size_t)K * Dh);
+  const hipError_t e = launch_connector(K, Dv, Dh, Do, eps, x, gamma, beta, w1, b1, w2, b2, out, xn, hid,
+                                        (hipStream_t)stream);
   return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
 }
 

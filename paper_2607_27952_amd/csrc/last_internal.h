@@ -174,6 +174,15 @@ hipError_t launch_gather(int32_t R, int64_t row_bytes, int64_t K_total, int64_t 
                          const void *feats, const int32_t *cu_vis, const int32_t *kept,
                          const int32_t *cu_keep, void *out, hipStream_t s);
 
+// ------------------------------------------------------------ connector
+// Dims the connector kernels take: Dv, Dh multiples of the 64-column stage,
+// Do of the 4-feature store, and a product grid that fits one launch.
+bool connector_shape_ok(int64_t K, int32_t Dv, int32_t Dh, int32_t Do);
+hipError_t launch_connector(int64_t K, int32_t Dv, int32_t Dh, int32_t Do, float eps, const void *x,
+                            const float *gamma, const float *beta, const void *w1, const float *b1,
+                            const void *w2, const float *b2, void *out, void *xn, void *hid,
+                            hipStream_t s);
+
 }  // namespace last
 
 // ----------------------------------------------------------------- device side

@@ -26,7 +26,7 @@ SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
 EXPORTS = ("last_token_scores_workspace", "last_token_scores", "last_source_rows",
            "last_rows_scores_workspace", "last_rows_scores", "last_prefill_attention_workspace",
            "last_prefill_attention", "diverse_select_workspace",
-           "diverse_select", "gather_kept", "last_budget", "last_status_string", "last_version",
+           "diverse_select", "gather_kept", "last_connector_workspace", "last_connector", "last_budget", "last_status_string", "last_version",
            "last_profile_enable", "last_profile_collect", "last_profile_reset",
            "last_profile_count", "last_profile_kernel")
 
@@ -78,6 +78,11 @@ def lib():
         L.diverse_select.restype = I32
         L.gather_kept.argtypes = [I32, I32, SZ, P, P, P, P, P, P, P, P]
         L.gather_kept.restype = I32
+        I64 = ctypes.c_int64
+        L.last_connector_workspace.argtypes = [I64, I32, I32]
+        L.last_connector_workspace.restype = SZ
+        L.last_connector.argtypes = [I32, I64, I32, I32, I32, ctypes.c_float, P, P, P, P, P, P, P, P, P, SZ, P]
+        L.last_connector.restype = I32
         L.last_budget.argtypes = [I32, I32, I32]
         L.last_budget.restype = I32
         L.last_status_string.argtypes = [I32]
@@ -330,6 +335,37 @@ def gather_kept(feats: torch.Tensor, cu_vis_h, kept: torch.Tensor, cu_keep_h, cu
                            _ptr(kept), _ptr(cu_keep), _ptr(ck), _ptr(out), _stream(stream))
     if st != LAST_OK:
         raise LastError(st, "gather_kept")
+    return out
+
+
+def connector_workspace(K: int, Dv: int, Dh: int) -> int:
+    return int(lib().last_connector_workspace(int(K), int(Dv), int(Dh)))
+
+
+def connector(x: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor,
+              w2: torch.Tensor, b2: torch.Tensor, eps: float = 1e-5, out=None, ws=None, stream=None):
+    """last_connector (Eq. 12, the cloud side): LayerNorm, Linear, GELU, Linear
+    on every row of x [K][Dv]; returns out [K][Do] in x's dtype."""
+    code = _dtype_code(x)
+    if w1.dtype != x.dtype or w2.dtype != x.dtype:
+        raise TypeError("x, w1 and w2 must share a dtype")
+    K, Dv = x.shape
+    Dh, Do = w1.shape[0], w2.shape[0]
+    if w1.shape[1] != Dv or w2.shape[1] != Dh:
+        raise ValueError("w1 must be [Dh][Dv] and w2 [Do][Dh]")
+    for t in (gamma, beta, b1, b2):
+        if t.dtype != torch.float32:
+            raise TypeError("gamma, beta, b1 and b2 must be float32")
+    if gamma.numel() != Dv or beta.numel() != Dv or b1.numel() != Dh or b2.numel() != Do:
+        raise ValueError("gamma and beta need Dv entries, b1 Dh and b2 Do")
+    if out is None:
+        out = torch.empty((K, Do), dtype=x.dtype, device=x.device)
+    if ws is None:
+        ws = _workspace(lib().last_connector_workspace(K, Dv, Dh), x.device)
+    st = lib().last_connector(code, K, Dv, Dh, Do, float(eps), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(w1),
+                              _ptr(b1), _ptr(w2), _ptr(b2), _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "last_connector")
     return out
 
 

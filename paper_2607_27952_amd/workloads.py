@@ -482,3 +482,11 @@ def connector_weights(Dv: int, Dh: int, Do: int, dtype: str = BF16, seed: int = 
     b2 = (0.02 * rng.standard_normal(Do, dtype=f32)).astype(f32)
     return ConnectorWeights(gamma=gamma, beta=beta, w1=_store(w1, dtype), b1=b1, w2=_store(w2, dtype), b2=b2,
                             dtype=dtype)
+
+
+def connector_dims(wl: Workload):
+    """(Dh, Do) of the cloud connector for a workload: a square token-wise MLP
+    at the feature width (Dv -> Dv -> Dv), the shape of a connector whose
+    encoder width already matches the language model's."""
+    return wl.Dv, wl.Dv
+

@@ -261,3 +261,52 @@ def test_prefill_rejects_bad_calls_on_the_host():
     assert L.last_prefill_attention_workspace(ctypes.byref(b32)) == 0
     b.Dh = 96
     assert _prefill_call(b) == last.LAST_ERR_UNSUPPORTED
+
+
+# ------------------------------------------------- cloud connector (Eq. 12)
+
+def _connector_call(dtype=last.LAST_BF16, K=5, Dv=128, Dh=192, Do=64, eps=1e-5, ws_bytes=1 << 34, null=None,
+                    shift=None):
+    bufs = {n: Fake() for n in ("x", "gamma", "beta", "w1", "b1", "w2", "b2", "out", "ws")}
+    ptr = {n: b.p for n, b in bufs.items()}
+    if null:
+        ptr[null] = None
+    if shift:
+        ptr[shift] += 8
+    st = last.lib().last_connector(dtype, K, Dv, Dh, Do, eps, ptr["x"], ptr["gamma"], ptr["beta"], ptr["w1"],
+                                   ptr["b1"], ptr["w2"], ptr["b2"], ptr["out"], ptr["ws"], ws_bytes, None)
+    assert all(b.untouched() for b in bufs.values())
+    return st
+
+
+def test_connector_workspace_query():
+    L = last.lib()
+    # xhat [K][Dv] and h [K][Dh] in bf16, each segment 256-byte aligned
+    assert L.last_connector_workspace(5, 128, 192) == 1280 + 2048
+    assert L.last_connector_workspace(0, 128, 192) == 0
+    assert L.last_connector_workspace(-1, 128, 192) == 0
+    assert L.last_connector_workspace(4, 0, 64) == 0
+
+
+def test_connector_rejects_bad_calls_on_the_host():
+    I, U, W_ = last.LAST_ERR_INVALID, last.LAST_ERR_UNSUPPORTED, last.LAST_ERR_WORKSPACE
+    assert _connector_call(K=-1) == I
+    assert _connector_call(K=1 << 31) == I
+    assert _connector_call(Do=0) == I
+    assert _connector_call(eps=0.0) == I
+    assert _connector_call(eps=float("nan")) == I
+    assert _connector_call(eps=float("inf")) == I
+    assert _connector_call(dtype=7) == I
+    assert _connector_call(dtype=last.LAST_F32) == U
+    assert _connector_call(Dv=96) == U          # not a multiple of 64
+    assert _connector_call(Dh=32) == U
+    assert _connector_call(Do=66) == U          # not a multiple of 4
+    assert _connector_call(Do=60) == U          # under 64
+    for n in ("x", "gamma", "beta", "w1", "b1", "w2", "b2", "out"):
+        assert _connector_call(null=n) == I, n
+    for n in ("x", "w1", "w2", "b1", "b2", "out"):
+        assert _connector_call(shift=n) == I, n
+    assert _connector_call(null="ws") == W_
+    assert _connector_call(ws_bytes=last.lib().last_connector_workspace(5, 128, 192) - 1) == W_
+    # nothing to do: no rows
+    assert _connector_call(K=0, null="x") == last.LAST_OK

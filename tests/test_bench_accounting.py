@@ -64,3 +64,14 @@ def test_prefill_flops_count_causal_rows():
     P = np.diff(wl.cu_seqlens)
     expect = sum(4 * wl.Dh * wl.G * wl.Hq * sum(p + 1 for p in range(n)) for n in P)
     assert bench.prefill_flops(wl) == expect
+
+
+def test_connector_work_counts_two_products_and_one_norm_pass():
+    wl = W.tiny(4, R=2, n_range=(40, 90), t_range=(3, 9), Dv=256)
+    work = bench.connector_work(wl)
+    K, D = wl.K_total, wl.Dv
+    assert W.connector_dims(wl) == (D, D)
+    assert work["connector_gemm1"] == ("mfma", 2.0 * K * D * D)
+    assert work["connector_gemm2"] == ("mfma", 2.0 * K * D * D)
+    # bf16 rows read and normalised rows written, plus gamma and beta in fp32
+    assert work["connector_layernorm"] == ("hbm", 2 * K * D * 2 + 2 * D * 4)
