@@ -257,10 +257,10 @@ size_t last_connector_workspace(int64_t K, int32_t Dv, int32_t Dh);
  *   out        [K][Do] out, dtype (rounded to nearest even)
  *   eps        > 0 and finite (LAST_ERR_INVALID otherwise)
  * Dv and Dh must be multiples of 64 and Do of 4, each in [64, 65536], and
- * ceil(K / 128) ceil(max(Dh, Do) / 256) below 2^31 (LAST_ERR_UNSUPPORTED
- * otherwise). x, w1, w2, b1, b2 and out must be
- * 16-byte aligned (LAST_ERR_INVALID). xhat and h are rounded to bf16 before
- * the products, which accumulate in fp32. The workspace (256-byte aligned,
+ * ceil(K / 256) ceil(max(Dh, Do) / 256) below 2^31 (LAST_ERR_UNSUPPORTED
+ * otherwise). Every pointer must be 16-byte aligned (LAST_ERR_INVALID).
+ * xhat and h are rounded to bf16 before the products, which accumulate in
+ * fp32; GELU's erf is evaluated to within 1e-6 (1 + |u|). The workspace (256-byte aligned,
  * last_connector_workspace bytes) holds xhat and h; the caller owns every
  * buffer.
  */

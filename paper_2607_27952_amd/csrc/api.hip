@@ -398,7 +398,7 @@ last_status last_connector(last_dtype dtype, int64_t K, int32_t Dv, int32_t Dh, 
   if (K == 0) return LAST_OK;
   if (!x || !gamma || !beta || !w1 || !b1 || !w2 || !b2 || !out) return LAST_ERR_INVALID;
   if (!aligned(x, 16) || !aligned(w1, 16) || !aligned(w2, 16) || !aligned(b1, 16) || !aligned(b2, 16) ||
-      !aligned(out, 16) || !aligned(gamma, 4) || !aligned(beta, 4))
+      !aligned(out, 16) || !aligned(gamma, 16) || !aligned(beta, 16))
     return LAST_ERR_INVALID;
   const size_t need = connector_ws(K, Dv, Dh);
   if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;

@@ -304,7 +304,7 @@ def test_connector_rejects_bad_calls_on_the_host():
     assert _connector_call(Do=60) == U          # under 64
     for n in ("x", "gamma", "beta", "w1", "b1", "w2", "b2", "out"):
         assert _connector_call(null=n) == I, n
-    for n in ("x", "w1", "w2", "b1", "b2", "out"):
+    for n in ("x", "gamma", "beta", "w1", "w2", "b1", "b2", "out"):
         assert _connector_call(shift=n) == I, n
     assert _connector_call(null="ws") == W_
     assert _connector_call(ws_bytes=last.lib().last_connector_workspace(5, 128, 192) - 1) == W_

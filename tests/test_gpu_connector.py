@@ -14,7 +14,9 @@ are independent. Propagated to first order (GELU' at the oracle's h):
   var_g  = GELU'(h)^2 var_h + (u g)^2 / 3
   var_y  = var_g (W2^2)^T,               acc2 = (Dh/16 + 4) 2^-23 (|g| |W2|^T + |b2|)
 (the fp32 LayerNorm term covers its reductions; acc1 and acc2 are worst-case
-fp32 accumulation, one ulp per matrix-core add). Bars, with s = sqrt(var_y):
+fp32 accumulation, one ulp per matrix-core add; acc2 also carries the GELU's
+evaluation error, at most 1e-6 (1 + |h|) per hidden feature, through |W2|).
+Bars, with s = sqrt(var_y):
   * every element: |y_gpu - y| <= 8 s + acc2 + u (|y| + 8 s) + 1e-6
     (Hoeffding: a bounded, zero-mean sum strays past 8 s with probability
     below 2 e^-32);
@@ -73,7 +75,7 @@ def expected(x, cw, eps=1e-5):
     dg = cdf + h * np.exp(-0.5 * h * h) / math.sqrt(2.0 * math.pi)
     var_g = dg ** 2 * var_h + (U * g) ** 2 / 3
     var_y = var_g @ (w2 ** 2).T
-    acc2 = (Dh / 16 + 4) * 2.0 ** -23 * (np.abs(g) @ np.abs(w2).T + np.abs(b2))
+    acc2 = (Dh / 16 + 4) * 2.0 ** -23 * (np.abs(g) @ np.abs(w2).T + np.abs(b2)) + (1e-6 * (1 + np.abs(h))) @ np.abs(w2).T
     return y, var_y, acc2
 
 
