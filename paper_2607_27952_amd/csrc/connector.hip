@@ -39,9 +39,10 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b) {
 
 // ---------------------------------------------------------------- LayerNorm
 // One wave per row, 16-byte pieces (8 values): lane l takes pieces l, l + 64,
-// ... The first pass reads the row from HBM; the second (squared deviations)
-// and third (normalise, write) read it again from cache. Sums are fp32, each
-// lane's in piece order, then across the wave in a fixed order.
+// ... Rows of up to 64 NP pieces are loaded once into registers (all loads
+// in flight together); longer rows stream, reading the row again from cache
+// for the deviations and the output. Sums are fp32, each lane's in piece
+// order, then across the wave in a fixed order.
 constexpr int kLnWaves = 4;
 
 __device__ __forceinline__ void unpack8(const uint4 &w, float *v) {
@@ -53,6 +54,23 @@ __device__ __forceinline__ void unpack8(const uint4 &w, float *v) {
   }
 }
 
+__device__ __forceinline__ uint4 norm8(const uint4 &w, float mean, float rstd, const float *__restrict__ gamma,
+                                       const float *__restrict__ beta, int p) {
+  float v[8];
+  unpack8(w, v);
+  const float4 *g4 = reinterpret_cast<const float4 *>(gamma);
+  const float4 *b4 = reinterpret_cast<const float4 *>(beta);
+  const float4 ga = g4[2 * p], gb = g4[2 * p + 1], ba = b4[2 * p], bb = b4[2 * p + 1];
+  const float g[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
+  const float b[8] = {ba.x, ba.y, ba.z, ba.w, bb.x, bb.y, bb.z, bb.w};
+  float y[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) y[i] = (v[i] - mean) * rstd * g[i] + b[i];
+  return make_uint4(pack_bf16(y[0], y[1]), pack_bf16(y[2], y[3]), pack_bf16(y[4], y[5]), pack_bf16(y[6], y[7]));
+}
+
+// NP > 0: at most NP pieces per lane, held in registers; NP == 0: streaming.
+template <int NP>
 __global__ __launch_bounds__(64 * kLnWaves) void k_layernorm(const uint16_t *__restrict__ x,
                                                              const float *__restrict__ gamma,
                                                              const float *__restrict__ beta, int64_t K,
@@ -61,34 +79,49 @@ __global__ __launch_bounds__(64 * kLnWaves) void k_layernorm(const uint16_t *__r
   const int64_t t = (int64_t)blockIdx.x * kLnWaves + (threadIdx.x >> 6);
   if (t >= K) return;
   const uint4 *row = reinterpret_cast<const uint4 *>(x + t * Dv);
+  uint4 *out = reinterpret_cast<uint4 *>(xn + t * Dv);
   const int np = Dv / 8;
   float v[8];
-  float s = 0.f;
-  for (int p = lane; p < np; p += 64) {
-    unpack8(row[p], v);
+  if constexpr (NP > 0) {
+    uint4 w[NP];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) s += v[i];
-  }
-  const float mean = wave_sum(s) / (float)Dv;
-  float c2 = 0.f;
-  for (int p = lane; p < np; p += 64) {
-    unpack8(row[p], v);
+    for (int i = 0; i < NP; ++i) w[i] = lane + 64 * i < np ? row[lane + 64 * i] : make_uint4(0, 0, 0, 0);
+    float s = 0.f;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) c2 = fmaf(v[i] - mean, v[i] - mean, c2);
-  }
-  const float rstd = 1.0f / sqrtf(wave_sum(c2) / (float)Dv + eps);
-  uint4 *out = reinterpret_cast<uint4 *>(xn + t * Dv);
-  const float4 *g4 = reinterpret_cast<const float4 *>(gamma);
-  const float4 *b4 = reinterpret_cast<const float4 *>(beta);
-  for (int p = lane; p < np; p += 64) {
-    unpack8(row[p], v);
-    const float4 ga = g4[2 * p], gb = g4[2 * p + 1], ba = b4[2 * p], bb = b4[2 * p + 1];
-    const float g[8] = {ga.x, ga.y, ga.z, ga.w, gb.x, gb.y, gb.z, gb.w};
-    const float b[8] = {ba.x, ba.y, ba.z, ba.w, bb.x, bb.y, bb.z, bb.w};
-    float y[8];
+    for (int i = 0; i < NP; ++i) {
+      unpack8(w[i], v);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) y[i] = (v[i] - mean) * rstd * g[i] + b[i];
-    out[p] = make_uint4(pack_bf16(y[0], y[1]), pack_bf16(y[2], y[3]), pack_bf16(y[4], y[5]), pack_bf16(y[6], y[7]));
+      for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    const float mean = wave_sum(s) / (float)Dv;
+    float c2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+      if (lane + 64 * i >= np) break;
+      unpack8(w[i], v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) c2 = fmaf(v[j] - mean, v[j] - mean, c2);
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(c2) / (float)Dv + eps);
+#pragma unroll
+    for (int i = 0; i < NP; ++i)
+      if (lane + 64 * i < np) out[lane + 64 * i] = norm8(w[i], mean, rstd, gamma, beta, lane + 64 * i);
+  } else {
+    float s = 0.f;
+    for (int p = lane; p < np; p += 64) {
+      unpack8(row[p], v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s += v[j];
+    }
+    const float mean = wave_sum(s) / (float)Dv;
+    float c2 = 0.f;
+    for (int p = lane; p < np; p += 64) {
+      unpack8(row[p], v);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) c2 = fmaf(v[j] - mean, v[j] - mean, c2);
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(c2) / (float)Dv + eps);
+    for (int p = lane; p < np; p += 64) out[p] = norm8(row[p], mean, rstd, gamma, beta, p);
   }
 }
 
@@ -311,8 +344,17 @@ hipError_t launch_connector(int64_t K, int32_t Dv, int32_t Dh, int32_t Do, float
                             hipStream_t s) {
   if (K == 0) return hipSuccess;
   launch_begin("connector_layernorm", s);
-  hipLaunchKernelGGL(k_layernorm, dim3((unsigned)((K + kLnWaves - 1) / kLnWaves)), dim3(64 * kLnWaves), 0, s,
-                     (const uint16_t *)x, gamma, beta, K, Dv, eps, (uint16_t *)xn);
+  const dim3 grid((unsigned)((K + kLnWaves - 1) / kLnWaves)), block(64 * kLnWaves);
+  const int per_lane = (Dv / 8 + 63) / 64;
+  if (per_lane <= 4)
+    hipLaunchKernelGGL(k_layernorm<4>, grid, block, 0, s, (const uint16_t *)x, gamma, beta, K, Dv, eps,
+                       (uint16_t *)xn);
+  else if (per_lane <= 8)
+    hipLaunchKernelGGL(k_layernorm<8>, grid, block, 0, s, (const uint16_t *)x, gamma, beta, K, Dv, eps,
+                       (uint16_t *)xn);
+  else
+    hipLaunchKernelGGL(k_layernorm<0>, grid, block, 0, s, (const uint16_t *)x, gamma, beta, K, Dv, eps,
+                       (uint16_t *)xn);
   hipError_t e = launch_end(s);
   if (e != hipSuccess) return e;
   e = launch_gemm<true>(w1, xn, b1, K, Dh, Dv, hid, s);

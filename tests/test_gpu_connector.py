@@ -124,6 +124,8 @@ CASES = [
     (3, 300, 512, 512, 512),     # several token tiles
     (4, 77, 1024, 768, 1024),    # deeper products, ragged features in the first GEMM
     (5, 256, 192, 1024, 100),    # Dv of three stages, small Do
+    (6, 40, 4160, 128, 64),      # rows too long for registers: streaming LayerNorm
+    (7, 33, 2560, 256, 128),     # register LayerNorm with lanes short of pieces
 ]
 
 
