@@ -604,6 +604,25 @@ def test_connector_layernorm_is_shift_and_scale_invariant():
     np.testing.assert_allclose(_orc_connector(x * np.float32(8.0), cw, eps=0.0), y, rtol=1e-12, atol=1e-14)
 
 
+def test_connector_one_hot_weights_closed_form():
+    """Hand-derived: x = (3, 1, -1, -3) has mean 0 and variance 5, so eps = 4
+    gives rstd = 1/3; beta shifts the last feature by 1/2. One-hot rows of W1
+    (not symmetric, Dh != Dv) pick features, b1 biases one hidden unit, and
+    W2 (Do != Dh) picks, scales and adds hidden units; b2 shifts one output."""
+    f32 = lambda a: np.asarray(a, np.float32)
+    gelu = lambda u: 0.5 * u * (1 + math.erf(u / math.sqrt(2)))
+    w1 = np.zeros((5, 4), np.float32)
+    for j, src in enumerate([1, 3, 0, 2, 1]):
+        w1[j, src] = 1.0
+    w2 = f32([[0, 0, 0, 0, 2], [-1, 0, 0, 0, 0], [0, 1, 1, 0, 0]])
+    cw = W.ConnectorWeights(gamma=f32([1, 1, 1, 1]), beta=f32([0, 0, 0, 0.5]), w1=w1,
+                            b1=f32([0, 0, 0, 0, 0.25]), w2=w2, b2=f32([0, 0.125, 0]), dtype=W.F32)
+    y, xh, h = _orc_connector(f32([[3, 1, -1, -3]]), cw, eps=4.0, want_intermediate=True)
+    np.testing.assert_allclose(xh[0], [1, 1 / 3, -1 / 3, -0.5], rtol=1e-15)
+    np.testing.assert_allclose(h[0], [1 / 3, -0.5, 1, -1 / 3, 7 / 12], rtol=1e-15)
+    np.testing.assert_allclose(y[0], [2 * gelu(7 / 12), -gelu(1 / 3) + 0.125, gelu(1) + gelu(-0.5)], rtol=1e-14)
+
+
 # ---------------------------------------------------------------- planted mistakes
 
 MUTANTS = {
@@ -655,6 +674,10 @@ MUTANTS = {
     "ln_no_mean": ("mean /= Dv;", "mean = 0.0;"),
     # connector: first bias dropped
     "no_b1": ("double acc = b1[j];", "double acc = 0.0 * b1[j];"),
+    # connector: first weight matrix read transposed
+    "w1_transposed": ("orc_widen(w1, (int64_t)j * Dv + d, dtype)", "orc_widen(w1, (int64_t)d * Dh + j, dtype)"),
+    # connector: eps added outside the square root
+    "eps_outside_sqrt": ("const double rstd = 1.0 / sqrt(var + eps);", "const double rstd = 1.0 / (sqrt(var) + eps);"),
     # Middle taken as q_(floor(M/2)+1) instead of q_ceil(M/2)
     "middle_floor": ("case 2: pos[0] = qb + (M + 1) / 2 - 1; return 1;", "case 2: pos[0] = qb + M / 2; return 1;"),
 }
@@ -683,7 +706,7 @@ def _pins_pass():
               lambda: test_rows_scores_match_bruteforce(1), lambda: test_rows_scores_match_bruteforce(2),
               test_rows_golden_causal, test_source_rows_golden,
               lambda: test_prefill_matches_bruteforce(1), test_prefill_equal_keys_give_prefix_means,
-              lambda: test_connector_matches_matrix_form(W.F32), test_connector_identity_weights_give_gelu_of_layernorm,
+              test_connector_one_hot_weights_closed_form, test_connector_identity_weights_give_gelu_of_layernorm,
               test_connector_layernorm_is_shift_and_scale_invariant]
     for c in checks:
         try:
