@@ -241,7 +241,7 @@ last_status gather_kept(int32_t R, int32_t Dv, size_t elem_bytes,
 size_t last_connector_workspace(int64_t K, int32_t Dv, int32_t Dh);
 
 /*
- * Sec. 3.4, Eq. 12 (H_S = phi_c(X_S)) and Sec. 3.1: the cloud connector
+ * Sec. 3.4 after Eq. 12 (H_S = phi_c(X_S)) and Sec. 3.2: the cloud connector
  * applied token by token to the K rows the edge transmitted. The paper names
  * phi_c without a formula; this is the token-wise connector of the model
  * family it builds on:

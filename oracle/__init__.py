@@ -15,7 +15,7 @@ Each function names the paper passage it follows (arXiv 2607.27952, Sec. 3):
   rows_scores -- Table 4 attention sources: Eq. 6-8 over any set of causal
              query rows per request (first / middle / every query token)
   source_rows -- the row positions of each Table 4 attention source
-  connector -- Sec. 3.4, Eq. 12: the cloud's token-wise connector on X_S
+  connector -- Sec. 3.4 (after Eq. 12), Sec. 3.2: the cloud's token-wise connector on X_S
   prefill -- Sec. 3.3: the guidance model's causal prefill attention
              (every query row), whose last row Eq. 7 reads
 """
@@ -129,7 +129,7 @@ SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
 
 
 def connector(x, gamma, beta, w1, b1, w2, b2, dtype, eps=1e-5, want_intermediate=False, nthreads=0):
-    """Eq. 12's phi_c in fp64: y [K][Do] (and xhat [K][Dv], h [K][Dh] if asked)."""
+    """phi_c of Sec. 3.2 / 3.4 on X_S (Eq. 12) in fp64: y [K][Do] (and xhat [K][Dv], h [K][Dh] if asked)."""
     x, xd = _storage(x, dtype)
     w1, _ = _storage(w1, dtype)
     w2, _ = _storage(w2, dtype)

@@ -28,7 +28,7 @@
  *   - Sec. 3.2, Eq. 2: K = ceil(rho * N).
  *   - Sec. 4.3, Table 4: other attention sources (first, middle or every
  *     query token instead of the last), each row causal.
- *   - Sec. 3.4, Eq. 12: the cloud's token-wise connector on the kept rows
+ *   - Sec. 3.4 (after Eq. 12) and Sec. 3.2: the cloud's token-wise connector on the kept rows
  *     (a LayerNorm and a two-layer GELU MLP; a reading of the model family).
  *   - Sec. 3.3: the causal prefill attention of the guidance model itself
  *     (every query row, softmax-weighted sum of the values), whose last row
@@ -327,7 +327,7 @@ int oracle_prefill(int R, int G, int Hq, int Hkv, int Dh, int qk_dtype,
 }
 
 /*
- * Sec. 3.4, Eq. 12: the cloud applies its token-wise connector to the
+ * Sec. 3.4 (after Eq. 12), Sec. 3.2: the cloud applies its token-wise connector to the
  * transmitted rows, H_S = phi_c(X_S). Reading (the paper gives no formula;
  * this is the token-wise connector structure of the InternVL models it uses):
  *   xhat = (x - mean(x)) / sqrt(var(x) + eps) * gamma + beta     (LayerNorm)

@@ -1,5 +1,6 @@
 // The cloud's token-wise connector on the transmitted rows (arXiv
-// 2607.27952, Sec. 3.4, Eq. 12: H_S = phi_c(X_S)) for gfx950, bf16:
+// 2607.27952: Sec. 3.4 applies phi_c to the rows of Eq. 12, H_S = phi_c(X_S);
+// Sec. 3.2 defines phi_c as a token-wise connector) for gfx950, bf16:
 //
 //   xhat = LayerNorm(x) = (x - mean) / sqrt(var + eps) * gamma + beta
 //   h    = GELU(W1 xhat + b1)        (GELU with erf)

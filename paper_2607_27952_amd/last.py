@@ -344,7 +344,7 @@ def connector_workspace(K: int, Dv: int, Dh: int) -> int:
 
 def connector(x: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor, w1: torch.Tensor, b1: torch.Tensor,
               w2: torch.Tensor, b2: torch.Tensor, eps: float = 1e-5, out=None, ws=None, stream=None):
-    """last_connector (Eq. 12, the cloud side): LayerNorm, Linear, GELU, Linear
+    """last_connector (Sec. 3.4 after Eq. 12, the cloud side): LayerNorm, Linear, GELU, Linear
     on every row of x [K][Dv]; returns out [K][Do] in x's dtype."""
     code = _dtype_code(x)
     if w1.dtype != x.dtype or w2.dtype != x.dtype:

@@ -263,7 +263,7 @@ def test_prefill_rejects_bad_calls_on_the_host():
     assert _prefill_call(b) == last.LAST_ERR_UNSUPPORTED
 
 
-# ------------------------------------------------- cloud connector (Eq. 12)
+# ------------------------------------- cloud connector (Sec. 3.2, 3.4 after Eq. 12)
 
 def _connector_call(dtype=last.LAST_BF16, K=5, Dv=128, Dh=192, Do=64, eps=1e-5, ws_bytes=1 << 34, null=None,
                     shift=None):

@@ -1,4 +1,5 @@
-"""The cloud connector phi_c on the transmitted rows (Eq. 12, H_S = phi_c(X_S))
+"""The cloud connector phi_c on the transmitted rows (Sec. 3.4 after Eq. 12:
+H_S = phi_c(X_S); Sec. 3.2: phi_c is token-wise)
 on the HIP path vs the CPU oracle (needs an MI355X).
 
 Tolerance, derived from the arithmetic. The kernels round xhat and the GELU
@@ -142,7 +143,7 @@ def test_connector_parity_small(case):
 
 def test_connector_deterministic_and_rowwise():
     """Same inputs give the same bits; a row's output does not depend on the
-    other rows or on where the row sits in the batch (token-wise, Eq. 12)."""
+    other rows or on where the row sits in the batch (token-wise, Sec. 3.2)."""
     cw = W.connector_weights(256, 256, 256, W.BF16, seed=9)
     x = rows(9, 300, 256, "wide")
     a = run(x, cw)

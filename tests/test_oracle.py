@@ -551,7 +551,7 @@ def test_prefill_last_row_weights_are_the_token_scores_rows():
 
 
 
-# ------------------------------------------------- cloud connector (Eq. 12)
+# ------------------------------------- cloud connector (Sec. 3.2, 3.4 after Eq. 12)
 
 def _orc_connector(x, cw, eps=1e-5, **kw):
     return oracle.connector(x, cw.gamma, cw.beta, cw.w1, cw.b1, cw.w2, cw.b2, _fcode(cw.dtype), eps=eps, **kw)
