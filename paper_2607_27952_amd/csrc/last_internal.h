@@ -118,7 +118,7 @@ hipError_t launch_rows(const last_batch *b, const RowsPlan &p, const RowsWs &w,
 
 // ------------------------------------------------------------ selection
 constexpr int kGramTile = 128;       // Gram tile edge (rows of X per side)
-constexpr int kSelMaxN = 16384;      // largest request the register-resident greedy holds
+constexpr int kSelMaxN = 32768;      // largest request the register-resident greedy holds
 
 // A request's coverage matrix is stored as nb x nb tiles of 128 x 128 floats
 // (nb = ceil(N_r / 128)), tile (I, J) at element (I * nb + J) * 128 * 128 and

@@ -942,13 +942,14 @@ __device__ __forceinline__ float clean_score(float w) { return w > 0.f ? w : 0.f
 
 // Ascending compaction of flagged elements (element e of thread t is index
 // t + e * blockDim). Writes dst[rank] = index.
-template <int EPT>
-__device__ void compact_ascending(const bool (&flag)[EPT], int32_t *dst, int *sh) {
+template <int EPT, typename Flag>
+__device__ void compact_ascending(Flag flag, int32_t *dst, int *sh) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int base = 0;
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
-    const unsigned long long m = __ballot(flag[e]);
+    const bool f = flag(e);
+    const unsigned long long m = __ballot(f);
     const int before_lane = __popcll(m & ((1ull << lane) - 1ull));
     if (lane == 0) sh[wave] = __popcll(m);
     __syncthreads();
@@ -957,14 +958,14 @@ __device__ void compact_ascending(const bool (&flag)[EPT], int32_t *dst, int *sh
       if (w < wave) before_wave += sh[w];
       tot += sh[w];
     }
-    if (flag[e]) dst[base + before_wave + before_lane] = (int32_t)(threadIdx.x + e * blockDim.x);
+    if (f) dst[base + before_wave + before_lane] = (int32_t)(threadIdx.x + e * blockDim.x);
     base += tot;
     __syncthreads();
   }
 }
 
-// Eq. 9-11 for one request per block of NTH threads (64, 256 or 512); thread t
-// holds tokens t + e * NTH. w is the relevance (NaN for tokens past N_r), dl
+// Eq. 9-11 for one request per block of NTH threads (64, 256, 512 or 1024);
+// thread t holds tokens t + e * NTH. w is the relevance (NaN for tokens past N_r), dl
 // the running minimum coverage distance to the picks so far. A pick j's row of
 // the coverage matrix carries -inf at j, so after it is folded in, the pick's
 // objective w * dl is -inf or NaN and never wins again. Each thread keeps the
@@ -994,13 +995,24 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // offset of this thread's element e within a row of the tile-major
   // coverage matrix (index clamped into the request, so the tail re-reads
-  // element N - 1; those lanes carry NaN relevance and never win)
-  int32_t coff[EPT];
-#pragma unroll
-  for (int e = 0; e < EPT; ++e) {
+  // element N - 1; those lanes carry NaN relevance and never win). With 1024
+  // threads a wave has 128 registers, too few to hold the offsets: there
+  // they are rebuilt every step as base + e * 8 tiles (1024 tokens span
+  // exactly eight 128-token tile columns), clamped at element N - 1's offset
+  // (offsets grow with the index, so the clamp maps exactly the tail).
+  constexpr bool kHoldOff = NTH < 1024;
+  static_assert(kHoldOff || NTH % kTile == 0, "rebuilt offsets need whole tile columns per e");
+  auto cov_off = [&](int e) -> int32_t {
     const int i = min(tid + e * NTH, N - 1);
-    coff[e] = (int32_t)((i / kTile) * kCovTileElems + i % kTile);
+    return (int32_t)((i / kTile) * kCovTileElems + i % kTile);
+  };
+  int32_t coff[kHoldOff ? EPT : 1];
+  if constexpr (kHoldOff) {
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) coff[e] = cov_off(e);
   }
+  const int32_t off0 = (int32_t)((tid / kTile) * kCovTileElems + tid % kTile);
+  const int32_t off_last = (int32_t)(((N - 1) / kTile) * kCovTileElems + (N - 1) % kTile);
 
   float w[EPT], dl[EPT];
 #pragma unroll
@@ -1068,13 +1080,19 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
     // fold the last pick's coverage row into the running minimum (Eq. 10);
     // every load is issued before any is used
     const float *row = D + ((int64_t)(j / kTile) * nbr) * kCovTileElems + (j % kTile) * kTile;
-    float rv[EPT];
+    float o[EPT];   // the row, then the objective in place
+    if constexpr (kHoldOff) {
 #pragma unroll
-    for (int e = 0; e < EPT; ++e) rv[e] = row[coff[e]];
-    float o[EPT];
+      for (int e = 0; e < EPT; ++e) o[e] = row[coff[e]];
+    } else {
+      int32_t lim = off_last;
+      asm volatile("" : "+v"(lim));   // opaque per step: the offsets are not hoisted into registers
+#pragma unroll
+      for (int e = 0; e < EPT; ++e) o[e] = row[min(off0 + e * (int32_t)((NTH / kTile) * kCovTileElems), lim)];
+    }
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-      dl[e] = fminf(dl[e], rv[e]);
+      dl[e] = fminf(dl[e], o[e]);
       o[e] = w[e] * dl[e];   // Eq. 11 objective; -inf or NaN once picked, NaN past N_r
     }
     thread_best(o, bo, bi);
@@ -1096,7 +1114,7 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
   }
   (void)taken;
   __syncthreads();
-  compact_ascending<EPT>(sel, kept + k0, s_cnt);
+  compact_ascending<EPT>([&](int e) { return sel[e]; }, kept + k0, s_cnt);
 }
 template <int EPT>
 __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
@@ -1118,14 +1136,12 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
   const int K = cu_keep[r + 1] - (int)k0;
   const int tid = threadIdx.x, nth = blockDim.x;
 
+  // validity and the take flags are recomputed or kept as bits: with 1024
+  // threads and 32 keys a thread, a wave has no registers to spare
   unsigned key[EPT];
-  bool valid[EPT];
+  auto valid = [&](int e) { return tid + e * nth < N; };
 #pragma unroll
-  for (int e = 0; e < EPT; ++e) {
-    const int i = tid + e * nth;
-    valid[e] = i < N;
-    key[e] = valid[e] ? __float_as_uint(clean_score(scores[n0 + i])) : 0u;
-  }
+  for (int e = 0; e < EPT; ++e) key[e] = valid(e) ? __float_as_uint(clean_score(scores[n0 + tid + e * nth])) : 0u;
   if (tid == 0) {
     s_prefix = 0u;
     s_remaining = K;
@@ -1137,7 +1153,7 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
     const unsigned prefix = s_prefix;
 #pragma unroll
     for (int e = 0; e < EPT; ++e)
-      if (valid[e] && (key[e] & mask) == prefix) atomicAdd(&hist[(key[e] >> shift) & 255u], 1);
+      if (valid(e) && (key[e] & mask) == prefix) atomicAdd(&hist[(key[e] >> shift) & 255u], 1);
     __syncthreads();
     if (tid == 0) {
       int cum = 0, rem = s_remaining, d = 255;
@@ -1153,14 +1169,15 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
   }
   const unsigned thr = s_prefix;
   const int need = s_remaining;   // how many keys equal to thr to take, lowest index first
-  bool take[EPT];
+  static_assert(EPT <= 32, "take flags are one 32-bit mask");
+  uint32_t take = 0u;
   // rank the threshold-equal keys by index
   {
     const int lane = tid & 63, wave = tid >> 6, nw = nth >> 6;
     int base = 0;
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-      const bool eq = valid[e] && key[e] == thr;
+      const bool eq = valid(e) && key[e] == thr;
       const unsigned long long m = __ballot(eq);
       if (lane == 0) s_cnt[wave] = __popcll(m);
       __syncthreads();
@@ -1170,12 +1187,12 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
         tot += s_cnt[w];
       }
       const int rank = base + bw + __popcll(m & ((1ull << lane) - 1ull));
-      take[e] = valid[e] && (key[e] > thr || (eq && rank < need));
+      take |= (valid(e) && (key[e] > thr || (eq && rank < need)) ? 1u : 0u) << e;
       base += tot;
       __syncthreads();
     }
   }
-  compact_ascending<EPT>(take, kept + k0, s_cnt);
+  compact_ascending<EPT>([&](int e) { return ((take >> e) & 1u) != 0u; }, kept + k0, s_cnt);
   __threadfence_block();
   __syncthreads();
   if (!order && !gains) return;
@@ -1192,7 +1209,7 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < EPT; ++e) {
-      if (!take[e]) continue;
+      if (!((take >> e) & 1u)) continue;
       const unsigned long long mine = obj_key(__uint_as_float(key[e]), tid + e * nth);
       int c = 0;
       for (int x = 0; x < ns; ++x) c += s_keys[x] > mine ? 1 : 0;
@@ -1202,7 +1219,7 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
   }
 #pragma unroll
   for (int e = 0; e < EPT; ++e) {
-    if (!take[e]) continue;
+    if (!((take >> e) & 1u)) continue;
     if (order) order[k0 + rank[e]] = tid + e * nth;
     if (gains) gains[k0 + rank[e]] = __uint_as_float(key[e]);
   }
@@ -1230,7 +1247,7 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   }
   p.threads = p.N_max > 1024 ? 1024 : std::max(64, (p.N_max + 63) / 64 * 64);
   const int ept = (p.N_max + p.threads - 1) / p.threads;
-  p.ept = ept <= 1 ? 1 : ept <= 2 ? 2 : ept <= 4 ? 4 : ept <= 8 ? 8 : 16;
+  p.ept = ept <= 1 ? 1 : ept <= 2 ? 2 : ept <= 4 ? 4 : ept <= 8 ? 8 : ept <= 16 ? 16 : 32;
   // greedy: one wave up to 1024 tokens (no block barrier per step), else 256
   // threads (one wave per SIMD) with up to 64 tokens each
   if (p.N_max <= 1024) {
@@ -1241,8 +1258,11 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
     p.g_threads = 256;
     const int e = (p.N_max + 255) / 256;
     p.g_ept = e <= 8 ? 8 : e <= 16 ? 16 : 32;
+  } else if (p.N_max <= 16384) {
+    p.g_threads = 512;   // 32 tokens a thread
+    p.g_ept = 32;
   } else {
-    p.g_threads = 512;   // up to kSelMaxN = 16384 tokens, 32 a thread
+    p.g_threads = 1024;  // up to kSelMaxN = 32768 tokens, 32 a thread
     p.g_ept = 32;
   }
   return p;
@@ -1280,7 +1300,8 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
       case 2: LAST_TOPK(2); break;
       case 4: LAST_TOPK(4); break;
       case 8: LAST_TOPK(8); break;
-      default: LAST_TOPK(16); break;
+      case 16: LAST_TOPK(16); break;
+      default: LAST_TOPK(32); break;
     }
 #undef LAST_TOPK
     return launch_end(s);
@@ -1353,8 +1374,10 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
       case 16: LAST_GREEDY(16, 256); break;
       default: LAST_GREEDY(32, 256); break;
     }
-  } else {
+  } else if (p.g_threads == 512) {
     LAST_GREEDY(32, 512);
+  } else {
+    LAST_GREEDY(32, 1024);
   }
 #undef LAST_GREEDY
   return launch_end(s);

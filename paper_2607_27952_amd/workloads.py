@@ -25,6 +25,11 @@ Five named workloads mirror the shapes of the paper's settings:
                   features with frame-to-frame redundancy and scene cuts
                   every 16 frames.
 
+One more, beyond the paper's settings, measures requests past 16384 tokens:
+
+  x1_long_video   2 requests of 128 frames x 256 = 32768 visual + 128 text
+                  tokens, otherwise shaped like c5_video; B=4096 (12.5%).
+
 Conventions (shared with the C-ABI):
   q     [G][R][Hq][Dh]         the last query token of each request
   k     [G][T_total][Hkv][Dh]  keys of every prefill token, CSR by cu_seqlens
@@ -48,7 +53,8 @@ F32 = "f32"
 BF16 = "bf16"
 
 CONFIGS = ("c1_single_fp32", "c2_llava15", "c3_llava_next", "c4_dynres", "c5_video")
-_CONFIG_IDS = {name: i for i, name in enumerate(CONFIGS)}
+EXTRA = ("x1_long_video",)
+_CONFIG_IDS = {name: i for i, name in enumerate(CONFIGS + EXTRA)}
 
 
 def to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -241,7 +247,7 @@ def make(name: str, budget: Optional[int] = None, sharp: bool = False, seed: int
     the streams for sizes, q, k, planted tokens and features; the k and feature
     streams spawn one child per request (per layer and request for k)."""
     if name not in _CONFIG_IDS:
-        raise ValueError(f"unknown workload {name!r}; expected one of {CONFIGS}")
+        raise ValueError(f"unknown workload {name!r}; expected one of {CONFIGS + EXTRA}")
     ss = np.random.SeedSequence([2607, 27952, _CONFIG_IDS[name], seed])
     ss_sizes, ss_q, ss_k, ss_plant, ss_feat = ss.spawn(5)
     s_sizes = np.random.default_rng(ss_sizes)
@@ -269,11 +275,16 @@ def make(name: str, budget: Optional[int] = None, sharp: bool = False, seed: int
         T = s_sizes.integers(32, 257, size=R)
         qkd, fd = BF16, BF16
         K = None if budget is None else budget
-    else:  # c5_video
+    elif name == "c5_video":
         R, G, Hq, Hkv, Dh, Dv = 8, 4, 28, 4, 128, 3584
         N = np.full(R, 64 * 256); T = np.full(R, 128)
         qkd, fd = BF16, BF16
         K = 1024 if budget is None else budget
+    else:  # x1_long_video
+        R, G, Hq, Hkv, Dh, Dv = 2, 4, 28, 4, 128, 3584
+        N = np.full(R, 128 * 256); T = np.full(R, 128)
+        qkd, fd = BF16, BF16
+        K = 4096 if budget is None else budget
 
     N = N.astype(np.int64)
     T = T.astype(np.int64)
@@ -322,7 +333,7 @@ def make(name: str, budget: Optional[int] = None, sharp: bool = False, seed: int
             x = _features_c3(rng, n, Dv)
         elif name == "c4_dynres":
             x = _mixture(rng, n, Dv, 128, 0.3)
-        else:
+        else:   # c5_video, x1_long_video
             x = _features_c5(rng, n, Dv)
         f_out[int(cu_vis[r]):int(cu_vis[r + 1])] = _store(x, fd)
 

@@ -161,7 +161,7 @@ def test_select_rejects_bad_budgets_and_shapes():
     assert _select_call([0, 10, 30], [0, 5, 6], mode=5) == E
     assert _select_call([0, 10, 30], [0, 5, 6], fdtype=3) == E
     U = last.LAST_ERR_UNSUPPORTED
-    assert _select_call([0, 16385], [0, 5]) == U                  # request larger than the greedy holds
+    assert _select_call([0, 32769], [0, 5]) == U                  # request larger than the greedy holds
     assert _select_call([0, 10, 30], [0, 5, 6], Dv=60) == U       # bf16 rows not 16-byte multiples
     assert _select_call([0, 10, 30], [0, 5, 6], Dv=62, fdtype=last.LAST_F32) == U
 

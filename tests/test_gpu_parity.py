@@ -151,6 +151,9 @@ SELECT_CASES = [
     (27, 2, (1025, 1100), 768, W.BF16, None, 12),  # greedy blocks of 256 threads
     (28, 1, (8193, 8300), 256, W.BF16, 0.05, 32),  # greedy blocks of 512 threads
     (29, 5, (1, 200), 32, W.F32, 0.5, 3),          # fp32 rows shorter than one staged chunk
+    (32, 1, (16385, 16600), 256, W.BF16, 0.03, 32),  # greedy blocks of 1024 threads
+    (33, 2, (30000, 32767), 64, W.BF16, 0.02, 16),   # up to the 32768-token limit, staged Gram
+    (34, 1, (20000, 24000), 48, W.F32, 0.02, 8),     # fp32 Gram beyond 16384 tokens
 ]
 
 
@@ -216,6 +219,16 @@ def test_select_edge_cases(dtype):
     assert list(order) == list(np.argsort(-w32.astype(np.float64), kind="stable")[:40])
 
 
+def test_select_largest_request():
+    """A request of exactly 32768 tokens (the register-resident greedy's limit)."""
+    rng = np.random.default_rng(35)
+    N, Dv = 32768, 64
+    centers = rng.standard_normal((64, Dv))
+    X = centers[rng.integers(0, 64, N)] + 0.4 * rng.standard_normal((N, Dv))
+    wl, w32, kept, order, _ = _select_handmade(X, rng.dirichlet(np.ones(N) * 0.5), 512, W.BF16)
+    check_selection(wl, w32, kept, order, "N=32768")
+
+
 def test_select_deterministic():
     wl = W.tiny(31, R=3, n_range=(400, 1200), Dv=512, k_frac=0.2, comps=12)
     w32 = np.random.default_rng(1).dirichlet(np.ones(wl.N_total)).astype(np.float32)
@@ -227,9 +240,9 @@ def test_select_deterministic():
         assert x.tobytes() == y.tobytes()
 
 
-@pytest.mark.parametrize("seed", [40, 41])
-def test_topk_parity(seed):
-    wl = W.tiny(seed, R=4, n_range=(1, 5000), Dv=64, k_frac=0.125)
+@pytest.mark.parametrize("seed,R,nr", [(40, 4, (1, 5000)), (41, 4, (1, 5000)), (42, 2, (16385, 32768))])
+def test_topk_parity(seed, R, nr):
+    wl = W.tiny(seed, R=R, n_range=nr, Dv=64, k_frac=0.125)
     rng = np.random.default_rng(seed)
     w32 = (rng.integers(0, 50, size=wl.N_total) / 50.0).astype(np.float32)   # many ties
     dw = last.DeviceWorkload.upload(wl)
@@ -330,6 +343,34 @@ def test_config_select(name, workloads):
         # end to end: the GPU's own scores and picks, replayed with the oracle's scores
         ex, exc = check_selection(sub, w_orc, kept[a:b], order[a:b], f"{name} request {r} (end to end)")
         assert ex + exc == b - a
+
+
+def test_long_requests_x1(workloads):
+    """Two requests of 32768 tokens (past the 512-thread greedy): scores of
+    one request against the oracle; the whole selection's invariants; and
+    the first 64 picks of each request replayed on the oracle (a full replay
+    costs about 1 TFLOP of fp64 per request), stage-isolated and end to end."""
+    wl, dw = workloads("x1_long_video")
+    g = last.token_scores(dw.batch, dw.q, dw.k)
+    gs = g.cpu().numpy()
+    assert_scores(gs[wl.cu_vis[1]:wl.cu_vis[2]], orc_scores(wl.subset([1])), "x1 request 1")
+    kept, order, gains = gpu_select(dw.feats, g, wl.cu_vis, dw.cu_keep_h)
+    P = 64
+    for r in range(wl.R):
+        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
+        kr = kept[a:b]
+        assert b - a == 4096 and np.all(np.diff(kr) > 0) and kr[0] >= 0 and kr[-1] < wl.n(r)
+        assert sorted(order[a:b]) == list(kr)
+        assert np.all(np.diff(gains[a + 1:b]) <= 0)
+        sub = wl.subset([r])
+        w_orc = orc_scores(sub).astype(np.float32)
+        _, o2, _ = gpu_select(last.to_torch(sub.feats, sub.f_dtype, "cuda"), torch.from_numpy(w_orc).cuda(),
+                              sub.cu_vis, sub.cu_keep)
+        cu_p = np.array([0, P], np.int32)
+        for what, picks in (("oracle scores", o2[:P]), ("end to end", order[a:a + P])):
+            st, mg = oracle.replay(1, wl.Dv, w_orc, sub.feats, sub.cu_vis, cu_p, np.ascontiguousarray(picks),
+                                   _fd(wl.f_dtype), rel_tol=TIE_RTOL)
+            assert not np.any(st == 2), f"x1 request {r} ({what}): failed steps {np.flatnonzero(st == 2)[:5]}"
 
 
 @pytest.mark.parametrize("budget", [128, 192])
