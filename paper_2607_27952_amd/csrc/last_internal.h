@@ -57,7 +57,7 @@ struct ScoreWs {
   float4 *stats;  // [G][Hq][C_total] (chunk max, sum exp, visual sum exp, 0)
   float *vlog;    // [G][N_total][Hq] scaled logits of visual columns, layer-major
   float2 *rowstat;  // [R][G * Hq] merged (max, 1 / sum exp) of every row
-  float *mass;      // [R] total visual mass sum_{l,h} V / Z
+  float *rowmass;   // [R][G * Hq] each row's visual mass V / Z (S sums them)
 };
 
 // row_pos (nullable, one entry per request): score the causal row at that

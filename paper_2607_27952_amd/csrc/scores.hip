@@ -6,7 +6,8 @@
 // whole prefix while the keys are streamed in chunks, so the pass is split:
 //
 //   k_score_plan      one block: per-request chunk/slice prefix sums and the
-//                     chunk -> request / slice -> request maps.
+//                     chunk -> request / slice -> request maps (a wave per
+//                     request fills its entries).
 //   k_score_stream    one block per (layer, chunk of tokens). The chunk's key
 //                     rows for all KV heads are one contiguous byte range,
 //                     streamed once: 8 lanes cover one row with 16-byte loads
@@ -23,11 +24,12 @@
 //   k_score_partial   fallback for KV-head counts that do not divide 32: one
 //                     block per (layer, chunk, KV head, query-head group), the
 //                     chunk's logits staged in LDS.
-//   k_score_merge     one block per request: merges the chunk statistics of
-//                     every (layer, head) row into the row's max M and
-//                     normaliser Z, and sums the visual mass S = sum V / Z,
+//   k_score_merge     one wave per (request, layer, head) row: merges the
+//                     row's chunk statistics into its max M and normaliser Z,
+//                     and its share V / Z of the visual mass S = sum V / Z,
 //                     which equals sum_i s_i (Eq. 8).
-//   k_score_finalize  one block per slice of a request's visual tokens:
+//   k_score_finalize  one block per slice of a request's visual tokens: S
+//                     from the rows' shares, then
 //                     s_i = sum_{l,h} exp(l_i - M) / Z   (Eq. 6-7), over S,
 //                     so no second pass over s is needed.
 //
@@ -92,6 +94,8 @@ __global__ __launch_bounds__(kThreads) void k_score_plan(
     int32_t *__restrict__ chunk_req, int32_t *__restrict__ slice_off,
     int32_t *__restrict__ slice_req) {
   __shared__ int sh[kThreads / 64];
+  __shared__ int s_pc[kThreads + 1], s_ps[kThreads + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int carry_c = 0, carry_s = 0;
   for (int base = 0; base < R; base += kThreads) {
     const int r = base + (int)threadIdx.x;
@@ -108,11 +112,23 @@ __global__ __launch_bounds__(kThreads) void k_score_plan(
     if (r < R) {
       chunk_off[r] = pc;
       slice_off[r] = ps;
-      for (int c = 0; c < nc; ++c)
-        if (pc + c < C_cap) chunk_req[pc + c] = r;
-      for (int c = 0; c < ns; ++c)
-        if (ps + c < S_cap) slice_req[ps + c] = r;
     }
+    s_pc[threadIdx.x] = pc;
+    s_ps[threadIdx.x] = ps;
+    if (threadIdx.x == 0) {
+      s_pc[kThreads] = carry_c + tc;
+      s_ps[kThreads] = carry_s + ts;
+    }
+    __syncthreads();
+    // the maps: a wave per request of this group, its lanes over the chunks
+    const int nr = min(kThreads, R - base);
+    for (int j = wave; j < nr; j += kWaves) {
+      const int c1 = j + 1 < nr ? s_pc[j + 1] : s_pc[kThreads];
+      const int s1 = j + 1 < nr ? s_ps[j + 1] : s_ps[kThreads];
+      for (int c = s_pc[j] + lane; c < c1 && c < C_cap; c += 64) chunk_req[c] = base + j;
+      for (int c = s_ps[j] + lane; c < s1 && c < S_cap; c += 64) slice_req[c] = base + j;
+    }
+    __syncthreads();
     carry_c += tc;
     carry_s += ts;
   }
@@ -184,6 +200,64 @@ struct QSlice<float, DH, GQ> {
   }
 };
 
+// A chunk's logits, token-major in LDS ([nt][Hq], scaled), into the chunk's
+// statistics per head (max over every token, then the sums of exp(l - max)
+// over every token and over the visual ones) and its visual logits (and every
+// logit when rows are asked). Called by all threads after the logits landed.
+__device__ __forceinline__ void chunk_epilogue(const float *s_log, float4 *s_part, int nt, int Hq, int l, int r,
+                                               int64_t c, int R, int64_t C_total, int64_t T_total, int64_t tok0,
+                                               int t_begin, const int32_t *__restrict__ vis_start,
+                                               const int32_t *__restrict__ cu_vis, float *__restrict__ vlog,
+                                               float4 *__restrict__ stats, float *__restrict__ rows) {
+  // tph threads per head take every tph-th token; their partials merge in a
+  // fixed order.
+  const int v_lo = vis_start[r] - t_begin;
+  const int v_hi = v_lo + (cu_vis[r + 1] - cu_vis[r]);
+  const int tph = max(1, kThreads / Hq);
+  for (int h0 = 0; h0 < Hq; h0 += kThreads / tph) {
+    const int h = h0 + (int)threadIdx.x / tph, sl = (int)threadIdx.x % tph;
+    const bool act = (int)threadIdx.x / tph < kThreads / tph && h < Hq;
+    float m = -INFINITY, z = 0.f, v = 0.f;
+    if (act) {
+      for (int t = sl; t < nt; t += tph) m = fmaxf(m, s_log[t * Hq + h]);
+      for (int t = sl; t < nt; t += tph) {
+        const float e = expf(s_log[t * Hq + h] - m);
+        z += e;
+        if (t >= v_lo && t < v_hi) v += e;
+      }
+    }
+    s_part[threadIdx.x] = make_float4(m, z, v, 0.f);
+    __syncthreads();
+    if (act && sl == 0) {
+      float M = -INFINITY;
+      for (int x = 0; x < tph; ++x) M = fmaxf(M, s_part[threadIdx.x + x].x);
+      float Z = 0.f, V = 0.f;
+      for (int x = 0; x < tph; ++x) {
+        const float4 e = s_part[threadIdx.x + x];
+        const float f = e.x == -INFINITY ? 0.f : expf(e.x - M);
+        Z = fmaf(e.y, f, Z);
+        V = fmaf(e.z, f, V);
+      }
+      stats[((int64_t)l * Hq + h) * C_total + c] = make_float4(M, Z, V, 0.f);
+    }
+    __syncthreads();
+  }
+
+  // Visual logits, layer-major ([layer][visual token][head]): this block's
+  // are one contiguous run of whole cache lines. Every logit if rows are asked.
+  const int vb = max(0, v_lo), ve = min(nt, v_hi);
+  const int64_t vtok0 = (int64_t)cu_vis[r] - vis_start[r] + t_begin;
+  for (int e = vb * Hq + (int)threadIdx.x; e < ve * Hq; e += kThreads) {
+    const int t = e / Hq, h = e - t * Hq;
+    vlog[((int64_t)l * cu_vis[R] + vtok0 + t) * Hq + h] = s_log[e];
+  }
+  if (rows)
+    for (int e = threadIdx.x; e < nt * Hq; e += kThreads) {
+      const int t = e / Hq, h = e - t * Hq;
+      rows[((int64_t)l * Hq + h) * T_total + tok0 + t_begin + t] = s_log[e];
+    }
+}
+
 // Requires (8 * kWaves) % Hkv == 0, so that every lane keeps one KV head.
 // LDS holds the chunk's logits token-major, [CH][Hq].
 template <typename T, int DH, int GQ>
@@ -244,55 +318,8 @@ __global__ __launch_bounds__(kThreads) void k_score_stream(
     }
   }
   __syncthreads();
-
-  // Chunk statistics per head: max over every token, then the sums of
-  // exp(l - max) over every token and over the visual ones. tph threads per
-  // head take every tph-th token; their partials merge in a fixed order.
-  const int v_lo = vis_start[r] - t_begin;
-  const int v_hi = v_lo + (cu_vis[r + 1] - cu_vis[r]);
-  const int tph = max(1, kThreads / Hq);
-  for (int h0 = 0; h0 < Hq; h0 += kThreads / tph) {
-    const int h = h0 + (int)threadIdx.x / tph, sl = (int)threadIdx.x % tph;
-    const bool act = (int)threadIdx.x / tph < kThreads / tph && h < Hq;
-    float m = -INFINITY, z = 0.f, v = 0.f;
-    if (act) {
-      for (int t = sl; t < nt; t += tph) m = fmaxf(m, s_log[t * Hq + h]);
-      for (int t = sl; t < nt; t += tph) {
-        const float e = expf(s_log[t * Hq + h] - m);
-        z += e;
-        if (t >= v_lo && t < v_hi) v += e;
-      }
-    }
-    s_part[threadIdx.x] = make_float4(m, z, v, 0.f);
-    __syncthreads();
-    if (act && sl == 0) {
-      float M = -INFINITY;
-      for (int x = 0; x < tph; ++x) M = fmaxf(M, s_part[threadIdx.x + x].x);
-      float Z = 0.f, V = 0.f;
-      for (int x = 0; x < tph; ++x) {
-        const float4 e = s_part[threadIdx.x + x];
-        const float f = e.x == -INFINITY ? 0.f : expf(e.x - M);
-        Z = fmaf(e.y, f, Z);
-        V = fmaf(e.z, f, V);
-      }
-      stats[((int64_t)l * Hq + h) * C_total + c] = make_float4(M, Z, V, 0.f);
-    }
-    __syncthreads();
-  }
-
-  // Visual logits, layer-major ([layer][visual token][head]): this block's
-  // are one contiguous run of whole cache lines. Every logit if rows are asked.
-  const int vb = max(0, v_lo), ve = min(nt, v_hi);
-  const int64_t vtok0 = (int64_t)cu_vis[r] - vis_start[r] + t_begin;
-  for (int e = vb * Hq + (int)threadIdx.x; e < ve * Hq; e += kThreads) {
-    const int t = e / Hq, h = e - t * Hq;
-    vlog[((int64_t)l * cu_vis[R] + vtok0 + t) * Hq + h] = s_log[e];
-  }
-  if (rows)
-    for (int e = threadIdx.x; e < nt * Hq; e += kThreads) {
-      const int t = e / Hq, h = e - t * Hq;
-      rows[((int64_t)l * Hq + h) * T_total + tok0 + t_begin + t] = s_log[e];
-    }
+  chunk_epilogue(s_log, s_part, nt, Hq, l, r, c, R, C_total, T_total, tok0, t_begin, vis_start, cu_vis,
+                 vlog, stats, rows);
 }
 
 template <typename T, int DH, int GM>
@@ -452,23 +479,21 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
   }
 }
 
-// Per request: merge the chunk statistics of every (layer, head) row into its
-// max M and 1/Z, and the total visual mass S = sum_{l,h} V / Z (= sum_i s_i).
-constexpr int kMergeThreads = 1024;
-__global__ __launch_bounds__(kMergeThreads) void k_score_merge(
+// Merge the chunk statistics of every (request, layer, head) row into its max
+// M and 1/Z, and its share V / Z of the request's visual mass
+// S = sum_{l,h} V / Z (= sum_i s_i). One wave per row, kWaves rows a block:
+// lanes merge the row's chunks lane-strided with the online rule, then the
+// wave combines the lanes (log-sum-exp over (max, sum) pairs).
+__global__ __launch_bounds__(kThreads) void k_score_merge(
     const float4 *__restrict__ stats, const int32_t *__restrict__ chunk_off, int GH,
-    int64_t C_total, float2 *__restrict__ rowstat, float *__restrict__ mass) {
-  // One wave per (layer, head) row at a time: lanes merge the row's chunks
-  // lane-strided with the online rule, then the wave combines the lanes
-  // (log-sum-exp over (max, sum) pairs). The visual mass adds V / Z over the
-  // rows, per wave and then over the waves, in a fixed order.
-  constexpr int kNW = kMergeThreads / 64;
-  __shared__ float s_red[kNW];
-  const int r = blockIdx.x;
-  const int c0 = chunk_off[r], c1 = chunk_off[r + 1];
+    int64_t C_total, float2 *__restrict__ rowstat, float *__restrict__ rowmass) {
+  const int bpr = (GH + kWaves - 1) / kWaves;   // blocks per request
+  const int r = blockIdx.x / bpr;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float part = 0.f;
-  for (int p = wave; p < GH; p += kNW) {
+  const int p = (blockIdx.x % bpr) * kWaves + wave;
+  if (p >= GH) return;
+  const int c0 = chunk_off[r], c1 = chunk_off[r + 1];
+  {
     const float4 *st = stats + (int64_t)p * C_total;
     float m = -INFINITY, z = 0.f, v = 0.f;
     for (int c = c0 + lane; c < c1; c += 64) {
@@ -487,33 +512,40 @@ __global__ __launch_bounds__(kMergeThreads) void k_score_merge(
     const float M = wave_max(m);
     const float f = m == -INFINITY ? 0.f : expf(m - M);
     const float Z = wave_sum(z * f), V = wave_sum(v * f);
-    if (lane == 0) rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
-    part += V / Z;
-  }
-  if (lane == 0) s_red[wave] = part;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float S = 0.f;
-    for (int w = 0; w < kNW; ++w) S += s_red[w];
-    mass[r] = S;
+    if (lane == 0) {
+      rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
+      rowmass[(int64_t)r * GH + p] = V / Z;
+    }
   }
 }
 
 // s_i = sum_{l,h} exp(l_i - M) / Z (Eq. 6-7), divided by S (Eq. 8).
 __global__ __launch_bounds__(kThreads) void k_score_finalize(
     const float *__restrict__ vlog, const float2 *__restrict__ rowstat,
-    const float *__restrict__ mass, const int32_t *__restrict__ cu_vis,
+    const float *__restrict__ rowmass, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ row_pos,
     const int32_t *__restrict__ slice_off, const int32_t *__restrict__ slice_req, int G, int Hq,
     int64_t N_total, int SL, float *__restrict__ scores) {
   const int GH = G * Hq;
   __shared__ float2 sMZ[kMaxPairs];
+  __shared__ float s_red[kWaves];
   const int b = blockIdx.x;
   const int r = slice_req[b];
   const int sl = b - slice_off[r];
-  for (int p = threadIdx.x; p < GH; p += kThreads) sMZ[p] = rowstat[(int64_t)r * GH + p];
+  // S = sum over the request's rows of V / Z: each thread its rows p = t,
+  // t + kThreads, ... in order, then the wave and the waves in a fixed order
+  float part = 0.f;
+  for (int p = threadIdx.x; p < GH; p += kThreads) {
+    sMZ[p] = rowstat[(int64_t)r * GH + p];
+    part += rowmass[(int64_t)r * GH + p];
+  }
+  part = wave_sum(part);
+  if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = part;
   __syncthreads();
-  const float invS = 1.0f / mass[r];
+  float S = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) S += s_red[w];
+  const float invS = 1.0f / S;
   const int64_t n0 = cu_vis[r];
   const int N_r = cu_vis[r + 1] - (int)n0;
   const int end = min(N_r, (sl + 1) * SL);
@@ -667,7 +699,7 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
   w.stats = cv.take<float4>((size_t)b->G * b->Hq * p.C_total);
   w.vlog = cv.take<float>((size_t)b->G * b->Hq * p.N_total);
   w.rowstat = cv.take<float2>((size_t)b->R * b->G * b->Hq);
-  w.mass = cv.take<float>(b->R);
+  w.rowmass = cv.take<float>((size_t)b->R * b->G * b->Hq);
   *bytes = cv.size();
   return w;
 }
@@ -686,13 +718,14 @@ hipError_t launch_score_plan(const last_batch *b, const ScorePlan &p, const Scor
 hipError_t launch_score_tail(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
                              const int32_t *row_pos, float *scores, hipStream_t s) {
   launch_begin("score_merge", s);
-  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)b->R), dim3(kMergeThreads), 0, s, w.stats, w.chunk_off,
-                     b->G * b->Hq, p.C_total, w.rowstat, w.mass);
+  const int GH = b->G * b->Hq;
+  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)((int64_t)b->R * ((GH + kWaves - 1) / kWaves))), dim3(kThreads), 0,
+                     s, w.stats, w.chunk_off, GH, p.C_total, w.rowstat, w.rowmass);
   hipError_t e = launch_end(s);
   if (e != hipSuccess) return e;
   launch_begin("score_finalize", s);
   hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog,
-                     w.rowstat, w.mass, b->cu_vis, b->vis_start, row_pos, w.slice_off, w.slice_req, b->G,
+                     w.rowstat, w.rowmass, b->cu_vis, b->vis_start, row_pos, w.slice_off, w.slice_req, b->G,
                      b->Hq, p.N_total, p.slice_tokens, scores);
   return launch_end(s);
 }
