@@ -45,7 +45,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
-constexpr int kUnroll = 4;                  // row groups (8 rows each) in flight per wave
+constexpr int kUnroll = 6;                  // row groups (8 rows each) in flight per wave
 
 // Key rows are read exactly once: non-temporal loads stream them without
 // displacing cache lines that other blocks still use (on this part a plain
@@ -244,12 +244,14 @@ __device__ __forceinline__ void chunk_epilogue(const float *s_log, float4 *s_par
   }
 
   // Visual logits, layer-major ([layer][visual token][head]): this block's
-  // are one contiguous run of whole cache lines. Every logit if rows are asked.
+  // are one contiguous run of whole cache lines, stored non-temporally (the
+  // finalize reads them once, after the whole pass; kept in cache they
+  // displace key lines still in flight). Every logit if rows are asked.
   const int vb = max(0, v_lo), ve = min(nt, v_hi);
   const int64_t vtok0 = (int64_t)cu_vis[r] - vis_start[r] + t_begin;
   for (int e = vb * Hq + (int)threadIdx.x; e < ve * Hq; e += kThreads) {
     const int t = e / Hq, h = e - t * Hq;
-    vlog[((int64_t)l * cu_vis[R] + vtok0 + t) * Hq + h] = s_log[e];
+    __builtin_nontemporal_store(s_log[e], &vlog[((int64_t)l * cu_vis[R] + vtok0 + t) * Hq + h]);
   }
   if (rows)
     for (int e = threadIdx.x; e < nt * Hq; e += kThreads) {
