@@ -118,6 +118,27 @@ def rows_work(wl, cu_rows, row_pos):
             "rows_stats_bytes": b1, "rows_stats_flops": f1, "rows_visual_bytes": b2, "rows_visual_flops": f2}
 
 
+def gram_work(wl):
+    """The two Gram launches, each bound by whichever of HBM bytes and matrix-core
+    (bf16) or fp64-vector (fp32 features) flops takes longer at the peaks. The
+    diagonal launch reads every feature row once and writes the diagonal
+    128 x 128 coverage blocks and the norms; the off-diagonal launch reads the
+    rows of every request with more than one row block again and writes each
+    off-diagonal block and its mirror."""
+    felt = 2 if wl.f_dtype == "bf16" else 4
+    n = np.diff(wl.cu_vis).astype(np.int64)
+    nb = (n + GRAM_TILE - 1) // GRAM_TILE
+    blk = GRAM_TILE * GRAM_TILE * 4
+    f_diag, f_off = gram_flops(n, wl.Dv)
+    b_diag = wl.N_total * wl.Dv * felt + int(np.sum(nb)) * blk + wl.N_total * 16
+    b_off = int(np.sum(n[nb > 1])) * wl.Dv * felt + int(np.sum(nb * (nb - 1))) * blk
+    peak, kind = (MFMA_FLOPS_PER_S, "mfma") if felt == 2 else (FP64_VECTOR_PEAK_TFLOPS * 1e12, "alu")
+
+    def bound(b, f):
+        return ("hbm", b) if b / HBM_BYTES_PER_S >= f / peak else (kind, f)
+    return {"gram_diag": bound(b_diag, f_diag), "gram": bound(b_off, f_off)}
+
+
 def prefill_flops(wl):
     """Causal attention of every position: row p takes p + 1 keys, 2 Dh flops
     each for the logits and 2 Dh for the value product."""
@@ -147,7 +168,7 @@ def kernel_work(wl, row_pos=None):
     k_bytes = wl.G * tokens * wl.Hkv * wl.Dh * elt
     q_bytes = wl.G * wl.R * wl.Hq * wl.Dh * elt
     vlog = wl.G * wl.Hq * wl.N_total * 4
-    g_diag, g_off = gram_flops(n, wl.Dv)
+    gw = gram_work(wl)
     return {
         # key rows of every guidance layer + the last-token queries, each read once
         "score_stream": ("hbm", k_bytes + q_bytes),
@@ -156,8 +177,8 @@ def kernel_work(wl, row_pos=None):
         "score_finalize": ("hbm", vlog + wl.N_total * 4),
         # features read once
         "sqnorm": ("hbm", wl.N_total * wl.Dv * felt),
-        "gram_diag": ("mfma" if felt == 2 else "alu", g_diag),
-        "gram": ("mfma" if felt == 2 else "alu", g_off),
+        "gram_diag": gw["gram_diag"],
+        "gram": gw["gram"],
         # one coverage row of N_r floats per pick, plus the weights
         "greedy": ("hbm", float(np.sum(kk * n)) * 4 + wl.N_total * 4),
         "topk": ("hbm", wl.N_total * 4 + wl.K_total * 4),

@@ -26,10 +26,31 @@ def test_kernel_work_matches_shapes():
     elt = 2 if wl.qk_dtype == W.BF16 else 4
     assert work["score_stream"] == ("hbm", wl.G * wl.T_total * wl.Hkv * wl.Dh * elt + wl.G * wl.R * wl.Hq * wl.Dh * elt)
     n = np.diff(wl.cu_vis)
-    assert work["gram_diag"][1] + work["gram"][1] == float(np.sum(n * (n + 1))) * wl.Dv
+    d, o = bench.gram_flops(n, wl.Dv)
+    assert d + o == float(np.sum(n * (n + 1))) * wl.Dv
     felt = 2 if wl.f_dtype == W.BF16 else 4
     assert work["gather"] == ("hbm", 2 * wl.K_total * wl.Dv * felt)
-    assert work["gram"][0] == ("mfma" if felt == 2 else "alu")
+
+
+def test_gram_bound_is_the_slower_resource():
+    """Each Gram launch is priced by whichever of its bytes and flops takes longer
+    at the published peaks: features read once and coverage blocks written."""
+    wl = W.make("c2_llava15")
+    n = np.diff(wl.cu_vis)
+    work = bench.gram_work(wl)
+    d, o = bench.gram_flops(n, wl.Dv)
+    blk = 128 * 128 * 4
+    b_diag = wl.N_total * wl.Dv * 2 + 64 * 5 * blk + wl.N_total * 16     # 576 tokens: 5 row blocks
+    b_off = wl.N_total * wl.Dv * 2 + 64 * 20 * blk                       # 5 x 4 off-diagonal blocks
+    # C2's 576-token requests: 57 flops a byte on the diagonal, 178 off it,
+    # both under the 312 that the peaks balance at, so both launches are HBM-bound
+    assert work["gram_diag"] == ("hbm", b_diag)
+    assert work["gram"] == ("hbm", b_off)
+    assert d / b_diag < 312 and o / b_off < 312
+    # long requests make the off-diagonal launch a contraction bound by the matrix cores
+    wl5 = W.tiny(5, R=1, n_range=(4000, 4000), Dv=2048, k_frac=0.1)
+    w5 = bench.gram_work(wl5)
+    assert w5["gram"] == ("mfma", bench.gram_flops(np.diff(wl5.cu_vis), 2048)[1])
 
 
 def test_multi_gpu_request_exits():
