@@ -146,6 +146,15 @@ def prefill_flops(wl):
     return 4.0 * wl.Dh * wl.G * wl.Hq * float(np.sum(P * (P + 1) / 2))
 
 
+def prefill_work(wl):
+    """The prefill attention, bound by whichever of its flops and its bytes (q,
+    k, v read once, the output written once) takes longer at the peaks."""
+    elt = 2
+    b = wl.G * wl.T_total * (2 * wl.Hq + 2 * wl.Hkv) * wl.Dh * elt
+    f = prefill_flops(wl)
+    return ("hbm", b) if b / HBM_BYTES_PER_S >= f / MFMA_FLOPS_PER_S else ("mfma", f)
+
+
 def connector_work(wl):
     """The cloud connector on the K_total kept rows: LayerNorm reads and writes
     K Dv bf16 values; the two products take 2 K Dv Dh and 2 K Dh Do flops."""
@@ -184,7 +193,7 @@ def kernel_work(wl, row_pos=None):
         "topk": ("hbm", wl.N_total * 4 + wl.K_total * 4),
         # kept rows read and written
         "gather": ("hbm", 2 * wl.K_total * wl.Dv * felt),
-        "prefill": ("mfma", prefill_flops(wl)),
+        "prefill": prefill_work(wl) if wl.qk_dtype == "bf16" else ("mfma", prefill_flops(wl)),
     }
 
 

@@ -96,3 +96,14 @@ def test_connector_work_counts_two_products_and_one_norm_pass():
     assert work["connector_gemm2"] == ("mfma", 2.0 * K * D * D)
     # bf16 rows read and normalised rows written, plus gamma and beta in fp32
     assert work["connector_layernorm"] == ("hbm", 2 * K * D * 2 + 2 * D * 4)
+
+
+def test_prefill_bound_is_the_slower_resource():
+    """C2's short MHA requests move more bytes than the matrix cores need time
+    for (q, k, v and the output, 2.7 GB against 430 GFLOP); long grouped-query
+    requests are bound by the products."""
+    wl = W.make("c2_llava15")
+    b = wl.G * wl.T_total * (2 * wl.Hq + 2 * wl.Hkv) * wl.Dh * 2
+    assert bench.prefill_work(wl) == ("hbm", b)
+    wl5 = W.tiny(6, R=1, Hq=8, Hkv=1, Dh=128, n_range=(6000, 6000), t_range=(10, 10))
+    assert bench.prefill_work(wl5) == ("mfma", bench.prefill_flops(wl5))
