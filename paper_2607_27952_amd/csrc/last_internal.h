@@ -97,6 +97,7 @@ struct RowsPlan {
   int64_t SC_total;         // per layer: sum_r Hq * M_r * key chunks_r row statistics
   int32_t RG_max;           // most row groups of any request
   int32_t RT;               // row tiles per block
+  int32_t MB;               // merge blocks per request (256 rows each, for the largest request)
 };
 
 struct RowsWs {
@@ -107,6 +108,7 @@ struct RowsWs {
   float4 *stats;            // [G][SC_total] (max, sum exp, visual sum exp, 0) per row and chunk
   float2 *rowstat;          // [G][Hq][M_total] (max, 1 / sum exp) per row
   float *mass;              // [R] sum over rows of visual mass V / Z
+  float *mass_part;         // [R][MB] the merge blocks' shares of it
   float *part;              // [G][Hkv][RG_max][N_total] visual probability sums per row group
 };
 
@@ -287,6 +289,15 @@ __device__ __forceinline__ int64_t uniform_i64(int64_t v) {
   const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
   return (int64_t)(((uint64_t)hi << 32) | lo);
 }
+// Blocks are dealt to the 8 XCDs in turn (block b to XCD b % 8). This maps
+// block b to a logical index so that each XCD runs one contiguous range of
+// the grid (the last gridDim % 8 blocks keep their own index): neighbouring
+// logical blocks, which read the same data, then share that XCD's L2.
+__device__ __forceinline__ int64_t xcd_contiguous(int64_t b, int64_t nblocks) {
+  const int64_t per = nblocks / 8;
+  return b < per * 8 ? (b % 8) * per + b / 8 : b;
+}
+
 // Wait until at most N vector memory loads of this wave are outstanding.
 template <int N>
 __device__ __forceinline__ void vm_wait() {

@@ -95,13 +95,10 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
   __shared__ uint4 s_k[2][kKS * SH::kPieces];
   __shared__ __align__(16) uint16_t s_vt[2][DH * SH::kVPitch];
 
-  // Blocks are dealt to the 8 XCDs in turn. Renumber them so that each XCD
-  // runs a contiguous range: the query blocks of one (layer, head, request)
-  // are neighbours in that order, so they run together on one XCD and re-read
-  // the request's keys and values from its L2 rather than from HBM.
-  const int64_t per_xcd = (int64_t)gridDim.x / 8;
-  int64_t bid = (int64_t)blockIdx.x < per_xcd * 8 ? (int64_t)(blockIdx.x % 8) * per_xcd + blockIdx.x / 8
-                                                  : (int64_t)blockIdx.x;
+  // The query blocks of one (layer, head, request) are neighbours in this
+  // order; XCD-contiguous numbering runs them together on one XCD, so they
+  // re-read the request's keys and values from its L2 rather than from HBM.
+  int64_t bid = xcd_contiguous(blockIdx.x, gridDim.x);
   const int64_t qbi = bid % QB_total;
   bid /= QB_total;
   const int h = (int)(bid % Hq);

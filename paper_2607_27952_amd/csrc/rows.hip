@@ -26,9 +26,10 @@
 //                    one multiply). The reference only moves when a logit
 //                    exceeds it by 64 (sums stay far from overflow), so a logit
 //                    costs one exponential and no rescaling.
-//   k_rows_merge     one block per request: every row's chunks merged into one
-//                    reference and 1/Z, and the visual mass S = sum V / Z over
-//                    the request's rows (= sum_i s_i).
+//   k_rows_merge     one thread per row, 256 rows a block: every row's chunks
+//                    merged into one reference and 1/Z, and the block's share
+//                    of the visual mass S = sum V / Z over the request's rows
+//                    (= sum_i s_i); k_rows_mass adds the shares per request.
 //   k_rows_visual    one block per (layer, KV head, request, row group, visual
 //                    chunk): the visual logits again, 2^(x - r) / Z summed over
 //                    the block's rows per key, written per row group.
@@ -212,15 +213,26 @@ __global__ __launch_bounds__(256) void k_rows_plan(
     int4 *__restrict__ rinfo, int4 *__restrict__ items1, int4 *__restrict__ items2) {
   __shared__ int sh[4];
   __shared__ long long s_sc[256];
+  __shared__ int s_p1[256], s_p2[256], s_kc[256], s_vc[256], s_rg[256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int carry1 = 0, carry2 = 0;
   long long carry_sc = 0;
   for (int base = 0; base < R; base += 256) {
     const int r = base + (int)threadIdx.x;
     int n1 = 0, n2 = 0, KC = 0, VC = 0, RG = 0, pmax = 0;
     long long nsc = 0;
+    // each request's last row position: a wave per request, lanes over its rows
+    for (int j = wave; j < min(256, R - base); j += 4) {
+      const int m0 = cu_rows[base + j], M = cu_rows[base + j + 1] - m0;
+      int pm = 0;
+      for (int m = lane; m < M; m += 64) pm = max(pm, row_pos[m0 + m]);
+      pm = (int)wave_max_u32((uint32_t)pm);
+      if (lane == 0) s_kc[j] = pm;
+    }
+    __syncthreads();
     if (r < R) {
       const int m0 = cu_rows[r], M = cu_rows[r + 1] - m0;
-      for (int m = 0; m < M; ++m) pmax = max(pmax, row_pos[m0 + m]);
+      pmax = s_kc[threadIdx.x];
       const int tiles = (g * M + 31) / 32;
       RG = (tiles + RT - 1) / RT;
       KC = (pmax + 1 + kCH - 1) / kCH;
@@ -248,13 +260,22 @@ __global__ __launch_bounds__(256) void k_rows_plan(
       off1[r] = p1;
       off2[r] = p2;
       sc_off[r] = psc;
-      for (int c = 0; c < KC; ++c)
-        for (int rg = 0; rg < RG; ++rg)
-          if (p1 + c * RG + rg < cap1) items1[p1 + c * RG + rg] = make_int4(r, rg, c, 0);
-      for (int c = 0; c < VC; ++c)
-        for (int rg = 0; rg < RG; ++rg)
-          if (p2 + c * RG + rg < cap2) items2[p2 + c * RG + rg] = make_int4(r, rg, c, 0);
     }
+    s_p1[threadIdx.x] = p1;
+    s_p2[threadIdx.x] = p2;
+    s_kc[threadIdx.x] = KC;
+    s_vc[threadIdx.x] = VC;
+    s_rg[threadIdx.x] = RG;
+    __syncthreads();
+    // the work items, chunk-major then row group: a wave per request
+    for (int j = wave; j < min(256, R - base); j += 4) {
+      const int rg_n = s_rg[j], q1 = s_p1[j], q2 = s_p2[j];
+      for (int x = lane; x < s_kc[j] * rg_n; x += 64)
+        if (q1 + x < cap1) items1[q1 + x] = make_int4(base + j, x % rg_n, x / rg_n, 0);
+      for (int x = lane; x < s_vc[j] * rg_n; x += 64)
+        if (q2 + x < cap2) items2[q2 + x] = make_int4(base + j, x % rg_n, x / rg_n, 0);
+    }
+    __syncthreads();
     carry1 += t1;
     carry2 += t2;
     carry_sc += tsc;
@@ -280,8 +301,11 @@ __global__ __launch_bounds__(kThreads, 2) void k_rows_stats(
   __shared__ uint4 s_k[2][KR::kStage];
   __shared__ float4 s_st[kW][32];
   __shared__ int s_pos[kW][32];     // position of each row of a wave's tile (-1: none)
-  const int64_t item = blockIdx.x % n_items;
-  const int lk = (int)(blockIdx.x / n_items);
+  // the row groups of one key chunk are neighbouring items: XCD-contiguous
+  // numbering runs them on one XCD, where they share the chunk in L2
+  const int64_t bid = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int64_t item = bid % n_items;
+  const int lk = (int)(bid / n_items);
   const int kv = lk % Hkv, l = lk / Hkv;
   const int4 it = items[item];
   const int r = it.x, rg = it.y, c = it.z;
@@ -436,17 +460,21 @@ __global__ __launch_bounds__(kThreads, 2) void k_rows_stats(
 }
 
 // ---------------------------------------------------------------- merge
+// Grid (MB, R): block (x, r) merges rows x * 256 .. x * 256 + 255 of request
+// r, one row a thread, and writes their visual mass V / Z summed in a fixed
+// order as part x of the request's mass; k_rows_mass adds the parts.
 __global__ __launch_bounds__(256) void k_rows_merge(
     const float4 *__restrict__ stats, const int32_t *__restrict__ cu_rows,
     const int4 *__restrict__ rinfo, const int64_t *__restrict__ sc_off, int G, int Hq,
-    int64_t M_total, int64_t SC_total, float2 *__restrict__ rowstat, float *__restrict__ mass) {
+    int64_t M_total, int64_t SC_total, float2 *__restrict__ rowstat, float *__restrict__ mass_part) {
   __shared__ float s_red[4];
-  const int r = blockIdx.x;
+  const int r = blockIdx.y;
   const int m0 = cu_rows[r], M = cu_rows[r + 1] - m0;
   const int KC = rinfo[r].x;
   const int per_layer = Hq * M;
   float part = 0.f;
-  for (int e = threadIdx.x; e < G * per_layer; e += 256) {
+  const int e = blockIdx.x * 256 + (int)threadIdx.x;
+  if (e < G * per_layer) {
     const int l = e / per_layer, rem = e - l * per_layer;
     const int h = rem / M, m = rem - h * M;
     const float4 *st = stats + (int64_t)l * SC_total + sc_off[r] + (int64_t)rem * KC;
@@ -456,12 +484,23 @@ __global__ __launch_bounds__(256) void k_rows_merge(
       merge2(mx, z, vz, x.x, x.y, x.z);
     }
     rowstat[((int64_t)l * Hq + h) * M_total + m0 + m] = make_float2(mx, 1.0f / z);
-    part += vz / z;
+    part = vz / z;
   }
   part = wave_sum(part);
   if ((threadIdx.x & 63) == 0) s_red[threadIdx.x >> 6] = part;
   __syncthreads();
-  if (threadIdx.x == 0) mass[r] = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+  if (threadIdx.x == 0) mass_part[(int64_t)r * gridDim.x + blockIdx.x] = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+}
+
+// A request's visual mass: its MB merge parts, lane-strided and then across
+// the wave, in a fixed order.
+__global__ __launch_bounds__(64) void k_rows_mass(const float *__restrict__ mass_part, int MB,
+                                                  float *__restrict__ mass) {
+  const int r = blockIdx.x;
+  float s = 0.f;
+  for (int x = threadIdx.x; x < MB; x += 64) s += mass_part[(int64_t)r * MB + x];
+  s = wave_sum(s);
+  if (threadIdx.x == 0) mass[r] = s;
 }
 
 // ---------------------------------------------------------------- pass 2
@@ -477,8 +516,11 @@ __global__ __launch_bounds__(kThreads, 2) void k_rows_visual(
   constexpr int KS = kW / RT;
   __shared__ uint4 s_k[2][KR::kStage];
   __shared__ float s_col[RT][kCH];
-  const int64_t item = blockIdx.x % n_items;
-  const int lk = (int)(blockIdx.x / n_items);
+  // the row groups of one key chunk are neighbouring items: XCD-contiguous
+  // numbering runs them on one XCD, where they share the chunk in L2
+  const int64_t bid = xcd_contiguous(blockIdx.x, gridDim.x);
+  const int64_t item = bid % n_items;
+  const int lk = (int)(bid / n_items);
   const int kv = lk % Hkv, l = lk / Hkv;
   const int4 it = items[item];
   const int r = it.x, rg = it.y, c = it.z;
@@ -626,8 +668,9 @@ hipError_t launch_passes(const last_batch *b, const last::RowsPlan &p, const las
   if (e != hipSuccess) return e;
 
   last::launch_begin("rows_merge", s);
-  hipLaunchKernelGGL(k_rows_merge, dim3((unsigned)b->R), dim3(256), 0, s, w.stats, cu_rows, w.rinfo,
-                     w.sc_off, b->G, b->Hq, p.M_total, p.SC_total, w.rowstat, w.mass);
+  hipLaunchKernelGGL(k_rows_merge, dim3((unsigned)p.MB, (unsigned)b->R), dim3(256), 0, s, w.stats, cu_rows,
+                     w.rinfo, w.sc_off, b->G, b->Hq, p.M_total, p.SC_total, w.rowstat, w.mass_part);
+  hipLaunchKernelGGL(k_rows_mass, dim3((unsigned)b->R), dim3(64), 0, s, w.mass_part, p.MB, w.mass);
   e = last::launch_end(s);
   if (e != hipSuccess) return e;
 
@@ -678,6 +721,7 @@ RowsPlan make_rows_plan(const last_batch *b, const int32_t *cu_rows_h, const int
     p.items2 += (int64_t)RG * VC;
     p.SC_total += (int64_t)b->Hq * M * KC;
     p.RG_max = std::max(p.RG_max, RG);
+    p.MB = std::max<int32_t>(p.MB, (int32_t)(((int64_t)b->G * b->Hq * M + 255) / 256));
   }
   return p;
 }
@@ -694,6 +738,7 @@ RowsWs carve_rows_ws(void *ws, const last_batch *b, const RowsPlan &p, size_t *b
   w.stats = cv.take<float4>((size_t)b->G * p.SC_total);
   w.rowstat = cv.take<float2>((size_t)b->G * b->Hq * p.M_total);
   w.mass = cv.take<float>(b->R);
+  w.mass_part = cv.take<float>((size_t)b->R * p.MB);
   w.part = cv.take<float>((size_t)b->G * b->Hkv * p.RG_max * p.N_total);
   *bytes = cv.size();
   return w;
