@@ -278,6 +278,11 @@ __device__ __forceinline__ uint32_t lds_u32(const void *p) {
 __device__ __forceinline__ void dma16(uint32_t lds, const void *base, uint32_t voff) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory");
 }
+// The same with the non-temporal hint: for data read exactly once, which
+// then streams past the caches instead of displacing lines others reuse.
+__device__ __forceinline__ void dma16_nt(uint32_t lds, const void *base, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt" ::"s"(lds), "v"(voff), "s"(base) : "memory");
+}
 __device__ __forceinline__ const void *uniform_ptr(const void *p) {
   const uint64_t v = (uint64_t)(uintptr_t)p;
   const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);

@@ -491,9 +491,13 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
       voff[x] = (uint32_t)((rr * (int64_t)Dv + piece * 8) * 2);
     }
   };
+  // diagonal tiles read every feature row exactly once (non-temporal: the
+  // rows stream past the caches); off-diagonal tiles share row blocks in L2
   auto issue_one = [&](int st, int x) {
-    dma16(dst[x] + (uint32_t)(st & (kRing - 1)) * kStageBytes, (const char *)gbase[x] + (int64_t)st * kDmaCols * 2,
-          voff[x]);
+    const uint32_t to = dst[x] + (uint32_t)(st & (kRing - 1)) * kStageBytes;
+    const char *from = (const char *)gbase[x] + (int64_t)st * kDmaCols * 2;
+    if (DIAG) dma16_nt(to, from, voff[x]);
+    else dma16(to, from, voff[x]);
   };
   auto issue = [&](int st) {
 #pragma unroll
