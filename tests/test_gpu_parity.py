@@ -58,8 +58,10 @@ def gpu_select(dw_feats, scores_t, cu_vis, cu_keep, mode=last.KCENTER):
     return kept.cpu().numpy(), order.cpu().numpy(), gains.cpu().numpy()
 
 
-def check_selection(wl, w32, kept, order, tag=""):
-    """Replay the GPU pick sequence on the oracle; returns (exact, excused) step counts."""
+def check_selection(wl, w32, kept, order, tag="", same_sets=None):
+    """Replay the GPU pick sequence on the oracle; returns (exact, excused) step
+    counts. With `same_sets` (a list), appends per request whether the kept set
+    equals the oracle's own free run."""
     R = wl.R
     st, mg = oracle.replay(R, wl.Dv, w32, wl.feats, wl.cu_vis, wl.cu_keep, order, _fd(wl.f_dtype),
                            rel_tol=TIE_RTOL)
@@ -73,6 +75,8 @@ def check_selection(wl, w32, kept, order, tag=""):
         assert sorted(order[a:b]) == list(kr), f"{tag}: kept is not the sorted pick set"
         if np.all(st[a:b] == 0):
             assert list(kr) == list(okept[a:b]), f"{tag}: request {r} set differs without any near-tie"
+        if same_sets is not None:
+            same_sets.append(list(kr) == list(okept[a:b]))
     return int((st == 0).sum()), int((st == 1).sum())
 
 
@@ -339,10 +343,13 @@ def test_config_select(name, workloads):
         # stage-isolated: the oracle's scores into the GPU selection
         k2, o2, _ = gpu_select(last.to_torch(sub.feats, sub.f_dtype, "cuda"), torch.from_numpy(w_orc).cuda(),
                                sub.cu_vis, sub.cu_keep)
-        check_selection(sub, w_orc, k2, o2, f"{name} request {r} (oracle scores)")
+        same = []
+        ex1, exc1 = check_selection(sub, w_orc, k2, o2, f"{name} request {r} (oracle scores)", same)
         # end to end: the GPU's own scores and picks, replayed with the oracle's scores
-        ex, exc = check_selection(sub, w_orc, kept[a:b], order[a:b], f"{name} request {r} (end to end)")
+        ex, exc = check_selection(sub, w_orc, kept[a:b], order[a:b], f"{name} request {r} (end to end)", same)
         assert ex + exc == b - a
+        print(f"{name} request {r}: N={wl.n(r)} K={b - a}; oracle scores: {ex1} exact, {exc1} excused; "
+              f"end to end: {ex} exact, {exc} excused; kept sets equal to the oracle's: {same}")
 
 
 def test_long_requests_x1(workloads):
