@@ -230,12 +230,12 @@ def cpu_baseline(wl, target_s):
     qd = oracle.BF16 if wl.qk_dtype == "bf16" else oracle.F32
     threads = len(os.sched_getaffinity(0))
 
-    def run(sub):
+    def run(sub, nth=threads):
         t0 = time.perf_counter()
         w = oracle.scores(sub.R, sub.G, sub.Hq, sub.Hkv, sub.Dh, sub.q, sub.k, sub.cu_seqlens,
-                          sub.vis_start, sub.cu_vis, qd, scale=sub.scale, nthreads=threads)
+                          sub.vis_start, sub.cu_vis, qd, scale=sub.scale, nthreads=nth)
         kept, _, _ = oracle.select(sub.R, sub.Dv, w.astype(np.float32), sub.feats, sub.cu_vis,
-                                   sub.cu_keep, fd, nthreads=threads)
+                                   sub.cu_keep, fd, nthreads=nth)
         oracle.gather(sub.R, sub.feats, sub.cu_vis, kept, sub.cu_keep)
         return time.perf_counter() - t0
 
@@ -247,9 +247,16 @@ def cpu_baseline(wl, target_s):
         dt += run(sub)
         passes += 1
     what = f"all {wl.R} requests" if n == wl.R else f"first {n} of {wl.R} requests"
+    # the same path on one thread, over requests taken in order for about a quarter of the time
+    n1, dt1 = 0, 0.0
+    while dt1 < target_s / 4 and n1 < wl.R:
+        dt1 += run(wl.subset([n1]), 1)
+        n1 += 1
     return {"value": round(n * passes / dt, 3), "unit": "requests/s", "cores": threads, "kind": "oracle",
             "sample": f"{what} x {passes} pass(es), whole path (scores, k-center, gather) in fp64, "
-                      f"{dt:.1f} s on {threads} threads"}
+                      f"{dt:.1f} s on {threads} threads",
+            "single_thread": {"value": round(n1 / dt1, 3), "unit": "requests/s",
+                              "sample": f"first {n1} request(s) one at a time, {dt1:.1f} s on 1 thread"}}
 
 
 def main():
