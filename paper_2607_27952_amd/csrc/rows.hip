@@ -288,8 +288,9 @@ __global__ __launch_bounds__(256) void k_rows_plan(
 }
 
 // ---------------------------------------------------------------- pass 1
+// two blocks a CU for bf16 keys; fp32 keys need the registers of one
 template <typename T, int DH, int RT>
-__global__ __launch_bounds__(kThreads, 2) void k_rows_stats(
+__global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_rows_stats(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ cu_rows, const int32_t *__restrict__ row_pos,
@@ -504,8 +505,9 @@ __global__ __launch_bounds__(64) void k_rows_mass(const float *__restrict__ mass
 }
 
 // ---------------------------------------------------------------- pass 2
+// two blocks a CU for bf16 keys; fp32 keys need the registers of one
 template <typename T, int DH, int RT>
-__global__ __launch_bounds__(kThreads, 2) void k_rows_visual(
+__global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_rows_visual(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ cu_rows, const int32_t *__restrict__ row_pos,
