@@ -423,6 +423,7 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16_staged(
 // tile are issued before the epilogue of the current one, so their latency
 // hides behind the epilogue's arithmetic and stores.
 constexpr int kRingOff = 4, kRingDiag = 8;
+constexpr int kChunkTiles = 4;                              // off-diagonal tiles per block per list chunk (about)
 static_assert((kRingOff & (kRingOff - 1)) == 0 && (kRingDiag & (kRingDiag - 1)) == 0, "power-of-two ring");
 constexpr int kDmaCols = kKS;                               // columns per ring stage (64)
 constexpr int kDmaPieces = kTile * kDmaCols * 2 / 16;       // 16-byte pieces per operand stage (1024)
@@ -453,17 +454,31 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
   __shared__ TileMeta s_next;                        // the next tile, fetched during this one
 
   // Off the diagonal, XCD x receives blocks x, x + 8, ... (gridDim.x is a
-  // multiple of 8) and owns the contiguous range [lo, hi) of the
-  // region-ordered tile list; its blocks take every per-th tile of it, so the
-  // tiles that run together on one XCD are neighbours and share row blocks in
-  // that XCD's L2. Diagonal tiles share nothing: blocks take them with a plain
-  // grid stride, and the list puts every request's last (possibly partial)
-  // row block at its tail, so a block takes at most one full tile and one
-  // last-block tile before a second full one.
+  // multiple of 8). The XCDs walk the region-ordered tile list together, a
+  // chunk of 8 ch tiles at a time: XCD x takes the contiguous slice
+  // [x ch, (x + 1) ch) of each chunk and its blocks every per-th tile of that
+  // slice. So the tiles that run together on one XCD are neighbours and share
+  // row blocks in that XCD's L2, and all XCDs stay in one stretch of the list
+  // (mostly one request), whose features then stay in the last-level cache.
+  // (Giving XCD x the x-th eighth of the whole list put the XCDs on eight
+  // different requests at once.) Diagonal tiles share nothing: blocks take
+  // them with a plain grid stride, and the list puts every request's last
+  // (possibly partial) row block at its tail, so a block takes at most one
+  // full tile and one last-block tile before a second full one.
   const int per = DIAG ? (int)gridDim.x : (int)(gridDim.x / 8), xcd = (int)(blockIdx.x % 8);
-  const int64_t lo = DIAG ? 0 : tiles * xcd / 8, hi = DIAG ? tiles : tiles * (xcd + 1) / 8;
-  int64_t t = lo + (int64_t)(DIAG ? blockIdx.x : blockIdx.x / 8);
-  if (t >= hi) return;
+  const int k_in = DIAG ? (int)blockIdx.x : (int)(blockIdx.x / 8);
+  // chunks of about 8 per kChunkTiles tiles, sized evenly so that the last
+  // one does not leave most XCDs idle
+  const int64_t nchunks = DIAG ? 1 : std::max<int64_t>(1, (tiles + 8LL * per * kChunkTiles - 1) / (8LL * per * kChunkTiles));
+  const int64_t ch = DIAG ? 1 : (tiles + 8 * nchunks - 1) / (8 * nchunks);
+  auto pos = [&](int64_t c, int j) -> int64_t {
+    return DIAG ? k_in + (int64_t)j * per : c * 8 * ch + (int64_t)xcd * ch + k_in + (int64_t)j * per;
+  };
+  int64_t chunk = 0;
+  int step = 0;
+  if (!DIAG && k_in >= ch) return;
+  int64_t t = pos(0, 0);
+  if (t >= tiles) return;
 
   // the wave index is uniform: keep it (and all that derives from it) scalar
   const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
@@ -549,8 +564,14 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
     const int nA = min(kTile, N - rowA0), nB = min(kTile, N - rowB0);
     // (recomputed rather than kept alive through the previous epilogue)
     aim(lane, n0, rowA0, rowB0, nA, nB);
-    const int64_t t_next = t + per;
-    const bool has_next = t_next < hi;
+    int64_t chunk_next = chunk;
+    int step_next = step + 1;
+    if (!DIAG && k_in + (int64_t)step_next * per >= ch) {
+      chunk_next = chunk + 1;
+      step_next = 0;
+    }
+    const int64_t t_next = pos(chunk_next, step_next);
+    const bool has_next = t_next < tiles;
 
     // This tile's work in pairs of 32 x 32 sub-tiles: A rows [32 a, 32 a + 32)
     // against B rows [64 c, 64 c + 64). Sub-tile (a, b) is needed iff A row
@@ -827,6 +848,8 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
 
     if (!has_next) break;
     t = t_next;
+    chunk = chunk_next;
+    step = step_next;
     n0 = n0_next;
     doff = doff_next;
     N = N_next;
