@@ -52,6 +52,10 @@ def parse():
     ap.add_argument("--connector", action="store_true",
                     help="apply the cloud connector (last_connector: LayerNorm, Linear, GELU, Linear, "
                          "Dv -> Dv -> Dv, seeded weights) to the gathered rows in every step")
+    ap.add_argument("--overlap", action="store_true",
+                    help="run the k-center's distances (diverse_select_similarity) on a second stream "
+                         "beside the score pass, then diverse_select_pick; by default every call runs "
+                         "in order on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time for the oracle sample")
@@ -337,15 +341,28 @@ def main():
         log(f"[bench] calibration copy: {nbytes} bytes read, {nbytes} bytes written")
         del src, dst
 
+    # The distances of Eq. 10 need only the features: on a second stream (default
+    # priority) they overlap the score pass; the pick waits for both streams.
+    overlap = args.overlap
+    side = torch.cuda.Stream(device=dev)
+
     def step():
+        if overlap:
+            side.wait_stream(stream)
+            last.diverse_select_similarity(dw.feats, wl.cu_vis, ws_k, cu_vis=b.cu_vis, stream=side)
         if pre is not None:
             last.prefill_attention(b, pre[0], dw.k, pre[1], out=pre_out, scores=scores, ws=ws_s)
         elif rows is None:
             last.token_scores(b, dw.q, dw.k, scores=scores, ws=ws_s)
         else:
             last.rows_scores(b, rows, q_rows, dw.k, scores=scores, ws=ws_s)
-        last.diverse_select(scores, dw.feats, wl.cu_vis, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep,
-                            kept=kept, order=order, gains=gains, ws=ws_k)
+        if overlap:
+            stream.wait_stream(side)
+            last.diverse_select_pick(scores, wl.cu_vis, dw.cu_keep_h, ws_k, wl.Dv, dw.feats.dtype, cu_vis=b.cu_vis,
+                                     cu_keep=dw.cu_keep, kept=kept, order=order, gains=gains)
+        else:
+            last.diverse_select(scores, dw.feats, wl.cu_vis, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep,
+                                kept=kept, order=order, gains=gains, ws=ws_k)
         last.gather_kept(dw.feats, wl.cu_vis, kept, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep, out=out)
         if conn is not None:
             last.connector(out, conn["gamma"], conn["beta"], conn["w1"], conn["b1"], conn["w2"], conn["b2"],
@@ -438,6 +455,9 @@ def main():
                                                              f"; scores from the {args.source} query rows")
                    + ("; scores from the causal prefill attention of every position" if pre is not None else "")
                    + (f"; cloud connector {wl.Dv}->{wl.Dv}->{wl.Dv} on the kept rows" if conn is not None else ""),
+                   "schedule": ("one stream" if not overlap else
+                                "distances (plan, Gram) on a second stream beside the score pass; "
+                                "greedy and gather after both"),
                    "requests": wl.R, "visual_tokens": wl.N_total,
                    "kept_tokens": wl.K_total, "arithmetic": (
                        "bf16 inputs, " + ("fp32 FMA score pass" if args.source != "all_mean" else

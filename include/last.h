@@ -17,6 +17,9 @@
  *                      over unit-normalised encoder features under a budget
  *                      K = ceil(rho N) (Eq. 2); or the Top-k ablation of
  *                      Sec. 4.3, Table 5. Kept indices come out ascending.
+ *   diverse_select_similarity, diverse_select_pick  the k-center of
+ *                      diverse_select in two calls (distances, then greedy),
+ *                      so the distances can overlap the score pass.
  *   gather_kept        Sec. 3.4, Eq. 12: the kept rows X_S, in original order,
  *                      copied byte for byte for transmission.
  *
@@ -222,6 +225,37 @@ last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype,
                            const int32_t *cu_keep_h, int32_t *kept,
                            int32_t *order, float *gains, void *ws,
                            size_t ws_bytes, void *stream);
+
+/*
+ * diverse_select in mode LAST_SEL_KCENTER, as two calls (Sec. 3.4): the
+ * pairwise coverage distances of Eq. 10 depend only on the features, the
+ * greedy of Eq. 9-11 also on the relevance scores. Splitting them lets a
+ * caller compute the distances on a second stream while the scores of the
+ * same batch are still being computed (Eq. 6-8), and join the streams before
+ * the pick call. Together the two calls enqueue the same kernels as one
+ * diverse_select call and give bit-identical kept, order and gains.
+ *   ws         the diverse_select_workspace(R, cu_vis_h, Dv, fdtype,
+ *              LAST_SEL_KCENTER) bytes, 256-byte aligned. The similarity
+ *              call writes the distances there; the pick call reads them, so
+ *              both calls take the same workspace and the same R, Dv, fdtype
+ *              and cu_vis (checked only for shape; distances of other
+ *              features give a selection over those features).
+ *   ordering   the pick call must run after the similarity call has
+ *              finished (same stream, or an event the pick stream waits on),
+ *              and no other call may reuse the workspace in between.
+ * Arguments, errors and outputs are otherwise those of diverse_select; the
+ * similarity call does not need the scores, the pick call not the features.
+ */
+last_status diverse_select_similarity(int32_t R, int32_t Dv, last_dtype fdtype,
+                                      const void *feats, const int32_t *cu_vis,
+                                      const int32_t *cu_vis_h, void *ws,
+                                      size_t ws_bytes, void *stream);
+last_status diverse_select_pick(int32_t R, int32_t Dv, last_dtype fdtype,
+                                const float *scores, const int32_t *cu_vis,
+                                const int32_t *cu_vis_h, const int32_t *cu_keep,
+                                const int32_t *cu_keep_h, int32_t *kept,
+                                int32_t *order, float *gains, void *ws,
+                                size_t ws_bytes, void *stream);
 
 /*
  * Sec. 3.4, Eq. 12: out[t] = feats[cu_vis[r] + kept[t]] for every kept slot

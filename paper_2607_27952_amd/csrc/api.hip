@@ -356,6 +356,53 @@ last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mo
   return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
 }
 
+// Workspace check and carve shared by the two k-center phases: the same
+// (R, cu_vis_h, Dv, fdtype) give the same layout in both calls.
+static last_status kcenter_ws(int32_t R, const int32_t *cu_vis_h, int32_t Dv, last_dtype fdtype,
+                              void *ws, size_t ws_bytes, SelectPlan *p, SelectWs *w) {
+  const size_t need = diverse_select_workspace(R, cu_vis_h, Dv, fdtype, LAST_SEL_KCENTER);
+  if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
+  *p = make_select_plan(R, cu_vis_h, cu_vis_h, LAST_SEL_KCENTER);
+  size_t used = 0;
+  *w = carve_select_ws(ws, R, *p, LAST_SEL_KCENTER, &used);
+  return LAST_OK;
+}
+
+last_status diverse_select_similarity(int32_t R, int32_t Dv, last_dtype fdtype, const void *feats,
+                                      const int32_t *cu_vis, const int32_t *cu_vis_h, void *ws,
+                                      size_t ws_bytes, void *stream) {
+  last_status st = check_select(R, cu_vis_h, Dv, fdtype, LAST_SEL_KCENTER, nullptr);
+  if (st != LAST_OK) return st;
+  if (!feats || !cu_vis) return LAST_ERR_INVALID;
+  if (!aligned(feats, 16)) return LAST_ERR_INVALID;
+  SelectPlan p;
+  SelectWs w;
+  if ((st = kcenter_ws(R, cu_vis_h, Dv, fdtype, ws, ws_bytes, &p, &w)) != LAST_OK) return st;
+  const hipError_t e = launch_similarity(R, Dv, fdtype, p, w, feats, cu_vis, (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
+last_status diverse_select_pick(int32_t R, int32_t Dv, last_dtype fdtype, const float *scores,
+                                const int32_t *cu_vis, const int32_t *cu_vis_h, const int32_t *cu_keep,
+                                const int32_t *cu_keep_h, int32_t *kept, int32_t *order, float *gains,
+                                void *ws, size_t ws_bytes, void *stream) {
+  if (!cu_keep_h) return LAST_ERR_INVALID;
+  last_status st = check_select(R, cu_vis_h, Dv, fdtype, LAST_SEL_KCENTER, cu_keep_h);
+  if (st != LAST_OK) return st;
+  if (!scores || !cu_vis || !cu_keep || !kept) return LAST_ERR_INVALID;
+  SelectPlan p;
+  SelectWs w;
+  if ((st = kcenter_ws(R, cu_vis_h, Dv, fdtype, ws, ws_bytes, &p, &w)) != LAST_OK) return st;
+  size_t used = 0;
+  carve_select_ws(nullptr, R, p, LAST_SEL_KCENTER, &used);
+  char *tail = static_cast<char *>(ws) + used;
+  int32_t *order_ws = reinterpret_cast<int32_t *>(tail);
+  float *gains_ws = reinterpret_cast<float *>(tail + align_up((size_t)p.N_total * sizeof(int32_t), 256));
+  const hipError_t e = launch_pick(R, LAST_SEL_KCENTER, p, w, scores, cu_vis, cu_keep, kept,
+                                   order ? order : order_ws, gains ? gains : gains_ws, (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
 last_status gather_kept(int32_t R, int32_t Dv, size_t elem_bytes, const void *feats,
                         const int32_t *cu_vis, const int32_t *cu_vis_h, const int32_t *kept,
                         const int32_t *cu_keep, const int32_t *cu_keep_h, void *out, void *stream) {

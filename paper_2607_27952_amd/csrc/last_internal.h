@@ -170,6 +170,15 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
                          const SelectPlan &p, const SelectWs &w, const float *scores,
                          const void *feats, const int32_t *cu_vis, const int32_t *cu_keep,
                          int32_t *kept, int32_t *order, float *gains, hipStream_t s);
+// The two halves of launch_select for k-center: the plan and the coverage
+// matrices (features only), then the greedy (or Top-k, which needs no first
+// half) on what the first half left in the workspace.
+hipError_t launch_similarity(int32_t R, int32_t Dv, last_dtype fdtype, const SelectPlan &p,
+                             const SelectWs &w, const void *feats, const int32_t *cu_vis,
+                             hipStream_t s);
+hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const SelectWs &w,
+                       const float *scores, const int32_t *cu_vis, const int32_t *cu_keep,
+                       int32_t *kept, int32_t *order, float *gains, hipStream_t s);
 
 // ------------------------------------------------------------ gather
 hipError_t launch_gather(int32_t R, int64_t row_bytes, int64_t K_total, int64_t N_total,

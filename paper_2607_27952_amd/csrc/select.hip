@@ -1317,7 +1317,16 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
                          const SelectPlan &p, const SelectWs &w, const float *scores,
                          const void *feats, const int32_t *cu_vis, const int32_t *cu_keep,
                          int32_t *kept, int32_t *order, float *gains, hipStream_t s) {
-  hipError_t e;
+  if (mode == LAST_SEL_KCENTER) {
+    const hipError_t e = launch_similarity(R, Dv, fdtype, p, w, feats, cu_vis, s);
+    if (e != hipSuccess) return e;
+  }
+  return launch_pick(R, mode, p, w, scores, cu_vis, cu_keep, kept, order, gains, s);
+}
+
+hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const SelectWs &w,
+                       const float *scores, const int32_t *cu_vis, const int32_t *cu_keep,
+                       int32_t *kept, int32_t *order, float *gains, hipStream_t s) {
   if (mode == LAST_SEL_TOPK) {
     launch_begin("topk", s);
 #define LAST_TOPK(E) \
@@ -1334,6 +1343,37 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
     return launch_end(s);
   }
 
+  launch_begin("greedy", s);
+#define LAST_GREEDY(E, T)                                                                          \
+  hipLaunchKernelGGL((k_greedy<E, T>), dim3(R), dim3(T), 0, s, scores, w.dmat, w.d_off, cu_vis, cu_keep, \
+                     kept, order, gains)
+  if (p.g_threads == 64) {
+    switch (p.g_ept) {
+      case 2: LAST_GREEDY(2, 64); break;
+      case 4: LAST_GREEDY(4, 64); break;
+      case 8: LAST_GREEDY(8, 64); break;
+      case 12: LAST_GREEDY(12, 64); break;
+      default: LAST_GREEDY(16, 64); break;
+    }
+  } else if (p.g_threads == 256) {
+    switch (p.g_ept) {
+      case 8: LAST_GREEDY(8, 256); break;
+      case 16: LAST_GREEDY(16, 256); break;
+      default: LAST_GREEDY(32, 256); break;
+    }
+  } else if (p.g_threads == 512) {
+    LAST_GREEDY(32, 512);
+  } else {
+    LAST_GREEDY(32, 1024);
+  }
+#undef LAST_GREEDY
+  return launch_end(s);
+}
+
+hipError_t launch_similarity(int32_t R, int32_t Dv, last_dtype fdtype, const SelectPlan &p,
+                             const SelectWs &w, const void *feats, const int32_t *cu_vis,
+                             hipStream_t s) {
+  hipError_t e;
   launch_begin("select_plan", s);
   hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, w.dtile_off, w.otile_off, w.d_off);
   hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, cu_vis, w.dtile_off, w.otile_off, w.d_off,
@@ -1382,32 +1422,7 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
       if ((e = launch_end(s)) != hipSuccess) return e;
     }
   }
-
-  launch_begin("greedy", s);
-#define LAST_GREEDY(E, T)                                                                          \
-  hipLaunchKernelGGL((k_greedy<E, T>), dim3(R), dim3(T), 0, s, scores, w.dmat, w.d_off, cu_vis, cu_keep, \
-                     kept, order, gains)
-  if (p.g_threads == 64) {
-    switch (p.g_ept) {
-      case 2: LAST_GREEDY(2, 64); break;
-      case 4: LAST_GREEDY(4, 64); break;
-      case 8: LAST_GREEDY(8, 64); break;
-      case 12: LAST_GREEDY(12, 64); break;
-      default: LAST_GREEDY(16, 64); break;
-    }
-  } else if (p.g_threads == 256) {
-    switch (p.g_ept) {
-      case 8: LAST_GREEDY(8, 256); break;
-      case 16: LAST_GREEDY(16, 256); break;
-      default: LAST_GREEDY(32, 256); break;
-    }
-  } else if (p.g_threads == 512) {
-    LAST_GREEDY(32, 512);
-  } else {
-    LAST_GREEDY(32, 1024);
-  }
-#undef LAST_GREEDY
-  return launch_end(s);
+  return hipSuccess;
 }
 
 }  // namespace last

@@ -26,7 +26,7 @@ SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
 EXPORTS = ("last_token_scores_workspace", "last_token_scores", "last_source_rows",
            "last_rows_scores_workspace", "last_rows_scores", "last_prefill_attention_workspace",
            "last_prefill_attention", "diverse_select_workspace",
-           "diverse_select", "gather_kept", "last_connector_workspace", "last_connector", "last_budget", "last_status_string", "last_version",
+           "diverse_select", "diverse_select_similarity", "diverse_select_pick", "gather_kept", "last_connector_workspace", "last_connector", "last_budget", "last_status_string", "last_version",
            "last_profile_enable", "last_profile_collect", "last_profile_reset",
            "last_profile_count", "last_profile_kernel")
 
@@ -76,6 +76,10 @@ def lib():
         L.diverse_select_workspace.restype = SZ
         L.diverse_select.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
         L.diverse_select.restype = I32
+        L.diverse_select_similarity.argtypes = [I32, I32, I32, P, P, P, P, SZ, P]
+        L.diverse_select_similarity.restype = I32
+        L.diverse_select_pick.argtypes = [I32, I32, I32, P, P, P, P, P, P, P, P, P, SZ, P]
+        L.diverse_select_pick.restype = I32
         L.gather_kept.argtypes = [I32, I32, SZ, P, P, P, P, P, P, P, P]
         L.gather_kept.restype = I32
         I64 = ctypes.c_int64
@@ -315,6 +319,46 @@ def diverse_select(scores: torch.Tensor, feats: torch.Tensor, cu_vis_h, cu_keep_
                               _ptr(ws), ws.numel(), _stream(stream))
     if st != LAST_OK:
         raise LastError(st, "diverse_select")
+    return kept, order, gains
+
+
+def diverse_select_similarity(feats: torch.Tensor, cu_vis_h, ws: torch.Tensor, cu_vis=None, stream=None):
+    """diverse_select_similarity (Eq. 10): the coverage distances of every request into ws."""
+    dev = feats.device
+    cv = _i32_host(cu_vis_h)
+    if cu_vis is None:
+        cu_vis = _i32_dev(cv, dev)
+    st = lib().diverse_select_similarity(len(cv) - 1, feats.shape[-1], _dtype_code(feats), _ptr(feats),
+                                         _ptr(cu_vis), _ptr(cv), _ptr(ws), ws.numel(), _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "diverse_select_similarity")
+    return ws
+
+
+def diverse_select_pick(scores: torch.Tensor, cu_vis_h, cu_keep_h, ws: torch.Tensor, Dv: int,
+                        f_dtype=torch.bfloat16, cu_vis=None, cu_keep=None, kept=None, order=None,
+                        gains=None, want_order=True, stream=None):
+    """diverse_select_pick (Eq. 9-12) on the distances diverse_select_similarity left in ws:
+    returns (kept, order, gains)."""
+    dev = scores.device
+    cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
+    code = LAST_BF16 if f_dtype == torch.bfloat16 else LAST_F32
+    if cu_vis is None:
+        cu_vis = _i32_dev(cv, dev)
+    if cu_keep is None:
+        cu_keep = _i32_dev(ck, dev)
+    Kt = int(ck[-1])
+    if kept is None:
+        kept = torch.empty(Kt, dtype=torch.int32, device=dev)
+    if want_order and order is None:
+        order = torch.empty(Kt, dtype=torch.int32, device=dev)
+    if want_order and gains is None:
+        gains = torch.empty(Kt, dtype=torch.float32, device=dev)
+    st = lib().diverse_select_pick(len(cv) - 1, Dv, code, _ptr(scores), _ptr(cu_vis), _ptr(cv), _ptr(cu_keep),
+                                   _ptr(ck), _ptr(kept), _ptr(order), _ptr(gains), _ptr(ws), ws.numel(),
+                                   _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "diverse_select_pick")
     return kept, order, gains
 
 

@@ -176,6 +176,41 @@ def test_select_workspace_and_small_workspace():
     assert last.lib().diverse_select_workspace(2, cv.ctypes.data, 0, last.LAST_BF16, last.KCENTER) == 0
 
 
+def _two_phase_call(phase, cv, ck, Dv=64, fdtype=last.LAST_BF16, ws_bytes=1 << 40, misalign=0):
+    """Status of diverse_select_similarity ("sim") or diverse_select_pick ("pick"); every
+    case here must be rejected on the host, so no buffer may change."""
+    cv = np.asarray(cv, np.int32)
+    ck = None if ck is None else np.asarray(ck, np.int32)
+    dev, out, ws = Fake(), Fake(), Fake()
+    L = last.lib()
+    if phase == "sim":
+        st = L.diverse_select_similarity(len(cv) - 1, Dv, fdtype, dev.p + misalign, dev.p, cv.ctypes.data,
+                                         ws.p, ws_bytes, None)
+    else:
+        st = L.diverse_select_pick(len(cv) - 1, Dv, fdtype, dev.p, dev.p, cv.ctypes.data, dev.p,
+                                   None if ck is None else ck.ctypes.data, out.p, out.p, out.p, ws.p, ws_bytes,
+                                   None)
+    assert st != last.LAST_OK
+    assert out.untouched() and ws.untouched() and dev.untouched()
+    return st
+
+
+def test_two_phase_select_rejects_what_diverse_select_rejects():
+    E, U, W = last.LAST_ERR_INVALID, last.LAST_ERR_UNSUPPORTED, last.LAST_ERR_WORKSPACE
+    assert _two_phase_call("pick", [0, 10, 30], [0, 11, 15]) == E     # K_r > N_r
+    assert _two_phase_call("pick", [0, 10, 30], None) == E            # no host budgets
+    assert _two_phase_call("sim", [0, 10, 30], None, misalign=2) == E  # features not 16-byte aligned
+    for ph in ("sim", "pick"):
+        assert _two_phase_call(ph, [0, 10, 10], [0, 5, 5]) == E        # N_r = 0
+        assert _two_phase_call(ph, [0, 10, 30], [0, 5, 6], Dv=0) == E
+        assert _two_phase_call(ph, [0, 10, 30], [0, 5, 6], fdtype=3) == E
+        assert _two_phase_call(ph, [0, 32769], [0, 5]) == U
+        assert _two_phase_call(ph, [0, 10, 30], [0, 5, 6], Dv=60) == U
+        cv = np.array([0, 100, 350], np.int32)
+        need = last.lib().diverse_select_workspace(2, cv.ctypes.data, 64, last.LAST_BF16, last.KCENTER)
+        assert _two_phase_call(ph, cv, [0, 5, 6], ws_bytes=need - 1) == W
+
+
 def test_gather_rejects_bad_arguments():
     cv = np.array([0, 10, 30], np.int32)
     ck = np.array([0, 4, 6], np.int32)

@@ -352,6 +352,54 @@ def test_config_select(name, workloads):
               f"end to end: {ex} exact, {exc} excused; kept sets equal to the oracle's: {same}")
 
 
+def _two_phase(dw_feats, cu_vis_h, cu_keep_h, make_scores):
+    """The k-center as diverse_select_similarity on a side stream, overlapped with
+    `make_scores()` on the current stream, then diverse_select_pick after a join."""
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+    ws = torch.empty(last.select_workspace(cu_vis_h, dw_feats.shape[-1], dw_feats.dtype), dtype=torch.uint8,
+                     device="cuda")
+    side.wait_stream(main)
+    last.diverse_select_similarity(dw_feats, cu_vis_h, ws, stream=side)
+    scores = make_scores()
+    main.wait_stream(side)
+    kept, order, gains = last.diverse_select_pick(scores, cu_vis_h, cu_keep_h, ws, dw_feats.shape[-1],
+                                                  dw_feats.dtype)
+    torch.cuda.synchronize()
+    return scores, kept.cpu().numpy(), order.cpu().numpy(), gains.cpu().numpy()
+
+
+@pytest.mark.parametrize("case", [c for c in SELECT_CASES if c[0] in (20, 23, 24, 27)], ids=lambda c: f"k{c[0]}")
+def test_two_phase_select_small(case):
+    """Split k-center (bf16 streamed and staged Gram, fp32 Gram, 256-thread greedy):
+    the oracle replay accepts it, and it is bit-identical to one diverse_select call."""
+    seed, R, nr, Dv, dt, kf, comps = case
+    wl = W.tiny(seed, R=R, n_range=nr, Dv=Dv, f_dtype=dt, k_frac=kf, comps=comps)
+    rng = np.random.default_rng(seed)
+    w32 = np.concatenate([rng.dirichlet(np.ones(wl.n(r)) * 0.7) for r in range(R)]).astype(np.float32)
+    dw = last.DeviceWorkload.upload(wl)
+    st = torch.from_numpy(w32).cuda()
+    _, kept, order, gains = _two_phase(dw.feats, wl.cu_vis, wl.cu_keep, lambda: st)
+    check_selection(wl, w32, kept, order, f"two-phase case {seed}")
+    one = gpu_select(dw.feats, st, wl.cu_vis, wl.cu_keep)
+    for x, y in zip((kept, order, gains), one):
+        assert x.tobytes() == y.tobytes()
+
+
+@pytest.mark.parametrize("name", W.CONFIGS)
+def test_config_two_phase_overlapped(name, workloads):
+    """The bench's overlapped schedule (distances on a side stream while the scores
+    run) gives bit-identical scores, kept, order and gains to the serial calls."""
+    wl, dw = workloads(name)
+    g, kept, order, gains = _two_phase(dw.feats, wl.cu_vis, dw.cu_keep_h,
+                                       lambda: last.token_scores(dw.batch, dw.q, dw.k))
+    g1 = last.token_scores(dw.batch, dw.q, dw.k)
+    one = gpu_select(dw.feats, g1, wl.cu_vis, dw.cu_keep_h)
+    assert g.cpu().numpy().tobytes() == g1.cpu().numpy().tobytes()
+    for x, y in zip((kept, order, gains), one):
+        assert x.tobytes() == y.tobytes()
+
+
 def test_long_requests_x1(workloads):
     """Two requests of 32768 tokens (past the 512-thread greedy): scores of
     one request against the oracle; the whole selection's invariants; and
