@@ -140,6 +140,9 @@ def gram_work(wl):
 
     def bound(b, f):
         return ("hbm", b) if b / HBM_BYTES_PER_S >= f / peak else (kind, f)
+    if felt == 4:
+        # fp32 features: one launch covers every sub-tile (its blocks compute their own norms)
+        return {"gram": bound(b_diag + b_off, f_diag + f_off)}
     return {"gram_diag": bound(b_diag, f_diag), "gram": bound(b_off, f_off)}
 
 
@@ -190,8 +193,7 @@ def kernel_work(wl, row_pos=None):
         "score_finalize": ("hbm", vlog + wl.N_total * 4),
         # features read once
         "sqnorm": ("hbm", wl.N_total * wl.Dv * felt),
-        "gram_diag": gw["gram_diag"],
-        "gram": gw["gram"],
+        **gw,
         # one coverage row of N_r floats per pick, plus the weights
         "greedy": ("hbm", float(np.sum(kk * n)) * 4 + wl.N_total * 4),
         "topk": ("hbm", wl.N_total * 4 + wl.K_total * 4),
@@ -426,7 +428,7 @@ def main():
     gram_ms = sum(kernels[k]["ms_per_step"] for k in ("gram_diag", "gram") if k in kernels)
     similarity = None
     if gram_ms > 0:
-        exec_flops = work["gram_diag"][1] + work["gram"][1]
+        exec_flops = sum(work[k][1] for k in ("gram_diag", "gram") if k in work)
         similarity = {"paper_flops": paper_flops, "gram_unique_flops": exec_flops,
                       "gram_ms_per_step": round(gram_ms, 4),
                       "tflops_on_paper_work": round(paper_flops / (gram_ms * 1e-3) / 1e12, 2),

@@ -860,33 +860,34 @@ __global__ __launch_bounds__(kGramThreads) void k_gram_bf16(
 
 // fp32 features: every dot product, squared norms included, is one fp64 FMA
 // chain over d = 0..Dv-1 in order, so a row and its bitwise duplicate get
-// distance exactly 0. Block b computes 32 x 32 sub-tile b % 16 of 128 x 128
-// tile b / 16 (4 x 4 sub-tiles), 2 x 2 outputs a thread, over 64-column
-// chunks staged through LDS; the next chunk is loaded into registers while
-// the current one is used. Three launches:
-//   kF32Self   sub-tiles on the diagonal of the diagonal tiles: their own
-//              diagonal gives the squared norms of their 32 rows (written
-//              out for the other launches) and their coverage values;
-//   kF32Upper  sub-tiles above the diagonal of the diagonal tiles (each
-//              also writes its mirror);
-//   kF32Off    every sub-tile of the off-diagonal tiles (mirrored).
+// distance exactly 0. One launch covers every 32 x 32 sub-tile that a
+// request's coverage matrix needs: blocks [0, 16 tiles_diag) take sub-tile
+// b % 16 of diagonal tile b / 16 (those below its diagonal return at once),
+// the rest the sub-tiles of the off-diagonal tiles. 2 x 2 outputs a thread,
+// over 64-column chunks staged through LDS, with four chunks of loads in
+// flight. Wave 0 also runs the squared-norm chains of the block's 32 A rows
+// and 32 B rows, the same FMAs in the same order as a dot product of a row
+// with itself, so no block waits for another's norms. Sub-tiles on a
+// diagonal write the norms out; those above it, and every off-diagonal
+// sub-tile, also write the mirror.
 constexpr int kF32Sub = 32, kF32KS = 64, kF32Subs = (kTile / kF32Sub) * (kTile / kF32Sub);
-constexpr int kF32Self = 0, kF32Upper = 1, kF32Off = 2;
 constexpr int kF32Per = kF32Sub * kF32KS / 256;   // staged elements per thread and operand
+constexpr int kF32Ahead = 4;                      // chunks of loads in flight
 
-template <int MODE>
 __global__ __launch_bounds__(256) void k_gram_f32(
-    const float *__restrict__ X, const TileMeta *__restrict__ meta, double *__restrict__ nn,
-    double *__restrict__ inv, int Dv, int64_t tiles_total, int64_t d_cap, float *__restrict__ dmat) {
+    const float *__restrict__ X, const TileMeta *__restrict__ dmeta, const TileMeta *__restrict__ ometa,
+    double *__restrict__ nn, double *__restrict__ inv, int Dv, int64_t tiles_diag, int64_t tiles_off,
+    int64_t d_cap, float *__restrict__ dmat) {
   __shared__ float sA[kF32KS][kF32Sub + 1];
   __shared__ float sB[kF32KS][kF32Sub + 1];
-  __shared__ double s_nn[kF32Sub], s_inv[kF32Sub];
+  __shared__ double s_nn[2][kF32Sub], s_inv[2][kF32Sub];   // [0]: A rows, [1]: B rows
   const int64_t t_glob = blockIdx.x / kF32Subs;
   const int sub = blockIdx.x % kF32Subs, sa = sub / (kTile / kF32Sub), sb = sub % (kTile / kF32Sub);
-  if (t_glob >= tiles_total) return;
-  if (MODE == kF32Self && sb != sa) return;
-  if (MODE == kF32Upper && sb <= sa) return;
-  const TileMeta m = meta[t_glob];
+  const bool on_diag = t_glob < tiles_diag;
+  if (t_glob >= tiles_diag + tiles_off) return;
+  if (on_diag && sb < sa) return;
+  const bool self = on_diag && sb == sa;
+  const TileMeta m = on_diag ? dmeta[t_glob] : ometa[t_glob - tiles_diag];
   const int64_t n0 = m.n0;
   const int N = m.n, I = m.ij >> 16, J = m.ij & 0xFFFF;
   const int rowA0 = I * kTile + sa * kF32Sub, rowB0 = J * kTile + sb * kF32Sub;
@@ -895,67 +896,83 @@ __global__ __launch_bounds__(256) void k_gram_f32(
   const int64_t nbr = cov_blocks(N), dlim = d_cap - m.doff;
   const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
 
-  float pa[kF32Per], pb[kF32Per];
-  auto fetch = [&](int k0) {
+  // A block has one wave per SIMD, so a chunk's loads cannot hide behind
+  // other waves: kF32Ahead chunks are in flight in a register ring while the
+  // current one is multiplied.
+  float pa[kF32Ahead][kF32Per], pb[kF32Ahead][kF32Per];
+  auto fetch = [&](int k0, float (&fa)[kF32Per], float (&fb)[kF32Per]) {
 #pragma unroll
     for (int q = 0; q < kF32Per; ++q) {
       const int e = tid + 256 * q, row = e / kF32KS, kk = e % kF32KS;
       const int ia = rowA0 + row, ib = rowB0 + row;
-      pa[q] = (ia < N && k0 + kk < Dv) ? X[(n0 + ia) * Dv + k0 + kk] : 0.f;
-      pb[q] = (ib < N && k0 + kk < Dv) ? X[(n0 + ib) * Dv + k0 + kk] : 0.f;
+      fa[q] = (ia < N && k0 + kk < Dv) ? X[(n0 + ia) * Dv + k0 + kk] : 0.f;
+      fb[q] = (ib < N && k0 + kk < Dv) ? X[(n0 + ib) * Dv + k0 + kk] : 0.f;
     }
   };
   double acc[2][2] = {{0.0, 0.0}, {0.0, 0.0}};
-  fetch(0);
-  for (int k0 = 0; k0 < Dv; k0 += kF32KS) {
-    __syncthreads();
+  double nacc = 0.0;   // wave 0: lane l < 32 row l of A, lane l >= 32 row l - 32 of B
+  const int nch = (Dv + kF32KS - 1) / kF32KS;
 #pragma unroll
-    for (int q = 0; q < kF32Per; ++q) {
-      const int e = tid + 256 * q, row = e / kF32KS, kk = e % kF32KS;
-      sA[kk][row] = pa[q];
-      sB[kk][row] = pb[q];
-    }
-    __syncthreads();
-    if (k0 + kF32KS < Dv) fetch(k0 + kF32KS);
-    const int kmax = min(kF32KS, Dv - k0);
-    for (int kk = 0; kk < kmax; ++kk) {
-      const double a0 = sA[kk][ty], a1 = sA[kk][ty + 16];
-      const double b0 = sB[kk][tx], b1 = sB[kk][tx + 16];
-      acc[0][0] = fma(a0, b0, acc[0][0]);
-      acc[0][1] = fma(a0, b1, acc[0][1]);
-      acc[1][0] = fma(a1, b0, acc[1][0]);
-      acc[1][1] = fma(a1, b1, acc[1][1]);
-    }
-  }
-  // norms of the rows (MODE kF32Self: from this block's own diagonal)
-  if (MODE == kF32Self) {
-    if (tx == ty) {
-      s_nn[ty] = acc[0][0];
-      s_nn[ty + 16] = acc[1][1];
-    }
-    __syncthreads();
-    if (tid < kF32Sub) {
-      const double v = s_nn[tid];
-      s_inv[tid] = v > 0.0 ? 1.0 / sqrt(v) : 0.0;
-      if (rowA0 + tid < N) {
-        nn[n0 + rowA0 + tid] = v;
-        inv[n0 + rowA0 + tid] = s_inv[tid];
+  for (int b = 0; b < kF32Ahead; ++b)
+    if (b < nch) fetch(b * kF32KS, pa[b], pb[b]);
+  for (int c0 = 0; c0 < nch; c0 += kF32Ahead) {
+#pragma unroll
+    for (int b = 0; b < kF32Ahead; ++b) {
+      const int c = c0 + b;
+      if (c >= nch) break;
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < kF32Per; ++q) {
+        const int e = tid + 256 * q, row = e / kF32KS, kk = e % kF32KS;
+        sA[kk][row] = pa[b][q];
+        sB[kk][row] = pb[b][q];
+      }
+      __syncthreads();
+      if (c + kF32Ahead < nch) fetch((c + kF32Ahead) * kF32KS, pa[b], pb[b]);
+      // full chunks unrolled, so the LDS reads of later columns are issued
+      // while earlier FMAs run; the FMA order along d is the same either way
+      auto mac = [&](int kk) {
+        const double a0 = sA[kk][ty], a1 = sA[kk][ty + 16];
+        const double b0 = sB[kk][tx], b1 = sB[kk][tx + 16];
+        acc[0][0] = fma(a0, b0, acc[0][0]);
+        acc[0][1] = fma(a0, b1, acc[0][1]);
+        acc[1][0] = fma(a1, b0, acc[1][0]);
+        acc[1][1] = fma(a1, b1, acc[1][1]);
+        if (tid < 64) {
+          const double v = tid < 32 ? sA[kk][tid] : sB[kk][tid - 32];
+          nacc = fma(v, v, nacc);
+        }
+      };
+      const int kmax = min(kF32KS, Dv - c * kF32KS);
+      if (kmax == kF32KS) {
+#pragma unroll
+        for (int kk = 0; kk < kF32KS; ++kk) mac(kk);
+      } else {
+        for (int kk = 0; kk < kmax; ++kk) mac(kk);
       }
     }
-    __syncthreads();
   }
+  if (tid < 64) {
+    const int side = tid >> 5, r = tid & 31;
+    s_nn[side][r] = nacc;
+    s_inv[side][r] = nacc > 0.0 ? 1.0 / sqrt(nacc) : 0.0;
+    if (self && side == 0 && rowA0 + r < N) {
+      nn[n0 + rowA0 + r] = nacc;
+      inv[n0 + rowA0 + r] = s_inv[0][r];
+    }
+  }
+  __syncthreads();
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
       const int il = ty + 16 * a, jl = tx + 16 * b, i = rowA0 + il, j = rowB0 + jl;
       if (i >= N || j >= N) continue;
-      const double nni = MODE == kF32Self ? s_nn[il] : nn[n0 + i], nnj = MODE == kF32Self ? s_nn[jl] : nn[n0 + j];
-      const double ivi = MODE == kF32Self ? s_inv[il] : inv[n0 + i], ivj = MODE == kF32Self ? s_inv[jl] : inv[n0 + j];
-      const float dv = i == j ? kSelfMark : coverage(acc[a][b], nni, nnj, ivi, ivj);
+      const float dv = self && i == j ? kSelfMark
+                                      : coverage(acc[a][b], s_nn[0][il], s_nn[1][jl], s_inv[0][il], s_inv[1][jl]);
       const int64_t oij = cov_index(i, j, nbr), oji = cov_index(j, i, nbr);
       if (oij < dlim) D[oij] = dv;
-      if (MODE != kF32Self && oji < dlim) D[oji] = dv;
+      if (!self && oji < dlim) D[oji] = dv;
     }
 }
 
@@ -1280,7 +1297,7 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   if (p.N_max <= 1024) {
     p.g_threads = 64;
     const int e = (p.N_max + 63) / 64;
-    p.g_ept = e <= 2 ? 2 : e <= 4 ? 4 : e <= 8 ? 8 : e <= 12 ? 12 : 16;
+    p.g_ept = e <= 2 ? 2 : e <= 4 ? 4 : e <= 6 ? 6 : e <= 8 ? 8 : e <= 10 ? e : e <= 12 ? 12 : e <= 14 ? 14 : 16;
   } else if (p.N_max <= 8192) {
     p.g_threads = 256;
     const int e = (p.N_max + 255) / 256;
@@ -1351,8 +1368,12 @@ hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const
     switch (p.g_ept) {
       case 2: LAST_GREEDY(2, 64); break;
       case 4: LAST_GREEDY(4, 64); break;
+      case 6: LAST_GREEDY(6, 64); break;
       case 8: LAST_GREEDY(8, 64); break;
+      case 9: LAST_GREEDY(9, 64); break;
+      case 10: LAST_GREEDY(10, 64); break;
       case 12: LAST_GREEDY(12, 64); break;
+      case 14: LAST_GREEDY(14, 64); break;
       default: LAST_GREEDY(16, 64); break;
     }
   } else if (p.g_threads == 256) {
@@ -1409,18 +1430,12 @@ hipError_t launch_similarity(int32_t R, int32_t Dv, last_dtype fdtype, const Sel
       }
     }
   } else {
-    launch_begin("gram_diag", s);
-    hipLaunchKernelGGL(k_gram_f32<kF32Self>, dim3((unsigned)(p.tiles_diag * kF32Subs)), dim3(256), 0, s,
-                       (const float *)feats, w.dtile, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
-    hipLaunchKernelGGL(k_gram_f32<kF32Upper>, dim3((unsigned)(p.tiles_diag * kF32Subs)), dim3(256), 0, s,
-                       (const float *)feats, w.dtile, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
+    // one launch: every block computes its own rows' norms
+    launch_begin("gram", s);
+    hipLaunchKernelGGL(k_gram_f32, dim3((unsigned)((p.tiles_diag + p.tiles_off) * kF32Subs)), dim3(256), 0, s,
+                       (const float *)feats, w.dtile, w.otile, w.nn, w.inv, Dv, p.tiles_diag, p.tiles_off,
+                       p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
-    if (p.tiles_off > 0) {
-      launch_begin("gram", s);
-      hipLaunchKernelGGL(k_gram_f32<kF32Off>, dim3((unsigned)(p.tiles_off * kF32Subs)), dim3(256), 0, s,
-                         (const float *)feats, w.otile, w.nn, w.inv, Dv, p.tiles_off, p.d_elems, w.dmat);
-      if ((e = launch_end(s)) != hipSuccess) return e;
-    }
   }
   return hipSuccess;
 }

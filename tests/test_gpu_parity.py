@@ -158,6 +158,8 @@ SELECT_CASES = [
     (32, 1, (16385, 16600), 256, W.BF16, 0.03, 32),  # greedy blocks of 1024 threads
     (33, 2, (30000, 32767), 64, W.BF16, 0.02, 16),   # up to the 32768-token limit, staged Gram
     (34, 1, (20000, 24000), 48, W.F32, 0.02, 8),     # fp32 Gram beyond 16384 tokens
+    (36, 3, (840, 896), 128, W.BF16, 0.1, 8),        # one-wave greedy, 14 tokens a lane
+    (37, 2, (513, 576), 256, W.BF16, 0.15, 6),       # one-wave greedy, 9 tokens a lane
 ]
 
 
