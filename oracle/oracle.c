@@ -43,7 +43,10 @@
  *   - a zero-norm feature normalises to the zero vector;
  *   - the cosine is evaluated as x_i.x_j / sqrt(|x_i|^2 |x_j|^2), so that
  *     bitwise-identical features are at coverage distance exactly 0;
- *   - the selection consumes the fp32 relevance scores it is given.
+ *   - the selection consumes the fp32 relevance scores it is given; one that
+ *     is not > 0 (negative, NaN) counts as 0, and a NaN objective (+inf
+ *     relevance times a coverage distance of 0) counts as 0. Eq. 8's scores
+ *     are probabilities, so neither rule touches the paper's inputs.
  */
 #include <math.h>
 #include <stdint.h>
@@ -458,6 +461,16 @@ static double orc_cover(const orc_feats *f, int64_t i, int64_t j) {
   return t > 0.0 ? t : 0.0;
 }
 
+/*
+ * Eq. 8 makes the relevance a probability, finite and >= 0; on such inputs the
+ * two helpers below are the identity. Relevance from elsewhere is read as
+ * follows: a value that is not > 0 (negative, NaN) counts as 0, and an
+ * objective w * delta that is NaN (+inf relevance on a covered token, delta = 0)
+ * counts as 0.
+ */
+static double orc_rel(float w) { return (double)w > 0.0 ? (double)w : 0.0; }
+static double orc_obj(double v) { return v == v ? v : 0.0; }
+
 /* Lowest index attaining the maximum of o over unselected i. */
 static int64_t orc_argmax(const double *o, const unsigned char *sel, int64_t N) {
   int64_t best = -1;
@@ -477,7 +490,7 @@ static int orc_cmp_i32(const void *a, const void *b) {
 static const float *orc_sort_keys;
 static int orc_cmp_topk(const void *a, const void *b) {
   const int32_t x = *(const int32_t *)a, y = *(const int32_t *)b;
-  const double wx = orc_sort_keys[x], wy = orc_sort_keys[y];
+  const double wx = orc_rel(orc_sort_keys[x]), wy = orc_rel(orc_sort_keys[y]);
   if (wx > wy) return -1;
   if (wx < wy) return 1;
   return (x > y) - (x < y);
@@ -509,7 +522,7 @@ int oracle_select(int R, int Dv, int f_dtype, int mode, const float *w,
       qsort(idx, (size_t)N, sizeof(int32_t), orc_cmp_topk);
       for (int64_t t = 0; t < K; ++t) {
         order[out0 + t] = idx[t];
-        gains[out0 + t] = (double)w[row0 + idx[t]];
+        gains[out0 + t] = orc_rel(w[row0 + idx[t]]);
         kept[out0 + t] = idx[t];
       }
       qsort(kept + out0, (size_t)K, sizeof(int32_t), orc_cmp_i32);
@@ -526,7 +539,7 @@ int oracle_select(int R, int Dv, int f_dtype, int mode, const float *w,
       return 2;
     }
     /* Eq. 9: start from the most relevant token */
-    for (int64_t i = 0; i < N; ++i) o[i] = (double)w[row0 + i];
+    for (int64_t i = 0; i < N; ++i) o[i] = orc_rel(w[row0 + i]);
     int64_t j = orc_argmax(o, sel, N);
     if (j < 0) {
       orc_free_feats(&xf); free(delta); free(o); free(sel);
@@ -542,7 +555,7 @@ int oracle_select(int R, int Dv, int f_dtype, int mode, const float *w,
       for (int64_t i = 0; i < N; ++i) {
         const double c = orc_cover(&xf, i, j);
         if (c < delta[i]) delta[i] = c;
-        o[i] = (double)w[row0 + i] * delta[i];
+        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);
       }
       /* Eq. 11 */
       j = orc_argmax(o, sel, N);
@@ -594,7 +607,7 @@ int oracle_replay(int R, int Dv, int f_dtype, const float *w,
     }
     for (int64_t i = 0; i < N; ++i) {
       delta[i] = INFINITY;
-      o[i] = (double)w[row0 + i];
+      o[i] = orc_rel(w[row0 + i]);
     }
     int broken = 0;
     for (int64_t t = 0; t < K; ++t) {
@@ -625,7 +638,7 @@ int oracle_replay(int R, int Dv, int f_dtype, const float *w,
       for (int64_t i = 0; i < N; ++i) {
         const double c = orc_cover(&xf, i, gp);
         if (c < delta[i]) delta[i] = c;
-        o[i] = (double)w[row0 + i] * delta[i];
+        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);
       }
     }
     orc_free_feats(&xf); free(delta); free(o); free(sel);

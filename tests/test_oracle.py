@@ -338,6 +338,51 @@ def test_topk_is_stable_sort():
     np.testing.assert_array_equal(gains, w[expect])
 
 
+def _golden_float(v):
+    return float(v)  # json carries "inf" / "nan" as strings; float() reads both
+
+
+def test_select_clamp_golden():
+    """Reading 10: a coverage term that rounds below 0 is clamped, so the tie at 0 goes to the lower index."""
+    c = _load("select_clamp_replay.json")["clamp"]
+    X = np.array([[float.fromhex(v) for v in row] for row in c["feats_hex"]], np.float32)
+    assert X[0, 2] != X[1, 2] and np.array_equal(X[0], X[2])
+    kept, order, gains = _sel(c["w"], X, c["K"])
+    assert list(order) == c["order"]
+    np.testing.assert_array_equal(gains, c["gains"])      # exactly 0, never negative
+
+
+def test_select_gains_never_negative_on_near_parallel_rows():
+    """Eq. 10 with the clamp: every objective is >= 0 even where 1 - cos rounds below 0."""
+    rng = np.random.default_rng(11)
+    base = rng.standard_normal((8, 3)).astype(np.float32)
+    base[:, 2] *= np.float32(1e-4)
+    X = np.repeat(base, 4, axis=0)
+    for k in range(X.shape[0]):                      # one-ulp nudges of the small component
+        X[k, 2] = np.nextafter(X[k, 2], np.float32(np.inf)) if k % 2 else X[k, 2]
+    w = rng.dirichlet(np.ones(X.shape[0])).astype(np.float32)
+    _, order, gains = _sel(w, X, X.shape[0])
+    assert np.all(gains >= 0.0)
+    assert sorted(order) == list(range(X.shape[0]))
+
+
+def test_select_edge_values_golden():
+    g = _load("select_edge_values.json")
+    for case in g["cases"]:
+        X = np.asarray(case["feats"], np.float32)
+        w = np.array([_golden_float(v) for v in case["w"]], np.float32)
+        _, order, gains = _sel(w, X, case["K"])
+        assert list(order) == case["order"], case["name"]
+        # every delta here is exactly 0 or 1, so each gain is an fp32 relevance value or 0
+        expect = np.array([_golden_float(v) for v in case["gains"]], np.float32).astype(np.float64)
+        np.testing.assert_array_equal(gains, expect, err_msg=case["name"])
+    t = g["topk"]
+    w = np.array([_golden_float(v) for v in t["w"]], np.float32)
+    kept, order, gains = _sel(w, np.eye(len(w), dtype=np.float32), t["K"], mode=oracle.TOPK)
+    assert list(order) == t["order"] and list(kept) == t["kept"]
+    np.testing.assert_array_equal(gains, np.array(t["gains"], np.float32).astype(np.float64))
+
+
 # ---------------------------------------------------------------- replay, gather, budget
 
 def test_replay_classifies_steps():
@@ -362,6 +407,16 @@ def test_replay_excuses_near_ties():
     w = np.array([0.5, 0.25, 0.25 * (1 - 2 ** -22), 0.0], np.float32)   # 2.4e-7 relative gap
     st, mg = oracle.replay(1, 4, w, X, [0, 4], [0, 3], np.array([0, 2, 1], np.int32), oracle.F32)
     assert list(st) == [0, 1, 0] and 0 < mg[1] < 1e-6
+
+
+def test_replay_folds_the_candidates_pick_golden():
+    """Eq. 10-11 under teacher forcing: after an excused pick the replay folds the candidate's pick."""
+    c = _load("select_clamp_replay.json")["replay"]
+    X = np.asarray(c["feats"], np.float32)
+    st, mg = oracle.replay(1, X.shape[1], np.asarray(c["w"], np.float32), X, [0, X.shape[0]],
+                           [0, c["K"]], np.asarray(c["picks"], np.int32), oracle.F32)
+    assert list(st) == c["status"]
+    np.testing.assert_array_equal(mg, c["margin"])
 
 
 def test_gather_is_byte_copy():
@@ -643,11 +698,27 @@ MUTANTS = {
     # ties broken towards the highest index
     "tie_high": ("if (best < 0 || o[i] > o[best]) best = i;", "if (best < 0 || o[i] >= o[best]) best = i;"),
     # additive instead of multiplicative objective (Eq. 11)
-    "additive": ("o[i] = (double)w[row0 + i] * delta[i];\n      }\n      /* Eq. 11 */",
-                 "o[i] = (double)w[row0 + i] + delta[i];\n      }\n      /* Eq. 11 */"),
+    "additive": ("o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);\n      }\n      /* Eq. 11 */",
+                 "o[i] = orc_obj(orc_rel(w[row0 + i]) + delta[i]);\n      }\n      /* Eq. 11 */"),
     # coverage from the first pick only (delta not folded with later picks)
-    "no_min": ("if (c < delta[i]) delta[i] = c;\n        o[i] = (double)w[row0 + i] * delta[i];\n      }\n      /* Eq. 11 */",
-               "if (t == 1) delta[i] = c;\n        o[i] = (double)w[row0 + i] * delta[i];\n      }\n      /* Eq. 11 */"),
+    "no_min": ("if (c < delta[i]) delta[i] = c;\n        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);\n      }\n      /* Eq. 11 */",
+               "if (t == 1) delta[i] = c;\n        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);\n      }\n      /* Eq. 11 */"),
+    # max instead of min over the selected set in Eq. 10 (coverage by the farthest pick)
+    "max_not_min": ("if (c < delta[i]) delta[i] = c;\n        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);\n      }\n      /* Eq. 11 */",
+                    "if (delta[i] == INFINITY || c > delta[i]) delta[i] = c;\n        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);\n      }\n      /* Eq. 11 */"),
+    # the replay folds max instead of min as well
+    "replay_max_not_min": ("if (c < delta[i]) delta[i] = c;\n        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);\n      }\n    }\n    orc_free_feats",
+                           "if (delta[i] == INFINITY || c > delta[i]) delta[i] = c;\n        o[i] = orc_obj(orc_rel(w[row0 + i]) * delta[i]);\n      }\n    }\n    orc_free_feats"),
+    # Eq. 10's coverage term left unclamped (1 - cos may round below 0)
+    "unclamped": ("return t > 0.0 ? t : 0.0;", "return t;"),
+    # the replay folds the oracle's own argmax instead of the candidate's pick
+    "replay_fold_best": ("const double c = orc_cover(&xf, i, gp);", "const double c = orc_cover(&xf, i, best);"),
+    # a NaN objective (+inf relevance on a covered token) kept as is instead of counting as 0
+    "raw_objective": ("static double orc_obj(double v) { return v == v ? v : 0.0; }",
+                      "static double orc_obj(double v) { return v; }"),
+    # negative relevance kept as is instead of counting as 0
+    "raw_relevance": ("static double orc_rel(float w) { return (double)w > 0.0 ? (double)w : 0.0; }",
+                      "static double orc_rel(float w) { return (double)w; }"),
     # zero-norm rows treated as covered (delta 0) instead of cosine 0 (delta 1)
     "zero_norm": ("if (f->nn[i] <= 0.0 || f->nn[j] <= 0.0) return 1.0;",
                   "if (f->nn[i] <= 0.0 || f->nn[j] <= 0.0) return 0.0;"),
@@ -690,7 +761,7 @@ def _build_mutant(tmp_path, name):
     d = tmp_path / name
     d.mkdir()
     (d / "oracle.c").write_text(src.replace(old, new))
-    subprocess.run(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-o", str(d / "liboracle.so"),
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-o", str(d / "liboracle.so"),
                     str(d / "oracle.c"), "-lm"], check=True)
     (d / "__init__.py").write_text(open(oracle.__file__).read())
     return d
@@ -701,6 +772,9 @@ def _pins_pass():
     checks = [test_scores_golden_two_heads, lambda: test_scores_match_bruteforce(1),
               lambda: test_scores_match_bruteforce(2), lambda: test_scores_planted_key_closed_form(3.0),
               test_select_golden_cases, lambda: test_select_matches_bruteforce(0),
+              test_select_clamp_golden, test_select_edge_values_golden,
+              test_replay_classifies_steps, test_replay_excuses_near_ties,
+              test_replay_folds_the_candidates_pick_golden,
               lambda: test_select_matches_bruteforce(5), test_select_orthogonal_features_is_topk,
               test_select_uniform_weights_is_farthest_point, lambda: test_select_invariants(0),
               lambda: test_rows_scores_match_bruteforce(1), lambda: test_rows_scores_match_bruteforce(2),
