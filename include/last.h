@@ -320,8 +320,11 @@ int32_t last_version(void);
  * (event creation happens on first use; no device memory is allocated).
  * After the caller has synchronised the streams, last_profile_collect()
  * folds the finished pairs into per-kernel totals, which
- * last_profile_kernel() reports. Process-wide state, not thread-safe; off by
- * default. Event pairs beyond the internal pool of 8192 are not recorded.
+ * last_profile_kernel() reports. The totals are process-wide and guarded by a
+ * lock; with timing off (the default) a launch only reads an atomic flag, so
+ * the compute calls stay free of shared mutable state. Event pairs beyond the
+ * internal pool of 8192 are not recorded. A name returned by
+ * last_profile_kernel() stays valid until the process ends.
  */
 last_status last_profile_enable(int32_t on);
 last_status last_profile_collect(void);

@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <cmath>
 #include <atomic>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -30,26 +31,30 @@ struct Pending {
   hipEvent_t start, stop;
 };
 struct Totals {
-  std::string name;
+  const char *name;  // a string literal of the launch site
   int64_t launches = 0;
   double ms = 0.0;
 };
+// Per-kernel event timing. The switch is an atomic read on every launch; the
+// pools and totals are touched only while timing is on, under one lock. The
+// launch being bracketed is per calling thread, so concurrent calls from
+// different host threads never see each other's half-open pair.
 struct Profiler {
-  bool on = false;
+  std::atomic<bool> on{false};
+  std::mutex mu;
   std::vector<hipEvent_t> free_events;
   std::vector<Pending> pending;
   std::vector<Totals> totals;
   int created = 0;
-  Pending open{-1, nullptr, nullptr};
 };
 Profiler &prof() {
   static Profiler p;
   return p;
 }
+thread_local Pending t_open{-1, nullptr, nullptr};
 constexpr int kMaxEventPairs = 8192;
 
-hipEvent_t take_event() {
-  Profiler &p = prof();
+hipEvent_t take_event(Profiler &p) {  // p.mu held
   if (!p.free_events.empty()) {
     hipEvent_t e = p.free_events.back();
     p.free_events.pop_back();
@@ -62,20 +67,20 @@ hipEvent_t take_event() {
   return e;
 }
 
-int kernel_id(const char *name) {
-  Profiler &p = prof();
+int kernel_id(Profiler &p, const char *name) {  // p.mu held
   for (size_t i = 0; i < p.totals.size(); ++i)
-    if (p.totals[i].name == name) return (int)i;
+    if (strcmp(p.totals[i].name, name) == 0) return (int)i;
   p.totals.push_back(Totals{name, 0, 0.0});
   return (int)p.totals.size() - 1;
 }
 }  // namespace
 
 void launch_begin(const char *name, hipStream_t s) {
+  t_open = Pending{-1, nullptr, nullptr};
   Profiler &p = prof();
-  p.open = Pending{-1, nullptr, nullptr};
-  if (!p.on) return;
-  hipEvent_t a = take_event(), b = take_event();
+  if (!p.on.load(std::memory_order_relaxed)) return;
+  std::lock_guard<std::mutex> lock(p.mu);
+  hipEvent_t a = take_event(p), b = take_event(p);
   if (!a || !b) {
     if (a) p.free_events.push_back(a);
     if (b) p.free_events.push_back(b);
@@ -86,20 +91,21 @@ void launch_begin(const char *name, hipStream_t s) {
     p.free_events.push_back(b);
     return;
   }
-  p.open = Pending{kernel_id(name), a, b};
+  t_open = Pending{kernel_id(p, name), a, b};
 }
 
 hipError_t launch_end(hipStream_t s) {
   hipError_t e = hipGetLastError();
-  Profiler &p = prof();
-  if (p.open.kernel >= 0) {
-    if (hipEventRecord(p.open.stop, s) == hipSuccess) {
-      p.pending.push_back(p.open);
+  if (t_open.kernel >= 0) {
+    Profiler &p = prof();
+    std::lock_guard<std::mutex> lock(p.mu);
+    if (hipEventRecord(t_open.stop, s) == hipSuccess) {
+      p.pending.push_back(t_open);
     } else {
-      p.free_events.push_back(p.open.start);
-      p.free_events.push_back(p.open.stop);
+      p.free_events.push_back(t_open.start);
+      p.free_events.push_back(t_open.stop);
     }
-    p.open = Pending{-1, nullptr, nullptr};
+    t_open = Pending{-1, nullptr, nullptr};
   }
   if (e != hipSuccess) note_hip_error(e);
   return e;
@@ -482,12 +488,13 @@ const char *last_status_string(last_status s) {
 int32_t last_version(void) { return 100; }
 
 last_status last_profile_enable(int32_t on) {
-  prof().on = on != 0;
+  prof().on.store(on != 0, std::memory_order_relaxed);
   return LAST_OK;
 }
 
 last_status last_profile_collect(void) {
   Profiler &p = prof();
+  std::lock_guard<std::mutex> lock(p.mu);
   std::vector<Pending> keep;
   for (const Pending &x : p.pending) {
     float ms = 0.f;
@@ -509,18 +516,24 @@ last_status last_profile_collect(void) {
 
 void last_profile_reset(void) {
   Profiler &p = prof();
+  std::lock_guard<std::mutex> lock(p.mu);
   for (Totals &t : p.totals) {
     t.launches = 0;
     t.ms = 0.0;
   }
 }
 
-int32_t last_profile_count(void) { return (int32_t)prof().totals.size(); }
+int32_t last_profile_count(void) {
+  Profiler &p = prof();
+  std::lock_guard<std::mutex> lock(p.mu);
+  return (int32_t)p.totals.size();
+}
 
 int32_t last_profile_kernel(int32_t i, const char **name, int64_t *launches, double *total_ms) {
   Profiler &p = prof();
+  std::lock_guard<std::mutex> lock(p.mu);
   if (i < 0 || i >= (int32_t)p.totals.size()) return 0;
-  if (name) *name = p.totals[i].name.c_str();
+  if (name) *name = p.totals[i].name;
   if (launches) *launches = p.totals[i].launches;
   if (total_ms) *total_ms = p.totals[i].ms;
   return 1;

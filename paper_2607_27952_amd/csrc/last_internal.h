@@ -53,7 +53,7 @@ struct ScorePlan {
 };
 
 struct ScoreWs {
-  int32_t *chunk_off, *chunk_req, *slice_off, *slice_req;
+  int32_t *chunk_off, *slice_off;  // [R + 1] count prefixes (written only for large batches)
   float4 *stats;  // [G][Hq][C_total] (chunk max, sum exp, visual sum exp, 0)
   float *vlog;    // [G][N_total][Hq] scaled logits of visual columns, layer-major
   float2 *rowstat;  // [R][G * Hq] merged (max, 1 / sum exp) of every row
@@ -67,10 +67,11 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
 hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
                          const void *q, const void *k, const int32_t *row_pos, float *scores,
                          float *attn_rows, float scale, hipStream_t s);
-// The plan kernel alone, and merge + finalize alone (for scores whose chunk
+// The count prefixes (run only for batches too large for the blocks' own scan,
+// or when `always`), and merge + finalize alone (for scores whose chunk
 // statistics and visual logits another kernel wrote).
 hipError_t launch_score_plan(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
-                             const int32_t *row_pos, hipStream_t s);
+                             const int32_t *row_pos, hipStream_t s, bool always = false);
 hipError_t launch_score_tail(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
                              const int32_t *row_pos, float *scores, hipStream_t s);
 

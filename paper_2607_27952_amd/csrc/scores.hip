@@ -5,9 +5,11 @@
 // O(P) instead of O(P^2) work per head). The row needs a softmax over the
 // whole prefix while the keys are streamed in chunks, so the pass is split:
 //
-//   k_score_plan      one block: per-request chunk/slice prefix sums and the
-//                     chunk -> request / slice -> request maps (a wave per
-//                     request fills its entries).
+//   (no plan pass) every block finds the request it works on itself: a wave
+//                     scans the per-request chunk (or slice) counts, 64
+//                     requests at a time, up to the block's index. Batches of
+//                     more than kScanMaxR requests run k_score_prefix first
+//                     (one block: the count prefixes) and search those.
 //   k_score_stream    one block per (layer, chunk of tokens). The chunk's key
 //                     rows for all KV heads are one contiguous byte range,
 //                     streamed once: 8 lanes cover one row with 16-byte loads
@@ -60,6 +62,7 @@ constexpr int kMaxChunk = 4096;             // tokens per chunk (fallback kernel
 constexpr int kLdsLogitFloats = 8192;
 constexpr int kSliceTokens = 256;           // visual tokens per finalize block
 constexpr int kMaxPairs = 4096;             // G * Hq handled by the finalize block
+constexpr int kScanMaxR = 1024;             // larger batches search count prefixes instead
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
@@ -87,15 +90,14 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
                                          c, false);
 }
 
-__global__ __launch_bounds__(kThreads) void k_score_plan(
+// Count prefixes for batches of more than kScanMaxR requests (one block):
+// chunk_off[r] = sum over r' < r of ceil(P_r' / CH), slice_off likewise over
+// ceil(N_r' / SL).
+__global__ __launch_bounds__(kThreads) void k_score_prefix(
     const int32_t *__restrict__ cu_seqlens, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ row_pos, int R, int CH,
-    int SL, int64_t C_cap, int64_t S_cap, int32_t *__restrict__ chunk_off,
-    int32_t *__restrict__ chunk_req, int32_t *__restrict__ slice_off,
-    int32_t *__restrict__ slice_req) {
+    const int32_t *__restrict__ row_pos, int R, int CH, int SL, int32_t *__restrict__ chunk_off,
+    int32_t *__restrict__ slice_off) {
   __shared__ int sh[kThreads / 64];
-  __shared__ int s_pc[kThreads + 1], s_ps[kThreads + 1];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int carry_c = 0, carry_s = 0;
   for (int base = 0; base < R; base += kThreads) {
     const int r = base + (int)threadIdx.x;
@@ -113,22 +115,6 @@ __global__ __launch_bounds__(kThreads) void k_score_plan(
       chunk_off[r] = pc;
       slice_off[r] = ps;
     }
-    s_pc[threadIdx.x] = pc;
-    s_ps[threadIdx.x] = ps;
-    if (threadIdx.x == 0) {
-      s_pc[kThreads] = carry_c + tc;
-      s_ps[kThreads] = carry_s + ts;
-    }
-    __syncthreads();
-    // the maps: a wave per request of this group, its lanes over the chunks
-    const int nr = min(kThreads, R - base);
-    for (int j = wave; j < nr; j += kWaves) {
-      const int c1 = j + 1 < nr ? s_pc[j + 1] : s_pc[kThreads];
-      const int s1 = j + 1 < nr ? s_ps[j + 1] : s_ps[kThreads];
-      for (int c = s_pc[j] + lane; c < c1 && c < C_cap; c += 64) chunk_req[c] = base + j;
-      for (int c = s_ps[j] + lane; c < s1 && c < S_cap; c += 64) slice_req[c] = base + j;
-    }
-    __syncthreads();
     carry_c += tc;
     carry_s += ts;
   }
@@ -136,6 +122,74 @@ __global__ __launch_bounds__(kThreads) void k_score_plan(
     chunk_off[R] = carry_c;
     slice_off[R] = carry_s;
   }
+}
+
+// Where a block's item lies. Items are numbered request by request: request r
+// owns ceil(P_r / CH) chunks and ceil(N_r / SL) visual slices. Given a chunk
+// index (by_slice false) or a slice index (by_slice true), finds the request r
+// and the indices of its first chunk and first slice. With the prefixes of
+// k_score_prefix (batches over kScanMaxR) a binary search; otherwise wave 0
+// scans the counts 64 requests at a time. Every thread calls it; the result is
+// block-uniform (through LDS; the function ends with a block barrier).
+struct Where {
+  int r, c0, s0;
+};
+__device__ Where locate(int64_t x, bool by_slice, int R, int CH, int SL, const int32_t *__restrict__ cu_seqlens,
+                        const int32_t *__restrict__ cu_vis, const int32_t *__restrict__ row_pos,
+                        const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ slice_off,
+                        int *s_where) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    if (R > kScanMaxR) {
+      if (lane == 0) {
+        const int32_t *off = by_slice ? slice_off : chunk_off;
+        int lo = 0, hi = R - 1;   // last r with off[r] <= x
+        while (lo < hi) {
+          const int mid = (lo + hi + 1) >> 1;
+          if (off[mid] <= x) lo = mid; else hi = mid - 1;
+        }
+        s_where[0] = lo;
+        s_where[1] = chunk_off[lo];
+        s_where[2] = slice_off[lo];
+      }
+    } else {
+      int base_c = 0, base_s = 0;
+      for (int r0 = 0; r0 < R; r0 += 64) {
+        const int r = r0 + lane;
+        int nc = 0, ns = 0;
+        if (r < R) {
+          const int P = row_pos ? row_pos[r] + 1 : cu_seqlens[r + 1] - cu_seqlens[r];
+          const int N = cu_vis[r + 1] - cu_vis[r];
+          nc = (P + CH - 1) / CH;
+          ns = (N + SL - 1) / SL;
+        }
+        int ic = nc, is = ns;   // inclusive scans over the lanes
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int yc = __shfl_up(ic, o), ys = __shfl_up(is, o);
+          if (lane >= o) {
+            ic += yc;
+            is += ys;
+          }
+        }
+        const int64_t end = (int64_t)(by_slice ? base_s + is : base_c + ic);
+        const unsigned long long hit = __ballot(r < R && end > x);
+        if (hit) {
+          const int f = (int)__ffsll((long long)hit) - 1;
+          if (lane == f) {
+            s_where[0] = r;
+            s_where[1] = base_c + ic - nc;
+            s_where[2] = base_s + is - ns;
+          }
+          break;
+        }
+        base_c += __shfl(ic, 63);
+        base_s += __shfl(is, 63);
+      }
+    }
+  }
+  __syncthreads();
+  return Where{s_where[0], s_where[1], s_where[2]};
 }
 
 // Per-lane query slices: bf16 kept packed for v_dot2_f32_bf16, fp32 as is.
@@ -266,18 +320,21 @@ template <typename T, int DH, int GQ>
 __global__ __launch_bounds__(kThreads) void k_score_stream(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req,
+    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ slice_off,
     const int32_t *__restrict__ row_pos, int R, int Hq, int Hkv, int CH, int64_t C_total,
     int64_t T_total, float scale, float *__restrict__ vlog, float4 *__restrict__ stats,
     float *__restrict__ rows) {
   using RS = RowShape<T, DH>;
   extern __shared__ float s_log[];          // [CH][Hq]
   __shared__ float4 s_part[kThreads];
+  __shared__ int s_where[3];
 
   const int64_t c = blockIdx.x % C_total;
   const int l = (int)(blockIdx.x / C_total);
-  const int r = chunk_req[c];
-  const int c_local = (int)(c - chunk_off[r]);
+  const Where wh = locate(c, false, R, CH, kSliceTokens, cu_seqlens, cu_vis, row_pos, chunk_off, slice_off,
+                          s_where);
+  const int r = wh.r;
+  const int c_local = (int)(c - wh.c0);
   const int64_t tok0 = cu_seqlens[r];
   // the scored row sits at position P - 1 and sees keys 0 .. P - 1 (causal)
   const int P = row_pos ? row_pos[r] + 1 : cu_seqlens[r + 1] - (int)tok0;
@@ -328,13 +385,14 @@ template <typename T, int DH, int GM>
 __global__ __launch_bounds__(kThreads) void k_score_partial(
     const T *__restrict__ q, const T *__restrict__ k, const int32_t *__restrict__ cu_seqlens,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ cu_vis,
-    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ chunk_req,
+    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ slice_off,
     const int32_t *__restrict__ row_pos, int R, int Hq, int Hkv, int g, int HG, int CH,
     int64_t C_total, int64_t T_total, float scale, float *__restrict__ vlog,
     float4 *__restrict__ stats, float *__restrict__ rows) {
   using RS = RowShape<T, DH>;
   extern __shared__ float s_logit[];   // [GM][CH]
   __shared__ float s_red[kWaves][GM];
+  __shared__ int s_where[3];
 
   int64_t bid = blockIdx.x;
   const int hg = (int)(bid % HG);
@@ -343,8 +401,10 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
   bid /= Hkv;
   const int64_t c = bid % C_total;
   const int l = (int)(bid / C_total);
-  const int r = chunk_req[c];
-  const int c_local = (int)(c - chunk_off[r]);
+  const Where wh = locate(c, false, R, CH, kSliceTokens, cu_seqlens, cu_vis, row_pos, chunk_off, slice_off,
+                          s_where);
+  const int r = wh.r;
+  const int c_local = (int)(c - wh.c0);
   const int64_t tok0 = cu_seqlens[r];
   const int P = row_pos ? row_pos[r] + 1 : cu_seqlens[r + 1] - (int)tok0;
   const int t_begin = c_local * CH;
@@ -481,59 +541,93 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
   }
 }
 
+// The first chunk of request r: sum over r' < r of ceil(P_r' / CH), scanned
+// by wave 0 64 requests at a time (or read from the k_score_prefix output for
+// batches over kScanMaxR). Block-uniform, through LDS.
+__device__ int chunk_first(int r, int R, int CH, const int32_t *__restrict__ cu_seqlens,
+                           const int32_t *__restrict__ row_pos, const int32_t *__restrict__ chunk_off,
+                           int *s_out) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    int base = 0;
+    if (R > kScanMaxR) {
+      base = chunk_off[r];
+    } else {
+      for (int r0 = 0; r0 < r; r0 += 64) {
+        const int q = r0 + lane;
+        int nc = 0;
+        if (q < r) {
+          const int P = row_pos ? row_pos[q] + 1 : cu_seqlens[q + 1] - cu_seqlens[q];
+          nc = (P + CH - 1) / CH;
+        }
+        for (int o = 1; o < 64; o <<= 1) nc += __shfl_xor(nc, o);
+        base += nc;
+      }
+    }
+    if (lane == 0) s_out[0] = base;
+  }
+  __syncthreads();
+  return s_out[0];
+}
+
 // Merge the chunk statistics of every (request, layer, head) row into its max
 // M and 1/Z, and its share V / Z of the request's visual mass
 // S = sum_{l,h} V / Z (= sum_i s_i). One wave per row, kWaves rows a block:
 // lanes merge the row's chunks lane-strided with the online rule, then the
 // wave combines the lanes (log-sum-exp over (max, sum) pairs).
 __global__ __launch_bounds__(kThreads) void k_score_merge(
-    const float4 *__restrict__ stats, const int32_t *__restrict__ chunk_off, int GH,
+    const float4 *__restrict__ stats, const int32_t *__restrict__ cu_seqlens,
+    const int32_t *__restrict__ row_pos, const int32_t *__restrict__ chunk_off, int R, int GH, int CH,
     int64_t C_total, float2 *__restrict__ rowstat, float *__restrict__ rowmass) {
+  __shared__ int s_first[1];
   const int bpr = (GH + kWaves - 1) / kWaves;   // blocks per request
   const int r = blockIdx.x / bpr;
+  const int c0 = chunk_first(r, R, CH, cu_seqlens, row_pos, chunk_off, s_first);
+  const int P = row_pos ? row_pos[r] + 1 : cu_seqlens[r + 1] - cu_seqlens[r];
+  const int c1 = c0 + (P + CH - 1) / CH;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int p = (blockIdx.x % bpr) * kWaves + wave;
   if (p >= GH) return;
-  const int c0 = chunk_off[r], c1 = chunk_off[r + 1];
-  {
-    const float4 *st = stats + (int64_t)p * C_total;
-    float m = -INFINITY, z = 0.f, v = 0.f;
-    for (int c = c0 + lane; c < c1; c += 64) {
-      const float4 e = st[c];
-      if (e.x > m) {
-        const float f = m == -INFINITY ? 0.f : expf(m - e.x);
-        z = fmaf(z, f, e.y);
-        v = fmaf(v, f, e.z);
-        m = e.x;
-      } else {
-        const float f = expf(e.x - m);
-        z = fmaf(e.y, f, z);
-        v = fmaf(e.z, f, v);
-      }
+  const float4 *st = stats + (int64_t)p * C_total;
+  float m = -INFINITY, z = 0.f, v = 0.f;
+  for (int c = c0 + lane; c < c1; c += 64) {
+    const float4 e = st[c];
+    if (e.x > m) {
+      const float f = m == -INFINITY ? 0.f : expf(m - e.x);
+      z = fmaf(z, f, e.y);
+      v = fmaf(v, f, e.z);
+      m = e.x;
+    } else {
+      const float f = expf(e.x - m);
+      z = fmaf(e.y, f, z);
+      v = fmaf(e.z, f, v);
     }
-    const float M = wave_max(m);
-    const float f = m == -INFINITY ? 0.f : expf(m - M);
-    const float Z = wave_sum(z * f), V = wave_sum(v * f);
-    if (lane == 0) {
-      rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
-      rowmass[(int64_t)r * GH + p] = V / Z;
-    }
+  }
+  const float M = wave_max(m);
+  const float f = m == -INFINITY ? 0.f : expf(m - M);
+  const float Z = wave_sum(z * f), V = wave_sum(v * f);
+  if (lane == 0) {
+    rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
+    rowmass[(int64_t)r * GH + p] = V / Z;
   }
 }
 
-// s_i = sum_{l,h} exp(l_i - M) / Z (Eq. 6-7), divided by S (Eq. 8).
+// s_i = sum_{l,h} exp(l_i - M) / Z (Eq. 6-7), divided by S (Eq. 8), for one
+// slice of a request's visual tokens; a thread per token reads its layers'
+// Hq contiguous logits directly (every load independent of the others).
 __global__ __launch_bounds__(kThreads) void k_score_finalize(
-    const float *__restrict__ vlog, const float2 *__restrict__ rowstat,
-    const float *__restrict__ rowmass, const int32_t *__restrict__ cu_vis,
+    const float *__restrict__ vlog, const float2 *__restrict__ rowstat, const float *__restrict__ rowmass,
+    const int32_t *__restrict__ cu_seqlens, const int32_t *__restrict__ cu_vis,
     const int32_t *__restrict__ vis_start, const int32_t *__restrict__ row_pos,
-    const int32_t *__restrict__ slice_off, const int32_t *__restrict__ slice_req, int G, int Hq,
-    int64_t N_total, int SL, float *__restrict__ scores) {
+    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ slice_off, int R, int G, int Hq, int CH,
+    int SL, int64_t N_total, float *__restrict__ scores) {
   const int GH = G * Hq;
   __shared__ float2 sMZ[kMaxPairs];
   __shared__ float s_red[kWaves];
-  const int b = blockIdx.x;
-  const int r = slice_req[b];
-  const int sl = b - slice_off[r];
+  __shared__ int s_where[3];
+  const Where wh = locate(blockIdx.x, true, R, CH, SL, cu_seqlens, cu_vis, row_pos, chunk_off, slice_off,
+                          s_where);
+  const int r = wh.r, sl = (int)(blockIdx.x - wh.s0);
   // S = sum over the request's rows of V / Z: each thread its rows p = t,
   // t + kThreads, ... in order, then the wave and the waves in a fixed order
   float part = 0.f;
@@ -609,7 +703,7 @@ hipError_t launch_stream_dh(const last_batch *b, const last::ScorePlan &p, const
 #define LAST_LAUNCH_GQ(GQV)                                                                        \
   hipLaunchKernelGGL((k_score_stream<T, DH, GQV>), dim3((unsigned)blocks), dim3(kThreads), lds, s, \
                      (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,          \
-                     w.chunk_off, w.chunk_req, row_pos, b->R, b->Hq, b->Hkv, p.chunk_tokens,     \
+                     w.chunk_off, w.slice_off, row_pos, b->R, b->Hq, b->Hkv, p.chunk_tokens,     \
                      p.C_total, p.T_total, scale, w.vlog, w.stats, attn_rows)
   switch (g) {
     case 1: LAST_LAUNCH_GQ(1); break;
@@ -636,7 +730,7 @@ hipError_t launch_partial_dh(const last_batch *b, const last::ScorePlan &p,
 #define LAST_LAUNCH_GM(GMV)                                                                     \
   hipLaunchKernelGGL((k_score_partial<T, DH, GMV>), dim3((unsigned)blocks), dim3(kThreads), lds, \
                      s, (const T *)q, (const T *)k, b->cu_seqlens, b->vis_start, b->cu_vis,      \
-                     w.chunk_off, w.chunk_req, row_pos, b->R, b->Hq, b->Hkv, g, p.head_groups,  \
+                     w.chunk_off, w.slice_off, row_pos, b->R, b->Hq, b->Hkv, g, p.head_groups,  \
                      p.chunk_tokens, p.C_total, p.T_total, scale, w.vlog, w.stats,               \
                      attn_rows)
   switch (p.g_max) {
@@ -695,9 +789,7 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
   Carver cv(ws);
   ScoreWs w{};
   w.chunk_off = cv.take<int32_t>(b->R + 1);
-  w.chunk_req = cv.take<int32_t>(p.C_total);
   w.slice_off = cv.take<int32_t>(b->R + 1);
-  w.slice_req = cv.take<int32_t>(p.S_total);
   w.stats = cv.take<float4>((size_t)b->G * b->Hq * p.C_total);
   w.vlog = cv.take<float>((size_t)b->G * b->Hq * p.N_total);
   w.rowstat = cv.take<float2>((size_t)b->R * b->G * b->Hq);
@@ -709,33 +801,35 @@ ScoreWs carve_score_ws(void *ws, const last_batch *b, const ScorePlan &p, size_t
 int score_max_pairs() { return kMaxPairs; }
 
 hipError_t launch_score_plan(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
-                             const int32_t *row_pos, hipStream_t s) {
-  launch_begin("score_plan", s);
-  hipLaunchKernelGGL(k_score_plan, dim3(1), dim3(kThreads), 0, s, b->cu_seqlens, b->cu_vis,
-                     row_pos, b->R, p.chunk_tokens, p.slice_tokens, p.C_total, p.S_total, w.chunk_off,
-                     w.chunk_req, w.slice_off, w.slice_req);
+                             const int32_t *row_pos, hipStream_t s, bool always) {
+  if (b->R <= kScanMaxR && !always) return hipSuccess;   // the blocks scan the counts themselves
+  launch_begin("score_prefix", s);
+  hipLaunchKernelGGL(k_score_prefix, dim3(1), dim3(kThreads), 0, s, b->cu_seqlens, b->cu_vis, row_pos, b->R,
+                     p.chunk_tokens, p.slice_tokens, w.chunk_off, w.slice_off);
   return launch_end(s);
 }
 
 hipError_t launch_score_tail(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
                              const int32_t *row_pos, float *scores, hipStream_t s) {
-  launch_begin("score_merge", s);
   const int GH = b->G * b->Hq;
-  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)((int64_t)b->R * ((GH + kWaves - 1) / kWaves))), dim3(kThreads), 0,
-                     s, w.stats, w.chunk_off, GH, p.C_total, w.rowstat, w.rowmass);
+  launch_begin("score_merge", s);
+  hipLaunchKernelGGL(k_score_merge, dim3((unsigned)((int64_t)b->R * ((GH + kWaves - 1) / kWaves))), dim3(kThreads),
+                     0, s, w.stats, b->cu_seqlens, row_pos, w.chunk_off, b->R, GH, p.chunk_tokens, p.C_total,
+                     w.rowstat, w.rowmass);
   hipError_t e = launch_end(s);
   if (e != hipSuccess) return e;
   launch_begin("score_finalize", s);
-  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog,
-                     w.rowstat, w.rowmass, b->cu_vis, b->vis_start, row_pos, w.slice_off, w.slice_req, b->G,
-                     b->Hq, p.N_total, p.slice_tokens, scores);
+  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog, w.rowstat,
+                     w.rowmass, b->cu_seqlens, b->cu_vis, b->vis_start, row_pos, w.chunk_off, w.slice_off, b->R,
+                     b->G, b->Hq, p.chunk_tokens, p.slice_tokens, p.N_total, scores);
   return launch_end(s);
 }
 
 hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs &w,
                          const void *q, const void *k, const int32_t *row_pos, float *scores,
                          float *attn_rows, float scale, hipStream_t s) {
-  hipError_t e = launch_score_plan(b, p, w, row_pos, s);
+  // the debug rows read the chunk prefixes directly, so they are always computed then
+  hipError_t e = launch_score_plan(b, p, w, row_pos, s, attn_rows != nullptr);
   if (e != hipSuccess) return e;
 
   const bool bf = b->qk_dtype == LAST_BF16;

@@ -1141,7 +1141,20 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
     }
     thread_best(o, bo, bi);
     best = block_max(key_of(bo, bi), t);
-    if (best == 0ull) break;   // every token already picked (cannot happen for K <= N)
+    if ((best >> 32) == 0ull) {
+      // The best objective is 0, or every unpicked token's objective is NaN
+      // (+inf relevance at coverage distance 0). Both count as 0, so the pick
+      // is the lowest-index token not yet picked (block-uniform branch; never
+      // taken while some objective is positive).
+      int lo = 0x7FFFFFFF;
+#pragma unroll
+      for (int e = EPT - 1; e >= 0; --e)
+        if (tid + e * NTH < N && dl[e] != -INFINITY) lo = tid + e * NTH;
+      // every wave has read this step's exchange slots before they are reused
+      if (kNW > 1) __syncthreads();
+      best = block_max(lo < N ? (0xFFFFFFFFull - (unsigned)lo) : 0ull, t);
+      if (best == 0ull) break;   // every token already picked (cannot happen for K <= N)
+    }
     j = (int)(0xFFFFFFFFu - (unsigned)(best & 0xFFFFFFFFull));
     if (tid == 0) {
       order[k0 + t] = j;

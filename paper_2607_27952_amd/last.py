@@ -7,6 +7,7 @@ The library must be built (``python -m paper_2607_27952_amd._build`` or
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import os
 from dataclasses import dataclass
@@ -125,6 +126,14 @@ def _stream(stream) -> int:
     return s.cuda_stream
 
 
+def _on(stream):
+    """Allocate a call's temporaries (device CSR copies, outputs, workspace) on
+    the stream the call enqueues on. torch's caching allocator then frees them
+    in that stream's order, so a block cannot be handed to another stream's
+    allocation while the library's kernels still read it."""
+    return torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext()
+
+
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype == torch.bfloat16:
         return LAST_BF16
@@ -192,22 +201,23 @@ def token_scores_workspace(batch: Batch, qk_dtype=torch.bfloat16) -> int:
 def token_scores(batch: Batch, q: torch.Tensor, k: torch.Tensor, scores=None, attn_rows=None,
                  want_rows=False, ws=None, stream=None):
     """last_token_scores (Eq. 6-8): returns scores [N_total] fp32 (and rows if asked)."""
-    code = _dtype_code(q)
-    if k.dtype != q.dtype:
-        raise TypeError("q and k must share a dtype")
-    b = batch.struct(code)
-    if scores is None:
-        scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
-    if want_rows and attn_rows is None:
-        attn_rows = torch.empty((batch.G, batch.Hq, batch.T_total), dtype=torch.float32, device=q.device)
-    need = int(lib().last_token_scores_workspace(ctypes.byref(b)))
-    if ws is None:
-        ws = _workspace(need, q.device)
-    st = lib().last_token_scores(ctypes.byref(b), _ptr(q), _ptr(k), _ptr(scores), _ptr(attn_rows),
-                                 _ptr(ws), ws.numel(), _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "last_token_scores")
-    return (scores, attn_rows) if want_rows else scores
+    with _on(stream):
+        code = _dtype_code(q)
+        if k.dtype != q.dtype:
+            raise TypeError("q and k must share a dtype")
+        b = batch.struct(code)
+        if scores is None:
+            scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
+        if want_rows and attn_rows is None:
+            attn_rows = torch.empty((batch.G, batch.Hq, batch.T_total), dtype=torch.float32, device=q.device)
+        need = int(lib().last_token_scores_workspace(ctypes.byref(b)))
+        if ws is None:
+            ws = _workspace(need, q.device)
+        st = lib().last_token_scores(ctypes.byref(b), _ptr(q), _ptr(k), _ptr(scores), _ptr(attn_rows),
+                                     _ptr(ws), ws.numel(), _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "last_token_scores")
+        return (scores, attn_rows) if want_rows else scores
 
 
 def source_rows(src: int, q_begin: int, q_end: int) -> np.ndarray:
@@ -243,21 +253,22 @@ def rows_scores(batch: Batch, rows: Rows, q: torch.Tensor, k: torch.Tensor, scor
                 stream=None):
     """last_rows_scores (Table 4 sources): scores [N_total] fp32 from the causal rows
     at rows.row_pos; q is [G][M_total][Hq][Dh]."""
-    code = _dtype_code(q)
-    if k.dtype != q.dtype:
-        raise TypeError("q and k must share a dtype")
-    b = batch.struct(code)
-    if scores is None:
-        scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
-    need = int(lib().last_rows_scores_workspace(ctypes.byref(b), _ptr(rows.cu_rows_h), _ptr(rows.row_pos_h)))
-    if ws is None:
-        ws = _workspace(need, q.device)
-    st = lib().last_rows_scores(ctypes.byref(b), _ptr(rows.cu_rows), _ptr(rows.cu_rows_h), _ptr(rows.row_pos),
-                                _ptr(rows.row_pos_h), _ptr(q), _ptr(k), _ptr(scores), _ptr(ws), ws.numel(),
-                                _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "last_rows_scores")
-    return scores
+    with _on(stream):
+        code = _dtype_code(q)
+        if k.dtype != q.dtype:
+            raise TypeError("q and k must share a dtype")
+        b = batch.struct(code)
+        if scores is None:
+            scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
+        need = int(lib().last_rows_scores_workspace(ctypes.byref(b), _ptr(rows.cu_rows_h), _ptr(rows.row_pos_h)))
+        if ws is None:
+            ws = _workspace(need, q.device)
+        st = lib().last_rows_scores(ctypes.byref(b), _ptr(rows.cu_rows), _ptr(rows.cu_rows_h), _ptr(rows.row_pos),
+                                    _ptr(rows.row_pos_h), _ptr(q), _ptr(k), _ptr(scores), _ptr(ws), ws.numel(),
+                                    _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "last_rows_scores")
+        return scores
 
 
 def prefill_attention_workspace(batch: Batch) -> int:
@@ -269,21 +280,22 @@ def prefill_attention(batch: Batch, q: torch.Tensor, k: torch.Tensor, v: torch.T
                       ws=None, stream=None):
     """last_prefill_attention (Sec. 3.3): causal attention of every position,
     out [G][T_total][Hq][Dh] bf16, and the last-row scores [N_total] fp32."""
-    code = _dtype_code(q)
-    if k.dtype != q.dtype or v.dtype != q.dtype:
-        raise TypeError("q, k and v must share a dtype")
-    b = batch.struct(code)
-    if out is None:
-        out = torch.empty(q.shape, dtype=q.dtype, device=q.device)
-    if scores is None:
-        scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
-    if ws is None:
-        ws = _workspace(lib().last_prefill_attention_workspace(ctypes.byref(b)), q.device)
-    st = lib().last_prefill_attention(ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(scores),
-                                      _ptr(ws), ws.numel(), _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "last_prefill_attention")
-    return out, scores
+    with _on(stream):
+        code = _dtype_code(q)
+        if k.dtype != q.dtype or v.dtype != q.dtype:
+            raise TypeError("q, k and v must share a dtype")
+        b = batch.struct(code)
+        if out is None:
+            out = torch.empty(q.shape, dtype=q.dtype, device=q.device)
+        if scores is None:
+            scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
+        if ws is None:
+            ws = _workspace(lib().last_prefill_attention_workspace(ctypes.byref(b)), q.device)
+        st = lib().last_prefill_attention(ctypes.byref(b), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(scores),
+                                          _ptr(ws), ws.numel(), _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "last_prefill_attention")
+        return out, scores
 
 
 def select_workspace(cu_vis_h, Dv: int, f_dtype=torch.bfloat16, mode: int = KCENTER) -> int:
@@ -296,43 +308,45 @@ def diverse_select(scores: torch.Tensor, feats: torch.Tensor, cu_vis_h, cu_keep_
                    cu_keep=None, mode: int = KCENTER, kept=None, order=None, gains=None,
                    want_order=True, ws=None, stream=None):
     """diverse_select (Eq. 9-12 or the Top-k ablation): returns (kept, order, gains)."""
-    dev = feats.device
-    cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
-    R = len(cv) - 1
-    Dv = feats.shape[-1]
-    code = _dtype_code(feats)
-    if cu_vis is None:
-        cu_vis = _i32_dev(cv, dev)
-    if cu_keep is None:
-        cu_keep = _i32_dev(ck, dev)
-    Kt = int(ck[-1])
-    if kept is None:
-        kept = torch.empty(Kt, dtype=torch.int32, device=dev)
-    if want_order and order is None:
-        order = torch.empty(Kt, dtype=torch.int32, device=dev)
-    if want_order and gains is None:
-        gains = torch.empty(Kt, dtype=torch.float32, device=dev)
-    if ws is None:
-        ws = _workspace(lib().diverse_select_workspace(R, _ptr(cv), Dv, code, mode), dev)
-    st = lib().diverse_select(R, Dv, code, mode, _ptr(scores), _ptr(feats), _ptr(cu_vis), _ptr(cv),
-                              _ptr(cu_keep), _ptr(ck), _ptr(kept), _ptr(order), _ptr(gains),
-                              _ptr(ws), ws.numel(), _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "diverse_select")
-    return kept, order, gains
+    with _on(stream):
+        dev = feats.device
+        cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
+        R = len(cv) - 1
+        Dv = feats.shape[-1]
+        code = _dtype_code(feats)
+        if cu_vis is None:
+            cu_vis = _i32_dev(cv, dev)
+        if cu_keep is None:
+            cu_keep = _i32_dev(ck, dev)
+        Kt = int(ck[-1])
+        if kept is None:
+            kept = torch.empty(Kt, dtype=torch.int32, device=dev)
+        if want_order and order is None:
+            order = torch.empty(Kt, dtype=torch.int32, device=dev)
+        if want_order and gains is None:
+            gains = torch.empty(Kt, dtype=torch.float32, device=dev)
+        if ws is None:
+            ws = _workspace(lib().diverse_select_workspace(R, _ptr(cv), Dv, code, mode), dev)
+        st = lib().diverse_select(R, Dv, code, mode, _ptr(scores), _ptr(feats), _ptr(cu_vis), _ptr(cv),
+                                  _ptr(cu_keep), _ptr(ck), _ptr(kept), _ptr(order), _ptr(gains),
+                                  _ptr(ws), ws.numel(), _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "diverse_select")
+        return kept, order, gains
 
 
 def diverse_select_similarity(feats: torch.Tensor, cu_vis_h, ws: torch.Tensor, cu_vis=None, stream=None):
     """diverse_select_similarity (Eq. 10): the coverage distances of every request into ws."""
-    dev = feats.device
-    cv = _i32_host(cu_vis_h)
-    if cu_vis is None:
-        cu_vis = _i32_dev(cv, dev)
-    st = lib().diverse_select_similarity(len(cv) - 1, feats.shape[-1], _dtype_code(feats), _ptr(feats),
-                                         _ptr(cu_vis), _ptr(cv), _ptr(ws), ws.numel(), _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "diverse_select_similarity")
-    return ws
+    with _on(stream):
+        dev = feats.device
+        cv = _i32_host(cu_vis_h)
+        if cu_vis is None:
+            cu_vis = _i32_dev(cv, dev)
+        st = lib().diverse_select_similarity(len(cv) - 1, feats.shape[-1], _dtype_code(feats), _ptr(feats),
+                                             _ptr(cu_vis), _ptr(cv), _ptr(ws), ws.numel(), _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "diverse_select_similarity")
+        return ws
 
 
 def diverse_select_pick(scores: torch.Tensor, cu_vis_h, cu_keep_h, ws: torch.Tensor, Dv: int,
@@ -340,46 +354,48 @@ def diverse_select_pick(scores: torch.Tensor, cu_vis_h, cu_keep_h, ws: torch.Ten
                         gains=None, want_order=True, stream=None):
     """diverse_select_pick (Eq. 9-12) on the distances diverse_select_similarity left in ws:
     returns (kept, order, gains)."""
-    dev = scores.device
-    cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
-    code = LAST_BF16 if f_dtype == torch.bfloat16 else LAST_F32
-    if cu_vis is None:
-        cu_vis = _i32_dev(cv, dev)
-    if cu_keep is None:
-        cu_keep = _i32_dev(ck, dev)
-    Kt = int(ck[-1])
-    if kept is None:
-        kept = torch.empty(Kt, dtype=torch.int32, device=dev)
-    if want_order and order is None:
-        order = torch.empty(Kt, dtype=torch.int32, device=dev)
-    if want_order and gains is None:
-        gains = torch.empty(Kt, dtype=torch.float32, device=dev)
-    st = lib().diverse_select_pick(len(cv) - 1, Dv, code, _ptr(scores), _ptr(cu_vis), _ptr(cv), _ptr(cu_keep),
-                                   _ptr(ck), _ptr(kept), _ptr(order), _ptr(gains), _ptr(ws), ws.numel(),
-                                   _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "diverse_select_pick")
-    return kept, order, gains
+    with _on(stream):
+        dev = scores.device
+        cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
+        code = LAST_BF16 if f_dtype == torch.bfloat16 else LAST_F32
+        if cu_vis is None:
+            cu_vis = _i32_dev(cv, dev)
+        if cu_keep is None:
+            cu_keep = _i32_dev(ck, dev)
+        Kt = int(ck[-1])
+        if kept is None:
+            kept = torch.empty(Kt, dtype=torch.int32, device=dev)
+        if want_order and order is None:
+            order = torch.empty(Kt, dtype=torch.int32, device=dev)
+        if want_order and gains is None:
+            gains = torch.empty(Kt, dtype=torch.float32, device=dev)
+        st = lib().diverse_select_pick(len(cv) - 1, Dv, code, _ptr(scores), _ptr(cu_vis), _ptr(cv), _ptr(cu_keep),
+                                       _ptr(ck), _ptr(kept), _ptr(order), _ptr(gains), _ptr(ws), ws.numel(),
+                                       _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "diverse_select_pick")
+        return kept, order, gains
 
 
 def gather_kept(feats: torch.Tensor, cu_vis_h, kept: torch.Tensor, cu_keep_h, cu_vis=None,
                 cu_keep=None, out=None, stream=None):
     """gather_kept (Eq. 12): the kept rows of feats, byte for byte."""
-    dev = feats.device
-    cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
-    R = len(cv) - 1
-    Dv = feats.shape[-1]
-    if cu_vis is None:
-        cu_vis = _i32_dev(cv, dev)
-    if cu_keep is None:
-        cu_keep = _i32_dev(ck, dev)
-    if out is None:
-        out = torch.empty((int(ck[-1]), Dv), dtype=feats.dtype, device=dev)
-    st = lib().gather_kept(R, Dv, feats.element_size(), _ptr(feats), _ptr(cu_vis), _ptr(cv),
-                           _ptr(kept), _ptr(cu_keep), _ptr(ck), _ptr(out), _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "gather_kept")
-    return out
+    with _on(stream):
+        dev = feats.device
+        cv, ck = _i32_host(cu_vis_h), _i32_host(cu_keep_h)
+        R = len(cv) - 1
+        Dv = feats.shape[-1]
+        if cu_vis is None:
+            cu_vis = _i32_dev(cv, dev)
+        if cu_keep is None:
+            cu_keep = _i32_dev(ck, dev)
+        if out is None:
+            out = torch.empty((int(ck[-1]), Dv), dtype=feats.dtype, device=dev)
+        st = lib().gather_kept(R, Dv, feats.element_size(), _ptr(feats), _ptr(cu_vis), _ptr(cv),
+                               _ptr(kept), _ptr(cu_keep), _ptr(ck), _ptr(out), _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "gather_kept")
+        return out
 
 
 def connector_workspace(K: int, Dv: int, Dh: int) -> int:
@@ -390,27 +406,28 @@ def connector(x: torch.Tensor, gamma: torch.Tensor, beta: torch.Tensor, w1: torc
               w2: torch.Tensor, b2: torch.Tensor, eps: float = 1e-5, out=None, ws=None, stream=None):
     """last_connector (Sec. 3.4 after Eq. 12, the cloud side): LayerNorm, Linear, GELU, Linear
     on every row of x [K][Dv]; returns out [K][Do] in x's dtype."""
-    code = _dtype_code(x)
-    if w1.dtype != x.dtype or w2.dtype != x.dtype:
-        raise TypeError("x, w1 and w2 must share a dtype")
-    K, Dv = x.shape
-    Dh, Do = w1.shape[0], w2.shape[0]
-    if w1.shape[1] != Dv or w2.shape[1] != Dh:
-        raise ValueError("w1 must be [Dh][Dv] and w2 [Do][Dh]")
-    for t in (gamma, beta, b1, b2):
-        if t.dtype != torch.float32:
-            raise TypeError("gamma, beta, b1 and b2 must be float32")
-    if gamma.numel() != Dv or beta.numel() != Dv or b1.numel() != Dh or b2.numel() != Do:
-        raise ValueError("gamma and beta need Dv entries, b1 Dh and b2 Do")
-    if out is None:
-        out = torch.empty((K, Do), dtype=x.dtype, device=x.device)
-    if ws is None:
-        ws = _workspace(lib().last_connector_workspace(K, Dv, Dh), x.device)
-    st = lib().last_connector(code, K, Dv, Dh, Do, float(eps), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(w1),
-                              _ptr(b1), _ptr(w2), _ptr(b2), _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
-    if st != LAST_OK:
-        raise LastError(st, "last_connector")
-    return out
+    with _on(stream):
+        code = _dtype_code(x)
+        if w1.dtype != x.dtype or w2.dtype != x.dtype:
+            raise TypeError("x, w1 and w2 must share a dtype")
+        K, Dv = x.shape
+        Dh, Do = w1.shape[0], w2.shape[0]
+        if w1.shape[1] != Dv or w2.shape[1] != Dh:
+            raise ValueError("w1 must be [Dh][Dv] and w2 [Do][Dh]")
+        for t in (gamma, beta, b1, b2):
+            if t.dtype != torch.float32:
+                raise TypeError("gamma, beta, b1 and b2 must be float32")
+        if gamma.numel() != Dv or beta.numel() != Dv or b1.numel() != Dh or b2.numel() != Do:
+            raise ValueError("gamma and beta need Dv entries, b1 Dh and b2 Do")
+        if out is None:
+            out = torch.empty((K, Do), dtype=x.dtype, device=x.device)
+        if ws is None:
+            ws = _workspace(lib().last_connector_workspace(K, Dv, Dh), x.device)
+        st = lib().last_connector(code, K, Dv, Dh, Do, float(eps), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(w1),
+                                  _ptr(b1), _ptr(w2), _ptr(b2), _ptr(out), _ptr(ws), ws.numel(), _stream(stream))
+        if st != LAST_OK:
+            raise LastError(st, "last_connector")
+        return out
 
 
 def budget(n: int, num: int, den: int) -> int:

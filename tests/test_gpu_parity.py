@@ -225,6 +225,50 @@ def test_select_edge_cases(dtype):
     assert list(order) == list(np.argsort(-w32.astype(np.float64), kind="stable")[:40])
 
 
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_select_edge_values_golden(dtype):
+    """Relevance that is not a probability (+inf, NaN, negative): the same pick
+    sequence and gains as the oracle's golden cases (a non-positive relevance
+    counts as 0; a NaN objective, +inf on a covered duplicate, counts as 0)."""
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "select_edge_values.json")))
+    for case in g["cases"]:
+        w = np.array([float(v) for v in case["w"]], np.float32)
+        X = np.asarray(case["feats"], np.float32)
+        X = np.pad(X, ((0, 0), (0, 8 - X.shape[1])))   # zero columns change no norm or dot
+        _, _, kept, order, gains = _select_handmade(X, w, case["K"], dtype)
+        assert list(order) == case["order"], case["name"]
+        assert list(kept) == sorted(case["order"]), case["name"]
+        expect = np.array([float(v) for v in case["gains"]], np.float32)
+        np.testing.assert_array_equal(gains, expect, err_msg=case["name"])
+    t = g["topk"]
+    w = np.array([float(v) for v in t["w"]], np.float32)
+    X = np.eye(len(w), 8, dtype=np.float32)
+    feats = last.to_torch(W.to_bf16_bits(X) if dtype == W.BF16 else X, dtype, "cuda")
+    kept, order, gains = gpu_select(feats, torch.from_numpy(w).cuda(), [0, len(w)], [0, t["K"]], mode=last.TOPK)
+    assert list(order) == t["order"] and list(kept) == t["kept"]
+    np.testing.assert_array_equal(gains, np.array(t["gains"], np.float32))
+
+
+@pytest.mark.parametrize("N,nth", [(700, "one wave"), (3000, "several waves")])
+def test_select_infinite_relevance_on_duplicates(N, nth):
+    """+inf relevance on clusters of exact duplicates: once every uncovered token
+    is gone, the remaining objectives are 0 or NaN (+inf * 0), all counting as 0,
+    so the greedy takes the lowest remaining indices, as the oracle does."""
+    rng = np.random.default_rng(N)
+    C = 6
+    base = rng.standard_normal((C, 64)).astype(np.float32)
+    X = base[rng.integers(0, C, size=N)]
+    w = rng.dirichlet(np.ones(N)).astype(np.float32)
+    w[rng.choice(N, 40, replace=False)] = np.inf
+    K = 60
+    wl, w32, kept, order, gains = _select_handmade(X, w, K, W.F32)
+    okept, oorder, ogains = oracle.select(1, 64, w32, wl.feats, wl.cu_vis, wl.cu_keep, oracle.F32)
+    assert list(order) == list(oorder)
+    assert list(kept) == list(okept)
+    np.testing.assert_array_equal(gains, ogains.astype(np.float32))
+
+
 def test_select_largest_request():
     """A request of exactly 32768 tokens (the register-resident greedy's limit)."""
     rng = np.random.default_rng(35)
@@ -361,12 +405,13 @@ def _two_phase(dw_feats, cu_vis_h, cu_keep_h, make_scores):
     side = torch.cuda.Stream()
     ws = torch.empty(last.select_workspace(cu_vis_h, dw_feats.shape[-1], dw_feats.dtype), dtype=torch.uint8,
                      device="cuda")
+    cu_vis = torch.from_numpy(np.asarray(cu_vis_h, np.int32)).cuda()   # made on the main stream
     side.wait_stream(main)
-    last.diverse_select_similarity(dw_feats, cu_vis_h, ws, stream=side)
+    last.diverse_select_similarity(dw_feats, cu_vis_h, ws, cu_vis=cu_vis, stream=side)
     scores = make_scores()
     main.wait_stream(side)
     kept, order, gains = last.diverse_select_pick(scores, cu_vis_h, cu_keep_h, ws, dw_feats.shape[-1],
-                                                  dw_feats.dtype)
+                                                  dw_feats.dtype, cu_vis=cu_vis)
     torch.cuda.synchronize()
     return scores, kept.cpu().numpy(), order.cpu().numpy(), gains.cpu().numpy()
 
