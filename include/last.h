@@ -119,6 +119,28 @@ last_status last_token_scores(const last_batch *b, const void *q, const void *k,
                               size_t ws_bytes, void *stream);
 
 /*
+ * last_token_scores without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). Same arguments, kernels and results as
+ * last_token_scores; its scratch is a static device array of
+ * LAST_STATIC_SCRATCH_BYTES that every device running the library holds until
+ * the process ends. The call itself allocates nothing: the array's address is
+ * looked up once per device, on that device's first call.
+ *   - A batch whose workspace (last_token_scores_workspace) exceeds
+ *     LAST_STATIC_SCRATCH_BYTES is rejected with LAST_ERR_WORKSPACE before any
+ *     HIP call.
+ *   - The current device must be the one `stream` belongs to.
+ *   - All calls on one device share its array: calls that overlap in time on
+ *     one device (different streams, or different host threads) race and give
+ *     undefined results. Nothing in the array needs to start at zero; each call
+ *     writes every part it reads.
+ */
+#define LAST_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+last_status last_token_scores_static(const last_batch *b, const void *q,
+                                     const void *k, float *scores,
+                                     float *attn_rows, void *stream);
+
+/*
  * Sec. 4.3, Table 4 (attention-source ablation): the sources compared there,
  * for a text query of M tokens q_1 .. q_M at positions q_begin .. q_end - 1
  * of a request (M = q_end - q_begin; q_M is the last query token p*).

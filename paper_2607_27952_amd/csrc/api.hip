@@ -219,6 +219,66 @@ last_status last_token_scores(const last_batch *b, const void *q, const void *k,
   return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
 }
 
+}  // extern "C"
+
+// ------------------------------------------------------------ static scratch
+// The scratch of last_token_scores_static: one copy on every device that loads
+// the library, kept until the process ends. Host code never passes this name to
+// a kernel (on the host it is only a stand-in for the symbol); it uses the
+// device address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[LAST_STATIC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices] = {};
+}  // namespace
+
+// The current device's address of `scratch`, looked up on the device's first call.
+static last_status static_scratch(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    note_hip_error(e);
+    return LAST_ERR_DEVICE;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return LAST_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      note_hip_error(e);
+      return LAST_ERR_DEVICE;
+    }
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return LAST_OK;
+}
+
+extern "C" {
+
+last_status last_token_scores_static(const last_batch *b, const void *q, const void *k, float *scores,
+                                     float *attn_rows, void *stream) {
+  last_status st = check_batch(b);
+  if (st != LAST_OK) return st;
+  if (!q || !k || !scores) return LAST_ERR_INVALID;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(scores, 4) || (attn_rows && !aligned(attn_rows, 4)))
+    return LAST_ERR_INVALID;
+  const ScorePlan p = make_score_plan(b);
+  size_t need = 0;
+  carve_score_ws(nullptr, b, p, &need);
+  if (need > LAST_STATIC_SCRATCH_BYTES) return LAST_ERR_WORKSPACE;
+  void *ws = nullptr;
+  st = static_scratch(&ws);
+  if (st != LAST_OK) return st;
+  const ScoreWs w = carve_score_ws(ws, b, p, &need);
+  const float scale = b->softmax_scale > 0.f ? b->softmax_scale : 1.0f / sqrtf((float)b->Dh);
+  const hipError_t e = launch_scores(b, p, w, q, k, nullptr, scores, attn_rows, scale, (hipStream_t)stream);
+  return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
+}
+
 int32_t last_source_rows(last_source src, int32_t q_begin, int32_t q_end, int32_t *pos_h) {
   if (q_begin < 0 || q_end <= q_begin || !pos_h) return -1;
   const int32_t M = q_end - q_begin;

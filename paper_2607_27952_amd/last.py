@@ -24,7 +24,7 @@ LAST_F32, LAST_BF16 = 0, 1
 KCENTER, TOPK = 0, 1
 SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
 
-EXPORTS = ("last_token_scores_workspace", "last_token_scores", "last_source_rows",
+EXPORTS = ("last_token_scores_workspace", "last_token_scores", "last_token_scores_static", "last_source_rows",
            "last_rows_scores_workspace", "last_rows_scores", "last_prefill_attention_workspace",
            "last_prefill_attention", "diverse_select_workspace",
            "diverse_select", "diverse_select_similarity", "diverse_select_pick", "gather_kept", "last_connector_workspace", "last_connector", "last_budget", "last_status_string", "last_version",
@@ -63,6 +63,8 @@ def lib():
         L.last_token_scores_workspace.restype = SZ
         L.last_token_scores.argtypes = [ctypes.POINTER(_Batch), P, P, P, P, P, SZ, P]
         L.last_token_scores.restype = I32
+        L.last_token_scores_static.argtypes = [ctypes.POINTER(_Batch), P, P, P, P, P]
+        L.last_token_scores_static.restype = I32
         L.last_source_rows.argtypes = [I32, I32, I32, P]
         L.last_source_rows.restype = I32
         L.last_rows_scores_workspace.argtypes = [ctypes.POINTER(_Batch), P, P]
@@ -218,6 +220,29 @@ def token_scores(batch: Batch, q: torch.Tensor, k: torch.Tensor, scores=None, at
         if st != LAST_OK:
             raise LastError(st, "last_token_scores")
         return (scores, attn_rows) if want_rows else scores
+
+
+STATIC_SCRATCH_BYTES = 64 << 20   # LAST_STATIC_SCRATCH_BYTES
+
+
+def token_scores_static(batch: Batch, q: torch.Tensor, k: torch.Tensor, scores=None, attn_rows=None,
+                        want_rows=False, stream=None):
+    """last_token_scores_static: last_token_scores on the library's static per-device
+    scratch (no workspace). Allocates nothing when `scores` (and `attn_rows`) are given."""
+    code = _dtype_code(q)
+    if k.dtype != q.dtype:
+        raise TypeError("q and k must share a dtype")
+    b = batch.struct(code)
+    with _on(stream):
+        if scores is None:
+            scores = torch.empty(batch.N_total, dtype=torch.float32, device=q.device)
+        if want_rows and attn_rows is None:
+            attn_rows = torch.empty((batch.G, batch.Hq, batch.T_total), dtype=torch.float32, device=q.device)
+        st = lib().last_token_scores_static(ctypes.byref(b), _ptr(q), _ptr(k), _ptr(scores), _ptr(attn_rows),
+                                            _stream(stream))
+    if st != LAST_OK:
+        raise LastError(st, "last_token_scores_static")
+    return (scores, attn_rows) if want_rows else scores
 
 
 def source_rows(src: int, q_begin: int, q_end: int) -> np.ndarray:
