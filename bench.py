@@ -57,6 +57,9 @@ def parse():
                          "beside the score pass, then diverse_select_pick; by default every call runs "
                          "in order on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="time only the chosen workload (by default the other paper-shaped batches and the "
+                         "LLaVA-1.5 batch's other budgets are timed too and reported under \"configs\")")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target CPU time for the oracle sample")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -123,26 +126,27 @@ def rows_work(wl, cu_rows, row_pos):
 
 
 def gram_work(wl):
-    """The two Gram launches, each bound by whichever of HBM bytes and matrix-core
-    (bf16) or fp64-vector (fp32 features) flops takes longer at the peaks. The
-    diagonal launch reads every feature row once and writes the diagonal
-    128 x 128 coverage blocks and the norms; the off-diagonal launch reads the
-    rows of every request with more than one row block again and writes each
-    off-diagonal block and its mirror."""
+    """The two Gram launches, each bound by whichever of its algorithmic bytes and
+    matrix-core (bf16) or fp64-vector (fp32 features) flops takes longer at the
+    peaks. Algorithmic bytes are the features the launch must read once: every
+    row for the diagonal launch, the rows of every request with more than one
+    row block for the off-diagonal one. The coverage blocks both launches write
+    are a product of this design (the paper's method keeps no N x N matrix), so
+    they count as measured traffic, not as algorithmic work. Flops are the
+    launch's share of each request's symmetric Gram."""
     felt = 2 if wl.f_dtype == "bf16" else 4
     n = np.diff(wl.cu_vis).astype(np.int64)
     nb = (n + GRAM_TILE - 1) // GRAM_TILE
-    blk = GRAM_TILE * GRAM_TILE * 4
     f_diag, f_off = gram_flops(n, wl.Dv)
-    b_diag = wl.N_total * wl.Dv * felt + int(np.sum(nb)) * blk + wl.N_total * 16
-    b_off = int(np.sum(n[nb > 1])) * wl.Dv * felt + int(np.sum(nb * (nb - 1))) * blk
+    b_diag = wl.N_total * wl.Dv * felt
+    b_off = int(np.sum(n[nb > 1])) * wl.Dv * felt
     peak, kind = (MFMA_FLOPS_PER_S, "mfma") if felt == 2 else (FP64_VECTOR_PEAK_TFLOPS * 1e12, "alu")
 
     def bound(b, f):
         return ("hbm", b) if b / HBM_BYTES_PER_S >= f / peak else (kind, f)
     if felt == 4:
         # fp32 features: one launch covers every sub-tile (its blocks compute their own norms)
-        return {"gram": bound(b_diag + b_off, f_diag + f_off)}
+        return {"gram": bound(b_diag, f_diag + f_off)}
     return {"gram_diag": bound(b_diag, f_diag), "gram": bound(b_off, f_off)}
 
 
@@ -203,6 +207,61 @@ def kernel_work(wl, row_pos=None):
     }
 
 
+def stage_work(wl, row_pos=None):
+    """Algorithmic work of each stage of the path, as the paper defines the stage:
+    - scores (Eq. 6-8, O(L H N)): every key row of every guidance layer and the
+      scored query rows read once (HBM);
+    - similarity (Sec. 3.4, O(K N d_v), no N x N matrix): the features read once,
+      and one x_j^T X product per pick, 2 K N Dv flops; bound by whichever takes
+      longer at the peaks (matrix cores for bf16 features, the fp64 vector ALUs
+      that the fp32-feature path runs on);
+    - gather (Eq. 12): the kept rows read and written once (HBM)."""
+    elt = 2 if wl.qk_dtype == "bf16" else 4
+    felt = 2 if wl.f_dtype == "bf16" else 4
+    tokens = wl.T_total if row_pos is None else int(np.sum(np.asarray(row_pos, np.int64) + 1))
+    score_bytes = wl.G * tokens * wl.Hkv * wl.Dh * elt + wl.G * wl.R * wl.Hq * wl.Dh * elt
+    kk = np.diff(wl.cu_keep).astype(np.float64)
+    nv = np.diff(wl.cu_vis).astype(np.float64)
+    sim_flops = float(np.sum(2 * kk * nv)) * wl.Dv
+    sim_bytes = wl.N_total * wl.Dv * felt
+    peak, kind = (MFMA_FLOPS_PER_S, "mfma") if felt == 2 else (FP64_VECTOR_PEAK_TFLOPS * 1e12, "alu")
+    sim = ("hbm", sim_bytes) if sim_bytes / HBM_BYTES_PER_S >= sim_flops / peak else (kind, sim_flops)
+    return {"scores": ("hbm", score_bytes), "similarity": sim,
+            "gather": ("hbm", 2 * wl.K_total * wl.Dv * felt),
+            "similarity_bytes": sim_bytes, "similarity_flops": sim_flops}
+
+
+SCORE_KERNELS = ("score_prefix", "score_stream", "score_partial", "score_merge", "score_finalize")
+SIMILARITY_KERNELS = ("select_plan", "gram_diag", "gram")
+
+
+def similarity_summary(wl, kernels):
+    """The k-center's distance stage against the paper's work and against the
+    Gram's own executed work (each request's symmetric Gram, diagonal included)."""
+    gram_ms = sum(kernels[k]["ms_per_step"] for k in ("gram_diag", "gram") if k in kernels)
+    if gram_ms <= 0:
+        return None
+    sw = stage_work(wl)
+    d, o = gram_flops(np.diff(wl.cu_vis), wl.Dv)
+    unique = d + o
+    return {"paper_flops": sw["similarity_flops"], "gram_unique_flops": unique,
+            "gram_ms_per_step": round(gram_ms, 4),
+            "tflops_on_paper_work": round(sw["similarity_flops"] / (gram_ms * 1e-3) / 1e12, 2),
+            "tflops_on_gram_work": round(unique / (gram_ms * 1e-3) / 1e12, 2),
+            "gram_work_over_paper_work": round(unique / sw["similarity_flops"], 2)}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def roofline_entry(name, bound, work, avg_ms):
     if bound == "hbm":
         ach = work / (avg_ms * 1e-3) / 1e9
@@ -259,27 +318,27 @@ def cpu_baseline(wl, target_s):
         dt1 += run(wl.subset([n1]), 1)
         n1 += 1
     return {"value": round(n * passes / dt, 3), "unit": "requests/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{what} x {passes} pass(es), whole path (scores, k-center, gather) in fp64, "
                       f"{dt:.1f} s on {threads} threads",
             "single_thread": {"value": round(n1 / dt1, 3), "unit": "requests/s",
                               "sample": f"first {n1} request(s) one at a time, {dt1:.1f} s on 1 thread"}}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
-              file=sys.stderr)
-        sys.exit(2)
+def measure(args, name, budget, steps, warmup, source="last", prefill=False, connector=False, overlap=False,
+            copy_mib=0):
+    """Time `steps` steps of the path on one workload (after `warmup` steps) and
+    return the per-workload record: throughput, p50/p90 step latency, per-kernel
+    times (HIP events the library records around each kernel, in a second timed
+    pass), per-kernel and per-stage rooflines, and the workload object."""
     import torch
     from paper_2607_27952_amd import last
     from paper_2607_27952_amd import workloads as W
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     t0 = time.time()
-    wl = W.make(args.workload, budget=args.budget)
-    log(f"[bench] generated {wl.name} in {time.time() - t0:.1f}s")
+    wl = W.make(name, budget=budget)
+    log(f"[bench] generated {wl.name} (budget {budget}) in {time.time() - t0:.1f}s")
     dw = last.DeviceWorkload.upload(wl, device=dev)
     b = dw.batch
     stream = torch.cuda.current_stream()
@@ -292,17 +351,17 @@ def main():
     out = torch.empty((wl.K_total, wl.Dv), dtype=dw.feats.dtype, device=dev)
     rows = q_rows = None
     pre = None
-    if args.prefill:
-        if args.source != "last":
+    if prefill:
+        if source != "last":
             raise SystemExit("--prefill takes the scores from the last rows; --source must be last")
         pin = W.prefill_inputs(wl)
         pre = (last.to_torch(pin.q, wl.qk_dtype, dev), last.to_torch(pin.v, wl.qk_dtype, dev))
         pre_out = torch.empty(pre[0].shape, dtype=pre[0].dtype, device=dev)
         del pin
         log(f"[bench] scores from the causal prefill attention of all {wl.T_total} positions")
-    if args.source != "last":
+    if source != "last":
         qr = W.query_rows(wl)
-        src = {"first": last.SRC_FIRST, "middle": last.SRC_MIDDLE, "all_mean": last.SRC_ALL_MEAN}[args.source]
+        src = {"first": last.SRC_FIRST, "middle": last.SRC_MIDDLE, "all_mean": last.SRC_ALL_MEAN}[source]
         counts, pos, qs = [], [], []
         for r in range(wl.R):
             p = last.source_rows(src, int(qr.q_begin[r]), int(qr.q_end[r]))
@@ -312,7 +371,7 @@ def main():
         rows = last.Rows.make(np.concatenate([[0], np.cumsum(counts)]), pos, device=dev)
         q_rows = last.to_torch(np.ascontiguousarray(np.concatenate(qs, axis=1)), wl.qk_dtype, dev)
         ws_s = torch.empty(last.rows_scores_workspace(b, rows, dw.q.dtype), dtype=torch.uint8, device=dev)
-        log(f"[bench] scores from the {args.source} rows: {int(rows.cu_rows_h[-1])} query rows")
+        log(f"[bench] scores from the {source} rows: {int(rows.cu_rows_h[-1])} query rows")
     elif pre is not None:
         ws_s = torch.empty(last.prefill_attention_workspace(b), dtype=torch.uint8, device=dev)
     else:
@@ -320,7 +379,7 @@ def main():
     ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8, device=dev)
 
     conn = None
-    if args.connector:
+    if connector:
         if wl.f_dtype != "bf16":
             raise SystemExit("--connector runs on bf16 features")
         Dh, Do = W.connector_dims(wl)
@@ -333,19 +392,18 @@ def main():
         del cw
         log(f"[bench] cloud connector {wl.Dv} -> {Dh} -> {Do} on the {wl.K_total} kept rows")
 
-    if args.copy_calibration_mib > 0:
-        nbytes = args.copy_calibration_mib << 20
-        src = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
-        dst = torch.empty_like(src)
+    if copy_mib > 0:
+        nbytes = copy_mib << 20
+        src_t = torch.ones(nbytes // 4, dtype=torch.int32, device=dev)
+        dst_t = torch.empty_like(src_t)
         torch.cuda.synchronize()
-        dst.copy_(src)
+        dst_t.copy_(src_t)
         torch.cuda.synchronize()
         log(f"[bench] calibration copy: {nbytes} bytes read, {nbytes} bytes written")
-        del src, dst
+        del src_t, dst_t
 
     # The distances of Eq. 10 need only the features: on a second stream (default
     # priority) they overlap the score pass; the pick waits for both streams.
-    overlap = args.overlap
     side = torch.cuda.Stream(device=dev)
 
     def step():
@@ -370,84 +428,137 @@ def main():
             last.connector(out, conn["gamma"], conn["beta"], conn["w1"], conn["b1"], conn["w2"], conn["b2"],
                            out=conn_out, ws=ws_c)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
 
     def timed(profile):
-        """K steps bracketed by synchronisation; per-step HIP events on the launch stream.
+        """`steps` steps bracketed by synchronisation; per-step HIP events on the launch stream.
         With `profile`, the library also records events around each of its kernels."""
-        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
         last.profile_reset()
         last.profile_enable(profile)
         torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for i in range(args.steps):
+        t_a = time.perf_counter()
+        for i in range(steps):
             ev[i][0].record(stream)
             step()
             ev[i][1].record(stream)
         torch.cuda.synchronize()
-        t1 = time.perf_counter()
+        t_b = time.perf_counter()
         last.profile_enable(False)
         prof = last.profile_collect() if profile else {}
-        return t1 - t0, np.array([a.elapsed_time(bb) for a, bb in ev]), prof
+        return t_b - t_a, np.array([x.elapsed_time(y) for x, y in ev]), prof
 
     # throughput: the path alone; per-kernel times: a second timed pass with the
     # library's kernel events (they add a little time between kernels)
     elapsed, step_ms, _ = timed(False)
-    elapsed_prof, step_ms_prof, prof = timed(True)
-    ms_per_step = elapsed / args.steps * 1e3
+    elapsed_prof, _, prof = timed(True)
 
     single = rows is not None and int(rows.cu_rows_h[-1]) == wl.R
-    work = kernel_work(wl, rows.row_pos_h if single else None)
+    row_pos = rows.row_pos_h if single else None
+    work = kernel_work(wl, row_pos)
     if rows is not None and not single:
         work.update({k: v for k, v in rows_work(wl, rows.cu_rows_h, rows.row_pos_h).items()
                      if k in ("rows_stats", "rows_visual")})
     if conn is not None:
         work.update(connector_work(wl))
     kernels = {}
-    for name, (launches, total_ms) in prof.items():
-        kernels[name] = {"launches": launches, "avg_ms": round(total_ms / max(launches, 1), 5),
-                         "ms_per_step": round(total_ms / args.steps, 5)}
-    rooflines = []
-    for name, (bound, w) in work.items():
-        if name in kernels:
-            rooflines.append(roofline_entry(name, bound, w, kernels[name]["avg_ms"]))
+    for kname, (launches, total_ms) in prof.items():
+        kernels[kname] = {"launches": launches, "avg_ms": round(total_ms / max(launches, 1), 5),
+                          "ms_per_step": round(total_ms / steps, 5)}
+    rooflines = [roofline_entry(k, bd, w, kernels[k]["avg_ms"]) for k, (bd, w) in work.items() if k in kernels]
     dominant = max(kernels.items(), key=lambda kv: kv[1]["ms_per_step"])[0]
     main_roof = next((r for r in rooflines if r["kernel"] == dominant), None)
     if main_roof is not None:
-        tr = traffic_for(dominant, args.workload if args.source == "last" and pre is None else
-                         f"{args.workload}_{'prefill' if pre is not None else args.source}")
+        tr = traffic_for(dominant, name if source == "last" and pre is None else
+                         f"{name}_{'prefill' if pre is not None else source}")
         main_roof = {k: main_roof[k] for k in ("bound", "achieved", "peak", "unit", "frac")} | {
             "traffic": tr, "kernel": dominant}
-    # the paper's own similarity work (Sec. 3.4: one x_j^T X product per pick,
-    # 2 K N Dv flops) against the Gram's time, next to the Gram's executed work
-    kk = np.diff(wl.cu_keep).astype(np.float64)
-    nv = np.diff(wl.cu_vis).astype(np.float64)
-    paper_flops = float(np.sum(2 * kk * nv)) * wl.Dv
-    gram_ms = sum(kernels[k]["ms_per_step"] for k in ("gram_diag", "gram") if k in kernels)
-    similarity = None
-    if gram_ms > 0:
-        exec_flops = sum(work[k][1] for k in ("gram_diag", "gram") if k in work)
-        similarity = {"paper_flops": paper_flops, "gram_unique_flops": exec_flops,
-                      "gram_ms_per_step": round(gram_ms, 4),
-                      "tflops_on_paper_work": round(paper_flops / (gram_ms * 1e-3) / 1e12, 2),
-                      "tflops_on_gram_work": round(exec_flops / (gram_ms * 1e-3) / 1e12, 2)}
+
     score_ms = sum(kernels[k]["ms_per_step"] for k in kernels
                    if k.startswith("score") or k.startswith("rows") or k.startswith("prefill"))
-    select_ms = sum(kernels[k]["ms_per_step"] for k in kernels
-                    if k in ("select_plan", "sqnorm", "gram_diag", "gram", "greedy", "topk"))
+    similarity_ms = sum(kernels[k]["ms_per_step"] for k in SIMILARITY_KERNELS if k in kernels)
+    select_ms = similarity_ms + sum(kernels[k]["ms_per_step"] for k in ("greedy", "topk") if k in kernels)
     gather_ms = kernels.get("gather", {}).get("ms_per_step", 0.0)
     conn_ms = sum(kernels[k]["ms_per_step"] for k in kernels if k.startswith("connector"))
+    sw = stage_work(wl, row_pos)
+    stage_roof = {}
+    if rows is None and pre is None and score_ms > 0:
+        stage_roof["scores"] = roofline_entry("scores: " + "+".join(k for k in kernels if k in SCORE_KERNELS),
+                                              *sw["scores"], score_ms)
+    if similarity_ms > 0:
+        e = roofline_entry("similarity: " + "+".join(k for k in SIMILARITY_KERNELS if k in kernels),
+                           *sw["similarity"], similarity_ms)
+        e["paper_work"] = "features read once; 2 K N Dv flops (one x_j^T X product per pick)"
+        stage_roof["similarity"] = e
+    if gather_ms > 0:
+        stage_roof["gather"] = roofline_entry("gather", *sw["gather"], gather_ms)
+    if "greedy" in kernels:
+        kk = np.diff(wl.cu_keep)
+        stage_roof["greedy"] = {"bound": "latency", "steps_longest_request": int(kk.max()),
+                                "us_per_step_longest_request": round(kernels["greedy"]["ms_per_step"] * 1e3 / int(kk.max()), 3)}
+    ms_per_step = elapsed / steps * 1e3
+    return {
+        "wl": wl,
+        "value": round(wl.R * steps / elapsed, 2),
+        "ms_per_step": round(ms_per_step, 4),
+        "visual_tokens_scored_per_s": round(wl.N_total / (score_ms * 1e-3), 1) if score_ms > 0 else None,
+        "p50_select_latency_ms": round(float(np.median(step_ms)), 4),
+        "p90_select_latency_ms": round(float(np.percentile(step_ms, 90)), 4),
+        "ms_per_step_with_kernel_events": round(elapsed_prof / steps * 1e3, 4),
+        "stage_ms_per_step": {"scores": round(score_ms, 4), "select": round(select_ms, 4),
+                              "gather": round(gather_ms, 4)} | ({"connector": round(conn_ms, 4)} if conn else {}),
+        "kernels": kernels,
+        "roofline": main_roof,
+        "rooflines": rooflines,
+        "stage_rooflines": stage_roof,
+        "similarity": similarity_summary(wl, kernels),
+        "rows": rows,
+        "pre": pre,
+        "conn": conn,
+    }
 
+
+# The other workloads timed beside the headline one (each of the paper-shaped
+# batches, and the LLaVA-1.5 batch at its other two budgets): name, budget, steps.
+CONFIG_RUNS = (("c1_single_fp32", None, 50), ("c2_llava15", 128, 30), ("c2_llava15", 192, 30),
+               ("c3_llava_next", None, 20), ("c4_dynres", None, 10), ("c5_video", None, 10))
+
+
+def config_summary(m, budget):
+    wl = m["wl"]
+    ks = np.diff(wl.cu_keep)
+    return {"workload": describe(wl, budget), "requests": wl.R, "visual_tokens": wl.N_total,
+            "kept_tokens": wl.K_total, "budget": int(ks[0]) if ks.min() == ks.max() else "ceil(N/8)",
+            "requests_per_s": m["value"], "ms_per_step": m["ms_per_step"],
+            "visual_tokens_scored_per_s": m["visual_tokens_scored_per_s"],
+            "p50_select_latency_ms": m["p50_select_latency_ms"], "stage_ms_per_step": m["stage_ms_per_step"],
+            "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in m["kernels"].items()},
+            "roofline": m["roofline"], "stage_rooflines": m["stage_rooflines"], "similarity": m["similarity"]}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (this build has no multi-GPU path); got --gpus {args.gpus}",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    m = measure(args, args.workload, args.budget, args.steps, args.warmup, source=args.source,
+                prefill=args.prefill, connector=args.connector, overlap=args.overlap,
+                copy_mib=args.copy_calibration_mib)
+    wl = m["wl"]
     res = {
         "metric": "requests/sec and visual tokens scored/sec per GPU; p50 select latency",
-        "value": round(wl.R * args.steps / elapsed, 2),
+        "value": m["value"],
         "unit": "requests/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 4),
+        "ms_per_step": m["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -455,9 +566,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": describe(wl, args.budget) + ("" if args.source == "last" else
                                                              f"; scores from the {args.source} query rows")
-                   + ("; scores from the causal prefill attention of every position" if pre is not None else "")
-                   + (f"; cloud connector {wl.Dv}->{wl.Dv}->{wl.Dv} on the kept rows" if conn is not None else ""),
-                   "schedule": ("one stream" if not overlap else
+                   + ("; scores from the causal prefill attention of every position" if m["pre"] is not None else "")
+                   + (f"; cloud connector {wl.Dv}->{wl.Dv}->{wl.Dv} on the kept rows" if m["conn"] is not None else ""),
+                   "schedule": ("one stream" if not args.overlap else
                                 "distances (plan, Gram) on a second stream beside the score pass; "
                                 "greedy and gather after both"),
                    "requests": wl.R, "visual_tokens": wl.N_total,
@@ -465,23 +576,37 @@ def main():
                        "bf16 inputs, " + ("fp32 FMA score pass" if args.source != "all_mean" else
                                           "bf16 MFMA score passes with fp32 accumulation")
                        + ", bf16 MFMA Gram with fp32 partial sums folded into fp64, fp32 objective")},
-        "visual_tokens_scored_per_s": round(wl.N_total / (score_ms * 1e-3), 1) if score_ms > 0 else None,
-        "p50_select_latency_ms": round(float(np.median(step_ms)), 4),
-        "p90_select_latency_ms": round(float(np.percentile(step_ms, 90)), 4),
-        "ms_per_step_with_kernel_events": round(elapsed_prof / args.steps * 1e3, 4),
-        "stage_ms_per_step": {"scores": round(score_ms, 4), "select": round(select_ms, 4),
-                              "gather": round(gather_ms, 4)} | (
-                                  {"connector": round(conn_ms, 4)} if conn is not None else {}),
-        "kernels": kernels,
-        "roofline": main_roof,
-        "rooflines": rooflines,
-        "similarity": similarity,
+        "visual_tokens_scored_per_s": m["visual_tokens_scored_per_s"],
+        "p50_select_latency_ms": m["p50_select_latency_ms"],
+        "p90_select_latency_ms": m["p90_select_latency_ms"],
+        "ms_per_step_with_kernel_events": m["ms_per_step_with_kernel_events"],
+        "stage_ms_per_step": m["stage_ms_per_step"],
+        "kernels": m["kernels"],
+        "roofline": m["roofline"],
+        "rooflines": m["rooflines"],
+        "stage_rooflines": m["stage_rooflines"],
+        "similarity": m["similarity"],
+        "configs": None,
         "cpu_baseline": None,
         "device": torch.cuda.get_device_name(0),
     }
+    default_mode = not (args.prefill or args.connector or args.overlap or args.source != "last")
+    if default_mode and not args.no_configs:
+        res["configs"] = {}
+        del m
+        for name, budget, steps in CONFIG_RUNS:
+            if name == args.workload and budget == args.budget:
+                continue
+            torch.cuda.empty_cache()
+            t0 = time.time()
+            mc = measure(args, name, budget, steps, 3)
+            res["configs"][name if budget is None else f"{name}_b{budget}"] = config_summary(mc, budget)
+            log(f"[bench] {name} (budget {budget}): {mc['ms_per_step']} ms per step, {time.time() - t0:.1f}s")
+            del mc
     if not args.no_cpu_baseline:
         t0 = time.time()
-        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+        from paper_2607_27952_amd import workloads as W
+        res["cpu_baseline"] = cpu_baseline(W.make(args.workload, budget=args.budget), args.cpu_seconds)
         log(f"[bench] cpu baseline took {time.time() - t0:.1f}s")
     print(json.dumps(res), flush=True)
 

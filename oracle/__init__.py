@@ -45,7 +45,7 @@ def lib():
         L.oracle_scores.restype = I
         L.oracle_select.argtypes = [I, I, I, I, P, P, P, P, P, P, P, I]
         L.oracle_select.restype = I
-        L.oracle_replay.argtypes = [I, I, I, P, P, P, P, P, D, P, P, I]
+        L.oracle_replay.argtypes = [I, I, I, P, P, P, P, P, D, P, P, P, I]
         L.oracle_replay.restype = I
         L.oracle_gather.argtypes = [I, I64, P, P, P, P, P]
         L.oracle_gather.restype = I
@@ -187,10 +187,11 @@ def select(R, Dv, w32, feats, cu_vis, cu_keep, dtype, mode=KCENTER, nthreads=0):
     return kept, order, gains
 
 
-def replay(R, Dv, w32, feats, cu_vis, cu_keep, picks, dtype, rel_tol=1e-6, nthreads=0):
+def replay(R, Dv, w32, feats, cu_vis, cu_keep, picks, dtype, rel_tol=1e-6, nthreads=0, want_objective=False):
     """Teacher-forced replay of `picks` under Eq. 9-11.
 
-    Returns (status, margin): status 0 exact / 1 excused near-tie / 2 failed per step.
+    Returns (status, margin): status 0 exact / 1 excused near-tie / 2 failed per step;
+    with want_objective also the oracle's fp64 objective of each pick.
     """
     cu_vis, cu_keep, picks = _i32(cu_vis), _i32(cu_keep), _i32(picks)
     w32 = np.ascontiguousarray(w32, dtype=np.float32)
@@ -198,11 +199,12 @@ def replay(R, Dv, w32, feats, cu_vis, cu_keep, picks, dtype, rel_tol=1e-6, nthre
     Kt = int(cu_keep[R])
     status = np.zeros(Kt, np.int32)
     margin = np.zeros(Kt, np.float64)
+    obj = np.zeros(Kt, np.float64) if want_objective else None
     rc = lib().oracle_replay(R, Dv, fd, _ptr(w32), _ptr(feats), _ptr(cu_vis), _ptr(cu_keep),
-                             _ptr(picks), float(rel_tol), _ptr(status), _ptr(margin), nthreads)
+                             _ptr(picks), float(rel_tol), _ptr(status), _ptr(margin), _ptr(obj), nthreads)
     if rc != 0:
         raise RuntimeError(f"oracle_replay failed ({rc})")
-    return status, margin
+    return (status, margin, obj) if want_objective else (status, margin)
 
 
 def gather(R, feats, cu_vis, kept, cu_keep):

@@ -581,15 +581,16 @@ int oracle_select(int R, int Dv, int f_dtype, int mode, const float *w,
  *   0 exact   -- g_t is the lowest index attaining o*;
  *   1 excused -- o* - o_{g_t} <= rel_tol * o* (a near-tie);
  *   2 failed  -- anything else, including an out-of-range or repeated index.
- * margin[t] receives (o* - o_{g_t}) / o* (0 when o* == 0). After a failed
- * index that cannot be replayed (out of range / repeated) the remaining
- * steps of that request are marked failed.
+ * margin[t] receives (o* - o_{g_t}) / o* (0 when o* == 0), and objective[t]
+ * (nullable) the oracle's own objective o_{g_t} of the candidate's pick. After
+ * a failed index that cannot be replayed (out of range / repeated) the
+ * remaining steps of that request are marked failed.
  */
 int oracle_replay(int R, int Dv, int f_dtype, const float *w,
                   const void *feats, const int32_t *cu_vis,
                   const int32_t *cu_keep, const int32_t *picks,
                   double rel_tol, int32_t *status, double *margin,
-                  int nthreads) {
+                  double *objective, int nthreads) {
   orc_set_threads(nthreads);
   for (int r = 0; r < R; ++r) {
     const int64_t row0 = cu_vis[r];
@@ -614,6 +615,7 @@ int oracle_replay(int R, int Dv, int f_dtype, const float *w,
       if (broken) {
         status[out0 + t] = 2;
         margin[out0 + t] = INFINITY;
+        if (objective) objective[out0 + t] = NAN;
         continue;
       }
       const int64_t best = orc_argmax(o, sel, N);
@@ -621,9 +623,11 @@ int oracle_replay(int R, int Dv, int f_dtype, const float *w,
       if (gp < 0 || gp >= N || sel[gp]) {
         status[out0 + t] = 2;
         margin[out0 + t] = INFINITY;
+        if (objective) objective[out0 + t] = NAN;
         broken = 1;
         continue;
       }
+      if (objective) objective[out0 + t] = o[gp];
       const double ostar = o[best];
       const double gap = ostar - o[gp];
       margin[out0 + t] = ostar > 0.0 ? gap / ostar : 0.0;

@@ -33,20 +33,19 @@ def test_kernel_work_matches_shapes():
 
 
 def test_gram_bound_is_the_slower_resource():
-    """Each Gram launch is priced by whichever of its bytes and flops takes longer
-    at the published peaks: features read once and coverage blocks written."""
+    """Each Gram launch is priced by whichever of its algorithmic bytes (the
+    features it must read once; the coverage blocks it writes are this design's,
+    not the method's) and its flops takes longer at the published peaks."""
     wl = W.make("c2_llava15")
     n = np.diff(wl.cu_vis)
     work = bench.gram_work(wl)
     d, o = bench.gram_flops(n, wl.Dv)
-    blk = 128 * 128 * 4
-    b_diag = wl.N_total * wl.Dv * 2 + 64 * 5 * blk + wl.N_total * 16     # 576 tokens: 5 row blocks
-    b_off = wl.N_total * wl.Dv * 2 + 64 * 20 * blk                       # 5 x 4 off-diagonal blocks
-    # C2's 576-token requests: 57 flops a byte on the diagonal, 178 off it,
-    # both under the 312 that the peaks balance at, so both launches are HBM-bound
-    assert work["gram_diag"] == ("hbm", b_diag)
-    assert work["gram"] == ("hbm", b_off)
-    assert d / b_diag < 312 and o / b_off < 312
+    b = wl.N_total * wl.Dv * 2
+    # C2's 576-token requests: 7.6 flops a byte on the diagonal, 282 off it, both
+    # under the 312 that the peaks balance at, so both launches are HBM-bound
+    assert work["gram_diag"] == ("hbm", b)
+    assert work["gram"] == ("hbm", b)
+    assert d / b < 312 and o / b < 312
     # long requests make the off-diagonal launch a contraction bound by the matrix cores
     wl5 = W.tiny(5, R=1, n_range=(4000, 4000), Dv=2048, k_frac=0.1)
     w5 = bench.gram_work(wl5)
@@ -107,3 +106,32 @@ def test_prefill_bound_is_the_slower_resource():
     assert bench.prefill_work(wl) == ("hbm", b)
     wl5 = W.tiny(6, R=1, Hq=8, Hkv=1, Dh=128, n_range=(6000, 6000), t_range=(10, 10))
     assert bench.prefill_work(wl5) == ("mfma", bench.prefill_flops(wl5))
+
+
+def test_stage_work_follows_the_papers_costs():
+    """Scores: every key row and query read once (Eq. 6-8, O(L H N)); similarity:
+    features read once and 2 K N Dv flops (Sec. 3.4, one x_j^T X product per
+    pick, no N x N matrix); gather: the kept rows read and written."""
+    wl = W.make("c2_llava15")
+    sw = bench.stage_work(wl)
+    assert sw["scores"] == bench.kernel_work(wl)["score_stream"]
+    assert sw["similarity_bytes"] == 64 * 576 * 4096 * 2
+    assert sw["similarity_flops"] == 2.0 * 64 * 64 * 576 * 4096
+    # 302 MB at 8 TB/s (37.7 us) outlasts 19.3 GFLOP at 2.5 PFLOP/s (7.7 us)
+    assert sw["similarity"] == ("hbm", sw["similarity_bytes"])
+    assert sw["gather"] == ("hbm", 2 * 64 * 64 * 4096 * 2)
+    c1 = W.make("c1_single_fp32")
+    s1 = bench.stage_work(c1)
+    # fp32 features: the flops run on the fp64 vector ALUs (78.6 TFLOP/s)
+    assert s1["similarity"][0] == "alu" and s1["similarity_flops"] == 2.0 * 64 * 576 * 1024
+
+
+def test_similarity_summary_reports_flops_not_bytes():
+    wl = W.make("c2_llava15")
+    kernels = {"gram_diag": {"ms_per_step": 0.05}, "gram": {"ms_per_step": 0.15}}
+    sm = bench.similarity_summary(wl, kernels)
+    d, o = bench.gram_flops(np.diff(wl.cu_vis), wl.Dv)
+    assert sm["gram_unique_flops"] == d + o == 64 * 576 * 577 * 4096
+    assert sm["paper_flops"] == 2.0 * 64 * 64 * 576 * 4096
+    assert abs(sm["tflops_on_gram_work"] - (d + o) / 0.2e-3 / 1e12) < 0.01
+    assert abs(sm["gram_work_over_paper_work"] - 577 / 128) < 0.01

@@ -9,8 +9,8 @@ Bars (the oracle is fp64; the library computes in fp32 with exact bf16 widening)
              sets and must match exactly unless the replay excused a step;
   * top-k    identical set and order (both sides rank the same fp32 values);
   * gather   byte-identical rows.
-Small cases span several chunks/tiles with ragged tails; the five named
-workloads run at full size on the GPU and are checked on sampled requests.
+Small cases span several chunks/tiles with ragged tails; every request of
+the five named workloads is checked in tests/test_gpu_fullsize.py.
 """
 import numpy as np
 import pytest
@@ -334,15 +334,6 @@ def test_gather_out_of_range_index_gives_zero_row():
 
 # ------------------------------------------------------------------ full-size workloads
 
-CONFIG_SAMPLES = {
-    "c1_single_fp32": [0],
-    "c2_llava15": [0, 37],
-    "c3_llava_next": [5],
-    "c4_dynres": None,          # chosen from the drawn sizes: smallest, median and a large one
-    "c5_video": [3],
-}
-
-
 @pytest.fixture(scope="module")
 def workloads():
     cache = {}
@@ -354,48 +345,6 @@ def workloads():
             cache[key] = (wl, last.DeviceWorkload.upload(wl))
         return cache[key]
     return get
-
-
-def _samples(name, wl):
-    s = CONFIG_SAMPLES[name]
-    if s is not None:
-        return s
-    order = np.argsort(np.diff(wl.cu_vis))
-    return [int(order[0]), int(order[len(order) // 2]), int(order[-8])]
-
-
-@pytest.mark.parametrize("name", W.CONFIGS)
-def test_config_scores(name, workloads):
-    wl, dw = workloads(name)
-    g = gpu_scores(dw)
-    for r in range(wl.R):
-        seg = g[wl.cu_vis[r]:wl.cu_vis[r + 1]].astype(np.float64)
-        assert np.all(seg >= 0) and abs(seg.sum() - 1.0) < 1e-5
-    for r in _samples(name, wl):
-        sub = wl.subset([r])
-        assert_scores(g[wl.cu_vis[r]:wl.cu_vis[r + 1]], orc_scores(sub), f"{name} request {r}")
-
-
-@pytest.mark.parametrize("name", W.CONFIGS)
-def test_config_select(name, workloads):
-    wl, dw = workloads(name)
-    g = last.token_scores(dw.batch, dw.q, dw.k)
-    kept, order, gains = gpu_select(dw.feats, g, wl.cu_vis, dw.cu_keep_h)
-    gs = g.cpu().numpy()
-    for r in _samples(name, wl):
-        sub = wl.subset([r])
-        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
-        w_orc = orc_scores(sub).astype(np.float32)
-        # stage-isolated: the oracle's scores into the GPU selection
-        k2, o2, _ = gpu_select(last.to_torch(sub.feats, sub.f_dtype, "cuda"), torch.from_numpy(w_orc).cuda(),
-                               sub.cu_vis, sub.cu_keep)
-        same = []
-        ex1, exc1 = check_selection(sub, w_orc, k2, o2, f"{name} request {r} (oracle scores)", same)
-        # end to end: the GPU's own scores and picks, replayed with the oracle's scores
-        ex, exc = check_selection(sub, w_orc, kept[a:b], order[a:b], f"{name} request {r} (end to end)", same)
-        assert ex + exc == b - a
-        print(f"{name} request {r}: N={wl.n(r)} K={b - a}; oracle scores: {ex1} exact, {exc1} excused; "
-              f"end to end: {ex} exact, {exc} excused; kept sets equal to the oracle's: {same}")
 
 
 def _two_phase(dw_feats, cu_vis_h, cu_keep_h, make_scores):
@@ -448,14 +397,14 @@ def test_config_two_phase_overlapped(name, workloads):
 
 
 def test_long_requests_x1(workloads):
-    """Two requests of 32768 tokens (past the 512-thread greedy): scores of
-    one request against the oracle; the whole selection's invariants; and
+    """Two requests of 32768 tokens (past the 512-thread greedy): the scores of
+    both requests against the oracle; the whole selection's invariants; and
     the first 64 picks of each request replayed on the oracle (a full replay
     costs about 1 TFLOP of fp64 per request), stage-isolated and end to end."""
     wl, dw = workloads("x1_long_video")
     g = last.token_scores(dw.batch, dw.q, dw.k)
     gs = g.cpu().numpy()
-    assert_scores(gs[wl.cu_vis[1]:wl.cu_vis[2]], orc_scores(wl.subset([1])), "x1 request 1")
+    assert_scores(gs, orc_scores(wl), "x1, both requests")
     kept, order, gains = gpu_select(dw.feats, g, wl.cu_vis, dw.cu_keep_h)
     P = 64
     for r in range(wl.R):
@@ -475,26 +424,71 @@ def test_long_requests_x1(workloads):
             assert not np.any(st == 2), f"x1 request {r} ({what}): failed steps {np.flatnonzero(st == 2)[:5]}"
 
 
-@pytest.mark.parametrize("budget", [128, 192])
-def test_c2_other_budgets(budget, workloads):
-    wl, dw = workloads("c2_llava15", budget)
-    g = last.token_scores(dw.batch, dw.q, dw.k)
-    kept, order, _ = gpu_select(dw.feats, g, wl.cu_vis, dw.cu_keep_h)
-    for r in (1, 63):
-        sub = wl.subset([r])
-        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
-        w_orc = orc_scores(sub).astype(np.float32)
-        check_selection(sub, w_orc, kept[a:b], order[a:b], f"c2 B={budget} request {r}")
+@pytest.mark.parametrize("profile", [False, True])
+def test_two_host_threads_two_streams(profile):
+    """Two host threads, each on its own stream with its own workspaces, run the
+    whole path on different batches at the same time (with kernel timing on or
+    off): every result is bit-identical to the same call made alone."""
+    import threading
+    wls = [W.tiny(81, R=4, G=2, Hq=8, Hkv=2, Dh=128, n_range=(200, 900), t_range=(10, 60), Dv=256, k_frac=0.1),
+           W.tiny(82, R=3, G=1, Hq=16, Hkv=16, Dh=64, n_range=(100, 1300), t_range=(5, 40), Dv=512, k_frac=0.2)]
+    dws = [last.DeviceWorkload.upload(wl) for wl in wls]
 
+    def run(dw, wl, stream, ws_s, ws_k):
+        s = last.token_scores(dw.batch, dw.q, dw.k, ws=ws_s, stream=stream)
+        kept, order, gains = last.diverse_select(s, dw.feats, wl.cu_vis, wl.cu_keep, cu_vis=dw.batch.cu_vis,
+                                                 cu_keep=dw.cu_keep, ws=ws_k, stream=stream)
+        out = last.gather_kept(dw.feats, wl.cu_vis, kept, wl.cu_keep, cu_vis=dw.batch.cu_vis, cu_keep=dw.cu_keep,
+                               stream=stream)
+        return s, kept, order, gains, out
 
-@pytest.mark.parametrize("name", W.CONFIGS)
-def test_config_gather(name, workloads):
-    wl, dw = workloads(name)
-    rng = np.random.default_rng(7)
-    kept = np.concatenate([np.sort(rng.choice(wl.n(r), wl.kk(r), replace=False)) for r in range(wl.R)]).astype(np.int32)
-    out = last.gather_kept(dw.feats, wl.cu_vis, torch.from_numpy(kept).cuda(), wl.cu_keep)
+    def host(x):
+        return [t.cpu().view(torch.uint8).numpy().tobytes() if t.dtype == torch.bfloat16 else t.cpu().numpy().tobytes()
+                for t in x]
+
+    alone = []
+    for dw, wl in zip(dws, wls):
+        ws_s = torch.empty(last.token_scores_workspace(dw.batch, dw.q.dtype), dtype=torch.uint8, device="cuda")
+        ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8, device="cuda")
+        r = run(dw, wl, None, ws_s, ws_k)
+        torch.cuda.synchronize()
+        alone.append(host(r))
+
+    results = [[], []]
+    errors = []
+
+    def worker(i):
+        try:
+            dw, wl = dws[i], wls[i]
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                ws_s = torch.empty(last.token_scores_workspace(dw.batch, dw.q.dtype), dtype=torch.uint8, device="cuda")
+                ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8,
+                                   device="cuda")
+            for _ in range(6):
+                r = run(dw, wl, stream, ws_s, ws_k)
+                stream.synchronize()
+                results[i].append(host(r))
+        except Exception as e:   # reported below, in the main thread
+            errors.append(repr(e))
+
+    last.profile_reset()
+    last.profile_enable(profile)
+    try:
+        th = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+        for t in th:
+            t.start()
+        for t in th:
+            t.join(timeout=120)
+        assert not any(t.is_alive() for t in th), "a worker thread did not finish"
+    finally:
+        last.profile_enable(False)
     torch.cuda.synchronize()
-    expect = oracle.gather(wl.R, wl.feats, wl.cu_vis, kept, wl.cu_keep)
-    got = out.cpu()
-    got = got.view(torch.int16).numpy().view(np.uint16) if got.dtype == torch.bfloat16 else got.numpy()
-    assert got.tobytes() == expect.tobytes()
+    assert not errors, errors
+    for i in range(2):
+        assert len(results[i]) == 6
+        for rep in results[i]:
+            assert rep == alone[i], f"thread {i}: a result differs from the call made alone"
+    if profile:
+        prof = last.profile_collect()
+        assert prof.get("score_stream", (0, 0))[0] >= 12 and prof.get("gather", (0, 0))[0] >= 12

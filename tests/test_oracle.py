@@ -803,3 +803,15 @@ def test_pins_catch_planted_mistake(tmp_path, name):
     finally:
         oracle.LIB_PATH = path
         oracle._lib = saved
+
+
+def test_replay_objective_is_the_free_runs_gain():
+    """On the oracle's own pick sequence the replay's objective of each pick is
+    the gain the free run recorded (w at t = 1, then w * delta)."""
+    wl = W.tiny(52, R=2, n_range=(40, 90), Dv=24, comps=5, k_frac=0.3)
+    w = np.random.default_rng(4).dirichlet(np.ones(wl.N_total)).astype(np.float32)
+    _, order, gains = oracle.select(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, oracle.BF16)
+    st, _, obj = oracle.replay(wl.R, wl.Dv, w, wl.feats, wl.cu_vis, wl.cu_keep, order, oracle.BF16,
+                               want_objective=True)
+    assert np.all(st == 0)
+    np.testing.assert_array_equal(obj, gains)
