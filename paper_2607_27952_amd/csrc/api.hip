@@ -408,7 +408,7 @@ last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mo
   if (st != LAST_OK) return st;
   if (!scores || !feats || !cu_vis || !cu_keep || !kept) return LAST_ERR_INVALID;
   if (!aligned(feats, 16)) return LAST_ERR_INVALID;
-  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_keep_h, mode);
+  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_keep_h, mode, true, Dv);
   size_t need = diverse_select_workspace(R, cu_vis_h, Dv, fdtype, mode);
   if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
   size_t used = 0;

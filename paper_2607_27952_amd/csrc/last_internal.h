@@ -144,6 +144,13 @@ struct alignas(16) TileMeta {
 };
 static_assert(sizeof(TileMeta) == 32, "two 16-byte pieces");
 
+// Ragged batches: the requests in decreasing size (their ranks) are split into
+// at most kMaxGroups groups. The off-diagonal Gram runs group by group, and a
+// group's greedy runs on a side stream beside the Gram of the later groups.
+// Three groups: with the caller's stream they use four hardware queues, the
+// default number per process; more streams would share queues and serialise.
+constexpr int kMaxGroups = 3;
+constexpr int kRankMaxR = 1024;   // larger batches keep the natural order, one group
 struct SelectPlan {
   int64_t N_total, K_total;
   int32_t N_max, K_max;
@@ -152,6 +159,12 @@ struct SelectPlan {
   int64_t d_elems;         // sum of cov_elems(N_r) (coverage matrices)
   int32_t threads, ept;    // top-k block shape
   int32_t g_threads, g_ept;  // greedy block shape
+  int32_t groups;          // 1: the whole Gram, then every greedy
+  bool ranked;             // off-diagonal tiles listed in rank order (groups > 1)
+  int32_t reserve;         // compute units the Gram leaves to concurrent greedies
+  int64_t group_tile0[kMaxGroups + 1];  // off-diagonal tile range of each group
+  int32_t group_rank0[kMaxGroups + 1];  // rank range of each group
+  int32_t group_threads[kMaxGroups], group_ept[kMaxGroups];  // greedy shape per group
 };
 
 struct SelectWs {
@@ -161,10 +174,14 @@ struct SelectWs {
   double *nn, *inv;                // [N_total + 128] squared feature norms and 1 / norm
                                    // (the tail lets a tile read 128 entries from any row)
   float *dmat;                     // coverage distances, tile-major per request (cov_index)
+  int32_t *req_order;              // [R] the request of each rank (ranked plans)
 };
 
+// allow_groups: a single diverse_select call may pipeline a ragged batch (the
+// two-call form keeps one group, so both of its calls see the same plan); Dv
+// enters only that schedule's cost model.
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,
-                            last_sel_mode mode);
+                            last_sel_mode mode, bool allow_groups = false, int32_t Dv = 0);
 SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode mode,
                          size_t *bytes);
 hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode mode,

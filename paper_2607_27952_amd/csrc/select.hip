@@ -79,11 +79,18 @@ __device__ void block_excl_scan_i64(int64_t v, int64_t *sh, int64_t *total, int6
 // Per request: nb = ceil(N / 128) row blocks give nb diagonal Gram tiles and
 // nb (nb - 1) / 2 tiles above the diagonal; the coverage matrix (nb x nb
 // tiles of 128 x 128) starts at d_off.
-__global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__ cu_vis, int R,
+//
+// ranked (R <= kRankMaxR): the off-diagonal tiles are listed request by request
+// in decreasing size (ties: lower index first), rank k being request
+// req_order[k], so that a ragged batch's largest requests finish their Gram
+// first; otherwise in request order.
+__global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__ cu_vis, int R, int ranked,
                                                      int32_t *__restrict__ dtile_off,
                                                      int32_t *__restrict__ otile_off,
-                                                     int64_t *__restrict__ d_off) {
+                                                     int64_t *__restrict__ d_off,
+                                                     int32_t *__restrict__ req_order) {
   __shared__ int64_t sh[4];
+  __shared__ int32_t s_n[last::kRankMaxR], s_ord[last::kRankMaxR];
   int64_t carry_d = 0, carry_o = 0, carry_m = 0;
   for (int base = 0; base < R; base += 256) {
     const int r = base + (int)threadIdx.x;
@@ -103,7 +110,7 @@ __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__
     pm += carry_m;
     if (r < R) {
       dtile_off[r] = (int32_t)pd;
-      otile_off[r] = (int32_t)po;
+      if (!ranked) otile_off[r] = (int32_t)po;
       d_off[r] = pm;
     }
     carry_d += td;
@@ -114,6 +121,33 @@ __global__ __launch_bounds__(256) void k_select_plan(const int32_t *__restrict__
     dtile_off[R] = (int32_t)carry_d;
     otile_off[R] = (int32_t)carry_o;
     d_off[R] = carry_m;
+  }
+  if (!ranked) return;
+  // rank of r: the requests larger than r, and the equal ones before it
+  for (int r = threadIdx.x; r < R; r += 256) s_n[r] = cu_vis[r + 1] - cu_vis[r];
+  __syncthreads();
+  for (int r = threadIdx.x; r < R; r += 256) {
+    const int n = s_n[r];
+    int rank = 0;
+    for (int q = 0; q < R; ++q) rank += (s_n[q] > n) || (s_n[q] == n && q < r);
+    s_ord[rank] = r;
+  }
+  __syncthreads();
+  carry_o = 0;
+  for (int base = 0; base < R; base += 256) {
+    const int k = base + (int)threadIdx.x;
+    int64_t no = 0;
+    if (k < R) {
+      const int64_t nd = (s_n[s_ord[k]] + kTile - 1) / kTile;
+      no = nd * (nd - 1) / 2;
+    }
+    int64_t to, po;
+    block_excl_scan_i64(no, sh, &to, &po);
+    if (k < R) {
+      otile_off[s_ord[k]] = (int32_t)(po + carry_o);
+      req_order[k] = s_ord[k];
+    }
+    carry_o += to;
   }
 }
 
@@ -155,7 +189,8 @@ __global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ c
     m.pad = 0;
     return m;
   };
-  const int64_t o1 = min((int64_t)otile_off[r + 1], off_cap);
+  const int nbr = (N + kTile - 1) / kTile;
+  const int64_t o1 = min((int64_t)otile_off[r] + (int64_t)nbr * (nbr - 1) / 2, off_cap);
   // Diagonal tiles: the first nb - 1 row blocks of every request in request
   // order, then the last row block of every request (it may be partial), so
   // that a grid-stride walk meets the full tiles first.
@@ -1017,19 +1052,21 @@ __device__ void compact_ascending(Flag flag, int32_t *dst, int *sh) {
 // ascending index order; the block then takes the maximum 64-bit key
 // (objective bits, ~index), which orders by objective and breaks ties towards
 // the lowest index (objectives are >= 0 here, so their bits order like them).
+// req_order (nullable): block b takes the request of rank rank0 + b.
 template <int EPT, int NTH>
 __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores,
                                                 const float *__restrict__ dmat,
                                                 const int64_t *__restrict__ d_off,
                                                 const int32_t *__restrict__ cu_vis,
                                                 const int32_t *__restrict__ cu_keep,
+                                                const int32_t *__restrict__ req_order, int rank0,
                                                 int32_t *__restrict__ kept,
                                                 int32_t *__restrict__ order,
                                                 float *__restrict__ gains) {
   constexpr int kNW = NTH / 64;
   __shared__ unsigned long long s_key[2][kNW];
   __shared__ int s_cnt[16];
-  const int r = blockIdx.x;
+  const int r = req_order ? req_order[rank0 + (int)blockIdx.x] : (int)blockIdx.x;
   const int64_t n0 = cu_vis[r];
   const int N = cu_vis[r + 1] - (int)n0;
   const int64_t k0 = cu_keep[r];
@@ -1286,9 +1323,29 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
 
 namespace last {
 
+// Greedy block shape for requests of up to n tokens: one wave up to 1024
+// tokens (no block barrier per step), else 256, 512 or 1024 threads with up to
+// 32 tokens each.
+static void greedy_shape(int32_t n, int32_t *threads, int32_t *ept) {
+  if (n <= 1024) {
+    *threads = 64;
+    const int e = (n + 63) / 64;
+    *ept = e <= 2 ? 2 : e <= 4 ? 4 : e <= 6 ? 6 : e <= 8 ? 8 : e <= 10 ? e : e <= 12 ? 12 : e <= 14 ? 14 : 16;
+  } else if (n <= 8192) {
+    *threads = 256;
+    const int e = (n + 255) / 256;
+    *ept = e <= 8 ? 8 : e <= 16 ? 16 : 32;
+  } else if (n <= 16384) {
+    *threads = 512;   // 32 tokens a thread
+    *ept = 32;
+  } else {
+    *threads = 1024;  // up to kSelMaxN = 32768 tokens, 32 a thread
+    *ept = 32;
+  }
+}
+
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,
-                            last_sel_mode mode) {
-  (void)mode;
+                            last_sel_mode mode, bool allow_groups, int32_t Dv) {
   SelectPlan p{};
   p.N_total = cu_vis_h[R];
   p.K_total = cu_keep_h[R];
@@ -1305,23 +1362,137 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   p.threads = p.N_max > 1024 ? 1024 : std::max(64, (p.N_max + 63) / 64 * 64);
   const int ept = (p.N_max + p.threads - 1) / p.threads;
   p.ept = ept <= 1 ? 1 : ept <= 2 ? 2 : ept <= 4 ? 4 : ept <= 8 ? 8 : ept <= 16 ? 16 : 32;
-  // greedy: one wave up to 1024 tokens (no block barrier per step), else 256
-  // threads (one wave per SIMD) with up to 64 tokens each
-  if (p.N_max <= 1024) {
-    p.g_threads = 64;
-    const int e = (p.N_max + 63) / 64;
-    p.g_ept = e <= 2 ? 2 : e <= 4 ? 4 : e <= 6 ? 6 : e <= 8 ? 8 : e <= 10 ? e : e <= 12 ? 12 : e <= 14 ? 14 : 16;
-  } else if (p.N_max <= 8192) {
-    p.g_threads = 256;
-    const int e = (p.N_max + 255) / 256;
-    p.g_ept = e <= 8 ? 8 : e <= 16 ? 16 : 32;
-  } else if (p.N_max <= 16384) {
-    p.g_threads = 512;   // 32 tokens a thread
-    p.g_ept = 32;
-  } else {
-    p.g_threads = 1024;  // up to kSelMaxN = 32768 tokens, 32 a thread
-    p.g_ept = 32;
+  greedy_shape(p.N_max, &p.g_threads, &p.g_ept);
+  p.groups = 1;
+  p.group_tile0[0] = 0;
+  p.group_tile0[1] = p.tiles_off;
+  p.group_rank0[0] = 0;
+  p.group_rank0[1] = R;
+  p.group_threads[0] = p.g_threads;
+  p.group_ept[0] = p.g_ept;
+  if (!allow_groups || mode != LAST_SEL_KCENTER || R < 2 || R > kRankMaxR) return p;
+
+  // Ragged batches. A greedy takes about K_r (0.6 + 1.1e-4 N_r) microseconds
+  // on one compute unit (one dependent step per pick, each a coverage row of
+  // N_r floats), about 1.6 times that while the Gram loads the memory system
+  // (measured), and an off-diagonal Gram tile about 0.8 us per 64 columns of Dv
+  // plus 3 us on one compute unit. When the longest greedy is several times the
+  // median one, the requests are ordered by decreasing size and the
+  // off-diagonal Gram runs in groups; each group's greedies start, on side
+  // streams and on compute units the Gram leaves free, as soon as that group's
+  // Gram is done. The grouping (2 to kMaxGroups groups, with geometric or even
+  // tile shares) and the number of free compute units are chosen by simulating
+  // that schedule with these costs.
+  auto n_of = [&](int r) { return cu_vis_h[r + 1] - cu_vis_h[r]; };
+  auto k_of = [&](int r) { return cu_keep_h[r + 1] - cu_keep_h[r]; };
+  auto greedy_us = [&](int r) { return k_of(r) * (0.6 + 1.1e-4 * n_of(r)); };
+  std::vector<int32_t> ord(R);
+  std::vector<double> cost(R);
+  for (int r = 0; r < R; ++r) {
+    ord[r] = r;
+    cost[r] = greedy_us(r);
   }
+  std::vector<double> sorted_cost(cost);
+  std::nth_element(sorted_cost.begin(), sorted_cost.begin() + R / 2, sorted_cost.end());
+  const double median = sorted_cost[R / 2];
+  const double longest = *std::max_element(cost.begin(), cost.end());
+  if (!(longest >= 4.0 * median && longest >= 500.0) || p.tiles_off < 16 * 256) return p;
+  // the same order as k_select_plan: decreasing size, ties by index
+  std::sort(ord.begin(), ord.end(), [&](int a, int b) { return n_of(a) != n_of(b) ? n_of(a) > n_of(b) : a < b; });
+  std::vector<int64_t> cum(R + 1, 0);   // off-diagonal tiles of the first k ranks
+  for (int k = 0; k < R; ++k) {
+    const int64_t nb = (n_of(ord[k]) + kTile - 1) / kTile;
+    cum[k + 1] = cum[k] + nb * (nb - 1) / 2;
+  }
+  const int cus = device_cus();
+  const double tile_us = 0.8 * (Dv > 0 ? Dv : 1024) / 64.0 + 3.0;
+  struct Cand {
+    int G;
+    int32_t rank0[kMaxGroups + 1];
+    int reserve;
+    double span;
+  };
+  // group boundaries (ranks) for tile shares `frac` (cumulative, last 1)
+  auto split = [&](const double *frac, int G, Cand &c) {
+    c.G = 0;
+    c.rank0[0] = 0;
+    int k = 0;
+    for (int g = 0; g < G - 1; ++g) {
+      while (k < R - 1 && (double)cum[k + 1] < frac[g] * (double)cum[R]) ++k;
+      const int b = std::max(k + 1, c.rank0[c.G] + 1);
+      if (b >= R) break;
+      c.rank0[++c.G] = b;
+      k = b;
+    }
+    c.rank0[++c.G] = R;
+  };
+  // the schedule's length, and the free compute units its greedies need at once
+  auto simulate = [&](Cand &c) {
+    double best = 1e300;
+    for (int reserve : {8, 16, 24, 32, 48, 64}) {
+      const double rate = (cus - reserve) / tile_us;   // tiles per microsecond
+      double t = 0, span = 0;
+      std::vector<std::pair<double, double>> busy;      // greedy intervals
+      for (int g = 0; g < c.G; ++g) {
+        t += (double)(cum[c.rank0[g + 1]] - cum[c.rank0[g]]) / rate;
+        for (int k = c.rank0[g]; k < c.rank0[g + 1]; ++k) busy.push_back({t, t + 1.6 * cost[ord[k]]});
+      }
+      const double gram_end = t;
+      // concurrency before the Gram ends must fit the reserve; after it, every
+      // unit is free (a sweep over the interval ends)
+      std::vector<std::pair<double, int>> ev;
+      ev.reserve(2 * busy.size());
+      for (auto &x : busy) {
+        ev.push_back({x.first, +1});
+        ev.push_back({x.second, -1});
+      }
+      std::sort(ev.begin(), ev.end(), [](const std::pair<double, int> &a, const std::pair<double, int> &b) {
+        return a.first != b.first ? a.first < b.first : a.second < b.second;   // ends before starts
+      });
+      int peak = 0, now = 0;
+      for (auto &e : ev) {
+        if (e.first >= gram_end) break;
+        now += e.second;
+        peak = std::max(peak, now);
+      }
+      for (auto &x : busy) span = std::max(span, x.second);
+      span = std::max(span, gram_end);
+      if (peak > reserve) span += (double)(peak - reserve) / reserve * longest;   // queued greedies
+      if (span < best) {
+        best = span;
+        c.reserve = reserve;
+      }
+    }
+    c.span = best;
+  };
+  Cand best{};
+  best.span = 1e300;
+  for (int G = 2; G <= std::min<int>(kMaxGroups, R); ++G) {
+    for (int shape = 0; shape < 2; ++shape) {
+      double frac[kMaxGroups];
+      double tot = 0, x = 1;
+      for (int g = 0; g < G; ++g) {
+        tot += shape ? x : 1.0;
+        frac[g] = tot;
+        x *= 2;
+      }
+      for (int g = 0; g < G; ++g) frac[g] /= tot;
+      Cand c{};
+      split(frac, G, c);
+      if (c.G < 2) continue;
+      simulate(c);
+      if (c.span < best.span) best = c;
+    }
+  }
+  if (best.span >= 1e299) return p;
+  p.groups = best.G;
+  for (int g = 0; g <= p.groups; ++g) {
+    p.group_rank0[g] = best.rank0[g];
+    p.group_tile0[g] = cum[best.rank0[g]];
+  }
+  for (int x = 0; x < p.groups; ++x) greedy_shape(n_of(ord[p.group_rank0[x]]), &p.group_threads[x], &p.group_ept[x]);
+  p.ranked = true;
+  p.reserve = best.reserve;
   return p;
 }
 
@@ -1338,15 +1509,27 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
     w.nn = cv.take<double>(p.N_total + kTile);
     w.inv = cv.take<double>(p.N_total + kTile);
     w.dmat = cv.take<float>(p.d_elems);
+    w.req_order = cv.take<int32_t>(R);
   }
   *bytes = cv.size();
   return w;
 }
 
+static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t blocks, const int32_t *req_order,
+                                int32_t rank0, const SelectWs &w, const float *scores, const int32_t *cu_vis,
+                                const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
+                                hipStream_t s);
+static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, const SelectWs &w,
+                                   const float *scores, const void *feats, const int32_t *cu_vis,
+                                   const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
+                                   hipStream_t s);
+
 hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode mode,
                          const SelectPlan &p, const SelectWs &w, const float *scores,
                          const void *feats, const int32_t *cu_vis, const int32_t *cu_keep,
                          int32_t *kept, int32_t *order, float *gains, hipStream_t s) {
+  if (mode == LAST_SEL_KCENTER && p.groups > 1 && fdtype == LAST_BF16 && Dv % (4 * kDmaCols) == 0)
+    return launch_pipelined(R, Dv, p, w, scores, feats, cu_vis, cu_keep, kept, order, gains, s);
   if (mode == LAST_SEL_KCENTER) {
     const hipError_t e = launch_similarity(R, Dv, fdtype, p, w, feats, cu_vis, s);
     if (e != hipSuccess) return e;
@@ -1373,12 +1556,21 @@ hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const
     return launch_end(s);
   }
 
+  return launch_greedy(p.g_threads, p.g_ept, R, nullptr, 0, w, scores, cu_vis, cu_keep, kept, order, gains, s);
+}
+
+// One greedy launch: `blocks` requests (ranks rank0 .. rank0 + blocks - 1 of
+// req_order, or requests 0 .. blocks - 1 when req_order is null).
+static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t blocks, const int32_t *req_order,
+                                int32_t rank0, const SelectWs &w, const float *scores, const int32_t *cu_vis,
+                                const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
+                                hipStream_t s) {
   launch_begin("greedy", s);
 #define LAST_GREEDY(E, T)                                                                          \
-  hipLaunchKernelGGL((k_greedy<E, T>), dim3(R), dim3(T), 0, s, scores, w.dmat, w.d_off, cu_vis, cu_keep, \
-                     kept, order, gains)
-  if (p.g_threads == 64) {
-    switch (p.g_ept) {
+  hipLaunchKernelGGL((k_greedy<E, T>), dim3(blocks), dim3(T), 0, s, scores, w.dmat, w.d_off, cu_vis, cu_keep, \
+                     req_order, rank0, kept, order, gains)
+  if (threads == 64) {
+    switch (ept) {
       case 2: LAST_GREEDY(2, 64); break;
       case 4: LAST_GREEDY(4, 64); break;
       case 6: LAST_GREEDY(6, 64); break;
@@ -1389,13 +1581,13 @@ hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const
       case 14: LAST_GREEDY(14, 64); break;
       default: LAST_GREEDY(16, 64); break;
     }
-  } else if (p.g_threads == 256) {
-    switch (p.g_ept) {
+  } else if (threads == 256) {
+    switch (ept) {
       case 8: LAST_GREEDY(8, 256); break;
       case 16: LAST_GREEDY(16, 256); break;
       default: LAST_GREEDY(32, 256); break;
     }
-  } else if (p.g_threads == 512) {
+  } else if (threads == 512) {
     LAST_GREEDY(32, 512);
   } else {
     LAST_GREEDY(32, 1024);
@@ -1409,7 +1601,8 @@ hipError_t launch_similarity(int32_t R, int32_t Dv, last_dtype fdtype, const Sel
                              hipStream_t s) {
   hipError_t e;
   launch_begin("select_plan", s);
-  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, w.dtile_off, w.otile_off, w.d_off);
+  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, p.ranked ? 1 : 0, w.dtile_off, w.otile_off,
+                     w.d_off, w.req_order);
   hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, cu_vis, w.dtile_off, w.otile_off, w.d_off,
                      p.tiles_diag, p.tiles_off, w.dtile, w.otile);
   if ((e = launch_end(s)) != hipSuccess) return e;
@@ -1450,6 +1643,89 @@ hipError_t launch_similarity(int32_t R, int32_t Dv, last_dtype fdtype, const Sel
                        p.d_elems, w.dmat);
     if ((e = launch_end(s)) != hipSuccess) return e;
   }
+  return hipSuccess;
+}
+
+// Library-owned streams per host thread and device, one per group, for the
+// greedies that run beside the Gram of a ragged batch, with their events
+// (reused call after call: a wait takes the event's latest record at the time
+// it is enqueued). Created on first use, default priority, kept until the
+// process ends.
+namespace {
+struct SideStream {
+  hipStream_t s[kMaxGroups] = {};      // group g's greedies run on s[g]
+  hipEvent_t gram[kMaxGroups] = {};    // group g's Gram done (recorded on the caller's stream)
+  hipEvent_t done[kMaxGroups] = {};    // group g's greedies done
+  bool ok = false;
+};
+constexpr int kSideDevices = 64;
+thread_local SideStream t_side[kSideDevices];
+
+SideStream *side_stream() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kSideDevices) return nullptr;
+  SideStream &x = t_side[dev];
+  if (!x.ok) {
+    for (int g = 0; g < kMaxGroups; ++g) {
+      if (!x.s[g] && hipStreamCreateWithFlags(&x.s[g], hipStreamNonBlocking) != hipSuccess) return nullptr;
+      if (!x.gram[g] && hipEventCreateWithFlags(&x.gram[g], hipEventDisableTiming) != hipSuccess) return nullptr;
+      if (!x.done[g] && hipEventCreateWithFlags(&x.done[g], hipEventDisableTiming) != hipSuccess) return nullptr;
+    }
+    x.ok = true;
+  }
+  return &x;
+}
+}  // namespace
+
+// Ragged k-center: the plan (off-diagonal tiles in rank order) and every
+// diagonal tile, then the off-diagonal Gram group by group on `s`, each group's
+// greedies on its own side stream once that group's Gram is done, beside the
+// next groups' Gram. The Gram's persistent grid leaves p.reserve compute units
+// free for them. `s` waits for every side stream at the end.
+static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, const SelectWs &w,
+                                   const float *scores, const void *feats, const int32_t *cu_vis,
+                                   const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
+                                   hipStream_t s) {
+  SideStream *side = side_stream();
+  if (!side) {   // no side stream: the whole Gram, then every greedy, on `s`
+    SelectPlan q = p;
+    q.groups = 1;
+    hipError_t e = launch_similarity(R, Dv, LAST_BF16, q, w, feats, cu_vis, s);
+    if (e != hipSuccess) return e;
+    return launch_greedy(p.g_threads, p.g_ept, R, p.ranked ? w.req_order : nullptr, 0, w, scores, cu_vis, cu_keep,
+                         kept, order, gains, s);
+  }
+  hipError_t e;
+  launch_begin("select_plan", s);
+  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, 1, w.dtile_off, w.otile_off, w.d_off,
+                     w.req_order);
+  hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, cu_vis, w.dtile_off, w.otile_off, w.d_off,
+                     p.tiles_diag, p.tiles_off, w.dtile, w.otile);
+  if ((e = launch_end(s)) != hipSuccess) return e;
+  const int cus = device_cus();
+  launch_begin("gram_diag", s);
+  hipLaunchKernelGGL(k_gram_bf16<true>, dim3((unsigned)persistent_grid(p.tiles_diag, cus)), dim3(kGramThreads), 0,
+                     s, (const uint16_t *)feats, w.dtile, w.nn, w.inv, Dv, p.tiles_diag, p.d_elems, w.dmat);
+  if ((e = launch_end(s)) != hipSuccess) return e;
+  const int gram_cus = std::max(8, cus - p.reserve);
+  for (int g = 0; g < p.groups; ++g) {
+    const int64_t t0 = p.group_tile0[g], nt = p.group_tile0[g + 1] - t0;
+    if (nt > 0) {
+      launch_begin("gram", s);
+      hipLaunchKernelGGL(k_gram_bf16<false>, dim3((unsigned)persistent_grid(nt, gram_cus)), dim3(kGramThreads), 0,
+                         s, (const uint16_t *)feats, w.otile + t0, w.nn, w.inv, Dv, nt, p.d_elems, w.dmat);
+      if ((e = launch_end(s)) != hipSuccess) return e;
+    }
+    if ((e = hipEventRecord(side->gram[g], s)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side->s[g], side->gram[g], 0)) != hipSuccess) return e;
+    const int32_t r0 = p.group_rank0[g], nr = p.group_rank0[g + 1] - r0;
+    e = launch_greedy(p.group_threads[g], p.group_ept[g], nr, w.req_order, r0, w, scores, cu_vis, cu_keep, kept,
+                      order, gains, side->s[g]);
+    if (e != hipSuccess) return e;
+    if ((e = hipEventRecord(side->done[g], side->s[g])) != hipSuccess) return e;
+  }
+  for (int g = 0; g < p.groups; ++g)
+    if ((e = hipStreamWaitEvent(s, side->done[g], 0)) != hipSuccess) return e;
   return hipSuccess;
 }
 

@@ -492,3 +492,33 @@ def test_two_host_threads_two_streams(profile):
     if profile:
         prof = last.profile_collect()
         assert prof.get("score_stream", (0, 0))[0] >= 12 and prof.get("gather", (0, 0))[0] >= 12
+
+
+def test_ragged_batch_pipelined_greedy():
+    """A ragged batch (two long requests among short ones) takes the pipelined
+    schedule: the off-diagonal Gram in groups of decreasing request size, each
+    group's greedy on a side stream beside the later groups' Gram. The result is
+    bit-identical to the two-call form (the whole Gram, then every greedy) and
+    passes the oracle replay."""
+    sizes = [700, 12000, 500, 9000, 400, 600, 300, 650]
+    rng = np.random.default_rng(91)
+    R, Dv = len(sizes), 256
+    cu_vis = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    cu_keep = np.concatenate([[0], np.cumsum([(n + 7) // 8 for n in sizes])]).astype(np.int32)
+    # a 24-component mixture like the workloads': unit-norm centres, noise of norm 0.3
+    centres = rng.standard_normal((24, Dv)).astype(np.float32)
+    centres /= np.linalg.norm(centres, axis=1, keepdims=True)
+    X = (centres[rng.integers(0, 24, size=int(cu_vis[-1]))] + 0.3 / np.sqrt(Dv) * rng.standard_normal(
+        (int(cu_vis[-1]), Dv))).astype(np.float32)
+    w32 = np.concatenate([rng.dirichlet(np.ones(n) * 0.7) for n in sizes]).astype(np.float32)
+    feats_bits = W.to_bf16_bits(X)
+    feats = last.to_torch(feats_bits, W.BF16, "cuda")
+    st = torch.from_numpy(w32).cuda()
+    one = gpu_select(feats, st, cu_vis, cu_keep)
+    _, kept, order, gains = _two_phase(feats, cu_vis, cu_keep, lambda: st)
+    for x, y in zip(one, (kept, order, gains)):
+        assert x.tobytes() == y.tobytes()
+    wl = W.Workload(name="ragged", R=R, G=1, Hq=1, Hkv=1, Dh=64, qk_dtype=W.F32, scale=0.125,
+                    cu_seqlens=cu_vis + np.arange(R + 1, dtype=np.int32), vis_start=np.zeros(R, np.int32),
+                    cu_vis=cu_vis, q=None, k=None, Dv=Dv, f_dtype=W.BF16, feats=feats_bits, cu_keep=cu_keep)
+    check_selection(wl, w32, one[0], one[1], "ragged pipelined batch")
