@@ -194,6 +194,16 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
 hipError_t launch_similarity(int32_t R, int32_t Dv, last_dtype fdtype, const SelectPlan &p,
                              const SelectWs &w, const void *feats, const int32_t *cu_vis,
                              hipStream_t s);
+// The pieces of launch_similarity for the bf16 matrix-core path (gram.hip):
+// the plan, every diagonal tile (with the norms), and off-diagonal tiles
+// [t0, t0 + nt) of the list on a persistent grid for `cus` compute units.
+bool gram_streamed(last_dtype fdtype, int32_t Dv);
+hipError_t launch_gram_plan(int32_t R, const SelectPlan &p, const SelectWs &w, const int32_t *cu_vis,
+                            hipStream_t s);
+hipError_t launch_gram_diag(int32_t Dv, const SelectPlan &p, const SelectWs &w, const void *feats, int cus,
+                            hipStream_t s);
+hipError_t launch_gram_off(int32_t Dv, const SelectPlan &p, const SelectWs &w, const void *feats, int64_t t0,
+                           int64_t nt, int cus, hipStream_t s);
 hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const SelectWs &w,
                        const float *scores, const int32_t *cu_vis, const int32_t *cu_keep,
                        int32_t *kept, int32_t *order, float *gains, hipStream_t s);
