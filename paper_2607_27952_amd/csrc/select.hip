@@ -533,10 +533,12 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
   return w;
 }
 
+// `what` names the launch for the kernel timing ("greedy", or "greedy_side" for
+// a launch on a side stream, which overlaps the Gram).
 static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t blocks, const int32_t *req_order,
                                 int32_t rank0, const SelectWs &w, const float *scores, const int32_t *cu_vis,
                                 const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
-                                hipStream_t s);
+                                hipStream_t s, const char *what = "greedy");
 static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, const SelectWs &w,
                                    const float *scores, const void *feats, const int32_t *cu_vis,
                                    const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
@@ -582,8 +584,8 @@ hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const
 static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t blocks, const int32_t *req_order,
                                 int32_t rank0, const SelectWs &w, const float *scores, const int32_t *cu_vis,
                                 const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
-                                hipStream_t s) {
-  launch_begin("greedy", s);
+                                hipStream_t s, const char *what) {
+  launch_begin(what, s);
 #define LAST_GREEDY(E, T)                                                                          \
   hipLaunchKernelGGL((k_greedy<E, T>), dim3(blocks), dim3(T), 0, s, scores, w.dmat, w.d_off, cu_vis, cu_keep, \
                      req_order, rank0, kept, order, gains)
@@ -675,7 +677,7 @@ static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, c
     if ((e = hipStreamWaitEvent(side->s[g], side->gram[g], 0)) != hipSuccess) return e;
     const int32_t r0 = p.group_rank0[g], nr = p.group_rank0[g + 1] - r0;
     e = launch_greedy(p.group_threads[g], p.group_ept[g], nr, w.req_order, r0, w, scores, cu_vis, cu_keep, kept,
-                      order, gains, side->s[g]);
+                      order, gains, side->s[g], "greedy_side");
     if (e != hipSuccess) return e;
     if ((e = hipEventRecord(side->done[g], side->s[g])) != hipSuccess) return e;
   }
