@@ -123,6 +123,19 @@ int device_cus() {
   return v;
 }
 
+// Ticks per millisecond of the device's constant-rate wall clock (wall_clock64),
+// queried once per device.
+int64_t device_wall_khz() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 100000;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeWallClockRate, dev) != hipSuccess || v <= 0) v = 100000;
+  cache[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
+
 // ------------------------------------------------------------ validation
 static bool csr_ok(const int32_t *cu, int32_t R, int32_t min_len) {
   if (!cu || cu[0] != 0) return false;

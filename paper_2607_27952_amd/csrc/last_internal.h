@@ -22,6 +22,8 @@ void note_hip_error(hipError_t e);
 
 // Compute units of the current device (cached per device).
 int device_cus();
+// Ticks per millisecond of the current device's wall_clock64 (cached per device).
+int64_t device_wall_khz();
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
@@ -121,7 +123,9 @@ hipError_t launch_rows(const last_batch *b, const RowsPlan &p, const RowsWs &w,
 
 // ------------------------------------------------------------ selection
 constexpr int kGramTile = 128;       // Gram tile edge (rows of X per side)
-constexpr int kSelMaxN = 32768;      // largest request the register-resident greedy holds
+constexpr int kSelMaxN = 131072;     // largest request diverse_select takes
+constexpr int kGreedyMaxN = 32768;   // largest request one block's registers hold (k_greedy, k_topk)
+constexpr int kMcSlotWords = 256;    // exchange words per request of the multi-block greedy
 
 // A request's coverage matrix is stored as nb x nb tiles of 128 x 128 floats
 // (nb = ceil(N_r / 128)), tile (I, J) at element (I * nb + J) * 128 * 128 and
@@ -159,12 +163,14 @@ struct SelectPlan {
   int64_t d_elems;         // sum of cov_elems(N_r) (coverage matrices)
   int32_t threads, ept;    // top-k block shape
   int32_t g_threads, g_ept;  // greedy block shape
+  int32_t g_slices;        // > 0: blocks per request of the multi-block greedy (then g_ept is its EPT)
   int32_t groups;          // 1: the whole Gram, then every greedy
   bool ranked;             // off-diagonal tiles listed in rank order (groups > 1)
   int32_t reserve;         // compute units the Gram leaves to concurrent greedies
   int64_t group_tile0[kMaxGroups + 1];  // off-diagonal tile range of each group
   int32_t group_rank0[kMaxGroups + 1];  // rank range of each group
   int32_t group_threads[kMaxGroups], group_ept[kMaxGroups];  // greedy shape per group
+  int32_t group_slices[kMaxGroups];
 };
 
 struct SelectWs {
@@ -175,6 +181,7 @@ struct SelectWs {
                                    // (the tail lets a tile read 128 entries from any row)
   float *dmat;                     // coverage distances, tile-major per request (cov_index)
   int32_t *req_order;              // [R] the request of each rank (ranked plans)
+  unsigned long long *mc_slots;    // [R][kMcSlotWords] exchange words of the multi-block greedy, by rank
 };
 
 // allow_groups: a single diverse_select call may pipeline a ragged batch (the
@@ -314,6 +321,11 @@ __device__ __forceinline__ uint32_t lds_u32(const void *p) {
 // LDS it wrote.
 __device__ __forceinline__ void dma16(uint32_t lds, const void *base, uint32_t voff) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory");
+}
+// global_load_lds_dword: lane i's 4 bytes at base + voff land in LDS at
+// lds + 4 i (same conventions as dma16).
+__device__ __forceinline__ void dma4(uint32_t lds, const void *base, uint32_t voff) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(lds), "v"(voff), "s"(base) : "memory");
 }
 // The same with the non-temporal hint: for data read exactly once, which
 // then streams past the caches instead of displacing lines others reuse.

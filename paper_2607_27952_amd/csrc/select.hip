@@ -38,9 +38,9 @@ __device__ __forceinline__ unsigned long long obj_key(float o, int i) {
 __device__ __forceinline__ float clean_score(float w) { return w > 0.f ? w : 0.f; }  // NaN -> 0
 
 // Ascending compaction of flagged elements (element e of thread t is index
-// t + e * blockDim). Writes dst[rank] = index.
+// value0 + t + e * blockDim). Writes dst[rank] = index.
 template <int EPT, typename Flag>
-__device__ void compact_ascending(Flag flag, int32_t *dst, int *sh) {
+__device__ void compact_ascending(Flag flag, int32_t *dst, int *sh, int32_t value0 = 0) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   int base = 0;
 #pragma unroll
@@ -55,7 +55,7 @@ __device__ void compact_ascending(Flag flag, int32_t *dst, int *sh) {
       if (w < wave) before_wave += sh[w];
       tot += sh[w];
     }
-    if (f) dst[base + before_wave + before_lane] = (int32_t)(threadIdx.x + e * blockDim.x);
+    if (f) dst[base + before_wave + before_lane] = value0 + (int32_t)(threadIdx.x + e * blockDim.x);
     base += tot;
     __syncthreads();
   }
@@ -228,6 +228,281 @@ __global__ __launch_bounds__(NTH) void k_greedy(const float *__restrict__ scores
   __syncthreads();
   compact_ascending<EPT>([&](int e) { return sel[e]; }, kept + k0, s_cnt);
 }
+// The greedy of Eq. 9-11 over several compute units, for requests longer than
+// one block's registers hold. Request rb of the launch runs on S blocks of
+// kMcThreads; block s holds tokens [s SL, (s + 1) SL), SL = kMcThreads * EPT,
+// EPT a thread in registers. Every step each block folds its slice of the
+// newest pick's coverage row into delta, takes its slice's best (objective,
+// lowest index) and publishes it as a tagged 64-bit key in its slot of the
+// step's parity; wave 0 then polls the request's S slots until all carry this
+// step's tag and takes their maximum, the next pick, which every block of the
+// request so computes alike. Key: tag (bits 63-62) | objective bits (61-30) |
+// 2^30 - 1 - index (29-0); objectives are >= 0, so the maximum orders by
+// objective and breaks ties towards the lowest index, and a slice with nothing
+// left publishes the tag alone. The tag, step % 3 + 1, is never 0 (the slots
+// start zeroed) and tells a step from the one two steps earlier, the only
+// other content a slot of that parity can hold: a block cannot publish step
+// t + 2 before every block has published step t + 1, which each does only
+// after reading step t. An objective that is NaN (+inf relevance at distance
+// 0) counts as 0, as does relevance that is not > 0, as in the one-block
+// greedy. At the end the blocks exchange their pick counts the same way and
+// write their picks into `kept` at their offsets, in ascending order.
+//
+// The S blocks of a request must run at the same time: the host launches at
+// most a quarter of the blocks the device holds at once, so each request's
+// blocks are all resident as soon as other work leaves room. Every wait is
+// bounded by `limit` ticks of the constant-rate wall clock (the slots of the
+// launch's ranks are zeroed before it); a block that times out sets the
+// request's abort word, and every block that sees it, or times out itself,
+// fills the request's kept and order with -1 and its gains with NaN.
+constexpr int kMcThreads = 256;
+constexpr int kMcMaxS = 64;                // slices a request (one per lane of the polling wave)
+constexpr int kMcSlotWords = last::kMcSlotWords;  // per request: two step parities, the counts, the abort word
+static_assert(kMcSlotWords == 4 * kMcMaxS, "exchange words: two step parities, the counts, the abort word");
+
+__device__ __forceinline__ unsigned long long mc_key(unsigned tag, unsigned obits, int i) {
+  return ((unsigned long long)tag << 62) | ((unsigned long long)obits << 30) |
+         (unsigned long long)((1u << 30) - 1u - (unsigned)i);
+}
+
+__global__ __launch_bounds__(256) void k_zero_u64(unsigned long long *__restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) p[i] = 0ull;
+}
+
+template <int EPT>
+__global__ __launch_bounds__(kMcThreads) void k_greedy_mc(const float *__restrict__ scores,
+                                                          const float *__restrict__ dmat,
+                                                          const int64_t *__restrict__ d_off,
+                                                          const int32_t *__restrict__ cu_vis,
+                                                          const int32_t *__restrict__ cu_keep,
+                                                          const int32_t *__restrict__ req_order, int rank0, int nreq,
+                                                          int S,
+                                                          unsigned long long *__restrict__ slots, int64_t limit,
+                                                          int32_t *__restrict__ kept, int32_t *__restrict__ order,
+                                                          float *__restrict__ gains) {
+  constexpr int NTH = kMcThreads, kNW = NTH / 64, SL = NTH * EPT;
+  __shared__ unsigned long long s_key[2][kNW];
+  __shared__ unsigned long long s_pick, s_next;
+  __shared__ float s_pre[2][SL];   // this slice of two prefetched coverage rows
+  __shared__ int s_cnt[16];
+  __shared__ int s_abort;
+  // Workgroup b runs on XCD b % 8: the S blocks of a request share an XCD
+  // (request rb of the launch on XCD rb % 8), whose exchange is about a fifth
+  // faster than one spread over XCDs. Blocks past the last request exit.
+  const int xcd = (int)blockIdx.x % 8, kx = (int)blockIdx.x / 8;
+  const int rb = (kx / S) * 8 + xcd, sl = kx % S;
+  if (rb >= nreq) return;
+  const int r = req_order ? req_order[rank0 + rb] : rank0 + rb;
+  const int64_t n0 = cu_vis[r];
+  const int N = cu_vis[r + 1] - (int)n0;
+  const int64_t k0 = cu_keep[r];
+  const int K = cu_keep[r + 1] - (int)k0;
+  const float *D = dmat + d_off[r];
+  const int64_t nbr = cov_blocks(N);
+  unsigned long long *slot = slots + (int64_t)(rank0 + rb) * kMcSlotWords;
+  unsigned long long *abort_word = slot + 3 * kMcMaxS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int base = sl * SL;
+  if (tid == 0) s_abort = 0;
+
+  // tokens past N_r count as picked (delta -inf) and read element N_r - 1
+  int32_t coff[EPT];
+  float w[EPT], dl[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = min(base + tid + e * NTH, N - 1);
+    coff[e] = (int32_t)((i / kTile) * kCovTileElems + i % kTile);
+    const bool in = base + tid + e * NTH < N;
+    w[e] = in ? clean_score(scores[n0 + i]) : 0.f;
+    dl[e] = in ? INFINITY : -INFINITY;
+  }
+  auto block_max = [&](unsigned long long k, int t) {
+    unsigned long long key = wave_max_key((uint32_t)(k >> 32), (uint32_t)k);
+    if (lane == 0) s_key[t & 1][wave] = key;
+    __syncthreads();
+    key = s_key[t & 1][0];
+#pragma unroll
+    for (int wv = 1; wv < kNW; ++wv) {
+      const unsigned long long other = s_key[t & 1][wv];
+      key = other > key ? other : key;
+    }
+    return key;
+  };
+  // Wave 0: publish `mine` in slot `at + sl`, then wait until every slot
+  // at .. at + S - 1 carries `tag` in bits 63-62, or the abort word is set, or
+  // `limit` ticks pass (then set the abort word). Returns the slots' maximum
+  // (lanes >= S read as the tag alone) and the per-lane values in `v`.
+  auto publish_wait = [&](unsigned long long *at, unsigned long long mine, unsigned tag,
+                          unsigned long long &v) -> unsigned long long {
+    if (lane == 0) __hip_atomic_store(at + sl, mine, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long none = (unsigned long long)tag << 62;
+    const uint64_t t0 = wall_clock64();
+    for (;;) {
+      v = lane < S ? __hip_atomic_load(at + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : none;
+      if (__all((unsigned)(v >> 62) == tag)) break;
+      const unsigned long long ab = __hip_atomic_load(abort_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (ab != 0ull) {
+        if (lane == 0) s_abort = 1;
+        break;
+      }
+      if ((int64_t)(wall_clock64() - t0) > limit) {
+        if (lane == 0) {
+          __hip_atomic_store(abort_word, 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          s_abort = 1;
+        }
+        break;
+      }
+    }
+    return wave_max_key((uint32_t)(v >> 32), (uint32_t)v);
+  };
+  // the slice's best as a request-wide pick (block-uniform, after a barrier)
+  auto exchange = [&](const float (&o)[EPT], int t) -> unsigned long long {
+    float b0 = -1.f, b1 = -1.f;
+    int i0 = 0, i1 = 0;
+#pragma unroll
+    for (int e = 0; e < EPT; e += 2) {   // two chains, ascending index in each
+      if (o[e] > b0) {
+        b0 = o[e];
+        i0 = base + tid + e * NTH;
+      }
+      if (o[e + 1] > b1) {
+        b1 = o[e + 1];
+        i1 = base + tid + (e + 1) * NTH;
+      }
+    }
+    const bool take1 = b1 > b0 || (b1 == b0 && i1 < i0);
+    const float bo = take1 ? b1 : b0;
+    const int bi = take1 ? i1 : i0;
+    const unsigned long long lk =
+        block_max(bo >= 0.f ? ((unsigned long long)__float_as_uint(bo) << 32) | (0xFFFFFFFFu - (unsigned)bi) : 0ull, t);
+    if (wave == 0) {
+      const unsigned tag = (unsigned)(t % 3) + 1u;
+      const unsigned long long mine =
+          lk ? mc_key(tag, (unsigned)(lk >> 32), (int)(0xFFFFFFFFu - (unsigned)lk)) : (unsigned long long)tag << 62;
+      unsigned long long v;
+      const unsigned long long best = publish_wait(slot + (t & 1) * kMcMaxS, mine, tag, v);
+      // the runner-up: the best of the other slices' candidates
+      const unsigned long long v2 = v == best ? (unsigned long long)tag << 62 : v;
+      const unsigned long long next = wave_max_key((uint32_t)(v2 >> 32), (uint32_t)v2);
+      if (lane == 0) {
+        s_pick = best;
+        s_next = next;
+      }
+    }
+    __syncthreads();
+    return s_pick;
+  };
+  auto pick_of = [](unsigned long long k) { return (int)((1u << 30) - 1u - (unsigned)(k & ((1ull << 30) - 1ull))); };
+  auto gain_of = [](unsigned long long k) { return __uint_as_float((unsigned)(k >> 30)); };
+
+  // The runner-up of a step's exchange is usually the next step's pick. Its
+  // row (this slice of it) is copied into LDS straight away, into s_pre[t & 1]
+  // at step t, with one LDS-DMA load per token a thread, each wave filling the
+  // part its own threads read; if it is the pick, step t + 2 folds it from LDS
+  // instead of waiting on memory. pre[b]: the row in s_pre[b] (block-uniform),
+  // or -1; dma_t: the step whose exchange issued the newest copy.
+  int pre[2] = {-1, -1};
+  int dma_t = -2;
+  // this slice of row u into s_pre[b], each wave the tokens of its own threads
+  auto copy_row = [&](int u, int b) {
+    const float *urow = D + ((int64_t)(u / kTile) * nbr) * kCovTileElems + (u % kTile) * kTile;
+    const void *ub = uniform_ptr(urow);
+#pragma unroll
+    for (int e = 0; e < EPT; ++e)
+      dma4(__builtin_amdgcn_readfirstlane(lds_u32(&s_pre[b][e * NTH + wave * 64])), ub, (uint32_t)coff[e] * 4u);
+  };
+  auto prefetch = [&](int t) {
+    const unsigned long long nk = s_next;
+    const int u = (nk & ((1ull << 62) - 1ull)) != 0ull ? pick_of(nk) : -1;
+    pre[t & 1] = u;
+    if (u < 0) return;
+    dma_t = t;
+    copy_row(u, t & 1);
+  };
+
+  // t = 0: j_1 = argmax w (Eq. 9)
+  float o[EPT];
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) o[e] = dl[e] == -INFINITY ? -1.f : w[e];
+  unsigned long long pk = exchange(o, 0);
+  int j = pick_of(pk);
+  if (sl == 0 && tid == 0 && !s_abort) {
+    order[k0] = j;
+    gains[k0] = gain_of(pk);
+  }
+  if (!s_abort) prefetch(0);
+  for (int t = 1; t < K && !s_abort; ++t) {
+    // fold the last pick's coverage row into the running minimum (Eq. 10).
+    // The row always arrives through s_pre[t & 1]: copied at step t - 2 if the
+    // pick was that step's runner-up, else now. (Loading it into registers
+    // instead would leave the compiler, which does not see the copies, waiting
+    // for every load in flight on either path.)
+    if (pre[t & 1] != j) {
+      copy_row(j, t & 1);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    } else if (dma_t == t - 1) {
+      // the copy issued at step t - 1 (EPT loads a wave, the newest) may
+      // still be in flight; the older one has landed once at most EPT remain
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(EPT) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) o[e] = s_pre[t & 1][e * NTH + tid];
+#pragma unroll
+    for (int e = 0; e < EPT; ++e) {
+      dl[e] = fminf(dl[e], o[e]);
+      const float p = w[e] * dl[e];
+      o[e] = dl[e] == -INFINITY ? -1.f : (p == p ? p : 0.f);   // Eq. 11
+    }
+    pk = exchange(o, t);
+    // no slice had a candidate left (cannot happen for K_r <= N_r: coverage
+    // distances off the diagonal are never -inf); every block of the request
+    // sees the same key and stops
+    if ((pk & ((1ull << 62) - 1ull)) == 0ull) break;
+    j = pick_of(pk);
+    if (sl == 0 && tid == 0 && !s_abort) {
+      order[k0 + t] = j;
+      gains[k0 + t] = gain_of(pk);
+    }
+    if (!s_abort && t + 1 < K) prefetch(t);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // no LDS copy outlives the loop
+  // this slice's picks: marked by their own rows, and the last pick
+  bool sel[EPT];
+  int cnt = 0;
+#pragma unroll
+  for (int e = 0; e < EPT; ++e) {
+    const int i = base + tid + e * NTH;
+    sel[e] = i < N && (dl[e] == -INFINITY || i == j);
+    cnt += sel[e] ? 1 : 0;
+  }
+  for (int x = 1; x < 64; x <<= 1) cnt += __shfl_xor(cnt, x);
+  if (lane == 0) s_cnt[wave] = cnt;
+  __syncthreads();
+  if (wave == 0 && !s_abort) {
+    int tot = 0;
+    for (int wv = 0; wv < kNW; ++wv) tot += s_cnt[wv];
+    unsigned long long v;
+    publish_wait(slot + 2 * kMcMaxS, (1ull << 62) | (unsigned)tot, 1u, v);
+    int before = lane < sl ? (int)(v & 0xFFFFFFFFull) : 0;
+    for (int x = 1; x < 64; x <<= 1) before += __shfl_xor(before, x);
+    if (lane == 0) s_cnt[8] = before;
+  }
+  __syncthreads();
+  if (s_abort) {
+    for (int x = tid; x < K; x += NTH) {
+      kept[k0 + x] = -1;
+      order[k0 + x] = -1;
+      gains[k0 + x] = __builtin_nanf("");
+    }
+    return;
+  }
+  const int before = s_cnt[8];
+  __syncthreads();
+  compact_ascending<EPT>([&](int e) { return sel[e]; }, kept + k0 + before, s_cnt, base);
+}
+
 template <int EPT>
 __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
                                                const int32_t *__restrict__ cu_vis,
@@ -337,15 +612,138 @@ __global__ __launch_bounds__(1024) void k_topk(const float *__restrict__ scores,
   }
 }
 
+
+// Top-k (Table 5) for requests longer than one block's registers hold: one
+// block per request radix-selects the K largest scores as k_topk does, reading
+// the keys from memory on each of the four passes, then writes the kept tokens
+// in ascending order in rounds of one token a thread (threshold ties ranked by
+// index). The pick order is k_topk_rank's.
+__global__ __launch_bounds__(1024) void k_topk_large(const float *__restrict__ scores,
+                                                     const int32_t *__restrict__ cu_vis,
+                                                     const int32_t *__restrict__ cu_keep,
+                                                     int32_t *__restrict__ kept) {
+  __shared__ int hist[256];
+  __shared__ int s_cnt[2][16];
+  __shared__ unsigned s_prefix;
+  __shared__ int s_remaining;
+  const int r = blockIdx.x;
+  const int64_t n0 = cu_vis[r];
+  const int N = cu_vis[r + 1] - (int)n0;
+  const int64_t k0 = cu_keep[r];
+  const int K = cu_keep[r + 1] - (int)k0;
+  const int tid = threadIdx.x, nth = blockDim.x, lane = tid & 63, wave = tid >> 6, nw = nth >> 6;
+  auto key_at = [&](int i) { return __float_as_uint(clean_score(scores[n0 + i])); };
+  if (tid == 0) {
+    s_prefix = 0u;
+    s_remaining = K;
+  }
+  unsigned mask = 0u;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = tid; b < 256; b += nth) hist[b] = 0;
+    __syncthreads();
+    const unsigned prefix = s_prefix;
+    for (int i = tid; i < N; i += nth) {
+      const unsigned k = key_at(i);
+      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      int cum = 0, rem = s_remaining, d = 255;
+      for (; d > 0; --d) {
+        if (cum + hist[d] >= rem) break;
+        cum += hist[d];
+      }
+      s_remaining = rem - cum;
+      s_prefix = prefix | ((unsigned)d << shift);
+    }
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  const unsigned thr = s_prefix;
+  const int need = s_remaining;   // threshold-equal keys to take, lowest index first
+  // the rank of a flag among the round's earlier threads, and the round's total
+  auto count = [&](bool f, int buf, int &before, int &total) {
+    const unsigned long long m = __ballot(f);
+    if (lane == 0) s_cnt[buf][wave] = __popcll(m);
+    __syncthreads();
+    before = __popcll(m & ((1ull << lane) - 1ull));
+    total = 0;
+    for (int w = 0; w < nw; ++w) {
+      if (w < wave) before += s_cnt[buf][w];
+      total += s_cnt[buf][w];
+    }
+  };
+  int eq_seen = 0, out = 0;
+  for (int c = 0; c < N; c += nth) {
+    const int i = c + tid;
+    const unsigned k = i < N ? key_at(i) : 0u;
+    const bool eq = i < N && k == thr;
+    int eb, et, tb, tt;
+    count(eq, 0, eb, et);
+    const bool take = i < N && (k > thr || (eq && eq_seen + eb < need));
+    count(take, 1, tb, tt);
+    if (take) kept[k0 + out + tb] = i;
+    eq_seen += et;
+    out += tt;
+    __syncthreads();   // the counts are read before the next round rewrites them
+  }
+}
+
+// The pick order of Top-k: kept token i of request blockIdx.y goes to position
+// (number of kept tokens with a larger score, or an equal score and a lower
+// index), i.e. decreasing score, ties by index. Block x ranks kept slots
+// [1024 x, 1024 x + 1024) against all K_r, staged through LDS.
+__global__ __launch_bounds__(1024) void k_topk_rank(const float *__restrict__ scores,
+                                                    const int32_t *__restrict__ cu_vis,
+                                                    const int32_t *__restrict__ cu_keep,
+                                                    const int32_t *__restrict__ kept,
+                                                    int32_t *__restrict__ order, float *__restrict__ gains) {
+  constexpr int kStage = 4096;
+  __shared__ unsigned long long s_keys[kStage];
+  const int r = blockIdx.y;
+  const int64_t n0 = cu_vis[r];
+  const int64_t k0 = cu_keep[r];
+  const int K = cu_keep[r + 1] - (int)k0;
+  const int slot = (int)blockIdx.x * (int)blockDim.x + (int)threadIdx.x;
+  if ((int)blockIdx.x * (int)blockDim.x >= K) return;   // block-uniform
+  const int i = slot < K ? kept[k0 + slot] : 0;
+  const float sc = clean_score(scores[n0 + i]);
+  const unsigned long long mine = obj_key(sc, i);
+  int rank = 0;
+  for (int s0 = 0; s0 < K; s0 += kStage) {
+    const int ns = min(kStage, K - s0);
+    for (int x = threadIdx.x; x < ns; x += blockDim.x) {
+      const int ix = kept[k0 + s0 + x];
+      s_keys[x] = obj_key(clean_score(scores[n0 + ix]), ix);
+    }
+    __syncthreads();
+    for (int x = 0; x < ns; ++x) rank += s_keys[x] > mine ? 1 : 0;
+    __syncthreads();
+  }
+  if (slot < K) {
+    order[k0 + rank] = i;
+    gains[k0 + rank] = sc;
+  }
+}
+
 }  // namespace
 
 namespace last {
 
-// Greedy block shape for requests of up to n tokens: one wave up to 1024
+// Greedy block shape for requests of up to n tokens: beyond kMcMinN tokens, S
+// <= 16 blocks of kMcThreads (slices of 2048 tokens, 4096 past 32768, 8192
+// past 65536) that exchange their candidates every step; else one block a request: one wave up to 1024
 // tokens (no block barrier per step), else 256, 512 or 1024 threads with up to
 // 32 tokens each.
-static void greedy_shape(int32_t n, int32_t *threads, int32_t *ept) {
-  if (n <= 1024) {
+constexpr int kMcMinN = 16384;
+static_assert(kMcMinN <= kGreedyMaxN, "one block holds every request below the multi-block greedy");
+static void greedy_shape(int32_t n, int32_t *threads, int32_t *ept, int32_t *slices) {
+  *slices = 0;
+  if (n > kMcMinN) {
+    *threads = kMcThreads;
+    *ept = n <= 32768 ? 8 : n <= 65536 ? 16 : 32;
+    *slices = (n + kMcThreads * *ept - 1) / (kMcThreads * *ept);
+  } else if (n <= 1024) {
     *threads = 64;
     const int e = (n + 63) / 64;
     *ept = e <= 2 ? 2 : e <= 4 ? 4 : e <= 6 ? 6 : e <= 8 ? 8 : e <= 10 ? e : e <= 12 ? 12 : e <= 14 ? 14 : 16;
@@ -357,7 +755,7 @@ static void greedy_shape(int32_t n, int32_t *threads, int32_t *ept) {
     *threads = 512;   // 32 tokens a thread
     *ept = 32;
   } else {
-    *threads = 1024;  // up to kSelMaxN = 32768 tokens, 32 a thread
+    *threads = 1024;  // up to kGreedyMaxN tokens, 32 a thread
     *ept = 32;
   }
 }
@@ -380,7 +778,7 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   p.threads = p.N_max > 1024 ? 1024 : std::max(64, (p.N_max + 63) / 64 * 64);
   const int ept = (p.N_max + p.threads - 1) / p.threads;
   p.ept = ept <= 1 ? 1 : ept <= 2 ? 2 : ept <= 4 ? 4 : ept <= 8 ? 8 : ept <= 16 ? 16 : 32;
-  greedy_shape(p.N_max, &p.g_threads, &p.g_ept);
+  greedy_shape(p.N_max, &p.g_threads, &p.g_ept, &p.g_slices);
   p.groups = 1;
   p.group_tile0[0] = 0;
   p.group_tile0[1] = p.tiles_off;
@@ -388,6 +786,7 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   p.group_rank0[1] = R;
   p.group_threads[0] = p.g_threads;
   p.group_ept[0] = p.g_ept;
+  p.group_slices[0] = p.g_slices;
   if (!allow_groups || mode != LAST_SEL_KCENTER || R < 2 || R > kRankMaxR) return p;
 
   // Ragged batches. A greedy takes about K_r (0.6 + 1.1e-4 N_r) microseconds
@@ -508,7 +907,8 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
     p.group_rank0[g] = best.rank0[g];
     p.group_tile0[g] = cum[best.rank0[g]];
   }
-  for (int x = 0; x < p.groups; ++x) greedy_shape(n_of(ord[p.group_rank0[x]]), &p.group_threads[x], &p.group_ept[x]);
+  for (int x = 0; x < p.groups; ++x)
+    greedy_shape(n_of(ord[p.group_rank0[x]]), &p.group_threads[x], &p.group_ept[x], &p.group_slices[x]);
   p.ranked = true;
   p.reserve = best.reserve;
   return p;
@@ -528,6 +928,7 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
     w.inv = cv.take<double>(p.N_total + kTile);
     w.dmat = cv.take<float>(p.d_elems);
     w.req_order = cv.take<int32_t>(R);
+    w.mc_slots = cv.take<unsigned long long>((int64_t)R * kMcSlotWords);
   }
   *bytes = cv.size();
   return w;
@@ -535,10 +936,10 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
 
 // `what` names the launch for the kernel timing ("greedy", or "greedy_side" for
 // a launch on a side stream, which overlaps the Gram).
-static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t blocks, const int32_t *req_order,
-                                int32_t rank0, const SelectWs &w, const float *scores, const int32_t *cu_vis,
-                                const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
-                                hipStream_t s, const char *what = "greedy");
+static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t slices, int32_t blocks,
+                                const int32_t *req_order, int32_t rank0, const SelectWs &w, const float *scores,
+                                const int32_t *cu_vis, const int32_t *cu_keep, int32_t *kept, int32_t *order,
+                                float *gains, hipStream_t s, const char *what = "greedy");
 static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, const SelectWs &w,
                                    const float *scores, const void *feats, const int32_t *cu_vis,
                                    const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
@@ -560,6 +961,13 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
 hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const SelectWs &w,
                        const float *scores, const int32_t *cu_vis, const int32_t *cu_keep,
                        int32_t *kept, int32_t *order, float *gains, hipStream_t s) {
+  if (mode == LAST_SEL_TOPK && p.N_max > kGreedyMaxN) {
+    launch_begin("topk", s);
+    hipLaunchKernelGGL(k_topk_large, dim3(R), dim3(1024), 0, s, scores, cu_vis, cu_keep, kept);
+    hipLaunchKernelGGL(k_topk_rank, dim3((p.K_max + 1023) / 1024, R), dim3(1024), 0, s, scores, cu_vis, cu_keep, kept,
+                       order, gains);
+    return launch_end(s);
+  }
   if (mode == LAST_SEL_TOPK) {
     launch_begin("topk", s);
 #define LAST_TOPK(E) \
@@ -576,16 +984,72 @@ hipError_t launch_pick(int32_t R, last_sel_mode mode, const SelectPlan &p, const
     return launch_end(s);
   }
 
-  return launch_greedy(p.g_threads, p.g_ept, R, nullptr, 0, w, scores, cu_vis, cu_keep, kept, order, gains, s);
+  return launch_greedy(p.g_threads, p.g_ept, p.g_slices, R, nullptr, 0, w, scores, cu_vis, cu_keep, kept, order,
+                       gains, s);
+}
+
+// The blocks of k_greedy_mc<EPT> the current device holds at once.
+template <int EPT>
+static int mc_capacity() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v > 0) return v;
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_greedy_mc<EPT>, kMcThreads, 0) != hipSuccess ||
+      per_cu <= 0)
+    return 0;
+  v = per_cu * device_cus();
+  cache[dev].store(v, std::memory_order_relaxed);
+  return v;
+}
+
+// The multi-block greedy over `nreq` requests (ranks rank0 .. rank0 + nreq - 1),
+// in launches of at most as many blocks as the device holds at once, each after
+// zeroing its ranks' exchange words (a kernel, not a memset, so that a caller
+// may capture the sequence in a graph). A wait may last 10 s.
+template <int EPT>
+static hipError_t launch_mc(int32_t slices, int32_t nreq, const int32_t *req_order, int32_t rank0,
+                            const SelectWs &w, const float *scores, const int32_t *cu_vis, const int32_t *cu_keep,
+                            int32_t *kept, int32_t *order, float *gains, hipStream_t s) {
+  // A launch takes at most a quarter of what the device holds, so that as many
+  // such launches as the device has hardware queues (4) fit beside each other:
+  // a request's blocks never wait on blocks of another launch that in turn
+  // wait for room.
+  const int cap = mc_capacity<EPT>() / 4;
+  if (cap < slices) return hipErrorInvalidConfiguration;
+  const int per_launch = cap / slices;
+  const int64_t limit = device_wall_khz() * 10000;   // 10 s in wall-clock ticks
+  for (int32_t c = 0; c < nreq; c += per_launch) {
+    const int32_t n = std::min<int32_t>(per_launch, nreq - c);
+    unsigned long long *slots = w.mc_slots + (int64_t)(rank0 + c) * kMcSlotWords;
+    const int64_t words = (int64_t)n * kMcSlotWords;
+    hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)std::min<int64_t>((words + 255) / 256, 1024)), dim3(256), 0, s,
+                       slots, words);
+    hipLaunchKernelGGL(k_greedy_mc<EPT>, dim3(8 * slices * ((n + 7) / 8)), dim3(kMcThreads), 0, s, scores, w.dmat,
+                       w.d_off, cu_vis, cu_keep, req_order, rank0 + c, n, slices, w.mc_slots, limit, kept, order,
+                       gains);
+  }
+  return hipGetLastError();
 }
 
 // One greedy launch: `blocks` requests (ranks rank0 .. rank0 + blocks - 1 of
-// req_order, or requests 0 .. blocks - 1 when req_order is null).
-static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t blocks, const int32_t *req_order,
-                                int32_t rank0, const SelectWs &w, const float *scores, const int32_t *cu_vis,
-                                const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
-                                hipStream_t s, const char *what) {
+// req_order, or requests rank0 .. rank0 + blocks - 1 when req_order is null;
+// the one-block greedy takes rank0 = 0 there).
+static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t slices, int32_t blocks,
+                                const int32_t *req_order, int32_t rank0, const SelectWs &w, const float *scores,
+                                const int32_t *cu_vis, const int32_t *cu_keep, int32_t *kept, int32_t *order,
+                                float *gains, hipStream_t s, const char *what) {
   launch_begin(what, s);
+  if (slices > 0) {
+    const hipError_t e =
+        ept == 8    ? launch_mc<8>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains, s)
+        : ept == 16 ? launch_mc<16>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains, s)
+                    : launch_mc<32>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains, s);
+    const hipError_t e2 = launch_end(s);
+    return e != hipSuccess ? e : e2;
+  }
 #define LAST_GREEDY(E, T)                                                                          \
   hipLaunchKernelGGL((k_greedy<E, T>), dim3(blocks), dim3(T), 0, s, scores, w.dmat, w.d_off, cu_vis, cu_keep, \
                      req_order, rank0, kept, order, gains)
@@ -662,7 +1126,8 @@ static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, c
     q.groups = 1;
     hipError_t e = launch_similarity(R, Dv, LAST_BF16, q, w, feats, cu_vis, s);
     if (e != hipSuccess) return e;
-    return launch_greedy(p.g_threads, p.g_ept, R, p.ranked ? w.req_order : nullptr, 0, w, scores, cu_vis, cu_keep,
+    return launch_greedy(p.g_threads, p.g_ept, p.g_slices, R, p.ranked ? w.req_order : nullptr, 0, w, scores,
+                         cu_vis, cu_keep,
                          kept, order, gains, s);
   }
   hipError_t e;
@@ -676,7 +1141,8 @@ static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, c
     if ((e = hipEventRecord(side->gram[g], s)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(side->s[g], side->gram[g], 0)) != hipSuccess) return e;
     const int32_t r0 = p.group_rank0[g], nr = p.group_rank0[g + 1] - r0;
-    e = launch_greedy(p.group_threads[g], p.group_ept[g], nr, w.req_order, r0, w, scores, cu_vis, cu_keep, kept,
+    e = launch_greedy(p.group_threads[g], p.group_ept[g], p.group_slices[g], nr, w.req_order, r0, w, scores,
+                      cu_vis, cu_keep, kept,
                       order, gains, side->s[g], "greedy_side");
     if (e != hipSuccess) return e;
     if ((e = hipEventRecord(side->done[g], side->s[g])) != hipSuccess) return e;

@@ -161,7 +161,7 @@ def test_select_rejects_bad_budgets_and_shapes():
     assert _select_call([0, 10, 30], [0, 5, 6], mode=5) == E
     assert _select_call([0, 10, 30], [0, 5, 6], fdtype=3) == E
     U = last.LAST_ERR_UNSUPPORTED
-    assert _select_call([0, 32769], [0, 5]) == U                  # request larger than the greedy holds
+    assert _select_call([0, 131073], [0, 5]) == U                 # request beyond the largest selected
     assert _select_call([0, 10, 30], [0, 5, 6], Dv=60) == U       # bf16 rows not 16-byte multiples
     assert _select_call([0, 10, 30], [0, 5, 6], Dv=62, fdtype=last.LAST_F32) == U
 
@@ -204,7 +204,7 @@ def test_two_phase_select_rejects_what_diverse_select_rejects():
         assert _two_phase_call(ph, [0, 10, 10], [0, 5, 5]) == E        # N_r = 0
         assert _two_phase_call(ph, [0, 10, 30], [0, 5, 6], Dv=0) == E
         assert _two_phase_call(ph, [0, 10, 30], [0, 5, 6], fdtype=3) == E
-        assert _two_phase_call(ph, [0, 32769], [0, 5]) == U
+        assert _two_phase_call(ph, [0, 131073], [0, 5]) == U
         assert _two_phase_call(ph, [0, 10, 30], [0, 5, 6], Dv=60) == U
         cv = np.array([0, 100, 350], np.int32)
         need = last.lib().diverse_select_workspace(2, cv.ctypes.data, 64, last.LAST_BF16, last.KCENTER)

@@ -279,6 +279,87 @@ def test_select_largest_request():
     check_selection(wl, w32, kept, order, "N=32768")
 
 
+# Requests past 16384 tokens: the greedy on several compute units (slices of
+# 2048 tokens, of 4096 past 65536), one candidate exchange per step.
+MC_CASES = [
+    # seed, R, n_range, Dv, dtype, k_frac, comps
+    (50, 2, (32769, 40000), 32, W.BF16, 0.02, 16),   # 17-20 slices, ragged last slice
+    (51, 1, (63000, 65536), 16, W.BF16, 0.01, 24),   # up to 32 slices of 2048
+    (52, 1, (65537, 70000), 16, W.BF16, 0.01, 24),   # slices of 4096
+    (53, 2, (16385, 18000), 24, W.F32, 0.05, 12),    # fp32 features, 9 slices
+]
+
+
+@pytest.mark.parametrize("case", MC_CASES, ids=lambda c: f"mc{c[0]}")
+def test_select_parity_multiblock(case):
+    seed, R, nr, Dv, dt, kf, comps = case
+    wl = W.tiny(seed, R=R, n_range=nr, Dv=Dv, f_dtype=dt, k_frac=kf, comps=comps)
+    rng = np.random.default_rng(seed)
+    w32 = np.concatenate([rng.dirichlet(np.ones(wl.n(r)) * 0.7) for r in range(R)]).astype(np.float32)
+    dw = last.DeviceWorkload.upload(wl)
+    print(f"multi-block case {seed}: N = {np.diff(wl.cu_vis).tolist()}", flush=True)
+    kept, order, gains = gpu_select(dw.feats, torch.from_numpy(w32).cuda(), wl.cu_vis, wl.cu_keep)
+    check_selection(wl, w32, kept, order, f"case {seed}")
+    # gains against the oracle's fp64 objective of the same picks: 1e-6 relative
+    # plus w * 2^-20 (the cosine's fp32 partial sums)
+    obj = oracle.replay(R, wl.Dv, w32, wl.feats, wl.cu_vis, wl.cu_keep, order, _fd(wl.f_dtype),
+                        rel_tol=TIE_RTOL, want_objective=True)[2]
+    wpick = np.concatenate([w32[wl.cu_vis[r] + order[wl.cu_keep[r]:wl.cu_keep[r + 1]]] for r in range(R)])
+    gerr = np.abs(gains.astype(np.float64) - obj)
+    assert np.all(gerr <= 1e-6 * np.abs(obj) + 2.0 ** -20 * wpick.astype(np.float64)), f"gain off by {gerr.max():.3g}"
+
+
+def _select_batch(Xs, ws, Ks, dtype):
+    """Selection over handmade requests (feature rows Xs[r], relevance ws[r], budget Ks[r])."""
+    X = np.concatenate([np.asarray(x, np.float32) for x in Xs])
+    cu_vis = np.concatenate([[0], np.cumsum([len(x) for x in Xs])]).astype(np.int32)
+    cu_keep = np.concatenate([[0], np.cumsum(Ks)]).astype(np.int32)
+    R = len(Xs)
+    wl = W.Workload(name="hand", R=R, G=1, Hq=1, Hkv=1, Dh=64, qk_dtype=W.F32, scale=0.125,
+                    cu_seqlens=cu_vis + np.arange(R + 1, dtype=np.int32), vis_start=np.zeros(R, np.int32),
+                    cu_vis=cu_vis, q=None, k=None, Dv=X.shape[1], f_dtype=dtype,
+                    feats=W.to_bf16_bits(X) if dtype == W.BF16 else X, cu_keep=cu_keep)
+    w32 = np.concatenate([np.asarray(w, np.float32) for w in ws])
+    feats = last.to_torch(wl.feats, dtype, "cuda")
+    kept, order, gains = gpu_select(feats, torch.from_numpy(w32).cuda(), wl.cu_vis, wl.cu_keep)
+    return wl, w32, kept, order, gains
+
+
+@pytest.mark.parametrize("dtype", [W.F32, W.BF16])
+def test_select_mixed_batch_multiblock(dtype):
+    """One request past 16384 tokens puts the whole batch on the multi-block
+    greedy: a request of one token (every other slice empty), one of exactly
+    one slice, one kept whole (K = N, the last picks at objective 0), one with
+    a ragged last slice, and one of 40000 tokens, in one launch."""
+    rng = np.random.default_rng(54)
+    Dv = 32
+    centres = rng.standard_normal((20, Dv))
+    centres /= np.linalg.norm(centres, axis=1, keepdims=True)
+    sizes, Ks = [1, 2048, 600, 17000, 40000], [1, 100, 600, 170, 400]
+    Xs = [centres[rng.integers(0, 20, n)] + 0.3 / np.sqrt(Dv) * rng.standard_normal((n, Dv)) for n in sizes]
+    Xs[2][100:] = Xs[2][:500]   # duplicates, so that the whole-request budget reaches objective 0
+    ws = [rng.dirichlet(np.ones(n) * 0.7) for n in sizes]
+    wl, w32, kept, order, gains = _select_batch(Xs, ws, Ks, dtype)
+    check_selection(wl, w32, kept, order, "mixed multi-block batch")
+    assert list(kept[:1]) == [0] and list(order[:1]) == [0] and gains[0] == w32[0]
+    a = wl.cu_keep[2]
+    assert sorted(order[a:a + 600]) == list(range(600)) and gains[a + 599] == 0.0
+
+
+def test_select_largest_request_multiblock():
+    """A request of 131072 tokens, the largest diverse_select takes (32 slices
+    of 4096; 69 GB of coverage distances)."""
+    rng = np.random.default_rng(55)
+    N, Dv = 131072, 8
+    centres = rng.standard_normal((32, Dv))
+    centres /= np.linalg.norm(centres, axis=1, keepdims=True)
+    X = centres[rng.integers(0, 32, N)] + 0.3 / np.sqrt(Dv) * rng.standard_normal((N, Dv))
+    print("N = 131072", flush=True)
+    wl, w32, kept, order, _ = _select_batch([X], [rng.dirichlet(np.ones(N) * 0.5)], [256], W.BF16)
+    check_selection(wl, w32, kept, order, "N=131072")
+    torch.cuda.empty_cache()
+
+
 def test_select_deterministic():
     wl = W.tiny(31, R=3, n_range=(400, 1200), Dv=512, k_frac=0.2, comps=12)
     w32 = np.random.default_rng(1).dirichlet(np.ones(wl.N_total)).astype(np.float32)
@@ -290,7 +371,8 @@ def test_select_deterministic():
         assert x.tobytes() == y.tobytes()
 
 
-@pytest.mark.parametrize("seed,R,nr", [(40, 4, (1, 5000)), (41, 4, (1, 5000)), (42, 2, (16385, 32768))])
+@pytest.mark.parametrize("seed,R,nr", [(40, 4, (1, 5000)), (41, 4, (1, 5000)), (42, 2, (16385, 32768)),
+                                       (43, 3, (32769, 131072)), (44, 5, (1, 40000))])
 def test_topk_parity(seed, R, nr):
     wl = W.tiny(seed, R=R, n_range=nr, Dv=64, k_frac=0.125)
     rng = np.random.default_rng(seed)
