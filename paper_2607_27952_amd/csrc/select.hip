@@ -730,20 +730,28 @@ __global__ __launch_bounds__(1024) void k_topk_rank(const float *__restrict__ sc
 
 namespace last {
 
-// Greedy block shape for requests of up to n tokens: beyond kMcMinN tokens, S
-// <= 16 blocks of kMcThreads (slices of 2048 tokens, 4096 past 32768, 8192
-// past 65536) that exchange their candidates every step; else one block a request: one wave up to 1024
-// tokens (no block barrier per step), else 256, 512 or 1024 threads with up to
-// 32 tokens each.
-constexpr int kMcMinN = 16384;
-static_assert(kMcMinN <= kGreedyMaxN, "one block holds every request below the multi-block greedy");
-static void greedy_shape(int32_t n, int32_t *threads, int32_t *ept, int32_t *slices) {
+// Greedy block shape for `nreq` requests of up to n tokens each. Past
+// kGreedyMaxN tokens, and past kMcMinN tokens when the requests' blocks fit in
+// `budget` compute units, S <= 16 blocks of kMcThreads a request (slices of
+// 2048 tokens, 4096 past 32768, 8192 past 65536) that exchange their
+// candidates every step; else one block a request: one wave up to 1024 tokens
+// (no block barrier per step), else 256, 512 or 1024 threads with up to 32
+// tokens each.
+constexpr int kMcMinN = 8192;
+static void greedy_shape(int32_t n, int32_t nreq, int32_t budget, int32_t *threads, int32_t *ept,
+                         int32_t *slices) {
   *slices = 0;
   if (n > kMcMinN) {
-    *threads = kMcThreads;
-    *ept = n <= 32768 ? 8 : n <= 65536 ? 16 : 32;
-    *slices = (n + kMcThreads * *ept - 1) / (kMcThreads * *ept);
-  } else if (n <= 1024) {
+    const int e = n <= 32768 ? 8 : n <= 65536 ? 16 : 32;
+    const int S = (n + kMcThreads * e - 1) / (kMcThreads * e);
+    if (n > kGreedyMaxN || (int64_t)nreq * S <= budget) {
+      *threads = kMcThreads;
+      *ept = e;
+      *slices = S;
+      return;
+    }
+  }
+  if (n <= 1024) {
     *threads = 64;
     const int e = (n + 63) / 64;
     *ept = e <= 2 ? 2 : e <= 4 ? 4 : e <= 6 ? 6 : e <= 8 ? 8 : e <= 10 ? e : e <= 12 ? 12 : e <= 14 ? 14 : 16;
@@ -778,7 +786,7 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   p.threads = p.N_max > 1024 ? 1024 : std::max(64, (p.N_max + 63) / 64 * 64);
   const int ept = (p.N_max + p.threads - 1) / p.threads;
   p.ept = ept <= 1 ? 1 : ept <= 2 ? 2 : ept <= 4 ? 4 : ept <= 8 ? 8 : ept <= 16 ? 16 : 32;
-  greedy_shape(p.N_max, &p.g_threads, &p.g_ept, &p.g_slices);
+  greedy_shape(p.N_max, R, device_cus(), &p.g_threads, &p.g_ept, &p.g_slices);
   p.groups = 1;
   p.group_tile0[0] = 0;
   p.group_tile0[1] = p.tiles_off;
@@ -907,10 +915,13 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
     p.group_rank0[g] = best.rank0[g];
     p.group_tile0[g] = cum[best.rank0[g]];
   }
-  for (int x = 0; x < p.groups; ++x)
-    greedy_shape(n_of(ord[p.group_rank0[x]]), &p.group_threads[x], &p.group_ept[x], &p.group_slices[x]);
   p.ranked = true;
   p.reserve = best.reserve;
+  // a group's greedies run beside the later groups' Gram, on the compute units
+  // it leaves free
+  for (int x = 0; x < p.groups; ++x)
+    greedy_shape(n_of(ord[p.group_rank0[x]]), p.group_rank0[x + 1] - p.group_rank0[x], p.reserve,
+                 &p.group_threads[x], &p.group_ept[x], &p.group_slices[x]);
   return p;
 }
 
