@@ -230,11 +230,12 @@ size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,
  *   cu_vis     [R+1] as in last_batch; N_r <= 131072 per request (k-center
  *              keeps 4 ceil(N_r/128)^2 128^2 bytes of coverage distances per
  *              request in the workspace: 17 GB at 65536 tokens, 69 GB at
- *              131072). Requests longer than 16384 tokens run the greedy on
- *              several compute units that exchange their candidates every
- *              step; if they cannot all run at once for 10 s (the device
- *              kept full by other work), the request's kept and order are
- *              filled with -1 and its gains with NaN
+ *              131072). Requests longer than 32768 tokens (and longer than
+ *              8192 when the batch is small) run the greedy on several
+ *              compute units that exchange their candidates every step; if
+ *              they cannot all run at once for 10 s (the device kept full
+ *              by other work), the request's kept and order are filled
+ *              with -1 and its gains with NaN
  *   cu_keep    [R+1] budgets: K_r = cu_keep[r+1]-cu_keep[r], 1 <= K_r <= N_r
  *              (use last_budget for K = ceil(rho N), Eq. 2)
  *   kept       [K_total] out: the selected request-local indices, ascending

@@ -153,9 +153,9 @@ SELECT_CASES = [
     (25, 1, (1500, 2100), 512, W.BF16, 0.1, 24),
     (26, 7, (1, 260), 256, W.BF16, 0.3, 3),        # four 64-column stages only; one-block requests
     (27, 2, (1025, 1100), 768, W.BF16, None, 12),  # greedy blocks of 256 threads
-    (28, 1, (8193, 8300), 256, W.BF16, 0.05, 32),  # greedy blocks of 512 threads
+    (28, 1, (8193, 8300), 256, W.BF16, 0.05, 32),  # multi-block greedy (a small batch)
     (29, 5, (1, 200), 32, W.F32, 0.5, 3),          # fp32 rows shorter than one staged chunk
-    (32, 1, (16385, 16600), 256, W.BF16, 0.03, 32),  # greedy blocks of 1024 threads
+    (32, 1, (16385, 16600), 256, W.BF16, 0.03, 32),  # multi-block greedy, 9 slices
     (33, 2, (30000, 32767), 64, W.BF16, 0.02, 16),   # up to the 32768-token limit, staged Gram
     (34, 1, (20000, 24000), 48, W.F32, 0.02, 8),     # fp32 Gram beyond 16384 tokens
     (36, 3, (840, 896), 128, W.BF16, 0.1, 8),        # one-wave greedy, 14 tokens a lane
@@ -279,14 +279,15 @@ def test_select_largest_request():
     check_selection(wl, w32, kept, order, "N=32768")
 
 
-# Requests past 16384 tokens: the greedy on several compute units (slices of
-# 2048 tokens, of 4096 past 65536), one candidate exchange per step.
+# Long requests: the greedy on several compute units (slices of 2048 tokens,
+# 4096 past 32768, 8192 past 65536), one candidate exchange per step.
 MC_CASES = [
     # seed, R, n_range, Dv, dtype, k_frac, comps
-    (50, 2, (32769, 40000), 32, W.BF16, 0.02, 16),   # 17-20 slices, ragged last slice
-    (51, 1, (63000, 65536), 16, W.BF16, 0.01, 24),   # up to 32 slices of 2048
-    (52, 1, (65537, 70000), 16, W.BF16, 0.01, 24),   # slices of 4096
-    (53, 2, (16385, 18000), 24, W.F32, 0.05, 12),    # fp32 features, 9 slices
+    (50, 2, (32769, 40000), 32, W.BF16, 0.02, 16),   # 9-10 slices of 4096, ragged last slice
+    (51, 1, (63000, 65536), 16, W.BF16, 0.01, 24),   # up to 16 slices of 4096
+    (52, 1, (65537, 70000), 16, W.BF16, 0.01, 24),   # slices of 8192
+    (53, 2, (16385, 18000), 24, W.F32, 0.05, 12),    # fp32 features, 9 slices of 2048
+    (56, 3, (8193, 12000), 64, W.BF16, 0.05, 12),    # from 8193 tokens (a small batch)
 ]
 
 
@@ -346,9 +347,26 @@ def test_select_mixed_batch_multiblock(dtype):
     assert sorted(order[a:a + 600]) == list(range(600)) and gains[a + 599] == 0.0
 
 
+@pytest.mark.parametrize("n_long", [9000, 20000])
+def test_select_large_batch_one_block_per_request(n_long):
+    """A batch whose long request would need more blocks than the device has
+    compute units once every request gets its slices: every request then runs
+    on one block (512 threads up to 16384 tokens, 1024 threads beyond)."""
+    rng = np.random.default_rng(n_long)
+    Dv = 64
+    sizes = [n_long] + [int(x) for x in rng.integers(50, 400, size=63)]
+    centres = rng.standard_normal((16, Dv))
+    centres /= np.linalg.norm(centres, axis=1, keepdims=True)
+    Xs = [centres[rng.integers(0, 16, n)] + 0.3 / np.sqrt(Dv) * rng.standard_normal((n, Dv)) for n in sizes]
+    ws = [rng.dirichlet(np.ones(n) * 0.7) for n in sizes]
+    Ks = [max(1, n // 16) for n in sizes]
+    wl, w32, kept, order, _ = _select_batch(Xs, ws, Ks, W.BF16)
+    check_selection(wl, w32, kept, order, f"64 requests, the longest {n_long}")
+
+
 def test_select_largest_request_multiblock():
-    """A request of 131072 tokens, the largest diverse_select takes (32 slices
-    of 4096; 69 GB of coverage distances)."""
+    """A request of 131072 tokens, the largest diverse_select takes (16 slices
+    of 8192; 69 GB of coverage distances)."""
     rng = np.random.default_rng(55)
     N, Dv = 131072, 8
     centres = rng.standard_normal((32, Dv))
@@ -576,17 +594,20 @@ def test_two_host_threads_two_streams(profile):
         assert prof.get("score_stream", (0, 0))[0] >= 12 and prof.get("gather", (0, 0))[0] >= 12
 
 
-def test_ragged_batch_pipelined_greedy():
-    """A ragged batch (two long requests among short ones) takes the pipelined
+@pytest.mark.parametrize("sizes,div", [([700, 12000, 500, 9000, 400, 600, 300, 650], 8),
+                                       ([700, 40000, 500, 9000, 400, 600, 300, 650], 32)],
+                         ids=["12000", "40000"])
+def test_ragged_batch_pipelined_greedy(sizes, div):
+    """A ragged batch (long requests among short ones) takes the pipelined
     schedule: the off-diagonal Gram in groups of decreasing request size, each
-    group's greedy on a side stream beside the later groups' Gram. The result is
-    bit-identical to the two-call form (the whole Gram, then every greedy) and
-    passes the oracle replay."""
-    sizes = [700, 12000, 500, 9000, 400, 600, 300, 650]
+    group's greedy on a side stream beside the later groups' Gram (with a
+    40000-token request, the multi-block greedy). The result is bit-identical to
+    the two-call form (the whole Gram, then every greedy) and passes the oracle
+    replay."""
     rng = np.random.default_rng(91)
     R, Dv = len(sizes), 256
     cu_vis = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
-    cu_keep = np.concatenate([[0], np.cumsum([(n + 7) // 8 for n in sizes])]).astype(np.int32)
+    cu_keep = np.concatenate([[0], np.cumsum([(n + div - 1) // div for n in sizes])]).astype(np.int32)
     # a 24-component mixture like the workloads': unit-norm centres, noise of norm 0.3
     centres = rng.standard_normal((24, Dv)).astype(np.float32)
     centres /= np.linalg.norm(centres, axis=1, keepdims=True)
@@ -596,7 +617,12 @@ def test_ragged_batch_pipelined_greedy():
     feats_bits = W.to_bf16_bits(X)
     feats = last.to_torch(feats_bits, W.BF16, "cuda")
     st = torch.from_numpy(w32).cuda()
+    last.profile_enable(True)
+    last.profile_reset()
     one = gpu_select(feats, st, cu_vis, cu_keep)
+    prof = last.profile_collect()
+    last.profile_enable(False)
+    assert prof.get("greedy_side", (0, 0))[0] >= 2, f"no pipelined greedy launches: {sorted(prof)}"
     _, kept, order, gains = _two_phase(feats, cu_vis, cu_keep, lambda: st)
     for x, y in zip(one, (kept, order, gains)):
         assert x.tobytes() == y.tobytes()
