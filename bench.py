@@ -406,16 +406,21 @@ def measure(args, name, budget, steps, warmup, source="last", prefill=False, con
     # priority) they overlap the score pass; the pick waits for both streams.
     side = torch.cuda.Stream(device=dev)
 
-    def step():
+    def step(marks=None):
+        # marks: events recorded on the stream around each call (the score call,
+        # the selection, the gather, the connector)
+        mark = (lambda i: marks[i].record(stream)) if marks is not None else (lambda i: None)
         if overlap:
             side.wait_stream(stream)
             last.diverse_select_similarity(dw.feats, wl.cu_vis, ws_k, cu_vis=b.cu_vis, stream=side)
+        mark(0)
         if pre is not None:
             last.prefill_attention(b, pre[0], dw.k, pre[1], out=pre_out, scores=scores, ws=ws_s)
         elif rows is None:
             last.token_scores(b, dw.q, dw.k, scores=scores, ws=ws_s)
         else:
             last.rows_scores(b, rows, q_rows, dw.k, scores=scores, ws=ws_s)
+        mark(1)
         if overlap:
             stream.wait_stream(side)
             last.diverse_select_pick(scores, wl.cu_vis, dw.cu_keep_h, ws_k, wl.Dv, dw.feats.dtype, cu_vis=b.cu_vis,
@@ -423,10 +428,13 @@ def measure(args, name, budget, steps, warmup, source="last", prefill=False, con
         else:
             last.diverse_select(scores, dw.feats, wl.cu_vis, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep,
                                 kept=kept, order=order, gains=gains, ws=ws_k)
+        mark(2)
         last.gather_kept(dw.feats, wl.cu_vis, kept, dw.cu_keep_h, cu_vis=b.cu_vis, cu_keep=dw.cu_keep, out=out)
+        mark(3)
         if conn is not None:
             last.connector(out, conn["gamma"], conn["beta"], conn["w1"], conn["b1"], conn["w2"], conn["b2"],
                            out=conn_out, ws=ws_c)
+        mark(4)
 
     for _ in range(warmup):
         step()
@@ -450,10 +458,23 @@ def measure(args, name, budget, steps, warmup, source="last", prefill=False, con
         prof = last.profile_collect() if profile else {}
         return t_b - t_a, np.array([x.elapsed_time(y) for x, y in ev]), prof
 
+    def timed_calls():
+        """`steps` steps with events between the calls: each call's time on the
+        stream, inter-kernel gaps included (what a caller of that call waits)."""
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+        torch.cuda.synchronize()
+        for i in range(steps):
+            step(ev[i])
+        torch.cuda.synchronize()
+        t = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(4)] for i in range(steps)])
+        return t.mean(axis=0)
+
     # throughput: the path alone; per-kernel times: a second timed pass with the
-    # library's kernel events (they add a little time between kernels)
+    # library's kernel events (they add a little time between kernels); per-call
+    # times: a third pass with events between the calls only
     elapsed, step_ms, _ = timed(False)
     elapsed_prof, _, prof = timed(True)
+    call_ms = timed_calls()
 
     single = rows is not None and int(rows.cu_rows_h[-1]) == wl.R
     row_pos = rows.row_pos_h if single else None
@@ -465,12 +486,14 @@ def measure(args, name, budget, steps, warmup, source="last", prefill=False, con
         work.update(connector_work(wl))
     kernels = {}
     for kname, (launches, total_ms) in prof.items():
+        if launches == 0:   # timed in an earlier workload of this process, not in this one
+            continue
         kernels[kname] = {"launches": launches, "avg_ms": round(total_ms / max(launches, 1), 5),
                           "ms_per_step": round(total_ms / steps, 5)}
     # work figures are per step; a kernel launched several times a step (the Gram
     # of a ragged batch, in groups) does its share per launch
     rooflines = [roofline_entry(k, bd, w / max(1.0, kernels[k]["launches"] / steps), kernels[k]["avg_ms"])
-                 for k, (bd, w) in work.items() if k in kernels]
+                 for k, (bd, w) in work.items() if k in kernels and kernels[k]["avg_ms"] > 0]
     # greedies launched on the library's side streams overlap the Gram; they are
     # reported but neither counted in the stage sums nor taken as the dominant kernel
     dominant = max((kv for kv in kernels.items() if kv[0] != "greedy_side"), key=lambda kv: kv[1]["ms_per_step"])[0]
@@ -493,9 +516,17 @@ def measure(args, name, budget, steps, warmup, source="last", prefill=False, con
     conn_ms = sum(kernels[k]["ms_per_step"] for k in kernels if k.startswith("connector"))
     sw = stage_work(wl, row_pos)
     stage_roof = {}
+    calls = {"scores": float(call_ms[0]), "select": float(call_ms[1]), "gather": float(call_ms[2])}
+    if conn is not None:
+        calls["connector"] = float(call_ms[3])
     if rows is None and pre is None and score_ms > 0:
-        stage_roof["scores"] = roofline_entry("scores: " + "+".join(k for k in kernels if k in SCORE_KERNELS),
-                                              *sw["scores"], score_ms)
+        # the whole last_token_scores call, as a caller waits for it (events
+        # between the calls; its kernels and the gaps between them)
+        stage_roof["scores"] = roofline_entry("scores: the last_token_scores call (" +
+                                              "+".join(k for k in kernels if k in SCORE_KERNELS) + ")",
+                                              *sw["scores"], calls["scores"])
+        stage_roof["scores_kernels"] = roofline_entry("scores: sum of the score kernels' own event times",
+                                                      *sw["scores"], score_ms)
     if similarity_ms > 0:
         e = roofline_entry("similarity: " + "+".join(k for k in SIMILARITY_KERNELS if k in kernels),
                            *sw["similarity"], similarity_ms)
@@ -518,6 +549,7 @@ def measure(args, name, budget, steps, warmup, source="last", prefill=False, con
         "ms_per_step_with_kernel_events": round(elapsed_prof / steps * 1e3, 4),
         "stage_ms_per_step": {"scores": round(score_ms, 4), "select": round(select_ms, 4),
                               "gather": round(gather_ms, 4)} | ({"connector": round(conn_ms, 4)} if conn else {}),
+        "call_ms_per_step": {k: round(v, 4) for k, v in calls.items()},
         "kernels": kernels,
         "roofline": main_roof,
         "rooflines": rooflines,
@@ -543,6 +575,7 @@ def config_summary(m, budget):
             "requests_per_s": m["value"], "ms_per_step": m["ms_per_step"],
             "visual_tokens_scored_per_s": m["visual_tokens_scored_per_s"],
             "p50_select_latency_ms": m["p50_select_latency_ms"], "stage_ms_per_step": m["stage_ms_per_step"],
+            "call_ms_per_step": m["call_ms_per_step"],
             "kernels_ms_per_step": {k: v["ms_per_step"] for k, v in m["kernels"].items()},
             "roofline": m["roofline"], "stage_rooflines": m["stage_rooflines"], "similarity": m["similarity"]}
 
@@ -590,6 +623,7 @@ def main():
         "p90_select_latency_ms": m["p90_select_latency_ms"],
         "ms_per_step_with_kernel_events": m["ms_per_step_with_kernel_events"],
         "stage_ms_per_step": m["stage_ms_per_step"],
+        "call_ms_per_step": m["call_ms_per_step"],
         "kernels": m["kernels"],
         "roofline": m["roofline"],
         "rooflines": m["rooflines"],

@@ -150,10 +150,12 @@ static_assert(sizeof(TileMeta) == 32, "two 16-byte pieces");
 
 // Ragged batches: the requests in decreasing size (their ranks) are split into
 // at most kMaxGroups groups. The off-diagonal Gram runs group by group, and a
-// group's greedy runs on a side stream beside the Gram of the later groups.
-// Three groups: with the caller's stream they use four hardware queues, the
-// default number per process; more streams would share queues and serialise.
+// group's greedy runs on a side stream beside the Gram of the later groups,
+// group g on side stream g mod kSideStreams. Three side streams: with the
+// caller's stream they use four hardware queues, the default number per
+// process; more streams would share queues and serialise.
 constexpr int kMaxGroups = 3;
+constexpr int kSideStreams = 3;
 constexpr int kRankMaxR = 1024;   // larger batches keep the natural order, one group
 struct SelectPlan {
   int64_t N_total, K_total;

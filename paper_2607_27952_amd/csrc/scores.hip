@@ -674,6 +674,96 @@ __global__ __launch_bounds__(kThreads) void k_score_finalize(
   }
 }
 
+// The same as k_score_finalize, for Hq % 4 == 0 and G * Hq <= 4 kFinQ: the
+// slice's logits of a layer are one contiguous run of 256 Hq floats, read by
+// the whole block as 16-byte pieces in order (every load instruction covers
+// consecutive lines), all layers' pieces in flight at once. A piece holds 4
+// heads of one token; its share sum_h exp(l - M) / Z goes to LDS, and each
+// thread then adds its token's shares layer by layer, heads ascending (a fixed
+// order, as everywhere in the score pass).
+constexpr int kFinQMax = 32;   // pieces a thread, over all layers
+template <int kFinQ>
+__global__ __launch_bounds__(kThreads) void k_score_finalize_c(
+    const float *__restrict__ vlog, const float2 *__restrict__ rowstat, const float *__restrict__ rowmass,
+    const int32_t *__restrict__ cu_seqlens, const int32_t *__restrict__ cu_vis,
+    const int32_t *__restrict__ vis_start, const int32_t *__restrict__ row_pos,
+    const int32_t *__restrict__ chunk_off, const int32_t *__restrict__ slice_off, int R, int G, int Hq, int CH,
+    int64_t N_total, float *__restrict__ scores) {
+  extern __shared__ float s_part[];   // [G][kThreads][PS]
+  const int GH = G * Hq, P = Hq / 4, PS = P | 1, GP = G * P;
+  __shared__ float2 sMZ[4 * kFinQ];
+  __shared__ float s_red[kWaves];
+  __shared__ int s_where[3];
+  const Where wh = locate(blockIdx.x, true, R, CH, kThreads, cu_seqlens, cu_vis, row_pos, chunk_off, slice_off,
+                          s_where);
+  const int r = wh.r, sl = (int)(blockIdx.x - wh.s0);
+  const int t = threadIdx.x;
+  const int64_t n0 = cu_vis[r];
+  const int N_r = cu_vis[r + 1] - (int)n0;
+  const int tok0 = sl * kThreads, cnt = min(N_r - tok0, kThreads);
+  // piece q of this thread: layer q / P, piece k = (q % P) kThreads + t of the
+  // layer's run, token k / P (exact in fp32 for k < 2^13: the quotient's
+  // fraction is at least 1 / (2P) from the next integer)
+  const float invP = 1.0f / (float)P;
+  auto tok_of = [&](int k) { return (int)(((float)k + 0.5f) * invP); };
+  // every piece of every layer first: layer l's run starts at token tok0
+  float4 x[kFinQ];
+  {
+    int l = 0, j = 0;
+#pragma unroll
+    for (int q = 0; q < kFinQ; ++q) {
+      if (q < GP) {
+        const int k = j * kThreads + t;
+        if (tok_of(k) < cnt)
+          x[q] = *reinterpret_cast<const float4 *>(vlog + ((int64_t)l * N_total + n0 + tok0) * Hq + 4 * (int64_t)k);
+      }
+      ++j;
+      l += j == P ? 1 : 0;
+      j = j == P ? 0 : j;
+    }
+  }
+  float part = 0.f;
+  for (int p = t; p < GH; p += kThreads) {
+    sMZ[p] = rowstat[(int64_t)r * GH + p];
+    part += rowmass[(int64_t)r * GH + p];
+  }
+  part = wave_sum(part);
+  if ((t & 63) == 0) s_red[t >> 6] = part;
+  __syncthreads();
+  float S = 0.f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) S += s_red[w];
+  const float invS = 1.0f / S;
+  {
+    int l = 0, j = 0;
+#pragma unroll
+    for (int q = 0; q < kFinQ; ++q) {
+      if (q < GP) {
+        const int k = j * kThreads + t, tok = tok_of(k), jj = k - tok * P;
+        if (tok < cnt) {
+          const float2 *mz = sMZ + l * Hq + 4 * jj;
+          float v = expf(x[q].x - mz[0].x) * mz[0].y;
+          v = fmaf(expf(x[q].y - mz[1].x), mz[1].y, v);
+          v = fmaf(expf(x[q].z - mz[2].x), mz[2].y, v);
+          v = fmaf(expf(x[q].w - mz[3].x), mz[3].y, v);
+          s_part[(l * kThreads + tok) * PS + jj] = v;
+        }
+      }
+      ++j;
+      l += j == P ? 1 : 0;
+      j = j == P ? 0 : j;
+    }
+  }
+  __syncthreads();
+  if (t >= cnt) return;
+  // a row before the end of the visual span sees only the tokens up to itself
+  const int seen = row_pos ? min(N_r, row_pos[r] - vis_start[r] + 1) : N_r;
+  float acc = 0.f;
+  for (int l = 0; l < G; ++l)
+    for (int j = 0; j < P; ++j) acc += s_part[(l * kThreads + t) * PS + j];
+  scores[n0 + tok0 + t] = tok0 + t < seen ? acc * invS : 0.f;
+}
+
 // Optional full rows A[p*, :] for inspection: raw logits -> probabilities.
 __global__ __launch_bounds__(kThreads) void k_rows_finalize(
     const float4 *__restrict__ stats, const int32_t *__restrict__ cu_seqlens,
@@ -819,9 +909,23 @@ hipError_t launch_score_tail(const last_batch *b, const ScorePlan &p, const Scor
   hipError_t e = launch_end(s);
   if (e != hipSuccess) return e;
   launch_begin("score_finalize", s);
-  hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog, w.rowstat,
-                     w.rowmass, b->cu_seqlens, b->cu_vis, b->vis_start, row_pos, w.chunk_off, w.slice_off, b->R,
-                     b->G, b->Hq, p.chunk_tokens, p.slice_tokens, p.N_total, scores);
+  if (b->Hq % 4 == 0 && GH <= 4 * kFinQMax && p.slice_tokens == kThreads) {
+    const size_t lds = (size_t)b->G * kThreads * ((b->Hq / 4) | 1) * sizeof(float);
+    const int q = GH / 4;   // pieces a thread
+#define LAST_FIN(Q)                                                                                               \
+  hipLaunchKernelGGL(k_score_finalize_c<Q>, dim3((unsigned)p.S_total), dim3(kThreads), lds, s, w.vlog, w.rowstat, \
+                     w.rowmass, b->cu_seqlens, b->cu_vis, b->vis_start, row_pos, w.chunk_off, w.slice_off, b->R,   \
+                     b->G, b->Hq, p.chunk_tokens, p.N_total, scores)
+    if (q <= 4) LAST_FIN(4);
+    else if (q <= 8) LAST_FIN(8);
+    else if (q <= 16) LAST_FIN(16);
+    else LAST_FIN(32);
+#undef LAST_FIN
+  } else {
+    hipLaunchKernelGGL(k_score_finalize, dim3((unsigned)p.S_total), dim3(kThreads), 0, s, w.vlog, w.rowstat,
+                       w.rowmass, b->cu_seqlens, b->cu_vis, b->vis_start, row_pos, w.chunk_off, w.slice_off, b->R,
+                       b->G, b->Hq, p.chunk_tokens, p.slice_tokens, p.N_total, scores);
+  }
   return launch_end(s);
 }
 

@@ -14,6 +14,7 @@
 // their bits), breaks ties at the threshold towards the lowest index, and
 // ranks the kept tokens for the pick order.
 #include <algorithm>
+#include <cstring>
 #include <atomic>
 #include <math.h>
 
@@ -276,7 +277,7 @@ __global__ __launch_bounds__(kMcThreads) void k_greedy_mc(const float *__restric
                                                           const int32_t *__restrict__ cu_vis,
                                                           const int32_t *__restrict__ cu_keep,
                                                           const int32_t *__restrict__ req_order, int rank0, int nreq,
-                                                          int S,
+                                                          int S, int spread,
                                                           unsigned long long *__restrict__ slots, int64_t limit,
                                                           int32_t *__restrict__ kept, int32_t *__restrict__ order,
                                                           float *__restrict__ gains) {
@@ -286,11 +287,15 @@ __global__ __launch_bounds__(kMcThreads) void k_greedy_mc(const float *__restric
   __shared__ float s_pre[2][SL];   // this slice of two prefetched coverage rows
   __shared__ int s_cnt[16];
   __shared__ int s_abort;
-  // Workgroup b runs on XCD b % 8: the S blocks of a request share an XCD
-  // (request rb of the launch on XCD rb % 8), whose exchange is about a fifth
-  // faster than one spread over XCDs. Blocks past the last request exit.
+  // Workgroup b runs on XCD b % 8. Alone on the device, the S blocks of a
+  // request share an XCD (request rb of the launch on XCD rb % 8), whose
+  // exchange is about a fifth faster than one spread over XCDs; beside the
+  // Gram (`spread`), whose persistent grid leaves a few compute units free on
+  // every XCD, consecutive blocks form a request and so spread over the XCDs.
+  // Blocks past the last request exit.
   const int xcd = (int)blockIdx.x % 8, kx = (int)blockIdx.x / 8;
-  const int rb = (kx / S) * 8 + xcd, sl = kx % S;
+  const int rb = spread ? (int)blockIdx.x / S : (kx / S) * 8 + xcd;
+  const int sl = spread ? (int)blockIdx.x % S : kx % S;
   if (rb >= nreq) return;
   const int r = req_order ? req_order[rank0 + rb] : rank0 + rb;
   const int64_t n0 = cu_vis[r];
@@ -738,6 +743,7 @@ namespace last {
 // (no block barrier per step), else 256, 512 or 1024 threads with up to 32
 // tokens each.
 constexpr int kMcMinN = 8192;
+constexpr double kMcStepUs = 1.9;   // a step of the multi-block greedy (measured, 16k-32k tokens)
 static void greedy_shape(int32_t n, int32_t nreq, int32_t budget, int32_t *threads, int32_t *ept,
                          int32_t *slices) {
   *slices = 0;
@@ -799,8 +805,8 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
 
   // Ragged batches. A greedy takes about K_r (0.6 + 1.1e-4 N_r) microseconds
   // on one compute unit (one dependent step per pick, each a coverage row of
-  // N_r floats), about 1.6 times that while the Gram loads the memory system
-  // (measured), and an off-diagonal Gram tile about 0.8 us per 64 columns of Dv
+  // N_r floats), or K_r kMcStepUs on S of them (the multi-block greedy), about
+  // 1.6 times that while the Gram loads the memory system (measured), and an off-diagonal Gram tile about 0.8 us per 64 columns of Dv
   // plus 3 us on one compute unit. When the longest greedy is several times the
   // median one, the requests are ordered by decreasing size and the
   // off-diagonal Gram runs in groups; each group's greedies start, on side
@@ -858,18 +864,32 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
       const double rate = (cus - reserve) / tile_us;   // tiles per microsecond
       double t = 0, span = 0;
       std::vector<std::pair<double, double>> busy;      // greedy intervals
+      std::vector<int> width;                           // compute units of each greedy
+      double free_at[kSideStreams] = {};                // when each side stream's last greedies end
       for (int g = 0; g < c.G; ++g) {
-        t += (double)(cum[c.rank0[g + 1]] - cum[c.rank0[g]]) / rate;
-        for (int k = c.rank0[g]; k < c.rank0[g + 1]; ++k) busy.push_back({t, t + 1.6 * cost[ord[k]]});
+        // the group's Gram, plus about one tile time for its launch's tail
+        t += (double)(cum[c.rank0[g + 1]] - cum[c.rank0[g]]) / rate + tile_us;
+        // a group whose blocks fit the reserve runs the multi-block greedy;
+        // a group's greedies start after the previous ones on its stream
+        int32_t th, ep, S;
+        greedy_shape(n_of(ord[c.rank0[g]]), c.rank0[g + 1] - c.rank0[g], reserve, &th, &ep, &S);
+        const double start = std::max(t, free_at[g % kSideStreams]);
+        double end = start;
+        for (int k = c.rank0[g]; k < c.rank0[g + 1]; ++k) {
+          busy.push_back({start, start + 1.6 * (S > 0 ? k_of(ord[k]) * kMcStepUs : cost[ord[k]])});
+          width.push_back(S > 0 ? S : 1);
+          end = std::max(end, busy.back().second);
+        }
+        free_at[g % kSideStreams] = end;
       }
       const double gram_end = t;
       // concurrency before the Gram ends must fit the reserve; after it, every
       // unit is free (a sweep over the interval ends)
       std::vector<std::pair<double, int>> ev;
       ev.reserve(2 * busy.size());
-      for (auto &x : busy) {
-        ev.push_back({x.first, +1});
-        ev.push_back({x.second, -1});
+      for (size_t i = 0; i < busy.size(); ++i) {
+        ev.push_back({busy[i].first, +width[i]});
+        ev.push_back({busy[i].second, -width[i]});
       }
       std::sort(ev.begin(), ev.end(), [](const std::pair<double, int> &a, const std::pair<double, int> &b) {
         return a.first != b.first ? a.first < b.first : a.second < b.second;   // ends before starts
@@ -904,6 +924,29 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
       for (int g = 0; g < G; ++g) frac[g] /= tot;
       Cand c{};
       split(frac, G, c);
+      if (c.G < 2) continue;
+      simulate(c);
+      if (c.span < best.span) best = c;
+    }
+  }
+  // the m longest requests alone first (their greedies, the longest, start
+  // earliest), then the rest in groups of even tile shares
+  for (int m : {1, 2, 4}) {
+    if (m >= R) break;
+    for (int G = 2; G <= std::min<int>(kMaxGroups, R - m + 1); ++G) {
+      Cand c{};
+      c.G = 1;
+      c.rank0[0] = 0;
+      c.rank0[1] = m;
+      int k = m;
+      for (int g = 1; g < G - 1; ++g) {   // group g ends at share g / (G - 1) of the rest
+        while (k < R - 1 && (double)(cum[k + 1] - cum[m]) * (G - 1) < (double)g * (cum[R] - cum[m])) ++k;
+        const int b = std::max(k, c.rank0[c.G] + 1);
+        if (b >= R) break;
+        c.rank0[++c.G] = b;
+        k = b;
+      }
+      c.rank0[++c.G] = R;
       if (c.G < 2) continue;
       simulate(c);
       if (c.span < best.span) best = c;
@@ -1023,7 +1066,7 @@ static int mc_capacity() {
 template <int EPT>
 static hipError_t launch_mc(int32_t slices, int32_t nreq, const int32_t *req_order, int32_t rank0,
                             const SelectWs &w, const float *scores, const int32_t *cu_vis, const int32_t *cu_keep,
-                            int32_t *kept, int32_t *order, float *gains, hipStream_t s) {
+                            int32_t *kept, int32_t *order, float *gains, bool spread, hipStream_t s) {
   // A launch takes at most a quarter of what the device holds, so that as many
   // such launches as the device has hardware queues (4) fit beside each other:
   // a request's blocks never wait on blocks of another launch that in turn
@@ -1038,8 +1081,9 @@ static hipError_t launch_mc(int32_t slices, int32_t nreq, const int32_t *req_ord
     const int64_t words = (int64_t)n * kMcSlotWords;
     hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)std::min<int64_t>((words + 255) / 256, 1024)), dim3(256), 0, s,
                        slots, words);
-    hipLaunchKernelGGL(k_greedy_mc<EPT>, dim3(8 * slices * ((n + 7) / 8)), dim3(kMcThreads), 0, s, scores, w.dmat,
-                       w.d_off, cu_vis, cu_keep, req_order, rank0 + c, n, slices, w.mc_slots, limit, kept, order,
+    const unsigned grid = spread ? (unsigned)(n * slices) : (unsigned)(8 * slices * ((n + 7) / 8));
+    hipLaunchKernelGGL(k_greedy_mc<EPT>, dim3(grid), dim3(kMcThreads), 0, s, scores, w.dmat, w.d_off, cu_vis,
+                       cu_keep, req_order, rank0 + c, n, slices, spread ? 1 : 0, w.mc_slots, limit, kept, order,
                        gains);
   }
   return hipGetLastError();
@@ -1054,10 +1098,15 @@ static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t slices, in
                                 float *gains, hipStream_t s, const char *what) {
   launch_begin(what, s);
   if (slices > 0) {
+    // beside the Gram (the side launches) a request's blocks spread over the XCDs
+    const bool spread = strcmp(what, "greedy_side") == 0;
     const hipError_t e =
-        ept == 8    ? launch_mc<8>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains, s)
-        : ept == 16 ? launch_mc<16>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains, s)
-                    : launch_mc<32>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains, s);
+        ept == 8    ? launch_mc<8>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains,
+                                   spread, s)
+        : ept == 16 ? launch_mc<16>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains,
+                                    spread, s)
+                    : launch_mc<32>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains,
+                                    spread, s);
     const hipError_t e2 = launch_end(s);
     return e != hipSuccess ? e : e2;
   }
@@ -1098,9 +1147,9 @@ static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t slices, in
 // process ends.
 namespace {
 struct SideStream {
-  hipStream_t s[kMaxGroups] = {};      // group g's greedies run on s[g]
-  hipEvent_t gram[kMaxGroups] = {};    // group g's Gram done (recorded on the caller's stream)
-  hipEvent_t done[kMaxGroups] = {};    // group g's greedies done
+  hipStream_t s[kSideStreams] = {};      // group g's greedies run on s[g % kSideStreams]
+  hipEvent_t gram[kSideStreams] = {};    // a group's Gram done (recorded on the caller's stream)
+  hipEvent_t done[kSideStreams] = {};    // the stream's greedies done
   bool ok = false;
 };
 constexpr int kSideDevices = 64;
@@ -1111,7 +1160,7 @@ SideStream *side_stream() {
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kSideDevices) return nullptr;
   SideStream &x = t_side[dev];
   if (!x.ok) {
-    for (int g = 0; g < kMaxGroups; ++g) {
+    for (int g = 0; g < kSideStreams; ++g) {
       if (!x.s[g] && hipStreamCreateWithFlags(&x.s[g], hipStreamNonBlocking) != hipSuccess) return nullptr;
       if (!x.gram[g] && hipEventCreateWithFlags(&x.gram[g], hipEventDisableTiming) != hipSuccess) return nullptr;
       if (!x.done[g] && hipEventCreateWithFlags(&x.done[g], hipEventDisableTiming) != hipSuccess) return nullptr;
@@ -1148,18 +1197,21 @@ static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, c
   const int gram_cus = std::max(8, cus - p.reserve);
   for (int g = 0; g < p.groups; ++g) {
     const int64_t t0 = p.group_tile0[g], nt = p.group_tile0[g + 1] - t0;
+    const int q = g % kSideStreams;
     if ((e = launch_gram_off(Dv, p, w, feats, t0, nt, gram_cus, s)) != hipSuccess) return e;
-    if ((e = hipEventRecord(side->gram[g], s)) != hipSuccess) return e;
-    if ((e = hipStreamWaitEvent(side->s[g], side->gram[g], 0)) != hipSuccess) return e;
+    // (each wait is enqueued right after its record, so one event per side
+    // stream serves every group)
+    if ((e = hipEventRecord(side->gram[q], s)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(side->s[q], side->gram[q], 0)) != hipSuccess) return e;
     const int32_t r0 = p.group_rank0[g], nr = p.group_rank0[g + 1] - r0;
     e = launch_greedy(p.group_threads[g], p.group_ept[g], p.group_slices[g], nr, w.req_order, r0, w, scores,
-                      cu_vis, cu_keep, kept,
-                      order, gains, side->s[g], "greedy_side");
+                      cu_vis, cu_keep, kept, order, gains, side->s[q], "greedy_side");
     if (e != hipSuccess) return e;
-    if ((e = hipEventRecord(side->done[g], side->s[g])) != hipSuccess) return e;
   }
-  for (int g = 0; g < p.groups; ++g)
-    if ((e = hipStreamWaitEvent(s, side->done[g], 0)) != hipSuccess) return e;
+  for (int q = 0; q < std::min(p.groups, kSideStreams); ++q) {
+    if ((e = hipEventRecord(side->done[q], side->s[q])) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(s, side->done[q], 0)) != hipSuccess) return e;
+  }
   return hipSuccess;
 }
 
