@@ -235,7 +235,11 @@ size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,
  *              compute units that exchange their candidates every step; if
  *              they cannot all run at once for 10 s (the device kept full
  *              by other work), the request's kept and order are filled
- *              with -1 and its gains with NaN
+ *              with -1 and its gains with NaN (blocks that time out at the
+ *              very end may leave some of the request's valid indices
+ *              beside the -1 entries; either way the request is invalid).
+ *              The environment variable LAST_MC_WAIT_US, read at every
+ *              call, replaces the 10 s (in microseconds)
  *   cu_keep    [R+1] budgets: K_r = cu_keep[r+1]-cu_keep[r], 1 <= K_r <= N_r
  *              (use last_budget for K = ceil(rho N), Eq. 2)
  *   kept       [K_total] out: the selected request-local indices, ascending

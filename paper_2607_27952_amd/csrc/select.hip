@@ -14,7 +14,7 @@
 // their bits), breaks ties at the threshold towards the lowest index, and
 // ranks the kept tokens for the pick order.
 #include <algorithm>
-#include <cstring>
+#include <cstdlib>
 #include <atomic>
 #include <math.h>
 
@@ -492,7 +492,11 @@ __global__ __launch_bounds__(kMcThreads) void k_greedy_mc(const float *__restric
     publish_wait(slot + 2 * kMcMaxS, (1ull << 62) | (unsigned)tot, 1u, v);
     int before = lane < sl ? (int)(v & 0xFFFFFFFFull) : 0;
     for (int x = 1; x < 64; x <<= 1) before += __shfl_xor(before, x);
-    if (lane == 0) s_cnt[8] = before;
+    if (lane == 0) {
+      s_cnt[8] = before;
+      // a block of the request that timed out after publishing its count
+      if (__hip_atomic_load(abort_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0ull) s_abort = 1;
+    }
   }
   __syncthreads();
   if (s_abort) {
@@ -988,12 +992,12 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
   return w;
 }
 
-// `what` names the launch for the kernel timing ("greedy", or "greedy_side" for
-// a launch on a side stream, which overlaps the Gram).
+// beside_gram: a launch on a side stream, overlapping the Gram (timed as
+// "greedy_side"; a multi-block greedy then spreads its blocks over the XCDs).
 static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t slices, int32_t blocks,
                                 const int32_t *req_order, int32_t rank0, const SelectWs &w, const float *scores,
                                 const int32_t *cu_vis, const int32_t *cu_keep, int32_t *kept, int32_t *order,
-                                float *gains, hipStream_t s, const char *what = "greedy");
+                                float *gains, hipStream_t s, bool beside_gram = false);
 static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, const SelectWs &w,
                                    const float *scores, const void *feats, const int32_t *cu_vis,
                                    const int32_t *cu_keep, int32_t *kept, int32_t *order, float *gains,
@@ -1074,7 +1078,11 @@ static hipError_t launch_mc(int32_t slices, int32_t nreq, const int32_t *req_ord
   const int cap = mc_capacity<EPT>() / 4;
   if (cap < slices) return hipErrorInvalidConfiguration;
   const int per_launch = cap / slices;
-  const int64_t limit = device_wall_khz() * 10000;   // 10 s in wall-clock ticks
+  // 10 s in wall-clock ticks; LAST_MC_WAIT_US overrides it (tests force the
+  // timeout path with a tiny value)
+  int64_t wait_us = 10000000;
+  if (const char *env = getenv("LAST_MC_WAIT_US")) wait_us = std::max<int64_t>(0, atoll(env));
+  const int64_t limit = device_wall_khz() * wait_us / 1000;
   for (int32_t c = 0; c < nreq; c += per_launch) {
     const int32_t n = std::min<int32_t>(per_launch, nreq - c);
     unsigned long long *slots = w.mc_slots + (int64_t)(rank0 + c) * kMcSlotWords;
@@ -1095,11 +1103,12 @@ static hipError_t launch_mc(int32_t slices, int32_t nreq, const int32_t *req_ord
 static hipError_t launch_greedy(int32_t threads, int32_t ept, int32_t slices, int32_t blocks,
                                 const int32_t *req_order, int32_t rank0, const SelectWs &w, const float *scores,
                                 const int32_t *cu_vis, const int32_t *cu_keep, int32_t *kept, int32_t *order,
-                                float *gains, hipStream_t s, const char *what) {
+                                float *gains, hipStream_t s, bool beside_gram) {
+  const char *what = beside_gram ? "greedy_side" : "greedy";
   launch_begin(what, s);
   if (slices > 0) {
     // beside the Gram (the side launches) a request's blocks spread over the XCDs
-    const bool spread = strcmp(what, "greedy_side") == 0;
+    const bool spread = beside_gram;
     const hipError_t e =
         ept == 8    ? launch_mc<8>(slices, blocks, req_order, rank0, w, scores, cu_vis, cu_keep, kept, order, gains,
                                    spread, s)
@@ -1205,7 +1214,7 @@ static hipError_t launch_pipelined(int32_t R, int32_t Dv, const SelectPlan &p, c
     if ((e = hipStreamWaitEvent(side->s[q], side->gram[q], 0)) != hipSuccess) return e;
     const int32_t r0 = p.group_rank0[g], nr = p.group_rank0[g + 1] - r0;
     e = launch_greedy(p.group_threads[g], p.group_ept[g], p.group_slices[g], nr, w.req_order, r0, w, scores,
-                      cu_vis, cu_keep, kept, order, gains, side->s[q], "greedy_side");
+                      cu_vis, cu_keep, kept, order, gains, side->s[q], true);
     if (e != hipSuccess) return e;
   }
   for (int q = 0; q < std::min(p.groups, kSideStreams); ++q) {

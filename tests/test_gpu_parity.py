@@ -630,3 +630,36 @@ def test_ragged_batch_pipelined_greedy(sizes, div):
                     cu_seqlens=cu_vis + np.arange(R + 1, dtype=np.int32), vis_start=np.zeros(R, np.int32),
                     cu_vis=cu_vis, q=None, k=None, Dv=Dv, f_dtype=W.BF16, feats=feats_bits, cu_keep=cu_keep)
     check_selection(wl, w32, one[0], one[1], "ragged pipelined batch")
+
+
+def test_multiblock_wait_timeout_marks_request_invalid():
+    """The multi-block greedy's bounded waits, forced to time out from the host
+    (LAST_MC_WAIT_US=0, read by the library at every launch): every wave still
+    finishes, each request's outputs are either the normal ones or marked
+    invalid (-1 / NaN), and the next call with the normal limit is exact again."""
+    import os
+    rng = np.random.default_rng(57)
+    Dv, sizes = 32, [20000, 9000, 30000]
+    Xs = [rng.standard_normal((n, Dv)) for n in sizes]
+    ws = [rng.dirichlet(np.ones(n)) for n in sizes]
+    Ks = [n // 50 for n in sizes]
+    wl, w32, kept0, order0, gains0 = _select_batch(Xs, ws, Ks, W.BF16)
+    os.environ["LAST_MC_WAIT_US"] = "0"
+    try:
+        _, _, kept1, order1, gains1 = _select_batch(Xs, ws, Ks, W.BF16)
+    finally:
+        del os.environ["LAST_MC_WAIT_US"]
+    n_marked = 0
+    for r in range(wl.R):
+        a, b = wl.cu_keep[r], wl.cu_keep[r + 1]
+        same = (np.array_equal(kept1[a:b], kept0[a:b]) and np.array_equal(order1[a:b], order0[a:b])
+                and np.array_equal(gains1[a:b], gains0[a:b]))
+        marked = np.any(kept1[a:b] == -1) and np.any(order1[a:b] == -1) and np.any(np.isnan(gains1[a:b]))
+        assert same or marked, f"request {r}: neither the normal result nor marked invalid"
+        n_marked += int(marked)
+    # with no wait allowed, a block that polls before its request's last block
+    # has published times out: the timeout path did run
+    assert n_marked >= 1
+    _, _, kept2, order2, gains2 = _select_batch(Xs, ws, Ks, W.BF16)
+    for x, y in zip((kept0, order0, gains0), (kept2, order2, gains2)):
+        assert x.tobytes() == y.tobytes()
