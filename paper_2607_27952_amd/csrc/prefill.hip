@@ -12,8 +12,13 @@
 //
 // One block per (layer, request, query head, 128 query positions); each of
 // its four waves owns 32 positions. Keys and values go through LDS 64 at a
-// time (keys row-major and swizzled, values transposed to [Dh][key]); the
-// next stage is loaded into registers while the current one is used.
+// time, both row-major with XOR-swizzled 16-byte pieces, copied straight from
+// memory by LDS DMA (global_load_lds_dwordx4: no registers, no transposing
+// stores) one stage ahead of their use. The value fragments are read with the
+// LDS transpose load (ds_read_b64_tr_b16): in each group of 16 lanes, lane i's
+// element j comes from element i % 4 of the 8 bytes lane 4 j + i / 4 points
+// at, so lanes pointing at 4 keys x 4 four-dimension chunks receive 4 keys of
+// one dimension each.
 //
 // The product runs transposed so that every lane owns one query:
 //   S^T = K Q^T   (v_mfma_f32_32x32x16_bf16, A = 32 keys, B = the wave's 32
@@ -54,15 +59,26 @@ struct Shape {
   static constexpr int kPieces = DH * 2 / 16;            // 16-byte pieces per key row
   static constexpr int kSteps = kPieces / 2;             // S^T MFMA steps per key tile
   static constexpr int kDT = DH / 32;                    // value-dimension tiles of O^T
-  static constexpr int kVPitch = kKS + 8;                // bf16 per transposed value row
-  static constexpr int kKPer = kKS * kPieces / kThreads; // key pieces each thread stages
-  static constexpr int kVPer = kKS * kPieces / kThreads / 2;  // value piece pairs per thread
-  static_assert(kKPer >= 1 && kVPer >= 1, "stage split");
+  static constexpr int kDma = kKS * kPieces / 64;        // DMA instructions per operand stage
+  static constexpr int kDmaPerWave = kDma / kWaves;      // ... per wave
+  static_assert(kDmaPerWave >= 1 && kDma % kWaves == 0, "stage split");
 };
 
 template <int NP>
 __device__ __forceinline__ int kslot(int j, int p) {
   return j * NP + (p ^ (NP >= 16 ? (j & 15) : ((j >> 1) & 7)));
+}
+
+// Physical 16-byte piece of logical piece p in row j of a stage (keys and
+// values alike).
+template <int NP>
+__device__ __forceinline__ int pswz(int j, int p) {
+  return p ^ (NP >= 16 ? (j & 15) : ((j >> 1) & 7));
+}
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ s16x4_t read_tr(const uint16_t *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4_t *)p);
 }
 
 // Key of a 32-key tile that MFMA row i carries: lane half h, element v of the
@@ -93,7 +109,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
     float *__restrict__ vlog, float4 *__restrict__ stats) {
   using SH = Shape<DH>;
   __shared__ uint4 s_k[2][kKS * SH::kPieces];
-  __shared__ __align__(16) uint16_t s_vt[2][DH * SH::kVPitch];
+  __shared__ uint4 s_v[2][kKS * SH::kPieces];
 
   // The query blocks of one (layer, head, request) are neighbours in this
   // order; XCD-contiguous numbering runs them together on one XCD, so they
@@ -130,44 +146,20 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
   const uint16_t *kbase = k + ((int64_t)l * T_total + tok0) * kvstride + (int64_t)kv * DH;
   const uint16_t *vbase = v + ((int64_t)l * T_total + tok0) * kvstride + (int64_t)kv * DH;
 
-  // register staging of one stage: key pieces (row-major, swizzled in LDS)
-  // and value piece pairs of keys 2i, 2i + 1 (transposed in LDS)
-  uint4 rk[SH::kKPer], rv0[SH::kVPer], rv1[SH::kVPer];
-  auto load_stage = [&](int j0) {
+  // One stage: keys j0 .. j0 + 63 (clamped to the block's last needed key) of
+  // both operands. DMA instruction x of this wave covers 16-byte slots
+  // 64 q + lane, q = wave + kWaves x, of the stage: row (slot / kPieces),
+  // physical piece (slot % kPieces), which holds logical piece
+  // pswz(row, physical) (an XOR, its own inverse).
+  auto issue_stage = [&](int j0, int buf) {
 #pragma unroll
-    for (int i = 0; i < SH::kKPer; ++i) {
-      const int e = threadIdx.x + kThreads * i, j = e / SH::kPieces, p = e % SH::kPieces;
+    for (int x = 0; x < SH::kDmaPerWave; ++x) {
+      const int q = wave + kWaves * x, slot = q * 64 + lane;
+      const int j = slot / SH::kPieces, pp = slot % SH::kPieces;
       const int jj = min(j0 + j, kend - 1);
-      rk[i] = *reinterpret_cast<const uint4 *>(kbase + (int64_t)jj * kvstride + p * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < SH::kVPer; ++i) {
-      const int e = threadIdx.x + kThreads * i, jp = e / SH::kPieces, p = e % SH::kPieces;
-      const int ja = min(j0 + 2 * jp, kend - 1), jb = min(j0 + 2 * jp + 1, kend - 1);
-      rv0[i] = *reinterpret_cast<const uint4 *>(vbase + (int64_t)ja * kvstride + p * 8);
-      rv1[i] = *reinterpret_cast<const uint4 *>(vbase + (int64_t)jb * kvstride + p * 8);
-    }
-  };
-  auto store_stage = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < SH::kKPer; ++i) {
-      const int e = threadIdx.x + kThreads * i, j = e / SH::kPieces, p = e % SH::kPieces;
-      s_k[buf][kslot<SH::kPieces>(j, p)] = rk[i];
-    }
-#pragma unroll
-    for (int i = 0; i < SH::kVPer; ++i) {
-      const int e = threadIdx.x + kThreads * i, jp = e / SH::kPieces, p = e % SH::kPieces;
-      const uint32_t a[4] = {rv0[i].x, rv0[i].y, rv0[i].z, rv0[i].w};
-      const uint32_t b[4] = {rv1[i].x, rv1[i].y, rv1[i].z, rv1[i].w};
-      uint16_t *vt = s_vt[buf];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        // dimensions p * 8 + 2w and p * 8 + 2w + 1, keys 2jp and 2jp + 1
-        const uint32_t lo = (a[w] & 0xffffu) | (b[w] << 16);
-        const uint32_t hi = (a[w] >> 16) | (b[w] & 0xffff0000u);
-        *reinterpret_cast<uint32_t *>(vt + (p * 8 + 2 * w) * SH::kVPitch + 2 * jp) = lo;
-        *reinterpret_cast<uint32_t *>(vt + (p * 8 + 2 * w + 1) * SH::kVPitch + 2 * jp) = hi;
-      }
+      const uint32_t voff = (uint32_t)(((int64_t)jj * kvstride + pswz<SH::kPieces>(j, pp) * 8) * 2);
+      dma16(__builtin_amdgcn_readfirstlane(lds_u32(&s_k[buf][q * 64])), uniform_ptr(kbase), voff);
+      dma16(__builtin_amdgcn_readfirstlane(lds_u32(&s_v[buf][q * 64])), uniform_ptr(vbase), voff);
     }
   };
 
@@ -177,25 +169,32 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
   for (int dt = 0; dt < SH::kDT; ++dt) o[dt] = f32x16_t{};
 
   const int nst = (kend + kKS - 1) / kKS;
-  load_stage(0);
-  store_stage(0);
+  issue_stage(0, 0);
+  vm_wait<0>();
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) load_stage((st + 1) * kKS);
+    // the other buffer was last read in stage st - 1, which every wave has left
+    if (st + 1 < nst) issue_stage((st + 1) * kKS, (st + 1) & 1);
     const int k0 = st * kKS;
     if (k0 <= wave_last) {
       const uint4 *kb = s_k[st & 1];
-      const uint16_t *vt = s_vt[st & 1];
+      const uint16_t *vs = reinterpret_cast<const uint16_t *>(s_v[st & 1]);
+      // The fragment addresses derive from the lane index anew in every stage
+      // (opaque to the compiler), instead of two dozen of them being hoisted
+      // out of the loop and held in registers.
+      int ln = (int)threadIdx.x & 63;
+      asm volatile("" : "+v"(ln));
+      const int lcol = ln & 31, lhalf = ln >> 5;
       // S^T for the stage's two 32-key tiles
       f32x16_t sc[2];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         sc[t] = f32x16_t{};
-        const int krow = t * 32 + perm_key(col);
+        const int krow = t * 32 + perm_key(lcol);
 #pragma unroll
         for (int s = 0; s < SH::kSteps; ++s)
           sc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              __builtin_bit_cast(bf16x8_t, kb[kslot<SH::kPieces>(krow, 2 * s + half)]),
+              __builtin_bit_cast(bf16x8_t, kb[kslot<SH::kPieces>(krow, 2 * s + lhalf)]),
               __builtin_bit_cast(bf16x8_t, bq[s]), sc[t], 0, 0, 0);
       }
       // base-2 logits: the raw dots stay in place and the scale goes into the
@@ -257,7 +256,21 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
         const uint4 bp = make_uint4(pw[0], pw[1], pw[2], pw[3]);
 #pragma unroll
         for (int dt = 0; dt < SH::kDT; ++dt) {
-          const uint4 av = *reinterpret_cast<const uint4 *>(vt + (dt * 32 + col) * SH::kVPitch + 16 * s + 8 * half);
+          // A = V^T: lane l needs dimension dt 32 + l % 32 of keys 16 s + 8 half
+          // .. + 7, as two transpose reads of 4 keys; lane p of its 16-lane
+          // group points at key (p / 4) of the four and dimensions
+          // 4 (p % 4) .. + 3 of the group's 16
+          const int g = ln >> 4, pl = ln & 15;
+          const int d = dt * 32 + 16 * (g & 1) + 4 * (pl & 3);   // first dimension of the chunk
+          s16x4_t tv[2];
+#pragma unroll
+          for (int c = 0; c < 2; ++c) {
+            const int key = 16 * s + 8 * (g >> 1) + 4 * c + (pl >> 2);
+            tv[c] = read_tr(vs + key * DH + pswz<SH::kPieces>(key, d >> 3) * 8 + (d & 7));
+          }
+          const s16x4_t a0 = tv[0], a1 = tv[1];
+          typedef short s16x8_t __attribute__((ext_vector_type(8)));
+          const s16x8_t av = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
           o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, av),
                                                           __builtin_bit_cast(bf16x8_t, bp), o[dt], 0, 0, 0);
         }
@@ -274,10 +287,10 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
           }
       }
     }
-    if (st + 1 < nst) store_stage((st + 1) & 1);
+    // the next stage has landed (this wave's copies), and every wave's after
+    // the barrier
+    vm_wait<0>();
     __syncthreads();
-    // the stores of the next stage went to the other buffer; this barrier
-    // also orders them before its reads
   }
 
   // out_p = O^T column / sum; lane half h holds dimensions 4h + e % 4 + 8 (e / 4)
