@@ -14,12 +14,12 @@
 //   k_gemm_nt     C[m][n] = sum_k A[n][k] B[m][k] (both operands row-major
 //                 with k contiguous: weights one output feature per row,
 //                 tokens one row each) plus bias, optionally GELU, rounded to
-//                 bf16. Block tile 256 features x 128 tokens, eight waves of
-//                 64 x 64 (2 x 2 v_mfma_f32_32x32x16_bf16 tiles); the weights
-//                 are the MFMA's A operand, so a lane's accumulator holds one
-//                 token and four consecutive features per group, stored as
-//                 8-byte pieces. Operands stream through a 3-stage LDS ring by
-//                 LDS DMA, 64 columns a stage, one barrier per stage.
+//                 bf16. Block tile 256 features x 256 tokens, four waves of
+//                 128 x 128 (4 x 4 v_mfma_f32_32x32x16_bf16 tiles); the
+//                 weights are the MFMA's A operand. Operands stream through a
+//                 2-stage LDS ring by LDS DMA, 64 columns a stage, one barrier
+//                 per stage; the output tile leaves through the same LDS, so
+//                 that its stores cover whole rows.
 #include <algorithm>
 
 #include "last_internal.h"
@@ -147,6 +147,7 @@ constexpr int kPerWave = kInstr / kGWaves;
 constexpr int kSteps = kGK / 16;             // MFMA k-steps per stage
 static_assert(kInstr % kGWaves == 0 && (kAPieces / 64) % kGWaves == 0, "even DMA split");
 static_assert(kRowPieces == 8 || kRowPieces == 4, "swizzle assumes 4 or 8 pieces a row");
+static_assert(kGN == 256 && kGM * kGN * 2 <= kRing * kStagePieces * 16, "the output tile is staged in the ring");
 
 // A row's pieces are permuted so that 16 consecutive rows read at one piece
 // index hit 16 distinct 16-byte bank groups.
@@ -291,20 +292,27 @@ __global__ __launch_bounds__(kGThreads, 1) void k_gemm_nt(const uint16_t *__rest
   }
   mma(cur);
 
-  // Epilogue: lane holds token m0 + 128 wm + 32 j + lane % 32 and features
-  // n0 + 128 wn + 32 i + 8 g + 4 (lane / 32) + 0..3 at elements 4 g .. 4 g + 3.
+  // Epilogue, in two passes through the ring (free once every wave is past
+  // its last fragment read). A lane's accumulators hold one token and
+  // scattered groups of four features (token m0 + 128 wm + 32 j + lane % 32,
+  // features n0 + 128 wn + 32 i + 8 g + 4 (lane / 32) + 0..3 at elements
+  // 4 g .. 4 g + 3); stored as they are, every 8-byte piece would land in a
+  // different cache line. So the block's 256 x 256 tile goes to LDS as bf16
+  // (rows of 32 16-byte pieces, piece index XOR token % 32 so that the 32
+  // tokens of a write spread over the banks), then leaves row by row, 32
+  // lanes covering a row's 512 bytes.
+  __syncthreads();
+  uint2 *ot2 = reinterpret_cast<uint2 *>(&ring[0][0]);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int64_t m = m0 + 128 * wm + 32 * j + r32;
-    if (m >= M) continue;
-    uint16_t *crow = C + m * N;
+    const int t = 128 * wm + 32 * j + r32;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int n = n0 + 128 * wn + 32 * i + 8 * g + 4 * half;
-        if (n >= N) continue;
-        const float4 bb = *reinterpret_cast<const float4 *>(bias + n);
+        const int nl = 128 * wn + 32 * i + 8 * g;
+        const int n = n0 + nl + 4 * half;
+        const float4 bb = n < N ? *reinterpret_cast<const float4 *>(bias + n) : make_float4(0.f, 0.f, 0.f, 0.f);
         float y0 = acc[i][j][4 * g + 0] + bb.x, y1 = acc[i][j][4 * g + 1] + bb.y;
         float y2 = acc[i][j][4 * g + 2] + bb.z, y3 = acc[i][j][4 * g + 3] + bb.w;
         if (GELU) {
@@ -313,11 +321,29 @@ __global__ __launch_bounds__(kGThreads, 1) void k_gemm_nt(const uint16_t *__rest
           y2 = gelu(y2);
           y3 = gelu(y3);
         }
-        uint2 w;
-        w.x = pack_bf16(y0, y1);
-        w.y = pack_bf16(y2, y3);
-        *reinterpret_cast<uint2 *>(crow + n) = w;
+        ot2[(t * 32 + ((nl >> 3) ^ (t & 31))) * 2 + half] = make_uint2(pack_bf16(y0, y1), pack_bf16(y2, y3));
       }
+  }
+  __syncthreads();
+  const uint4 *ot = &ring[0][0];
+  const int piece = threadIdx.x & 31;
+  const int n = n0 + 8 * piece;
+  // N is a multiple of 4: a piece is whole, half (8-byte aligned rows when
+  // N % 8 == 4) or past the end.
+  const bool whole = N % 8 == 0;
+#pragma unroll 4
+  for (int k = 0; k < kGM / (kGThreads / 32); ++k) {
+    const int t = k * (kGThreads / 32) + ((int)threadIdx.x >> 5);
+    const int64_t m = m0 + t;
+    if (m >= M || n >= N) continue;
+    const uint4 v = ot[t * 32 + (piece ^ (t & 31))];
+    uint16_t *dst = C + m * N + n;
+    if (whole) {
+      *reinterpret_cast<uint4 *>(dst) = v;
+    } else {
+      *reinterpret_cast<uint2 *>(dst) = make_uint2(v.x, v.y);
+      if (n + 4 < N) *reinterpret_cast<uint2 *>(dst + 4) = make_uint2(v.z, v.w);
+    }
   }
 }
 

@@ -127,6 +127,7 @@ CASES = [
     (5, 256, 192, 1024, 100),    # Dv of three stages, small Do
     (6, 40, 4160, 128, 64),      # rows too long for registers: streaming LayerNorm
     (7, 33, 2560, 256, 128),     # register LayerNorm with lanes short of pieces
+    (8, 520, 256, 512, 388),     # three token tiles, two feature tiles with half a piece at the end
 ]
 
 
