@@ -136,25 +136,59 @@ __device__ __forceinline__ void load_query_frags(const T *q, const Place<RT> &pl
   }
 }
 
-// Keys [j0, j0 + nk) of one KV head into an LDS stage by LDS DMA (no
-// registers held): wave w issues instructions w, w + kW, ... of the stage,
-// each filling 64 consecutive 16-byte slots; a slot's lane fetches the piece
-// the swizzle puts there. Slots past the last key repeat key nk - 1 (callers
-// never use them). kbase must be wave-uniform.
+// Keys of one KV head into the LDS stages by LDS DMA (no registers hold
+// them): wave w issues instructions w, w + kW, ... of a stage, each filling
+// 64 consecutive 16-byte slots; a slot's lane fetches the piece the swizzle
+// puts there. Instruction n + kPat covers the rows of instruction n moved by
+// a multiple of the swizzle's period, so a lane's offsets within a stage take
+// kPat registers, worked out once; the rest is wave-uniform.
 template <typename T, int DH>
-__device__ __forceinline__ void stage_dma(uint4 *buf, const char *kbase, int64_t kstride, int j0, int nk) {
-  using KR = KeyRow<T, DH>;
-  constexpr int NP = KR::kPieces;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int n = 0; n < KR::kStage / 64 / kW; ++n) {
-    const int ins = wave + kW * n;
-    const int sl = ins * 64 + lane, j = sl / NP;
-    const int p = (sl % NP) ^ (NP >= 16 ? (j & 15) : ((j >> 1) & 7));
-    const uint32_t voff = (uint32_t)((int64_t)(j0 + min(j, nk - 1)) * kstride + p * 16);
-    dma16(__builtin_amdgcn_readfirstlane(lds_u32(buf + ins * 64)), kbase, voff);
+struct KeyStager {
+  static constexpr int NP = KeyRow<T, DH>::kPieces;
+  static constexpr int kN = KeyRow<T, DH>::kStage / 64 / kW;
+  static constexpr int kRowsPer = 64 * kW / NP;              // stage rows one instruction covers
+  static constexpr int kPat = NP >= 16 ? NP / 16 : 1;        // swizzle period 16 rows
+  static_assert(kN % kPat == 0 && (kPat * kRowsPer) % 16 == 0, "swizzle period");
+  uint32_t roff[kPat];   // byte offsets of this lane's piece from the stage's first key
+  uint32_t dst0;         // LDS address of this wave's first slot in stage buffer 0
+  __device__ static void place(int n, int &j, int &p) {
+    const int sl = ((int)(threadIdx.x >> 6) + kW * n) * 64 + (int)(threadIdx.x & 63);
+    j = sl / NP;
+    p = (sl % NP) ^ (NP >= 16 ? (j & 15) : ((j >> 1) & 7));
   }
-}
+  // kstride * kSub must stay below 2^32 (checked by the launcher)
+  __device__ KeyStager(const uint4 *buf0, int64_t kstride) {
+#pragma unroll
+    for (int n = 0; n < kPat; ++n) {
+      int j, p;
+      place(n, j, p);
+      roff[n] = (uint32_t)(j * kstride + p * 16);
+    }
+    dst0 = __builtin_amdgcn_readfirstlane(lds_u32(buf0 + (threadIdx.x >> 6) * 64));
+  }
+  // Keys [j0, j0 + kSub) of the chunk at kbase (nk keys) into stage buffer
+  // b; slots at or past key nk repeat key nk - 1 (callers never use them).
+  // kbase must be wave-uniform.
+  __device__ void issue(int b, const char *kbase, int64_t kstride, int j0, int nk) const {
+    const uint32_t d = dst0 + (uint32_t)b * (KeyRow<T, DH>::kStage * 16);
+    if (j0 + kSub <= nk) {
+#pragma unroll
+      for (int n = 0; n < kN; ++n) {
+        const char *base = (const char *)uniform_ptr(kbase + (int64_t)(j0 + n / kPat * kPat * kRowsPer) * kstride);
+        dma16(d + n * (kW * 64 * 16), base, roff[n % kPat]);
+      }
+    } else {
+      const char *base = (const char *)uniform_ptr(kbase + (int64_t)j0 * kstride);
+      const int last = nk - 1 - j0;
+#pragma unroll
+      for (int n = 0; n < kN; ++n) {
+        int j, p;
+        place(n, j, p);
+        dma16(d + n * (kW * 64 * 16), base, (uint32_t)(min(j, last) * kstride + p * 16));
+      }
+    }
+  }
+};
 
 // Dots (unscaled logits) of the wave's 32 query rows with the 32 keys of
 // stage key tile kt.
@@ -349,12 +383,13 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_rows_stats
     vz[v] = 0.f;
   }
 
-  stage_dma<T, DH>(s_k[0], kbase, kstride, 0, nk);
+  const KeyStager<T, DH> stager(s_k[0], kstride);
+  stager.issue(0, kbase, kstride, 0, nk);
   vm_wait<0>();
   __syncthreads();
   const int nst = (nk + kSub - 1) / kSub;
   for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) stage_dma<T, DH>(s_k[(st + 1) & 1], kbase, kstride, (st + 1) * kSub, nk - (st + 1) * kSub);
+    if (st + 1 < nst) stager.issue((st + 1) & 1, kbase, kstride, (st + 1) * kSub, nk);
     if (pl.active) {
       const int s0 = kb + st * kSub;                         // first key position of the stage
       const int s1 = s0 + kSub - 1;                          // last
@@ -563,12 +598,13 @@ __global__ __launch_bounds__(kThreads, sizeof(T) == 2 ? 2 : 1) void k_rows_visua
   const int64_t kstride = (int64_t)Hkv * DH * sizeof(T);
   const char *kbase = (const char *)uniform_ptr(k + (((int64_t)l * T_total + tok0 + vlo + ib) * Hkv + kv) * DH);
 
-  stage_dma<T, DH>(s_k[0], kbase, kstride, 0, nk);
+  const KeyStager<T, DH> stager(s_k[0], kstride);
+  stager.issue(0, kbase, kstride, 0, nk);
   vm_wait<0>();
   __syncthreads();
   const int nst = (nk + kSub - 1) / kSub;
   for (int st = 0; st < nst; ++st) {
-    if (st + 1 < nst) stage_dma<T, DH>(s_k[(st + 1) & 1], kbase, kstride, (st + 1) * kSub, nk - (st + 1) * kSub);
+    if (st + 1 < nst) stager.issue((st + 1) & 1, kbase, kstride, (st + 1) * kSub, nk);
     float sum[RT];
 #pragma unroll
     for (int i = 0; i < RT; ++i) sum[i] = 0.f;
