@@ -52,7 +52,6 @@ constexpr int kThreads = 64 * kWaves;
 constexpr int kQB = 32 * kWaves;              // query positions per block
 constexpr int kKS = 64;                       // keys per LDS stage
 constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kLn2 = 0.6931471805599453f;
 
 template <int DH>
 struct Shape {
@@ -275,7 +274,8 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
                                                           __builtin_bit_cast(bf16x8_t, bp), o[dt], 0, 0, 0);
         }
       }
-      // the request's last row: its scaled visual logits, in natural units
+      // the request's last row: its visual logits, in the score pass's base-2
+      // units
       if (has_last && qpos == P - 1) {
 #pragma unroll
         for (int t = 0; t < 2; ++t)
@@ -283,7 +283,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
           for (int e = 0; e < 16; ++e) {
             const int key = k0 + t * 32 + acc_key(half, e);
             if (key >= vlo && key < vhi && key < kend)
-              vlog[((int64_t)l * N_total + cu_vis[r] + key - vlo) * Hq + h] = sc[t][e] * scale;
+              vlog[((int64_t)l * N_total + cu_vis[r] + key - vlo) * Hq + h] = sc[t][e] * s2;
           }
       }
     }
@@ -310,7 +310,7 @@ __global__ __launch_bounds__(kThreads, 2) void k_prefill(
   }
   // the last row's statistics as one chunk of the score pass: (max, sum, visual sum)
   if (has_last && qpos == P - 1 && half == 0)
-    stats[((int64_t)l * Hq + h) * R + r] = make_float4(m * kLn2, lsum, vsum, 0.f);
+    stats[((int64_t)l * Hq + h) * R + r] = make_float4(m, lsum, vsum, 0.f);
 }
 
 // Per request: the number of 128-position query blocks, their prefix and the

@@ -64,6 +64,12 @@ constexpr int kSliceTokens = 256;           // visual tokens per finalize block
 constexpr int kMaxPairs = 4096;             // G * Hq handled by the finalize block
 constexpr int kScanMaxR = 1024;             // larger batches search count prefixes instead
 
+// Logits are kept in base-2 units (the softmax scale times log2 e, folded
+// into the dot's one multiply), so that every exponential is exp2f: one
+// v_exp_f32 plus the rescaling that keeps results below 2^-126 (which that
+// instruction flushes) as denormals, as expf does, in about half of expf's
+// instructions.
+
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 template <typename T, int DH>
@@ -275,7 +281,7 @@ __device__ __forceinline__ void chunk_epilogue(const float *s_log, float4 *s_par
     if (act) {
       for (int t = sl; t < nt; t += tph) m = fmaxf(m, s_log[t * Hq + h]);
       for (int t = sl; t < nt; t += tph) {
-        const float e = expf(s_log[t * Hq + h] - m);
+        const float e = exp2f(s_log[t * Hq + h] - m);
         z += e;
         if (t >= v_lo && t < v_hi) v += e;
       }
@@ -288,7 +294,7 @@ __device__ __forceinline__ void chunk_epilogue(const float *s_log, float4 *s_par
       float Z = 0.f, V = 0.f;
       for (int x = 0; x < tph; ++x) {
         const float4 e = s_part[threadIdx.x + x];
-        const float f = e.x == -INFINITY ? 0.f : expf(e.x - M);
+        const float f = e.x == -INFINITY ? 0.f : exp2f(e.x - M);
         Z = fmaf(e.y, f, Z);
         V = fmaf(e.z, f, V);
       }
@@ -494,7 +500,7 @@ __global__ __launch_bounds__(kThreads) void k_score_partial(
     float z = 0.f, v = 0.f;
     if (hh < gh)
       for (int t = threadIdx.x; t < nt; t += kThreads) {
-        const float e = expf(s_logit[hh * CH + t] - m[hh]);
+        const float e = exp2f(s_logit[hh * CH + t] - m[hh]);
         z += e;
         if (t >= vb && t < ve) v += e;
       }
@@ -593,18 +599,18 @@ __global__ __launch_bounds__(kThreads) void k_score_merge(
   for (int c = c0 + lane; c < c1; c += 64) {
     const float4 e = st[c];
     if (e.x > m) {
-      const float f = m == -INFINITY ? 0.f : expf(m - e.x);
+      const float f = m == -INFINITY ? 0.f : exp2f(m - e.x);
       z = fmaf(z, f, e.y);
       v = fmaf(v, f, e.z);
       m = e.x;
     } else {
-      const float f = expf(e.x - m);
+      const float f = exp2f(e.x - m);
       z = fmaf(e.y, f, z);
       v = fmaf(e.z, f, v);
     }
   }
   const float M = wave_max(m);
-  const float f = m == -INFINITY ? 0.f : expf(m - M);
+  const float f = m == -INFINITY ? 0.f : exp2f(m - M);
   const float Z = wave_sum(z * f), V = wave_sum(v * f);
   if (lane == 0) {
     rowstat[(int64_t)r * GH + p] = make_float2(M, 1.0f / Z);
@@ -661,13 +667,13 @@ __global__ __launch_bounds__(kThreads) void k_score_finalize(
       if ((Hq & 3) == 0) {
         for (int h = 0; h < Hq; h += 4) {
           const float4 x = *reinterpret_cast<const float4 *>(lg + h);
-          acc = fmaf(expf(x.x - mz[h].x), mz[h].y, acc);
-          acc = fmaf(expf(x.y - mz[h + 1].x), mz[h + 1].y, acc);
-          acc = fmaf(expf(x.z - mz[h + 2].x), mz[h + 2].y, acc);
-          acc = fmaf(expf(x.w - mz[h + 3].x), mz[h + 3].y, acc);
+          acc = fmaf(exp2f(x.x - mz[h].x), mz[h].y, acc);
+          acc = fmaf(exp2f(x.y - mz[h + 1].x), mz[h + 1].y, acc);
+          acc = fmaf(exp2f(x.z - mz[h + 2].x), mz[h + 2].y, acc);
+          acc = fmaf(exp2f(x.w - mz[h + 3].x), mz[h + 3].y, acc);
         }
       } else {
-        for (int h = 0; h < Hq; ++h) acc = fmaf(expf(lg[h] - mz[h].x), mz[h].y, acc);
+        for (int h = 0; h < Hq; ++h) acc = fmaf(exp2f(lg[h] - mz[h].x), mz[h].y, acc);
       }
     }
     scores[n0 + i] = acc * invS;
@@ -742,10 +748,10 @@ __global__ __launch_bounds__(kThreads) void k_score_finalize_c(
         const int k = j * kThreads + t, tok = tok_of(k), jj = k - tok * P;
         if (tok < cnt) {
           const float2 *mz = sMZ + l * Hq + 4 * jj;
-          float v = expf(x[q].x - mz[0].x) * mz[0].y;
-          v = fmaf(expf(x[q].y - mz[1].x), mz[1].y, v);
-          v = fmaf(expf(x[q].z - mz[2].x), mz[2].y, v);
-          v = fmaf(expf(x[q].w - mz[3].x), mz[3].y, v);
+          float v = exp2f(x[q].x - mz[0].x) * mz[0].y;
+          v = fmaf(exp2f(x[q].y - mz[1].x), mz[1].y, v);
+          v = fmaf(exp2f(x[q].z - mz[2].x), mz[2].y, v);
+          v = fmaf(exp2f(x[q].w - mz[3].x), mz[3].y, v);
           s_part[(l * kThreads + tok) * PS + jj] = v;
         }
       }
@@ -775,11 +781,11 @@ __global__ __launch_bounds__(kThreads) void k_rows_finalize(
   float M = -INFINITY;
   for (int c = c0; c < c1; ++c) M = fmaxf(M, st[c].x);
   float Z = 0.f;
-  for (int c = c0; c < c1; ++c) Z = fmaf(st[c].y, expf(st[c].x - M), Z);
+  for (int c = c0; c < c1; ++c) Z = fmaf(st[c].y, exp2f(st[c].x - M), Z);
   const float invZ = 1.0f / Z;
   float *row = rows + (int64_t)p * T_total;
   for (int t = cu_seqlens[r] + threadIdx.x; t < cu_seqlens[r + 1]; t += kThreads)
-    row[t] = expf(row[t] - M) * invZ;
+    row[t] = exp2f(row[t] - M) * invZ;
 }
 
 template <typename T, int DH>
@@ -935,6 +941,8 @@ hipError_t launch_scores(const last_batch *b, const ScorePlan &p, const ScoreWs 
   // the debug rows read the chunk prefixes directly, so they are always computed then
   hipError_t e = launch_score_plan(b, p, w, row_pos, s, attn_rows != nullptr);
   if (e != hipSuccess) return e;
+  // logits in base-2 units
+  scale = (float)((double)scale * 1.4426950408889634);
 
   const bool bf = b->qk_dtype == LAST_BF16;
   if (p.stream)
