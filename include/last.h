@@ -183,8 +183,6 @@ size_t last_rows_scores_workspace(const last_batch *b, const int32_t *cu_rows_h,
  * One row per request (Last, First, Middle) runs the streamed single-row
  * kernels; several rows (All Mean) run two matrix-core passes over the keys:
  * row statistics, then the visual probabilities summed over rows and heads.
- * Those passes need a token's keys (Hkv x Dh elements) under 32 MiB
- * (LAST_ERR_UNSUPPORTED otherwise).
  * The result with one row per request at P_r - 1 equals last_token_scores.
  */
 last_status last_rows_scores(const last_batch *b, const int32_t *cu_rows,

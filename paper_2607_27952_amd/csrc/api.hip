@@ -192,11 +192,6 @@ static last_status check_rows(const last_batch *b, const int32_t *cu_rows_h, con
     for (int32_t m = cu_rows_h[r]; m < cu_rows_h[r + 1]; ++m)
       if (row_pos_h[m] < b->vis_start_h[r] || row_pos_h[m] >= P) return LAST_ERR_INVALID;
   }
-  // the multi-row passes address a 128-key stage with 32-bit offsets
-  bool multi = false;
-  for (int32_t r = 0; r < b->R; ++r) multi |= cu_rows_h[r + 1] - cu_rows_h[r] != 1;
-  if (multi && (int64_t)b->Hkv * b->Dh * (b->qk_dtype == LAST_BF16 ? 2 : 4) >= (int64_t)1 << 25)
-    return LAST_ERR_UNSUPPORTED;
   return LAST_OK;
 }
 

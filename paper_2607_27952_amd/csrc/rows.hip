@@ -156,7 +156,8 @@ struct KeyStager {
     j = sl / NP;
     p = (sl % NP) ^ (NP >= 16 ? (j & 15) : ((j >> 1) & 7));
   }
-  // kstride * kSub must stay below 2^32 (checked by the launcher)
+  // kstride * kSub < 2^32: a batch has at most 4096 (layer, head) pairs, so
+  // a token's keys take at most 4096 x 128 x 4 bytes
   __device__ KeyStager(const uint4 *buf0, int64_t kstride) {
 #pragma unroll
     for (int n = 0; n < kPat; ++n) {
