@@ -157,16 +157,12 @@ __device__ __forceinline__ void tile_ij_upper(int t, int nb, int &I, int &J) {
 // tiles that run together share few row blocks and re-read them from cache,
 // not HBM. The caps bound every write.
 constexpr int kRegion = 8;
-__global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ cu_vis,
-                                                   const int32_t *__restrict__ dtile_off,
-                                                   const int32_t *__restrict__ otile_off,
-                                                   const int64_t *__restrict__ d_off,
-                                                   int64_t diag_cap, int64_t off_cap,
-                                                   TileMeta *__restrict__ dtile,
-                                                   TileMeta *__restrict__ otile) {
-  const int r = blockIdx.x;
+// Request r's tiles, given its first diagonal tile pd (of td in all) and its
+// first off-diagonal tile po.
+__device__ void fill_request_tiles(const int32_t *__restrict__ cu_vis, int r, int R, int64_t pd, int64_t td,
+                                   int64_t po, int64_t doff, int64_t diag_cap, int64_t off_cap,
+                                   TileMeta *__restrict__ dtile, TileMeta *__restrict__ otile) {
   const int n0 = cu_vis[r], N = cu_vis[r + 1] - n0;
-  const int64_t doff = d_off[r];
   auto meta = [&](int I, int J) {
     TileMeta m;
     m.n0 = n0;
@@ -177,21 +173,20 @@ __global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ c
     m.pad = 0;
     return m;
   };
-  const int nbr = (N + kTile - 1) / kTile;
-  const int64_t o1 = min((int64_t)otile_off[r] + (int64_t)nbr * (nbr - 1) / 2, off_cap);
+  const int nb = (N + kTile - 1) / kTile;
+  const int64_t o1 = min(po + (int64_t)nb * (nb - 1) / 2, off_cap);
   // Diagonal tiles: the first nb - 1 row blocks of every request in request
   // order, then the last row block of every request (it may be partial), so
   // that a grid-stride walk meets the full tiles first.
   {
-    const int nbd = dtile_off[r + 1] - dtile_off[r];
-    const int64_t head = dtile_off[r] - r, tail = (int64_t)dtile_off[gridDim.x] - gridDim.x;
-    for (int I = threadIdx.x; I < nbd; I += 256) {
-      const int64_t t = I + 1 < nbd ? head + I : tail + r;
+    const int64_t head = pd - r, tail = td - R;
+    for (int I = threadIdx.x; I < nb; I += 256) {
+      const int64_t t = I + 1 < nb ? head + I : tail + r;
       if (t < diag_cap) dtile[t] = meta(I, I);
     }
   }
-  const int nb = (N + kTile - 1) / kTile, nR = (nb + kRegion - 1) / kRegion;
-  int64_t base = otile_off[r];
+  const int nR = (nb + kRegion - 1) / kRegion;
+  int64_t base = po;
   for (int P = 0; P < nR; ++P)
     for (int Q = P; Q < nR; ++Q) {
       const int i0 = P * kRegion, hI = min(i0 + kRegion, nb) - i0;
@@ -211,6 +206,69 @@ __global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ c
       }
       base += cnt;
     }
+}
+
+// Tile descriptions, one block per request: every diagonal tile and every
+// tile strictly above the diagonal, with its row blocks packed as I << 16 | J.
+// Off-diagonal tiles are listed region by region (kRegion x kRegion row
+// blocks, regions in upper-triangle order, tiles I-major inside), so the
+// tiles that run together share few row blocks and re-read them from cache,
+// not HBM. The caps bound every write.
+__global__ __launch_bounds__(256) void k_tile_fill(const int32_t *__restrict__ cu_vis,
+                                                   const int32_t *__restrict__ dtile_off,
+                                                   const int32_t *__restrict__ otile_off,
+                                                   const int64_t *__restrict__ d_off,
+                                                   int64_t diag_cap, int64_t off_cap,
+                                                   TileMeta *__restrict__ dtile,
+                                                   TileMeta *__restrict__ otile) {
+  const int r = blockIdx.x, R = gridDim.x;
+  fill_request_tiles(cu_vis, r, R, dtile_off[r], dtile_off[R], otile_off[r], d_off[r], diag_cap, off_cap, dtile,
+                     otile);
+}
+
+// The same for a batch in request order (no ranking): the plan and the tile
+// lists in one launch, one block a request. A block sums the counts of the
+// requests before it (and of all of them, for the totals) itself, in a fixed
+// order, instead of reading k_select_plan's prefixes.
+__global__ __launch_bounds__(256) void k_plan_fill(const int32_t *__restrict__ cu_vis, int64_t diag_cap,
+                                                   int64_t off_cap, int32_t *__restrict__ dtile_off,
+                                                   int32_t *__restrict__ otile_off, int64_t *__restrict__ d_off,
+                                                   TileMeta *__restrict__ dtile, TileMeta *__restrict__ otile) {
+  __shared__ int64_t sh[4][4];
+  const int r = blockIdx.x, R = gridDim.x;
+  int64_t v[4] = {0, 0, 0, 0};   // diagonal, off-diagonal and matrix elements before r; diagonal in all
+  for (int q = threadIdx.x; q < R; q += 256) {
+    const int64_t N = cu_vis[q + 1] - cu_vis[q];
+    const int64_t nd = (N + kTile - 1) / kTile;
+    if (q < r) {
+      v[0] += nd;
+      v[1] += nd * (nd - 1) / 2;
+      v[2] += cov_elems(N);
+    }
+    v[3] += nd;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int x = 0; x < 4; ++x) {
+    for (int o = 32; o > 0; o >>= 1) v[x] += __shfl_xor(v[x], o);
+    if (lane == 0) sh[x][wave] = v[x];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int x = 0; x < 4; ++x) v[x] = sh[x][0] + sh[x][1] + sh[x][2] + sh[x][3];
+  if (threadIdx.x == 0) {
+    dtile_off[r] = (int32_t)v[0];
+    otile_off[r] = (int32_t)v[1];
+    d_off[r] = v[2];
+    if (r == R - 1) {
+      const int64_t N = cu_vis[r + 1] - cu_vis[r];
+      const int64_t nd = (N + kTile - 1) / kTile;
+      dtile_off[R] = (int32_t)(v[0] + nd);
+      otile_off[R] = (int32_t)(v[1] + nd * (nd - 1) / 2);
+      d_off[R] = v[2] + cov_elems(N);
+    }
+  }
+  fill_request_tiles(cu_vis, r, R, v[0], v[3], v[1], v[2], diag_cap, off_cap, dtile, otile);
 }
 
 // The coverage matrix holds -inf on its diagonal instead of a token's distance
@@ -1006,8 +1064,13 @@ namespace last {
 hipError_t launch_gram_plan(int32_t R, const SelectPlan &p, const SelectWs &w, const int32_t *cu_vis,
                             hipStream_t s) {
   launch_begin("select_plan", s);
-  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, p.ranked ? 1 : 0, w.dtile_off, w.otile_off,
-                     w.d_off, w.req_order);
+  if (!p.ranked) {
+    hipLaunchKernelGGL(k_plan_fill, dim3(R), dim3(256), 0, s, cu_vis, p.tiles_diag, p.tiles_off, w.dtile_off,
+                       w.otile_off, w.d_off, w.dtile, w.otile);
+    return launch_end(s);
+  }
+  hipLaunchKernelGGL(k_select_plan, dim3(1), dim3(256), 0, s, cu_vis, R, 1, w.dtile_off, w.otile_off, w.d_off,
+                     w.req_order);
   hipLaunchKernelGGL(k_tile_fill, dim3(R), dim3(256), 0, s, cu_vis, w.dtile_off, w.otile_off, w.d_off,
                      p.tiles_diag, p.tiles_off, w.dtile, w.otile);
   return launch_end(s);
