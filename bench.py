@@ -376,7 +376,8 @@ def measure(args, name, budget, steps, warmup, source="last", prefill=False, con
         ws_s = torch.empty(last.prefill_attention_workspace(b), dtype=torch.uint8, device=dev)
     else:
         ws_s = torch.empty(last.token_scores_workspace(b, dw.q.dtype), dtype=torch.uint8, device=dev)
-    ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype), dtype=torch.uint8, device=dev)
+    ws_k = torch.empty(last.select_workspace(wl.cu_vis, wl.Dv, dw.feats.dtype, pair=overlap), dtype=torch.uint8,
+                       device=dev)
 
     conn = None
     if connector:

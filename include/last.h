@@ -215,7 +215,9 @@ last_status last_prefill_attention(const last_batch *b, const void *q, const voi
                                    const void *v, void *out, float *scores, void *ws,
                                    size_t ws_bytes, void *stream);
 
-/* Workspace bytes diverse_select needs (0 if the arguments are invalid). */
+/* Workspace bytes diverse_select needs (0 if the arguments are invalid):
+ * for the k-center, those of the form it will take (see diverse_select),
+ * which LAST_KCENTER_FORM, read at every call, can change. */
 size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,
                                 last_dtype fdtype, last_sel_mode mode);
 
@@ -227,10 +229,27 @@ size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,
  *              negative or NaN entries are treated as 0)
  *   feats      [N_total][Dv] encoder features X of the visual tokens,
  *              row-major, fdtype (LAST_F32 or LAST_BF16); 1 <= Dv <= 65536
- *   cu_vis     [R+1] as in last_batch; N_r <= 131072 per request (k-center
- *              keeps 4 ceil(N_r/128)^2 128^2 bytes of coverage distances per
- *              request in the workspace: 17 GB at 65536 tokens, 69 GB at
- *              131072). Requests longer than 32768 tokens (and longer than
+ *   cu_vis     [R+1] as in last_batch; N_r <= 131072 per request. The
+ *              k-center takes one of two forms with the same results, bit
+ *              for bit:
+ *              - the matrix: all coverage distances of each request at once
+ *                (4 ceil(N_r/128)^2 128^2 bytes of workspace per request:
+ *                17 GB at 65536 tokens, 69 GB at 131072), then the greedy;
+ *              - the rounds (bf16 features, Dv a multiple of 256 up to 4096,
+ *                N_r <= 32768): only the distances to the tokens picked (the
+ *                paper's O(K N d_v) form, about 1 KB of workspace per token
+ *                and 148 KB per request), computed for up to 64 picks at a
+ *                time; the picks of a round are certified exact against every
+ *                token outside its 192 candidates.
+ *              By default the rounds take batches whose every request has
+ *              8192 tokens or more and the shapes above; the environment
+ *              variable LAST_KCENTER_FORM=gram or =rounds forces one (rounds
+ *              only where those shapes allow). The rounds run as a queue of
+ *              tasks on one block per compute unit in which no block waits
+ *              for one that has not started; a wait longer than 10 s (the
+ *              device kept busy by other work) fills every unfinished
+ *              request's kept and order with -1 and its gains with NaN.
+ *              In the matrix form, requests longer than 32768 tokens (and longer than
  *              8192 when the batch is small) run the greedy on several
  *              compute units that exchange their candidates every step; if
  *              they cannot all run at once for 10 s (the device kept full
@@ -239,7 +258,7 @@ size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv,
  *              very end may leave some of the request's valid indices
  *              beside the -1 entries; either way the request is invalid).
  *              The environment variable LAST_MC_WAIT_US, read at every
- *              call, replaces the 10 s (in microseconds)
+ *              call, replaces the 10 s of either form (in microseconds)
  *   cu_keep    [R+1] budgets: K_r = cu_keep[r+1]-cu_keep[r], 1 <= K_r <= N_r
  *              (use last_budget for K = ceil(rho N), Eq. 2)
  *   kept       [K_total] out: the selected request-local indices, ascending
@@ -268,8 +287,10 @@ last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype,
  * same batch are still being computed (Eq. 6-8), and join the streams before
  * the pick call. Together the two calls enqueue the same kernels as one
  * diverse_select call and give bit-identical kept, order and gains.
- *   ws         the diverse_select_workspace(R, cu_vis_h, Dv, fdtype,
- *              LAST_SEL_KCENTER) bytes, 256-byte aligned. The similarity
+ *   ws         the diverse_select_similarity_workspace(R, cu_vis_h, Dv,
+ *              fdtype) bytes, 256-byte aligned. The two calls always take the
+ *              matrix form (the pick call has no features to fold rounds
+ *              with). The similarity
  *              call writes the distances there; the pick call reads them, so
  *              both calls take the same workspace and the same R, Dv, fdtype
  *              and cu_vis (checked only for shape; distances of other
@@ -280,6 +301,8 @@ last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype,
  * Arguments, errors and outputs are otherwise those of diverse_select; the
  * similarity call does not need the scores, the pick call not the features.
  */
+size_t diverse_select_similarity_workspace(int32_t R, const int32_t *cu_vis_h,
+                                           int32_t Dv, last_dtype fdtype);
 last_status diverse_select_similarity(int32_t R, int32_t Dv, last_dtype fdtype,
                                       const void *feats, const int32_t *cu_vis,
                                       const int32_t *cu_vis_h, void *ws,

@@ -398,17 +398,27 @@ last_status last_prefill_attention(const last_batch *b, const void *q, const voi
   return e == hipSuccess ? LAST_OK : LAST_ERR_DEVICE;
 }
 
+// Workspace of a selection plan: its carve, then scratch for the pick order
+// and gains when the caller does not want them.
+static size_t select_ws_bytes(int32_t R, const SelectPlan &p, last_sel_mode mode) {
+  size_t bytes = 0;
+  carve_select_ws(nullptr, R, p, mode, &bytes);
+  bytes += align_up((size_t)p.N_total * sizeof(int32_t), 256) + align_up((size_t)p.N_total * sizeof(float), 256);
+  return bytes;
+}
+
 size_t diverse_select_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv, last_dtype fdtype,
                                 last_sel_mode mode) {
   if (check_select(R, cu_vis_h, Dv, fdtype, mode, nullptr) != LAST_OK) return 0;
-  // The budgets do not change the workspace; size the scratch order/gains for K_r = N_r.
-  std::vector<int32_t> cu_keep(cu_vis_h, cu_vis_h + R + 1);
-  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_keep.data(), mode);
-  size_t bytes = 0;
-  carve_select_ws(nullptr, R, p, mode, &bytes);
-  // scratch for the pick order and gains when the caller does not want them
-  bytes += align_up((size_t)p.N_total * sizeof(int32_t), 256) + align_up((size_t)p.N_total * sizeof(float), 256);
-  return bytes;
+  // The budgets change neither the form nor the workspace; plan with K_r = N_r.
+  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_vis_h, mode, Dv, fdtype, false, true);
+  return select_ws_bytes(R, p, mode);
+}
+
+size_t diverse_select_similarity_workspace(int32_t R, const int32_t *cu_vis_h, int32_t Dv, last_dtype fdtype) {
+  if (check_select(R, cu_vis_h, Dv, fdtype, LAST_SEL_KCENTER, nullptr) != LAST_OK) return 0;
+  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_vis_h, LAST_SEL_KCENTER, Dv, fdtype, false, false);
+  return select_ws_bytes(R, p, LAST_SEL_KCENTER);
 }
 
 last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode mode,
@@ -421,8 +431,8 @@ last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mo
   if (st != LAST_OK) return st;
   if (!scores || !feats || !cu_vis || !cu_keep || !kept) return LAST_ERR_INVALID;
   if (!aligned(feats, 16)) return LAST_ERR_INVALID;
-  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_keep_h, mode, true, Dv);
-  size_t need = diverse_select_workspace(R, cu_vis_h, Dv, fdtype, mode);
+  const SelectPlan p = make_select_plan(R, cu_vis_h, cu_keep_h, mode, Dv, fdtype, true, true);
+  const size_t need = select_ws_bytes(R, p, mode);
   if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
   size_t used = 0;
   const SelectWs w = carve_select_ws(ws, R, p, mode, &used);
@@ -439,9 +449,9 @@ last_status diverse_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mo
 // (R, cu_vis_h, Dv, fdtype) give the same layout in both calls.
 static last_status kcenter_ws(int32_t R, const int32_t *cu_vis_h, int32_t Dv, last_dtype fdtype,
                               void *ws, size_t ws_bytes, SelectPlan *p, SelectWs *w) {
-  const size_t need = diverse_select_workspace(R, cu_vis_h, Dv, fdtype, LAST_SEL_KCENTER);
+  *p = make_select_plan(R, cu_vis_h, cu_vis_h, LAST_SEL_KCENTER, Dv, fdtype, false, false);
+  const size_t need = select_ws_bytes(R, *p, LAST_SEL_KCENTER);
   if (!ws || ws_bytes < need || !aligned(ws, 256)) return LAST_ERR_WORKSPACE;
-  *p = make_select_plan(R, cu_vis_h, cu_vis_h, LAST_SEL_KCENTER);
   size_t used = 0;
   *w = carve_select_ws(ws, R, *p, LAST_SEL_KCENTER, &used);
   return LAST_OK;

@@ -127,6 +127,20 @@ constexpr int kSelMaxN = 131072;     // largest request diverse_select takes
 constexpr int kGreedyMaxN = 32768;   // largest request one block's registers hold (k_greedy, k_topk)
 constexpr int kMcSlotWords = 256;    // exchange words per request of the multi-block greedy
 
+// The k-center in rounds (rounds.hip), without the N x N matrix: candidates
+// a round, picks a round, tokens a fold task, and the largest Dv and N_r it
+// takes (its candidate-Gram chunks and select keys live in LDS).
+constexpr int kRoundCands = 192;
+constexpr int kRoundPicks = 64;
+constexpr int kRoundPairs = (kRoundCands / 32) * (kRoundCands / 32 + 1) / 2;   // 32 x 32 block pairs of the candidate Gram
+constexpr int kRoundFoldRows = 256;
+constexpr int kRoundMaxDv = 4096;
+constexpr int kRoundMaxN = 32768;
+// diverse_select takes the rounds by default when every request has at least
+// this many tokens (measured: the matrix form is faster on batches with
+// shorter requests)
+constexpr int kRoundAutoN = 8192;
+
 // A request's coverage matrix is stored as nb x nb tiles of 128 x 128 floats
 // (nb = ceil(N_r / 128)), tile (I, J) at element (I * nb + J) * 128 * 128 and
 // row-major inside. A Gram tile then writes two contiguous 64 KB blocks (its
@@ -173,6 +187,8 @@ struct SelectPlan {
   int32_t group_rank0[kMaxGroups + 1];  // rank range of each group
   int32_t group_threads[kMaxGroups], group_ept[kMaxGroups];  // greedy shape per group
   int32_t group_slices[kMaxGroups];
+  bool rounds;             // the k-center in rounds (rounds.hip) instead of the matrix
+  int64_t round_Q;         // tasks a round of the rounds kernel
 };
 
 struct SelectWs {
@@ -184,13 +200,33 @@ struct SelectWs {
   float *dmat;                     // coverage distances, tile-major per request (cov_index)
   int32_t *req_order;              // [R] the request of each rank (ranked plans)
   unsigned long long *mc_slots;    // [R][kMcSlotWords] exchange words of the multi-block greedy, by rank
+  // the rounds form (nn and inv as above; nothing else of the matrix form)
+  float *r_dl;                     // [N_total] running minimum coverage distance
+  int32_t *r_cand, *r_picks;       // [R][kRoundCands], [R][kRoundPicks]
+  float *r_cmat;                   // [R][kRoundCands][kRoundCands] candidate distances
+  int32_t *r_st;                   // [R][4] request state
+  unsigned long long *r_T;         // [R] bound keys
+  uint32_t *r_dcnt;                // [R] completed tasks
+  int64_t *r_qoff;                 // [R + 1] task prefixes
+  unsigned long long *r_ctl;       // [2] next task, live requests and the abort word
 };
 
 // allow_groups: a single diverse_select call may pipeline a ragged batch (the
 // two-call form keeps one group, so both of its calls see the same plan); Dv
-// enters only that schedule's cost model.
+// enters that schedule's cost model. allow_rounds: the k-center may run in
+// rounds (single calls only: the pick call of the two-call form has no
+// features); whether it does depends on the shapes and LAST_KCENTER_FORM.
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,
-                            last_sel_mode mode, bool allow_groups = false, int32_t Dv = 0);
+                            last_sel_mode mode, int32_t Dv, last_dtype fdtype, bool allow_groups,
+                            bool allow_rounds);
+// The rounds form: the shapes it takes, the norms (the first half, features
+// only), and the rounds themselves.
+bool rounds_supported(int32_t N_max, int32_t Dv, last_dtype fdtype);
+hipError_t launch_round_norms(int32_t Dv, const SelectPlan &p, const SelectWs &w, const void *feats,
+                              hipStream_t s);
+hipError_t launch_round_pick(int32_t R, int32_t Dv, const SelectPlan &p, const SelectWs &w, const float *scores,
+                             const void *feats, const int32_t *cu_vis, const int32_t *cu_keep, int32_t *kept,
+                             int32_t *order, float *gains, hipStream_t s);
 SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode mode,
                          size_t *bytes);
 hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode mode,

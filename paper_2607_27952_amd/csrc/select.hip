@@ -15,6 +15,7 @@
 // ranks the kept tokens for the pick order.
 #include <algorithm>
 #include <cstdlib>
+#include <cstring>
 #include <atomic>
 #include <math.h>
 
@@ -778,8 +779,22 @@ static void greedy_shape(int32_t n, int32_t nreq, int32_t budget, int32_t *threa
   }
 }
 
+// The k-center's form: the matrix (gram.hip + the greedy here) or the rounds
+// (rounds.hip). LAST_KCENTER_FORM=gram or =rounds, read at every call, forces
+// one (rounds only where rounds_supported); by default the rounds take
+// batches whose every request has kRoundAutoN tokens or more.
+static bool want_rounds(int32_t N_min, int32_t N_max, int32_t Dv, last_dtype fdtype) {
+  if (!rounds_supported(N_max, Dv, fdtype)) return false;
+  if (const char *env = getenv("LAST_KCENTER_FORM")) {
+    if (strcmp(env, "gram") == 0) return false;
+    if (strcmp(env, "rounds") == 0) return true;
+  }
+  return N_min >= kRoundAutoN;
+}
+
 SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *cu_keep_h,
-                            last_sel_mode mode, bool allow_groups, int32_t Dv) {
+                            last_sel_mode mode, int32_t Dv, last_dtype fdtype, bool allow_groups,
+                            bool allow_rounds) {
   SelectPlan p{};
   p.N_total = cu_vis_h[R];
   p.K_total = cu_keep_h[R];
@@ -805,6 +820,14 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   p.group_threads[0] = p.g_threads;
   p.group_ept[0] = p.g_ept;
   p.group_slices[0] = p.g_slices;
+  int32_t N_min = p.N_max;
+  for (int r = 0; r < R; ++r) N_min = std::min<int32_t>(N_min, cu_vis_h[r + 1] - cu_vis_h[r]);
+  if (allow_rounds && mode == LAST_SEL_KCENTER && want_rounds(N_min, p.N_max, Dv, fdtype)) {
+    p.rounds = true;
+    for (int r = 0; r < R; ++r)
+      p.round_Q += kRoundPairs + 2 + (cu_vis_h[r + 1] - cu_vis_h[r] + kRoundFoldRows - 1) / kRoundFoldRows;
+    return p;
+  }
   if (!allow_groups || mode != LAST_SEL_KCENTER || R < 2 || R > kRankMaxR) return p;
 
   // Ragged batches. A greedy takes about K_r (0.6 + 1.1e-4 N_r) microseconds
@@ -976,7 +999,19 @@ SelectWs carve_select_ws(void *ws, int32_t R, const SelectPlan &p, last_sel_mode
                          size_t *bytes) {
   Carver cv(ws);
   SelectWs w{};
-  if (mode == LAST_SEL_KCENTER) {
+  if (mode == LAST_SEL_KCENTER && p.rounds) {
+    w.nn = cv.take<double>(p.N_total + kTile);
+    w.inv = cv.take<double>(p.N_total + kTile);
+    w.r_dl = cv.take<float>(p.N_total);
+    w.r_cand = cv.take<int32_t>((int64_t)R * kRoundCands);
+    w.r_picks = cv.take<int32_t>((int64_t)R * kRoundPicks);
+    w.r_cmat = cv.take<float>((int64_t)R * kRoundCands * kRoundCands);
+    w.r_st = cv.take<int32_t>((int64_t)R * 4);
+    w.r_T = cv.take<unsigned long long>(R);
+    w.r_dcnt = cv.take<uint32_t>(R);
+    w.r_qoff = cv.take<int64_t>(R + 1);
+    w.r_ctl = cv.take<unsigned long long>(2);
+  } else if (mode == LAST_SEL_KCENTER) {
     w.dtile_off = cv.take<int32_t>(R + 1);
     w.otile_off = cv.take<int32_t>(R + 1);
     w.dtile = cv.take<TileMeta>(p.tiles_diag);
@@ -1007,6 +1042,11 @@ hipError_t launch_select(int32_t R, int32_t Dv, last_dtype fdtype, last_sel_mode
                          const SelectPlan &p, const SelectWs &w, const float *scores,
                          const void *feats, const int32_t *cu_vis, const int32_t *cu_keep,
                          int32_t *kept, int32_t *order, float *gains, hipStream_t s) {
+  if (mode == LAST_SEL_KCENTER && p.rounds) {
+    const hipError_t e = launch_round_norms(Dv, p, w, feats, s);
+    if (e != hipSuccess) return e;
+    return launch_round_pick(R, Dv, p, w, scores, feats, cu_vis, cu_keep, kept, order, gains, s);
+  }
   if (mode == LAST_SEL_KCENTER && p.groups > 1 && gram_streamed(fdtype, Dv))
     return launch_pipelined(R, Dv, p, w, scores, feats, cu_vis, cu_keep, kept, order, gains, s);
   if (mode == LAST_SEL_KCENTER) {

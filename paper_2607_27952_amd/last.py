@@ -26,7 +26,7 @@ SRC_LAST, SRC_FIRST, SRC_MIDDLE, SRC_ALL_MEAN = 0, 1, 2, 3
 
 EXPORTS = ("last_token_scores_workspace", "last_token_scores", "last_token_scores_static", "last_source_rows",
            "last_rows_scores_workspace", "last_rows_scores", "last_prefill_attention_workspace",
-           "last_prefill_attention", "diverse_select_workspace",
+           "last_prefill_attention", "diverse_select_workspace", "diverse_select_similarity_workspace",
            "diverse_select", "diverse_select_similarity", "diverse_select_pick", "gather_kept", "last_connector_workspace", "last_connector", "last_budget", "last_status_string", "last_version",
            "last_profile_enable", "last_profile_collect", "last_profile_reset",
            "last_profile_count", "last_profile_kernel")
@@ -77,6 +77,8 @@ def lib():
         L.last_prefill_attention.restype = I32
         L.diverse_select_workspace.argtypes = [I32, P, I32, I32, I32]
         L.diverse_select_workspace.restype = SZ
+        L.diverse_select_similarity_workspace.argtypes = [I32, P, I32, I32]
+        L.diverse_select_similarity_workspace.restype = SZ
         L.diverse_select.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P, P, P, P, SZ, P]
         L.diverse_select.restype = I32
         L.diverse_select_similarity.argtypes = [I32, I32, I32, P, P, P, P, SZ, P]
@@ -323,9 +325,13 @@ def prefill_attention(batch: Batch, q: torch.Tensor, k: torch.Tensor, v: torch.T
         return out, scores
 
 
-def select_workspace(cu_vis_h, Dv: int, f_dtype=torch.bfloat16, mode: int = KCENTER) -> int:
+def select_workspace(cu_vis_h, Dv: int, f_dtype=torch.bfloat16, mode: int = KCENTER, pair: bool = False) -> int:
+    """Workspace bytes of diverse_select, or (pair=True) of the two-call form
+    diverse_select_similarity + diverse_select_pick."""
     cv = _i32_host(cu_vis_h)
     code = LAST_BF16 if f_dtype == torch.bfloat16 else LAST_F32
+    if pair:
+        return int(lib().diverse_select_similarity_workspace(len(cv) - 1, _ptr(cv), Dv, code))
     return int(lib().diverse_select_workspace(len(cv) - 1, _ptr(cv), Dv, code, mode))
 
 

@@ -176,6 +176,35 @@ def test_select_workspace_and_small_workspace():
     assert last.lib().diverse_select_workspace(2, cv.ctypes.data, 0, last.LAST_BF16, last.KCENTER) == 0
 
 
+def test_kcenter_form_and_workspace(monkeypatch):
+    """The k-center's form decides its workspace: the rounds keep no N x N
+    matrix (about 1 KB a token and 148 KB a request), the matrix form 4 N_r^2
+    bytes. By default the rounds take batches whose every request has 8192
+    tokens or more (bf16, Dv a multiple of 256 up to 4096, N_r <= 32768);
+    LAST_KCENTER_FORM forces either; the two-call form always keeps the
+    matrix."""
+    L = last.lib()
+    long_ = np.array([0, 16384, 32768], np.int32)          # two 16384-token requests
+    mixed = np.array([0, 16384, 16384 + 500], np.int32)    # one short request
+    mat = (2 * 16384 * 16384) * 4
+    def ws(cv, Dv=3584, dt=last.LAST_BF16):
+        return L.diverse_select_workspace(2, cv.ctypes.data, Dv, dt, last.KCENTER)
+    monkeypatch.delenv("LAST_KCENTER_FORM", raising=False)
+    assert 0 < ws(long_) < 2 ** 20 * 40                    # rounds: no matrix
+    assert ws(mixed) > (16384 ** 2) * 4                    # matrix form
+    assert ws(long_, Dv=3600) > mat                        # Dv not a multiple of 256: matrix
+    assert ws(long_, dt=last.LAST_F32) > mat               # fp32 features: matrix
+    assert ws(long_, Dv=4352) > mat                        # wider than 4096: matrix
+    pair = L.diverse_select_similarity_workspace(2, long_.ctypes.data, 3584, last.LAST_BF16)
+    assert pair > mat
+    monkeypatch.setenv("LAST_KCENTER_FORM", "gram")
+    assert ws(long_) == pair
+    monkeypatch.setenv("LAST_KCENTER_FORM", "rounds")
+    assert ws(mixed) < 2 ** 20 * 40
+    big = np.array([0, 32769], np.int32)                   # past the rounds' 32768 tokens: matrix
+    assert L.diverse_select_workspace(1, big.ctypes.data, 256, last.LAST_BF16, last.KCENTER) > 32769 ** 2 * 4
+
+
 def _two_phase_call(phase, cv, ck, Dv=64, fdtype=last.LAST_BF16, ws_bytes=1 << 40, misalign=0):
     """Status of diverse_select_similarity ("sim") or diverse_select_pick ("pick"); every
     case here must be rejected on the host, so no buffer may change."""
@@ -207,7 +236,7 @@ def test_two_phase_select_rejects_what_diverse_select_rejects():
         assert _two_phase_call(ph, [0, 131073], [0, 5]) == U
         assert _two_phase_call(ph, [0, 10, 30], [0, 5, 6], Dv=60) == U
         cv = np.array([0, 100, 350], np.int32)
-        need = last.lib().diverse_select_workspace(2, cv.ctypes.data, 64, last.LAST_BF16, last.KCENTER)
+        need = last.lib().diverse_select_similarity_workspace(2, cv.ctypes.data, 64, last.LAST_BF16)
         assert _two_phase_call(ph, cv, [0, 5, 6], ws_bytes=need - 1) == W
 
 

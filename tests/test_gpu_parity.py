@@ -452,8 +452,8 @@ def _two_phase(dw_feats, cu_vis_h, cu_keep_h, make_scores):
     `make_scores()` on the current stream, then diverse_select_pick after a join."""
     main = torch.cuda.current_stream()
     side = torch.cuda.Stream()
-    ws = torch.empty(last.select_workspace(cu_vis_h, dw_feats.shape[-1], dw_feats.dtype), dtype=torch.uint8,
-                     device="cuda")
+    ws = torch.empty(last.select_workspace(cu_vis_h, dw_feats.shape[-1], dw_feats.dtype, pair=True),
+                     dtype=torch.uint8, device="cuda")
     cu_vis = torch.from_numpy(np.asarray(cu_vis_h, np.int32)).cuda()   # made on the main stream
     side.wait_stream(main)
     last.diverse_select_similarity(dw_feats, cu_vis_h, ws, cu_vis=cu_vis, stream=side)
