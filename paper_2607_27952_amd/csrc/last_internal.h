@@ -133,6 +133,7 @@ constexpr int kMcSlotWords = 256;    // exchange words per request of the multi-
 constexpr int kRoundCands = 192;
 constexpr int kRoundPicks = 64;
 constexpr int kRoundPairs = (kRoundCands / 32) * (kRoundCands / 32 + 1) / 2;   // 32 x 32 block pairs of the candidate Gram
+constexpr int kRoundCandTasks = kRoundPairs;                                      // one block pair a task
 constexpr int kRoundFoldRows = 256;
 constexpr int kRoundMaxDv = 4096;
 constexpr int kRoundMaxN = 32768;
@@ -207,7 +208,7 @@ struct SelectWs {
   int32_t *r_st;                   // [R][4] request state
   unsigned long long *r_T;         // [R] bound keys
   uint32_t *r_dcnt;                // [R] completed tasks
-  int64_t *r_qoff;                 // [R + 1] task prefixes
+  int64_t *r_qoff;                 // [R + 1] fold-tile prefixes
   unsigned long long *r_ctl;       // [2] next task, live requests and the abort word
 };
 

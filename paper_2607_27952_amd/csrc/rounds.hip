@@ -34,11 +34,12 @@
 //
 // Kernels:
 //   k_rnorm    |x_i|^2 and 1 / |x_i| of every token (one pass over X).
-//   k_rprep    task prefixes and the per-request state.
+//   k_rprep    fold-tile prefixes and the per-request state.
 //   k_rounds   the rounds, as a queue of tasks on a persistent grid; per
 //              request and round: S (select the candidates), C (one 32 x 32
 //              block pair of the candidate Gram each), G (the greedy on the
-//              candidates), F (fold the picks into 256 tokens each). A block
+//              candidates), F (fold the picks into 256 tokens each), listed
+//              round by round and, within a round, phase by phase. A block
 //              takes the next task index from a global counter and waits
 //              until the tasks it depends on (all with smaller indices, so
 //              already taken by running blocks) have completed: no block
@@ -77,7 +78,10 @@ constexpr int kFTokInstr = kFTokPieces / 64 / kRWaves;  // LDS-DMA instructions 
 static_assert(kFPickPieces == 64 * kRWaves, "one pick DMA instruction a wave");
 constexpr int kFPerWave = kFTokInstr + 1;
 constexpr int kMaxChunks = kRoundMaxDv / 128;
+constexpr int kCT = kRoundCandTasks;           // C tasks per request and round (one block pair each)
+static_assert(kCT == kRPairs, "C tasks");
 constexpr int kSelLds = kRoundMaxN;           // keys of a request held in LDS by the select
+constexpr int kFtLds = 2048;                  // fold-tile prefixes held in LDS (batches of fewer requests)
 static_assert(kRB % 64 == 0 && kRB <= 256, "candidate slots: whole waves");
 static_assert(kFRows == 32 * kRWaves, "a fold task: 32 tokens a wave");
 
@@ -159,7 +163,8 @@ struct RArgs {
   int32_t *st;                     // [R][4] picks so far, picks this round, candidates, finished
   unsigned long long *st_T;        // [R] the bound key T
   uint32_t *dcnt;                  // [R] completed tasks
-  const int64_t *qoff;             // [R + 1] task prefixes within a round
+  const int64_t *ftoff;            // [R + 1] fold-tile prefixes
+  const unsigned long long *ctl;   // live (low word) and abort (high word), read together
   unsigned long long *head;        // next task index
   uint32_t *live;                  // unfinished requests
   uint32_t *abort_word;            // set on a timeout or an impossible state
@@ -219,35 +224,46 @@ __device__ uint32_t block_sum_u32(uint32_t v, unsigned long long *sh) {
   return uniu(s);
 }
 
-// Tokens 0..N-1 in index order, kRThreads at a time; emit(rank, i) for the
-// first `limit` tokens with pred(i), rank = their order among those. Returns
-// how many were emitted. pred and emit run on the thread that owns i.
-template <typename Pred, typename Emit>
-__device__ int ordered_scan(int N, int limit, Pred pred, Emit emit, int *sh) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  int run = 0;
-  for (int base = 0; base < N && run < limit; base += kRThreads) {
-    const int i = base + (int)threadIdx.x;
-    const bool f = i < N && pred(i);
-    const unsigned long long m = __ballot(f);
-    if (lane == 0) sh[wave] = __popcll(m);
-    __syncthreads();
-    int before = 0, tot = 0;
+// Tokens 0..N-1 in index order: thread t owns the contiguous run of E =
+// ceil(N / kRThreads) <= 64 tokens from t E, tests them (loads issued eight at
+// a time) into a bit mask, and one block-wide scan of the counts orders the
+// runs. emit(rank, i) for the first `limit` tokens with test(load(i), i), on
+// the thread that owns i. Returns how many were emitted.
+template <typename Load, typename Test, typename Emit>
+__device__ int ordered_scan(int N, int limit, Load load, Test test, Emit emit, int *sh) {
+  const int E = (N + kRThreads - 1) / kRThreads;
+  const int i0 = (int)threadIdx.x * E;
+  // each thread starts its run at a different offset, so that the lanes of a
+  // wave read different LDS banks
+  const int rot = E > 1 ? (int)threadIdx.x % E : 0;
+  unsigned long long flags = 0ull;
+  for (int k0 = 0; k0 < E; k0 += 8) {
+    uint32_t v[8];
+    int e[8];
 #pragma unroll
-    for (int w = 0; w < kRWaves; ++w) {
-      const int c = sh[w];
-      if (w < wave) before += c;
-      tot += c;
+    for (int u = 0; u < 8; ++u) {
+      e[u] = k0 + u + rot;
+      e[u] -= e[u] >= E ? E : 0;
+      const int i = i0 + e[u];
+      v[u] = (k0 + u < E && i < N) ? load(i) : 0u;
     }
-    if (f) {
-      const int rank = run + before + __popcll(m & ((1ull << lane) - 1ull));
-      if (rank < limit) emit(rank, i);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = i0 + e[u];
+      if (k0 + u < E && i < N && test(v[u], i)) flags |= 1ull << e[u];
     }
-    run += uni(tot);
-    __syncthreads();
   }
-  return min(run, limit);
+  int total = 0;
+  int rank = block_exclusive_scan(__popcll(flags), sh, &total);
+  while (flags) {
+    const int e = __ffsll((long long)flags) - 1;
+    flags &= flags - 1ull;
+    if (rank < limit) emit(rank, i0 + e);
+    ++rank;
+  }
+  return min(uni(total), limit);
 }
+static_assert(kRoundMaxN <= 64 * kRThreads, "ordered_scan: one 64-bit mask a thread");
 
 // ------------------------------------------------------------------- norms
 // |x_i|^2 as the diagonal of a 32 x 32 MFMA Gram of 32 consecutive rows with
@@ -296,9 +312,9 @@ __global__ __launch_bounds__(256) void k_rnorm(const uint16_t *__restrict__ X, i
 }
 
 // ------------------------------------------------------------------- prep
-// Task prefixes (per request and round: S, kRPairs C tasks, G, one F task per
-// kFRows tokens), the state, the counters. One block.
-__global__ __launch_bounds__(1024) void k_rprep(const int32_t *__restrict__ cu_vis, int R, int64_t *__restrict__ qoff,
+// Fold-tile prefixes (one F task per kFRows tokens of a request), the state,
+// the counters. One block.
+__global__ __launch_bounds__(1024) void k_rprep(const int32_t *__restrict__ cu_vis, int R, int64_t *__restrict__ ftoff,
                                                 int32_t *__restrict__ st, uint32_t *__restrict__ dcnt,
                                                 unsigned long long *__restrict__ head, uint32_t *__restrict__ live,
                                                 uint32_t *__restrict__ abort_word) {
@@ -317,7 +333,7 @@ __global__ __launch_bounds__(1024) void k_rprep(const int32_t *__restrict__ cu_v
     int64_t c = 0;
     if (r < R) {
       const int N = cu_vis[r + 1] - cu_vis[r];
-      c = kRPairs + 2 + (N + kFRows - 1) / kFRows;
+      c = (N + kFRows - 1) / kFRows;
       st[4 * r + kStT] = 0;
       st[4 * r + kStNp] = 0;
       st[4 * r + kStNb] = 0;
@@ -336,12 +352,12 @@ __global__ __launch_bounds__(1024) void k_rprep(const int32_t *__restrict__ cu_v
       if (w < wave) before += sh[w];
       tot += sh[w];
     }
-    if (r < R) qoff[r] = s_run + before + x - c;
+    if (r < R) ftoff[r] = s_run + before + x - c;
     __syncthreads();
     if (threadIdx.x == 0) s_run += tot;
     __syncthreads();
   }
-  if (threadIdx.x == 0) qoff[R] = s_run;
+  if (threadIdx.x == 0) ftoff[R] = s_run;
 }
 
 // ------------------------------------------------------------------ tasks
@@ -353,12 +369,11 @@ struct Req {
 
 __device__ void finish_request(const RArgs &a, const Req &q, int *shi) {
   // kept = the tokens marked -inf, ascending (Eq. 12)
+  const uint32_t *dl = reinterpret_cast<const uint32_t *>(a.dl + q.n0);
   ordered_scan(
-      q.N, INT_MAX, [&](int i) { return ld_f32(a.dl + q.n0 + i) == -INFINITY; },
-      [&](int rank, int i) {
-        if (rank < q.K) a.kept[q.k0 + rank] = i;
-      },
-      shi);
+      q.N, q.K, [&](int i) { return ld_u32(dl + i); },
+      [&](uint32_t v, int) { return v == __float_as_uint(-INFINITY); },
+      [&](int rank, int i) { a.kept[q.k0 + rank] = i; }, shi);
   if (threadIdx.x == 0) {
     st_i32(a.st + 4 * q.r + kStFin, 1);
     __hip_atomic_fetch_add(a.live, 0xFFFFFFFFu, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -407,14 +422,26 @@ __device__ void task_select(const RArgs &a, SmAll &sm, const Req &q, unsigned lo
   // >= 0 (picked tokens: -inf or NaN)
   SmSelect &s = sm.s;
   uint32_t vmax = 0u, vmin = 0xFFFFFFFFu, nvalid = 0u;
-  for (int i = tid; i < q.N; i += kRThreads) {
-    const float o = clean_score(a.scores[q.n0 + i]) * ld_f32(a.dl + q.n0 + i);
-    const uint32_t v = o >= 0.f ? __float_as_uint(o) + 1u : 0u;
-    s.v[i] = v;
-    vmax = max(vmax, v);
-    if (v != 0u) {
-      vmin = min(vmin, v);
-      ++nvalid;
+  for (int base = 0; base < q.N; base += 8 * kRThreads) {
+    float d[8], w[8];   // eight loads in flight a thread
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = base + u * kRThreads + tid;
+      d[u] = i < q.N ? ld_f32(a.dl + q.n0 + i) : 0.f;
+      w[u] = i < q.N ? a.scores[q.n0 + i] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int i = base + u * kRThreads + tid;
+      if (i >= q.N) continue;
+      const float o = clean_score(w[u]) * d[u];
+      const uint32_t v = o >= 0.f ? __float_as_uint(o) + 1u : 0u;
+      s.v[i] = v;
+      vmax = max(vmax, v);
+      if (v != 0u) {
+        vmin = min(vmin, v);
+        ++nvalid;
+      }
     }
   }
   vmax = block_max_u32(vmax, shk);
@@ -425,8 +452,10 @@ __device__ void task_select(const RArgs &a, SmAll &sm, const Req &q, unsigned lo
     // the best objective is 0 (or none is a number): from here on every step
     // takes the lowest-index token not yet picked
     const int t0 = t, need = q.K - t;
+    const uint32_t *dl = reinterpret_cast<const uint32_t *>(a.dl + q.n0);
     ordered_scan(
-        q.N, need, [&](int i) { return ld_f32(a.dl + q.n0 + i) != -INFINITY; },
+        q.N, need, [&](int i) { return ld_u32(dl + i); },
+        [&](uint32_t v, int) { return v != __float_as_uint(-INFINITY); },
         [&](int rank, int i) {
           a.order[q.k0 + t0 + rank] = i;
           a.gains[q.k0 + t0 + rank] = 0.f;
@@ -440,26 +469,29 @@ __device__ void task_select(const RArgs &a, SmAll &sm, const Req &q, unsigned lo
     return;
   }
 
-  __shared__ uint32_t s_digit, s_want;
+  // Candidates: the tokens whose v exceeds a cut, at most kRB of them. The
+  // cut is a boundary of 256 bins of width 2^shift over [lo, hi], refined
+  // inside the bin that overflows kRB until at least kRB / 2 tokens lie above
+  // it; if that bin has shrunk to a single value, its lowest-index tokens
+  // fill the candidates up to kRB (at most four passes). T, the largest key
+  // not taken, bounds every other token for the rest of the round.
+  __shared__ uint32_t s_bin, s_acc;
   __shared__ int s_tie;
-  uint32_t vstar = 0u;    // candidates: v > vstar, and v == vstar below index tie
-  int tie = q.N;
+  uint32_t cut = 0u;   // candidates: v > cut, and (tie mode) v == cut at indices below tie
+  int tie = 0;
   unsigned long long T = 0ull;
   if (nvalid > (uint32_t)kRB) {
-    // the (kRB + 1)-th largest v, 8 bits at a time from the highest digit in
-    // which the valid keys differ
-    const uint32_t diff = vmin ^ vmax;
-    int top = diff ? 31 - __clz(diff) : 0;
-    uint32_t prefix = vmax & ~((top >= 31) ? 0u : ((2u << top) - 1u));
-    uint32_t mask = (top >= 31) ? 0u : ~((2u << top) - 1u);
-    uint32_t want = kRB + 1;
-    for (int shift = (top / 8) * 8; shift >= 0; shift -= 8) {
+    uint32_t lo = vmin, hi = vmax, above = 0u;   // `above`: valid tokens with v > hi
+    bool tied = false;
+    for (;;) {
+      const uint32_t d = hi - lo;
+      const int shift = d < 256u ? 0 : 24 - __clz(d);   // (hi - lo) >> shift < 256
       for (int x = tid; x < kRWaves * 257; x += kRThreads) (&s.hist[0][0])[x] = 0u;
       __syncthreads();
       const int wave = tid >> 6;
       for (int i = tid; i < q.N; i += kRThreads) {
         const uint32_t v = s.v[i];
-        if (v != 0u && (v & mask) == prefix) atomicAdd(&s.hist[wave][(v >> shift) & 255u], 1u);
+        if (v >= lo && v <= hi && v != 0u) atomicAdd(&s.hist[wave][(v - lo) >> shift], 1u);
       }
       __syncthreads();
       if (tid < 256) {
@@ -470,59 +502,83 @@ __device__ void task_select(const RArgs &a, SmAll &sm, const Req &q, unsigned lo
       }
       __syncthreads();
       if (tid < 64) {
-        // digits 4 lane .. 4 lane + 3; counts at or above each lane's digits
+        // bins 4 lane .. 4 lane + 3; the one bin whose tokens push the count
+        // (from the top) past kRB, and the count above it
         const uint32_t c0 = s.tot[4 * lane], c1 = s.tot[4 * lane + 1], c2 = s.tot[4 * lane + 2],
                        c3 = s.tot[4 * lane + 3];
         const uint32_t mine = c0 + c1 + c2 + c3;
-        uint32_t above = mine;   // inclusive suffix sum over lanes >= lane
+        uint32_t incl = mine;   // suffix sum over lanes >= lane
         for (int o = 1; o < 64; o <<= 1) {
-          const uint32_t y = __shfl_down(above, o);
-          if (lane + o < 64) above += y;
+          const uint32_t y = __shfl_down(incl, o);
+          if (lane + o < 64) incl += y;
         }
-        const uint32_t after = above - mine;   // lanes > lane
-        if (after < want && above >= want) {
-          uint32_t acc = after, d = 0, wv = want;
-          if (acc + c3 >= want) {
-            d = 3;
-            wv = want - acc;
-          } else if ((acc += c3) + c2 >= want) {
-            d = 2;
-            wv = want - acc;
-          } else if ((acc += c2) + c1 >= want) {
-            d = 1;
-            wv = want - acc;
+        const uint32_t after = above + incl - mine;
+        if (after <= (uint32_t)kRB && after + mine > (uint32_t)kRB) {
+          uint32_t acc = after, b;
+          if (acc + c3 > (uint32_t)kRB) {
+            b = 4 * lane + 3;
+          } else if ((acc += c3) + c2 > (uint32_t)kRB) {
+            b = 4 * lane + 2;
+          } else if ((acc += c2) + c1 > (uint32_t)kRB) {
+            b = 4 * lane + 1;
           } else {
             acc += c1;
-            d = 0;
-            wv = want - acc;
+            b = 4 * lane;
           }
-          s_digit = 4 * lane + d;
-          s_want = wv;
+          s_bin = b;
+          s_acc = acc;
         }
       }
       __syncthreads();
-      prefix |= uniu(s_digit) << shift;
-      mask |= 255u << shift;
-      want = uniu(s_want);
+      const uint32_t b = uniu(s_bin), acc = uniu(s_acc);
       __syncthreads();
+      const uint32_t blo = lo + (b << shift);
+      const uint32_t bhi = (uint32_t)min<uint64_t>((uint64_t)hi, (uint64_t)blo + ((1ull << shift) - 1ull));
+      if (acc >= (uint32_t)kRB / 2) {
+        cut = bhi;
+        break;
+      }
+      if (shift == 0) {   // one value: its lowest-index tokens fill the rest
+        cut = blo;
+        tied = true;
+        above = acc;
+        break;
+      }
+      lo = blo;
+      hi = bhi;
+      above = acc;
     }
-    vstar = prefix;
-    // the want-th token (in index order) with v == vstar bounds the rest
-    if (tid == 0) s_tie = q.N;
-    __syncthreads();
-    ordered_scan(
-        q.N, (int)want, [&](int i) { return s.v[i] == vstar; },
-        [&](int rank, int i) {
-          if (rank == (int)want - 1) s_tie = i;
-        },
-        shi);
-    tie = uni(s_tie);
-    T = ((unsigned long long)(vstar - 1u) << 32) | (0xFFFFFFFFu - (unsigned)tie);
+    if (tied) {
+      // the (kRB - above + 1)-th token (in index order) with v == cut bounds the rest
+      const int want = kRB - (int)above + 1;
+      if (tid == 0) s_tie = q.N;
+      __syncthreads();
+      const uint32_t c = cut;
+      ordered_scan(
+          q.N, want, [&](int i) { return s.v[i]; }, [&](uint32_t v, int) { return v == c; },
+          [&](int rank, int i) {
+            if (rank == want - 1) s_tie = i;
+          },
+          shi);
+      tie = uni(s_tie);
+      T = ((unsigned long long)(cut - 1u) << 32) | (0xFFFFFFFFu - (unsigned)tie);
+    } else {
+      // T: the largest key among the valid tokens at or below the cut
+      unsigned long long best = 0ull;
+      for (int i = tid; i < q.N; i += kRThreads) {
+        const uint32_t v = s.v[i];
+        const unsigned long long k =
+            (v != 0u && v <= cut) ? ((unsigned long long)(v - 1u) << 32) | (0xFFFFFFFFu - (unsigned)i) : 0ull;
+        best = k > best ? k : best;
+      }
+      T = block_max_u64(best, shk);
+    }
   }
-  const uint32_t vs = vstar;
+  const uint32_t vs = cut;
   const int ti = tie;
   const int nb = ordered_scan(
-      q.N, kRB, [&](int i) { const uint32_t v = s.v[i]; return v > vs || (v == vs && v != 0u && i < ti); },
+      q.N, kRB, [&](int i) { return s.v[i]; },
+      [&](uint32_t v, int i) { return v > vs || (v == vs && v != 0u && i < ti); },
       [&](int rank, int i) { st_i32(a.cand + (int64_t)q.r * kRB + rank, i); }, shi);
   if (tid == 0) {
     st_i32(a.st + 4 * q.r + kStNb, nb);
@@ -592,9 +648,15 @@ __device__ void task_greedy(const RArgs &a, SmAll &sm, const Req &q) {
   if (nb == 0) return;
   SmGreedy &g = sm.g;
   const float *M = a.cmat + (int64_t)q.r * kRB * kRB;
-  for (int x = tid; x < nb * nb; x += kRThreads) {
-    const int row = x / nb, col = x - row * nb;
-    g.mat[row * kRB + col] = ld_f32(M + (int64_t)row * kRB + col);
+  // rows 0..nb-1 whole (columns past nb are never read), eight loads in flight
+  const int ne = nb * kRB;
+  for (int x0 = tid; x0 < ne; x0 += 8 * kRThreads) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = x0 + u * kRThreads < ne ? ld_f32(M + x0 + u * kRThreads) : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (x0 + u * kRThreads < ne) g.mat[x0 + u * kRThreads] = v[u];
   }
   __syncthreads();
   if (wave != 0) return;
@@ -792,9 +854,14 @@ __global__ __launch_bounds__(kRThreads) void k_rounds(RArgs a) {
   __shared__ SmAll sm;
   __shared__ unsigned long long shk[kRWaves];
   __shared__ int shi[kRWaves];
-  __shared__ int s_task[4];   // status (0 run, 1 skip, 2 exit), request, kind, sub-index
+  __shared__ int s_task[4];   // status (0 run, 1 skip, 2 exit, 3 no task), request, kind, sub-index
+  __shared__ int s_ft[kFtLds];   // fold-tile prefixes of batches of fewer than kFtLds requests
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = uni(tid >> 6);
+  if (a.R < kFtLds)
+    for (int x = tid; x <= a.R; x += kRThreads) s_ft[x] = (int)a.ftoff[x];
+  __syncthreads();
+  auto ft_at = [&](int64_t i) -> int64_t { return a.R < kFtLds ? (int64_t)s_ft[i] : uni_i64(a.ftoff[i]); };
   int prev = -1;   // the request of the task this block has just completed
   for (;;) {
     // Wave 0 publishes the completed task (every wave waited for its stores
@@ -808,32 +875,81 @@ __global__ __launch_bounds__(kRThreads) void k_rounds(RArgs a) {
       }
       qi = uni64(qi);
       int status = 0, r = 0, kind = 0, sub = 0;
-      if (uniu(ld_u32(a.abort_word)) != 0u || uniu(ld_u32(a.live)) == 0u) {
+      const unsigned long long ctl = uni64(ld_u64(a.ctl));   // live requests | abort word << 32
+      if ((ctl >> 32) != 0ull || (uint32_t)ctl == 0u) {
         status = 2;
       } else {
-        const int64_t n = (int64_t)(qi / (unsigned long long)a.Q);
-        const int64_t u = (int64_t)qi - n * a.Q;
-        if (n > a.max_rounds) {
+        const int64_t m = (int64_t)(qi / (unsigned long long)a.Q);   // macro-round
+        const int64_t u = (int64_t)qi - m * a.Q;
+        if (m > a.max_rounds) {
           // every request ends by round K_r, and a block runs at most one
           // task ahead of the others: an index this far means a fault
           if (lane == 0) st_u32(a.abort_word, 1u);
           status = 2;
         } else {
-          int lo = 0, hi = a.R - 1;   // the last r with qoff[r] <= u
-          while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (uni_i64(a.qoff[mid]) <= u)
-              lo = mid;
-            else
-              hi = mid - 1;
+          // The requests form two halves, A = [0, RA) and B = [RA, R), half a
+          // round apart, so that one half's serial chain (select, candidate
+          // Gram, greedy) runs while the other half folds: macro-round m
+          // lists S, C (kCT each), G of A's round m, the folds of B's round
+          // m - 1, S, C, G of B's round m, then the folds of A's round m.
+          // Each task depends only on tasks listed before it.
+          const int64_t R = a.R, RA = (R + 1) / 2, RB = R - RA;
+          const int64_t FA = ft_at(RA), FB = ft_at(R) - FA;
+          int64_t n = m, x = u;
+          auto chain = [&](int64_t r0, int64_t nr) {   // S, C, G of requests [r0, r0 + nr); false: past them
+            if (x < nr) {
+              kind = 0;
+              r = (int)(r0 + x);
+              return true;
+            }
+            x -= nr;
+            if (x < nr * kCT) {
+              kind = 1;
+              r = (int)(r0 + x / kCT);
+              sub = (int)(x % kCT);
+              return true;
+            }
+            x -= nr * kCT;
+            if (x < nr) {
+              kind = 2;
+              r = (int)(r0 + x);
+              return true;
+            }
+            x -= nr;
+            return false;
+          };
+          auto folds = [&](int64_t r0, int64_t nr, int64_t nf) {   // F of requests [r0, r0 + nr)
+            if (x >= nf) {
+              x -= nf;
+              return false;
+            }
+            kind = 3;
+            const int64_t f = ft_at(r0) + x;
+            int lo = (int)r0, hi = (int)(r0 + nr - 1);   // the last r with ftoff[r] <= f
+            while (lo < hi) {
+              const int mid = (lo + hi + 1) >> 1;
+              if (ft_at(mid) <= f)
+                lo = mid;
+              else
+                hi = mid - 1;
+            }
+            r = lo;
+            sub = (int)(f - ft_at(r));
+            return true;
+          };
+          if (!chain(0, RA)) {
+            if (folds(RA, RB, FB)) {
+              n = m - 1;
+            } else if (!chain(RA, RB)) {
+              folds(0, RA, FA);
+            }
           }
-          r = lo;
-          const int64_t q0 = uni_i64(a.qoff[r]);
-          const int64_t v = u - q0, c = uni_i64(a.qoff[r + 1]) - q0;
-          kind = v == 0 ? 0 : v <= kRPairs ? 1 : v == kRPairs + 1 ? 2 : 3;
-          sub = kind == 1 ? (int)(v - 1) : kind == 3 ? (int)(v - kRPairs - 2) : 0;
-          const int64_t need = n * c + (kind == 0 ? 0 : kind == 1 ? 1 : kind == 2 ? 1 + kRPairs : 2 + kRPairs);
-          if (uni(ld_i32(a.st + 4 * r + kStFin)) != 0) {
+          const int64_t tiles = ft_at(r + 1) - ft_at(r);
+          const int64_t c = 2 + kCT + tiles;
+          const int64_t need = n * c + (kind == 0 ? 0 : kind == 1 ? 1 : kind == 2 ? 1 + kCT : 2 + kCT);
+          if (n < 0) {
+            status = 3;   // B's folds before its first round: no task (nothing to publish)
+          } else if (uni(ld_i32(a.st + 4 * r + kStFin)) != 0) {
             status = 1;
           } else {
             const uint64_t t0 = wall_clock64();
@@ -889,7 +1005,7 @@ __global__ __launch_bounds__(kRThreads) void k_rounds(RArgs a) {
     // this task's stores are complete before wave 0 publishes it
     vm_wait<0>();
     __syncthreads();
-    prev = r;
+    prev = status == 3 ? -1 : r;
   }
 }
 
@@ -949,16 +1065,18 @@ hipError_t launch_round_pick(int32_t R, int32_t Dv, const SelectPlan &p, const S
   a.st = w.r_st;
   a.st_T = w.r_T;
   a.dcnt = w.r_dcnt;
-  a.qoff = w.r_qoff;
+  a.ftoff = w.r_qoff;
   a.head = w.r_ctl;
   a.live = reinterpret_cast<uint32_t *>(w.r_ctl + 1);
   a.abort_word = reinterpret_cast<uint32_t *>(w.r_ctl + 1) + 1;
+  a.ctl = w.r_ctl + 1;
   a.R = R;
   a.Dv = Dv;
   const int grid = std::max(1, device_cus());
-  // rounds: at most K_max + 1 per request, plus the rounds the blocks can be
-  // ahead of the last one (each holds one task)
-  a.max_rounds = (int)std::min<int64_t>(INT_MAX / 2, p.K_max + 3 + (grid + Q - 1) / Q);
+  // macro-rounds: at most K_max + 1 rounds per request, one more for the
+  // second half's last folds, plus those the blocks can be ahead of the last
+  // one (each holds one task)
+  a.max_rounds = (int)std::min<int64_t>(INT_MAX / 2, p.K_max + 4 + (grid + Q - 1) / Q);
   a.Q = Q;
   a.limit = device_wall_khz() * wait_us / 1000;
   launch_begin("rounds", s);

@@ -825,7 +825,7 @@ SelectPlan make_select_plan(int32_t R, const int32_t *cu_vis_h, const int32_t *c
   if (allow_rounds && mode == LAST_SEL_KCENTER && want_rounds(N_min, p.N_max, Dv, fdtype)) {
     p.rounds = true;
     for (int r = 0; r < R; ++r)
-      p.round_Q += kRoundPairs + 2 + (cu_vis_h[r + 1] - cu_vis_h[r] + kRoundFoldRows - 1) / kRoundFoldRows;
+      p.round_Q += kRoundCandTasks + 2 + (cu_vis_h[r + 1] - cu_vis_h[r] + kRoundFoldRows - 1) / kRoundFoldRows;
     return p;
   }
   if (!allow_groups || mode != LAST_SEL_KCENTER || R < 2 || R > kRankMaxR) return p;
