@@ -185,7 +185,7 @@ struct SmCand {
   int tok[2][32];
 };
 struct SmGreedy {
-  float mat[kRB * kRB];
+  alignas(16) float mat[kRB * kRB];
 };
 struct SmSelect {
   uint32_t v[kSelLds];            // key of each token: objective bits + 1, or 0
@@ -648,15 +648,18 @@ __device__ void task_greedy(const RArgs &a, SmAll &sm, const Req &q) {
   if (nb == 0) return;
   SmGreedy &g = sm.g;
   const float *M = a.cmat + (int64_t)q.r * kRB * kRB;
-  // rows 0..nb-1 whole (columns past nb are never read), eight loads in flight
-  const int ne = nb * kRB;
+  // rows 0..nb-1 whole (columns past nb are never read), two floats a load,
+  // eight loads in flight
+  const int ne = nb * kRB / 2;
+  const unsigned long long *M2 = reinterpret_cast<const unsigned long long *>(M);
+  unsigned long long *mat2 = reinterpret_cast<unsigned long long *>(g.mat);
   for (int x0 = tid; x0 < ne; x0 += 8 * kRThreads) {
-    float v[8];
+    unsigned long long v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = x0 + u * kRThreads < ne ? ld_f32(M + x0 + u * kRThreads) : 0.f;
+    for (int u = 0; u < 8; ++u) v[u] = x0 + u * kRThreads < ne ? ld_u64(M2 + x0 + u * kRThreads) : 0ull;
 #pragma unroll
     for (int u = 0; u < 8; ++u)
-      if (x0 + u * kRThreads < ne) g.mat[x0 + u * kRThreads] = v[u];
+      if (x0 + u * kRThreads < ne) mat2[x0 + u * kRThreads] = v[u];
   }
   __syncthreads();
   if (wave != 0) return;

@@ -135,3 +135,21 @@ def test_similarity_summary_reports_flops_not_bytes():
     assert sm["paper_flops"] == 2.0 * 64 * 64 * 576 * 4096
     assert abs(sm["tflops_on_gram_work"] - (d + o) / 0.2e-3 / 1e12) < 0.01
     assert abs(sm["gram_work_over_paper_work"] - 577 / 128) < 0.01
+
+
+def test_rounds_kernels_accounting():
+    """The rounds form (kernels norms and rounds): the norms read the features
+    once; the rounds are priced on the paper's similarity work (2 K N Dv flops
+    against the features read once), and the summary reports that form."""
+    wl = W.make("c5_video")
+    kw = bench.kernel_work(wl)
+    sw = bench.stage_work(wl)
+    assert kw["norms"] == ("hbm", wl.N_total * wl.Dv * 2)
+    assert kw["rounds"] == sw["similarity"]
+    assert sw["similarity_flops"] == 2.0 * 8 * 1024 * 16384 * 3584
+    kernels = {"norms": {"ms_per_step": 0.2}, "rounds": {"ms_per_step": 6.2}}
+    sm = bench.similarity_summary(wl, kernels)
+    assert sm["form"] == "rounds" and abs(sm["rounds_ms_per_step"] - 6.4) < 1e-9
+    assert abs(sm["tflops_on_paper_work"] - sw["similarity_flops"] / 6.4e-3 / 1e12) < 0.01
+    assert bench.kcenter_form(kernels) == "rounds"
+    assert bench.kcenter_form({"gram": {}}) == "matrix" and bench.kcenter_form({"topk": {}}) is None
