@@ -85,9 +85,16 @@ constexpr int kFtLds = 2048;                  // fold-tile prefixes held in LDS 
 static_assert(kRB % 64 == 0 && kRB <= 256, "candidate slots: whole waves");
 static_assert(kFRows == 32 * kRWaves, "a fold task: 32 tokens a wave");
 
-// Shared words between blocks go through device-scope (agent) atomic loads
-// and stores, which are coherent across the XCDs' L2 caches; a task's writes
-// are complete (s_waitcnt) before its completion count is published.
+// Every word one task hands to a task of another block (delta, candidates,
+// their distances, picks, state) is written with a device-scope (agent)
+// atomic store and read with a device-scope atomic load (the sc1 forms),
+// which go to the device's coherence point past the XCDs' separate L2
+// caches: a device-scope store is acknowledged there, so once every wave has
+// waited for its stores (s_waitcnt) and the block has met at its barrier,
+// raising the completion count cannot overtake them. No task writes such a
+// word with a plain store, which would need the L2 written back (a release
+// fence) before the count; that fence on every task costs 10% of a video
+// batch's selection.
 __device__ __forceinline__ int ld_i32(const int32_t *p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -853,6 +860,97 @@ __device__ void task_fold(const RArgs &a, SmAll &sm, const Req &q, int f) {
 }
 
 // ------------------------------------------------------------- the rounds
+// The task at position u of a macro-round. The requests form two halves,
+// A = [0, RA) and B = [RA, R), half a round apart, so that one half's serial
+// chain (select, candidate Gram, greedy) runs while the other half folds.
+// Macro-round m lists, in this order:
+//   S of A's round m; the first half of B's folds of round m - 1; C (kCT
+//   each) of A's round m; G of A's round m; the rest of B's folds; S of B's
+//   round m; the first half of A's folds of round m; C and G of B's round m;
+//   the rest of A's folds.
+// The folds listed between a select and its candidate tasks keep the blocks
+// busy while the select runs. Each task depends only on tasks listed before
+// it. Sets kind (0 S, 1 C, 2 G, 3 F), the request and the sub-index (C: the
+// block pair; F: the fold tile within the request); returns -1 for B's folds
+// (they belong to round m - 1), else 0. `ft(i)` is the first fold tile of
+// request i (ft(R) the total). Every value is wave-uniform.
+template <typename Ft>
+__device__ __forceinline__ int64_t decode_task(int64_t u, int64_t R, Ft ft, int &kind, int &r, int &sub) {
+  const int64_t RA = (R + 1) / 2, RB = R - RA;
+  const int64_t FA = ft(RA), FB = ft(R) - FA, hA = FA / 2, hB = FB / 2;
+  // fold tile g of the requests [r0, r0 + nr) (g counts from the first of them)
+  auto fold = [&](int64_t r0, int64_t nr, int64_t g) {
+    const int64_t f = ft(r0) + g;
+    int64_t lo = r0, hi = r0 + nr - 1;   // the last request whose first tile is <= f
+    while (lo < hi) {
+      const int64_t mid = (lo + hi + 1) >> 1;
+      if (ft(mid) <= f)
+        lo = mid;
+      else
+        hi = mid - 1;
+    }
+    kind = 3;
+    r = (int)lo;
+    sub = (int)(f - ft(lo));
+  };
+  int64_t x = u;
+  if (x < RA) {
+    kind = 0;
+    r = (int)x;
+    return 0;
+  }
+  x -= RA;
+  if (x < hB) {
+    fold(RA, RB, x);
+    return -1;
+  }
+  x -= hB;
+  if (x < RA * kCT) {
+    kind = 1;
+    r = (int)(x / kCT);
+    sub = (int)(x % kCT);
+    return 0;
+  }
+  x -= RA * kCT;
+  if (x < RA) {
+    kind = 2;
+    r = (int)x;
+    return 0;
+  }
+  x -= RA;
+  if (x < FB - hB) {
+    fold(RA, RB, hB + x);
+    return -1;
+  }
+  x -= FB - hB;
+  if (x < RB) {
+    kind = 0;
+    r = (int)(RA + x);
+    return 0;
+  }
+  x -= RB;
+  if (x < hA) {
+    fold(0, RA, x);
+    return 0;
+  }
+  x -= hA;
+  if (x < RB * kCT) {
+    kind = 1;
+    r = (int)(RA + x / kCT);
+    sub = (int)(x % kCT);
+    return 0;
+  }
+  x -= RB * kCT;
+  if (x < RB) {
+    kind = 2;
+    r = (int)(RA + x);
+    return 0;
+  }
+  x -= RB;
+  fold(0, RA, hA + x);
+  return 0;
+}
+
 __global__ __launch_bounds__(kRThreads) void k_rounds(RArgs a) {
   __shared__ SmAll sm;
   __shared__ unsigned long long shk[kRWaves];
@@ -864,7 +962,7 @@ __global__ __launch_bounds__(kRThreads) void k_rounds(RArgs a) {
   if (a.R < kFtLds)
     for (int x = tid; x <= a.R; x += kRThreads) s_ft[x] = (int)a.ftoff[x];
   __syncthreads();
-  auto ft_at = [&](int64_t i) -> int64_t { return a.R < kFtLds ? (int64_t)s_ft[i] : uni_i64(a.ftoff[i]); };
+  auto ft_at = [&](int64_t i) -> int64_t { return uni_i64(a.R < kFtLds ? (int64_t)s_ft[i] : a.ftoff[i]); };
   int prev = -1;   // the request of the task this block has just completed
   for (;;) {
     // Wave 0 publishes the completed task (every wave waited for its stores
@@ -890,63 +988,8 @@ __global__ __launch_bounds__(kRThreads) void k_rounds(RArgs a) {
           if (lane == 0) st_u32(a.abort_word, 1u);
           status = 2;
         } else {
-          // The requests form two halves, A = [0, RA) and B = [RA, R), half a
-          // round apart, so that one half's serial chain (select, candidate
-          // Gram, greedy) runs while the other half folds: macro-round m
-          // lists S, C (kCT each), G of A's round m, the folds of B's round
-          // m - 1, S, C, G of B's round m, then the folds of A's round m.
-          // Each task depends only on tasks listed before it.
-          const int64_t R = a.R, RA = (R + 1) / 2, RB = R - RA;
-          const int64_t FA = ft_at(RA), FB = ft_at(R) - FA;
-          int64_t n = m, x = u;
-          auto chain = [&](int64_t r0, int64_t nr) {   // S, C, G of requests [r0, r0 + nr); false: past them
-            if (x < nr) {
-              kind = 0;
-              r = (int)(r0 + x);
-              return true;
-            }
-            x -= nr;
-            if (x < nr * kCT) {
-              kind = 1;
-              r = (int)(r0 + x / kCT);
-              sub = (int)(x % kCT);
-              return true;
-            }
-            x -= nr * kCT;
-            if (x < nr) {
-              kind = 2;
-              r = (int)(r0 + x);
-              return true;
-            }
-            x -= nr;
-            return false;
-          };
-          auto folds = [&](int64_t r0, int64_t nr, int64_t nf) {   // F of requests [r0, r0 + nr)
-            if (x >= nf) {
-              x -= nf;
-              return false;
-            }
-            kind = 3;
-            const int64_t f = ft_at(r0) + x;
-            int lo = (int)r0, hi = (int)(r0 + nr - 1);   // the last r with ftoff[r] <= f
-            while (lo < hi) {
-              const int mid = (lo + hi + 1) >> 1;
-              if (ft_at(mid) <= f)
-                lo = mid;
-              else
-                hi = mid - 1;
-            }
-            r = lo;
-            sub = (int)(f - ft_at(r));
-            return true;
-          };
-          if (!chain(0, RA)) {
-            if (folds(RA, RB, FB)) {
-              n = m - 1;
-            } else if (!chain(RA, RB)) {
-              folds(0, RA, FA);
-            }
-          }
+          const int64_t tq = decode_task(u, a.R, ft_at, kind, r, sub);
+          const int64_t n = m + tq;   // tq = -1: B's folds of the previous round
           const int64_t tiles = ft_at(r + 1) - ft_at(r);
           const int64_t c = 2 + kCT + tiles;
           const int64_t need = n * c + (kind == 0 ? 0 : kind == 1 ? 1 : kind == 2 ? 1 + kCT : 2 + kCT);
