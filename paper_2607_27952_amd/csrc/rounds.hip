@@ -597,7 +597,9 @@ __device__ void task_select(const RArgs &a, SmAll &sm, const Req &q, unsigned lo
 // C: candidate slots [32 sa, 32 sa + 32) against [32 sb, 32 sb + 32), both
 // directions. The eight waves take the 128-column chunks in turn (chunk c on
 // wave c % 8), keep each chunk's fp32 partial sums in LDS, and the chunks
-// are then added in column order in fp64, as the Gram folds them.
+// are then added in column order in fp64, as the Gram folds them. A wave's
+// next chunk is loaded while the matrix cores work on the current one, and
+// the norms the distances need are loaded before the chunks.
 __device__ void task_cand(const RArgs &a, SmAll &sm, const Req &q, int pair) {
   const int tid = threadIdx.x, lane = tid & 63, wave = uni(tid >> 6);
   int sa = 0, rest = pair;
@@ -614,36 +616,61 @@ __device__ void task_cand(const RArgs &a, SmAll &sm, const Req &q, int pair) {
     c.tok[side][tid & 31] = ld_i32(a.cand + (int64_t)q.r * kRB + min(slot, nb - 1));
   }
   __syncthreads();
+  // this thread's two outputs e = tid + 512 h: A row i, B column j of the
+  // 32 x 32 accumulator layout, and the norms of their tokens
+  constexpr int kOut = 1024 / kRThreads;
+  int ti[kOut], tj[kOut];
+  double nni[kOut], nnj[kOut], invi[kOut], invj[kOut];
+#pragma unroll
+  for (int h = 0; h < kOut; ++h) {
+    const int e = tid + h * kRThreads, v = e >> 6, l = e & 63;
+    ti[h] = c.tok[0][(l >> 5) * 4 + (v & 3) + 8 * (v >> 2)];
+    tj[h] = c.tok[1][l & 31];
+    nni[h] = a.nn[q.n0 + ti[h]];
+    nnj[h] = a.nn[q.n0 + tj[h]];
+    invi[h] = a.inv[q.n0 + ti[h]];
+    invj[h] = a.inv[q.n0 + tj[h]];
+  }
   const int nc = a.Dv / 128;
   const uint16_t *pa = a.X + (q.n0 + c.tok[0][lane & 31]) * (int64_t)a.Dv + 8 * (lane >> 5);
   const uint16_t *pb = a.X + (q.n0 + c.tok[1][lane & 31]) * (int64_t)a.Dv + 8 * (lane >> 5);
-  for (int ch = wave; ch < nc; ch += kRWaves) {
-    uint4 fa[8], fb[8];
+  auto load = [&](int ch, uint4 (&fa)[8], uint4 (&fb)[8]) {
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
       fa[s] = *reinterpret_cast<const uint4 *>(pa + ch * 128 + 16 * s);
       fb[s] = *reinterpret_cast<const uint4 *>(pb + ch * 128 + 16 * s);
     }
+  };
+  auto product = [&](int ch, const uint4 (&fa)[8], const uint4 (&fb)[8]) {
     f32x16 acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fa[0]), as_bf16x8(fb[0]), f32x16{}, 0, 0, 0);
 #pragma unroll
     for (int s = 1; s < 8; ++s)
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(fa[s]), as_bf16x8(fb[s]), acc, 0, 0, 0);
 #pragma unroll
     for (int v = 0; v < 16; ++v) c.part[ch][v * 64 + lane] = acc[v];
+  };
+  // chunks wave, wave + 8, ... in two register sets, one chunk ahead
+  uint4 xa[8], xb[8], ya[8], yb[8];
+  if (wave < nc) load(wave, xa, xb);
+  for (int ch = wave; ch < nc; ch += 2 * kRWaves) {
+    const int c1 = ch + kRWaves, c2 = ch + 2 * kRWaves;
+    if (c1 < nc) load(c1, ya, yb);
+    product(ch, xa, xb);
+    if (c2 < nc) load(c2, xa, xb);
+    if (c1 < nc) product(c1, ya, yb);
   }
   __syncthreads();
   float *M = a.cmat + (int64_t)q.r * kRB * kRB;
-  for (int e = tid; e < 1024; e += kRThreads) {
-    const int v = e >> 6, l = e & 63;
+#pragma unroll
+  for (int h = 0; h < kOut; ++h) {
+    const int e = tid + h * kRThreads, v = e >> 6, l = e & 63;
     const int i = (l >> 5) * 4 + (v & 3) + 8 * (v >> 2), j = l & 31;   // A row, B column
     const int si = 32 * sa + i, sj = 32 * sb + j;
     if (si >= nb || sj >= nb) continue;
     double dot = 0.0;
     for (int ch = 0; ch < nc; ++ch) dot += (double)c.part[ch][e];
-    const int ti = c.tok[0][i], tj = c.tok[1][j];
-    const double nni = a.nn[q.n0 + ti], nnj = a.nn[q.n0 + tj], invi = a.inv[q.n0 + ti], invj = a.inv[q.n0 + tj];
-    st_f32(M + (int64_t)si * kRB + sj, coverage_dir(ti, tj, dot, nni, nnj, invi, invj));
-    if (sa != sb) st_f32(M + (int64_t)sj * kRB + si, coverage_dir(tj, ti, dot, nnj, nni, invj, invi));
+    st_f32(M + (int64_t)si * kRB + sj, coverage_dir(ti[h], tj[h], dot, nni[h], nnj[h], invi[h], invj[h]));
+    if (sa != sb) st_f32(M + (int64_t)sj * kRB + si, coverage_dir(tj[h], ti[h], dot, nnj[h], nni[h], invj[h], invi[h]));
   }
 }
 
