@@ -99,6 +99,24 @@ def test_rounds_small(case):
     replay(wl, w32, kept, order, f"case {seed}")
 
 
+def test_rounds_many_requests():
+    """2100 requests: past the 2048 whose fold-tile prefixes the rounds keep
+    in LDS, so the task decode reads them from the workspace, and the prefix
+    kernel takes several passes. Bit-identical to the matrix form; a few
+    requests replayed on the oracle."""
+    R = 2100
+    wl = W.tiny(41, R=R, n_range=(1, 64), t_range=(1, 4), Hq=2, Hkv=1, Dh=64, Dv=256, f_dtype=W.BF16,
+                k_frac=0.3, comps=3)
+    rng = np.random.default_rng(41)
+    w32 = np.concatenate([rng.dirichlet(np.ones(wl.n(r)) * 0.7) for r in range(R)]).astype(np.float32)
+    dw = last.DeviceWorkload.upload(wl)
+    kept, order, _ = both(dw.feats, torch.from_numpy(w32).cuda(), wl.cu_vis, wl.cu_keep, "2100 requests")
+    sub = [0, 1, 1023, 2047, 2048, 2099]
+    idx = np.concatenate([np.arange(wl.cu_keep[r], wl.cu_keep[r + 1]) for r in sub])
+    vis = np.concatenate([np.arange(wl.cu_vis[r], wl.cu_vis[r + 1]) for r in sub])
+    replay(wl.subset(sub), w32[vis], kept[idx], order[idx], "2100 requests, sampled")
+
+
 def _hand(X, w, K):
     X = np.asarray(X, np.float32)
     X = np.pad(X, ((0, 0), (0, (-X.shape[1]) % 256)))   # zero columns change no norm or dot
